@@ -1,0 +1,436 @@
+"""Plain CPU oracle for loop-partitioned tensor programs (PartIR:Core semantics).
+
+TEST INFRASTRUCTURE ONLY.  Nothing on the product path may import, call or
+execute this module; only the test suite, the smoke check and the CPU-baseline
+leg of the benchmark do.  It shares no code with the HIP library.
+
+What it computes
+----------------
+PartIR:Core (paper Sec. 5 and App. C, figure "Interpretation of PartIR:Core")
+gives a denotational meaning to three constructs:
+
+* ``slice d x[r]``  -- the r-th of n equal contiguous chunks of x along dim d,
+  i.e. ``x[..., r*n_d:(r+1)*n_d, ...]`` with ``n_d = x.shape[d] / n`` (typing
+  rule TSlice requires n to divide the dimension exactly);
+* ``loop a [#tile<d>] e`` -- the direct sum (concatenation along dim d) of the
+  body evaluated at r = 0..n-1 (typing rule TTile multiplies dim d by n);
+* ``loop a [#sum] e`` -- the sum of the body over r = 0..n-1 (rule TSum keeps
+  the type).
+
+Any other op is evaluated by its plain definition.  This module evaluates the
+loop nests of the partitioned programs *literally*, enumerating every virtual
+shard (the "shard interpreter"), and separately evaluates the same programs
+unpartitioned on whole tensors (the "unpartitioned evaluator").  By the
+paper's correctness theorem for the lowering (App. C, theorem "correctness of
+translation") and the matmul program equivalences (Sec. 5.2.1, figure
+"matmul-examples"), both must agree up to rounding.
+
+Arithmetic is float64 throughout.  Inputs arrive already decoded (exactly)
+from their float32 / bfloat16 storage; no intermediate is rounded.  Library
+primitives used as single steps: ``numpy.matmul`` (fp64 matrix product),
+``numpy.exp``, ``numpy.sqrt`` and ``scipy.special.erf``.
+
+Readings of the paper that this module fixes (where it is silent):
+* the sum of a ``#sum`` loop is taken in increasing r;
+* GELU is the exact erf form 0.5*x*(1+erf(x/sqrt 2));
+* causal attention lets query i see keys j <= i of its own sequence, with
+  scores scaled by ``scale`` and a max-subtracted softmax;
+* RMSNorm is g * x / sqrt(mean(x^2) + eps) over the last dim;
+* a bias of a ``#sum`` loop is added once, after the loop; a bias of a
+  ``#tile`` loop is sliced with the tiled operand (add's tile-mapping entry
+  needs both operands tiled alike, Sec. 5.2.1);
+* weight matrices are passed in their logical [fan_in, fan_out] orientation.
+
+Parity pins for every function here live in ``tests/test_oracle_*.py``.
+"""
+from __future__ import annotations
+
+import math
+from typing import Callable, Optional, Sequence
+
+import numpy as np
+from scipy.special import erf as _erf
+
+AXIS_NONE, AXIS_M, AXIS_N, AXIS_K = -1, 0, 1, 2
+
+
+# ---------------------------------------------------------------------------
+# PartIR:Core constructs (App. C, figure "Interpretation of PartIR:Core")
+# ---------------------------------------------------------------------------
+def slice_(x: np.ndarray, d: int, r: int, n: int) -> np.ndarray:
+    """``slice d x[r]`` over an axis of size n (rule TSlice)."""
+    size = x.shape[d]
+    if n <= 0 or size % n != 0:
+        raise ValueError(f"axis size {n} does not divide dim {d} of size {size}")
+    if not 0 <= r < n:
+        raise ValueError(f"range value {r} outside range<{n}>")
+    nd = size // n
+    index = [slice(None)] * x.ndim
+    index[d] = slice(r * nd, (r + 1) * nd)
+    return x[tuple(index)]
+
+
+def loop_tile(n: int, d: int, body: Callable[[int], np.ndarray]) -> np.ndarray:
+    """``loop a [#tile<d>] (r: range<n>) { body }``: direct sum along dim d."""
+    parts = [body(r) for r in range(n)]
+    return np.concatenate(parts, axis=d)
+
+
+def loop_sum(n: int, body: Callable[[int], np.ndarray]) -> np.ndarray:
+    """``loop a [#sum] (r: range<n>) { body }``: sum over r, r increasing."""
+    acc = np.array(body(0), dtype=np.float64, copy=True)
+    for r in range(1, n):
+        acc = acc + body(r)
+    return acc
+
+
+# ---------------------------------------------------------------------------
+# Plain ops (fp64)
+# ---------------------------------------------------------------------------
+def matmul(a: np.ndarray, b: np.ndarray) -> np.ndarray:
+    return np.matmul(np.asarray(a, np.float64), np.asarray(b, np.float64))
+
+
+def gelu_erf(x: np.ndarray) -> np.ndarray:
+    x = np.asarray(x, np.float64)
+    return 0.5 * x * (1.0 + _erf(x / math.sqrt(2.0)))
+
+
+def activation(x: np.ndarray, act: str) -> np.ndarray:
+    if act == "none":
+        return np.asarray(x, np.float64)
+    if act == "gelu":
+        return gelu_erf(x)
+    raise ValueError(f"unknown activation {act!r}")
+
+
+def rmsnorm(x: np.ndarray, g: np.ndarray, eps: float) -> np.ndarray:
+    x = np.asarray(x, np.float64)
+    ms = np.mean(x * x, axis=-1, keepdims=True)
+    return np.asarray(g, np.float64) * x / np.sqrt(ms + eps)
+
+
+def causal_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, scale: float,
+                     causal: bool = True, q_pos: Optional[np.ndarray] = None) -> np.ndarray:
+    """Softmax attention of one head of one sequence.
+
+    q: [nq, dh] queries at positions ``q_pos`` (default 0..nq-1);
+    k, v: [nk, dh] keys/values at positions 0..nk-1.
+    o_i = sum_j p_ij v_j with p_ij = exp(s_ij - max_j s_ij) / sum_j(...),
+    s_ij = scale * q_i . k_j over keys j <= pos(i) when causal.
+    """
+    q = np.asarray(q, np.float64)
+    k = np.asarray(k, np.float64)
+    v = np.asarray(v, np.float64)
+    if q_pos is None:
+        q_pos = np.arange(q.shape[0])
+    s = matmul(q, k.T) * scale
+    if causal:
+        key_pos = np.arange(k.shape[0])
+        s = np.where(key_pos[None, :] <= np.asarray(q_pos)[:, None], s, -np.inf)
+    m = np.max(s, axis=1, keepdims=True)
+    p = np.exp(s - m)
+    p = p / np.sum(p, axis=1, keepdims=True)
+    return matmul(p, v)
+
+
+# ---------------------------------------------------------------------------
+# Single partitioned matmul: the three TMR forms of matmul (Sec. 5.2.1)
+# ---------------------------------------------------------------------------
+def loop_matmul(A: np.ndarray, B: np.ndarray, tile_axis: int, sum_axis: int, R: int) -> np.ndarray:
+    """C = A @ B written as a loop over R virtual shards.
+
+    tile_axis M: ``loop [#tile<0>] { matmul(slice 0 A[r], B) }``
+    tile_axis N: ``loop [#tile<1>] { matmul(A, slice 1 B[r]) }``
+    sum_axis  K: ``loop [#sum]     { matmul(slice 1 A[r], slice 0 B[r]) }``
+    tile and sum together: the tile loop outside, the sum loop inside, over two
+    distinct axes of size R each (nested loops over one axis are forbidden,
+    Sec. 5.2.3).
+    """
+    if tile_axis not in (AXIS_NONE, AXIS_M, AXIS_N):
+        raise ValueError("tile_axis must be NONE, M or N")
+    if sum_axis not in (AXIS_NONE, AXIS_K):
+        raise ValueError("sum_axis must be NONE or K")
+
+    def summed(a, b):
+        if sum_axis == AXIS_K:
+            return loop_sum(R, lambda r: matmul(slice_(a, 1, r, R), slice_(b, 0, r, R)))
+        return matmul(a, b)
+
+    if tile_axis == AXIS_M:
+        return loop_tile(R, 0, lambda r: summed(slice_(A, 0, r, R), B))
+    if tile_axis == AXIS_N:
+        return loop_tile(R, 1, lambda r: summed(A, slice_(B, 1, r, R)))
+    return summed(A, B)
+
+
+def abs_product(A: np.ndarray, B: np.ndarray) -> np.ndarray:
+    """|A|.|B|: the elementwise error normaliser of a product (Higham Sec. 3.5)."""
+    return matmul(np.abs(A), np.abs(B))
+
+
+# ---------------------------------------------------------------------------
+# Megatron MLP block, optionally nested in a batch #tile
+# ---------------------------------------------------------------------------
+def mlp_block(X, W1, W2, b1=None, b2=None, act="gelu", R_batch=1, R_model=1,
+              rows: Optional[Sequence[int]] = None, return_norm=False):
+    """Y = loop b [#tile<0>](R_batch) { loop m [#sum](R_model) {
+              act(slice 0 X[b] @ slice 1 W1[m] + slice 0 b1[m]) @ slice 0 W2[m] } + b2 }
+
+    X [T, D], W1 [D, F], W2 [F, D], b1 [F] or None, b2 [D] or None.
+    ``rows``: evaluate only these output rows (each row is computed by the batch
+    shard that owns it, exactly as in the full evaluation).
+    With ``return_norm`` also returns the normaliser |H|.|W2| (+|b2|) of the
+    last contraction.
+    """
+    T = X.shape[0]
+    F = W1.shape[1]
+    sel = np.arange(T) if rows is None else np.asarray(rows)
+    out = np.zeros((len(sel), W2.shape[1]))
+    norm = np.zeros_like(out)
+    Tb = T // R_batch
+    if T % R_batch or F % R_model:
+        raise ValueError("indivisible partition")
+    for b in range(R_batch):
+        xb = slice_(X, 0, b, R_batch)
+        mine = [(i, r - b * Tb) for i, r in enumerate(sel) if b * Tb <= r < (b + 1) * Tb]
+        if not mine:
+            continue
+        local = np.array([t for _, t in mine])
+        xr = xb[local]
+
+        def shard(m):
+            h = matmul(xr, slice_(W1, 1, m, R_model))
+            if b1 is not None:
+                h = h + slice_(np.asarray(b1), 0, m, R_model)
+            h = activation(h, act)
+            w2 = slice_(W2, 0, m, R_model)
+            return matmul(h, w2), (abs_product(h, w2) if return_norm else None)
+
+        parts = [shard(m) for m in range(R_model)]
+        y = loop_sum(R_model, lambda m: parts[m][0])
+        nrm = loop_sum(R_model, lambda m: parts[m][1]) if return_norm else None
+        if b2 is not None:
+            y = y + np.asarray(b2, np.float64)
+            if return_norm:
+                nrm = nrm + np.abs(np.asarray(b2, np.float64))
+        idx = np.array([i for i, _ in mine])
+        out[idx] = y
+        if return_norm:
+            norm[idx] = nrm
+    return (out, norm) if return_norm else out
+
+
+def mlp_ref(X, W1, W2, b1=None, b2=None, act="gelu"):
+    """Unpartitioned MLP: act(X W1 + b1) W2 + b2."""
+    h = matmul(X, W1)
+    if b1 is not None:
+        h = h + b1
+    y = matmul(activation(h, act), W2)
+    if b2 is not None:
+        y = y + b2
+    return y
+
+
+# ---------------------------------------------------------------------------
+# Attention block: heads #tile inside a Megatron #sum, in a batch #tile
+# ---------------------------------------------------------------------------
+def _attend_shard(xb, Wq_m, Wk_m, Wv_m, n_seq, S, heads, d_head, scale, causal, sel_local):
+    """Heads-#tile loop of one model shard over the sequences of one batch shard.
+
+    Returns the attention output rows ``sel_local`` ([n_sel, heads*d_head]).
+    For each sequence only its key prefix up to the largest selected position is
+    projected (keys beyond it are masked for every selected query)."""
+    out = np.zeros((len(sel_local), heads * d_head))
+    for s in range(n_seq):
+        mine = [(i, t - s * S) for i, t in enumerate(sel_local) if s * S <= t < (s + 1) * S]
+        if not mine:
+            continue
+        pos = np.array([p for _, p in mine])
+        nk = (int(pos.max()) + 1) if causal else S
+        xs = xb[s * S: s * S + nk]
+        q_rows = xs[pos]
+        Q = matmul(q_rows, Wq_m)
+        K = matmul(xs, Wk_m)
+        V = matmul(xs, Wv_m)
+        o = loop_tile(heads, 1, lambda h: causal_attention(
+            slice_(Q, 1, h, heads), slice_(K, 1, h, heads), slice_(V, 1, h, heads),
+            scale, causal, q_pos=pos))
+        out[np.array([i for i, _ in mine])] = o
+    return out
+
+
+def attn_block(X, Wq, Wk, Wv, Wo, B, S, n_heads, d_head, causal=True, scale=None,
+               R_batch=1, R_model=1, rows=None, return_norm=False):
+    """Y = loop b [#tile<0>](R_batch) { loop m [#sum](R_model) {
+              (loop h [#tile<1>](heads/R_model) { attn(q_h, k_h, v_h) }) @ slice 0 Wo[m] } }
+    with q = slice 0 X[b] @ slice 1 Wq[m] (and k, v likewise); X is [B*S, D]
+    sequence-major.  Batch shards hold whole sequences."""
+    if scale is None:
+        scale = 1.0 / math.sqrt(d_head)
+    T, D = X.shape
+    if T != B * S or n_heads * d_head != Wq.shape[1]:
+        raise ValueError("shape mismatch")
+    if B % R_batch or n_heads % R_model:
+        raise ValueError("indivisible partition")
+    sel = np.arange(T) if rows is None else np.asarray(rows)
+    out = np.zeros((len(sel), Wo.shape[1]))
+    norm = np.zeros_like(out)
+    Tb = T // R_batch
+    hps = n_heads // R_model
+    for b in range(R_batch):
+        xb = slice_(X, 0, b, R_batch)
+        mine = [(i, r - b * Tb) for i, r in enumerate(sel) if b * Tb <= r < (b + 1) * Tb]
+        if not mine:
+            continue
+        local = np.array([t for _, t in mine])
+
+        def shard(m):
+            a = _attend_shard(xb, slice_(Wq, 1, m, R_model), slice_(Wk, 1, m, R_model),
+                              slice_(Wv, 1, m, R_model), B // R_batch, S, hps, d_head,
+                              scale, causal, local)
+            wo = slice_(Wo, 0, m, R_model)
+            return matmul(a, wo), (abs_product(a, wo) if return_norm else None)
+
+        parts = [shard(m) for m in range(R_model)]
+        y = loop_sum(R_model, lambda m: parts[m][0])
+        idx = np.array([i for i, _ in mine])
+        out[idx] = y
+        if return_norm:
+            norm[idx] = loop_sum(R_model, lambda m: parts[m][1])
+    return (out, norm) if return_norm else out
+
+
+def attn_ref(X, Wq, Wk, Wv, Wo, B, S, n_heads, d_head, causal=True, scale=None):
+    """Unpartitioned attention block on whole tensors."""
+    if scale is None:
+        scale = 1.0 / math.sqrt(d_head)
+    Q, K, V = matmul(X, Wq), matmul(X, Wk), matmul(X, Wv)
+    A = np.zeros_like(Q)
+    for s in range(B):
+        rs = slice(s * S, (s + 1) * S)
+        for h in range(n_heads):
+            cs = slice(h * d_head, (h + 1) * d_head)
+            A[rs, cs] = causal_attention(Q[rs, cs], K[rs, cs], V[rs, cs], scale, causal)
+    return matmul(A, Wo)
+
+
+# ---------------------------------------------------------------------------
+# Pre-norm decoder layer / stack (residual stream kept unrounded)
+# ---------------------------------------------------------------------------
+def decoder_layer(x, p, B, S, n_heads, d_head, eps=1e-6, R_batch=1, R_model=1,
+                  rows=None, return_norm=False):
+    """x' = loop b [#tile<0>](R_batch) { xb = slice 0 x[b];
+              h  = xb + loop m [#sum](R_model) { attn_m(rms(xb, g1)) @ slice 0 Wo[m] };
+              h + loop m [#sum](R_model) { gelu(rms(h, g2) @ slice 1 W1[m]) @ slice 0 W2[m] } }
+
+    p: dict with g1, g2 [D], Wq, Wk, Wv, Wo [D, D], W1 [D, F], W2 [F, D].
+    rms(xb, g1) is a replicated value of the batch shard: every model shard
+    reads the same normalised rows.  ``rows`` restricts the output rows; the
+    attention then reads every key position of the touched sequences up to the
+    largest requested one.  The normaliser returned with ``return_norm`` is
+    |h| + |gelu(.)|.|W2| of the final residual add."""
+    T, D = x.shape
+    if T != B * S or B % R_batch or n_heads % R_model or p["W1"].shape[1] % R_model:
+        raise ValueError("indivisible partition")
+    scale = 1.0 / math.sqrt(d_head)
+    x = np.asarray(x, np.float64)
+    sel = np.arange(T) if rows is None else np.asarray(rows)
+    out = np.zeros((len(sel), D))
+    norm = np.zeros_like(out)
+    Tb = T // R_batch
+    hps = n_heads // R_model
+    for b in range(R_batch):
+        xb = slice_(x, 0, b, R_batch)
+        mine = [(i, r - b * Tb) for i, r in enumerate(sel) if b * Tb <= r < (b + 1) * Tb]
+        if not mine:
+            continue
+        local = np.array([t for _, t in mine])
+        xn = rmsnorm(xb, p["g1"], eps)
+
+        def attn_shard(m):
+            a = _attend_shard(xn, slice_(p["Wq"], 1, m, R_model), slice_(p["Wk"], 1, m, R_model),
+                              slice_(p["Wv"], 1, m, R_model), B // R_batch, S, hps, d_head,
+                              scale, True, local)
+            return matmul(a, slice_(p["Wo"], 0, m, R_model))
+
+        h = xb[local] + loop_sum(R_model, attn_shard)
+        hn = rmsnorm(h, p["g2"], eps)
+        parts = []
+        for m in range(R_model):
+            g = gelu_erf(matmul(hn, slice_(p["W1"], 1, m, R_model)))
+            w2 = slice_(p["W2"], 0, m, R_model)
+            parts.append((matmul(g, w2), abs_product(g, w2) if return_norm else None))
+        idx = np.array([i for i, _ in mine])
+        out[idx] = h + loop_sum(R_model, lambda m: parts[m][0])
+        if return_norm:
+            norm[idx] = np.abs(h) + loop_sum(R_model, lambda m: parts[m][1])
+    return (out, norm) if return_norm else out
+
+
+def decoder_rows_needed(rows, T, S):
+    """Rows of a layer's input that its attention needs for output ``rows``:
+    every position up to the largest requested one in each touched sequence."""
+    need = set()
+    for r in np.asarray(rows):
+        s0 = (int(r) // S) * S
+        need.update(range(s0, int(r) + 1))
+    return np.array(sorted(need))
+
+
+def decoder(x, layers, B, S, n_heads, d_head, eps=1e-6, R_batch=1, R_model=1,
+            rows=None, return_norm=False):
+    """A stack of decoder layers applied in order.  With ``rows``, each layer
+    is evaluated on the rows the following layers need (prefixes of the touched
+    sequences), and the last layer on ``rows`` only."""
+    T = x.shape[0]
+    x = np.asarray(x, np.float64)
+    if rows is None:
+        out, nrm = x, None
+        for p in layers:
+            out, nrm = decoder_layer(out, p, B, S, n_heads, d_head, eps, R_batch, R_model,
+                                     return_norm=True)
+        return (out, nrm) if return_norm else out
+    rows = np.asarray(rows)
+    need = decoder_rows_needed(rows, T, S)
+    # x restricted to the needed prefix rows; positions keep their sequence index
+    cur = {int(r): x[r] for r in need}
+    for li, p in enumerate(layers):
+        last = li == len(layers) - 1
+        want = rows if last else need
+        full = np.zeros_like(x)
+        for r, v in cur.items():
+            full[r] = v
+        # rows outside `need` are never read: attention of a needed row only
+        # looks at earlier positions of its own sequence, all of which are needed
+        res, nrm = decoder_layer(full, p, B, S, n_heads, d_head, eps, R_batch, R_model,
+                                 rows=want, return_norm=True)
+        cur = {int(r): res[i] for i, r in enumerate(want)}
+    out = np.stack([cur[int(r)] for r in rows])
+    return (out, nrm) if return_norm else out
+
+
+def decoder_ref(x, layers, B, S, n_heads, d_head, eps=1e-6):
+    """Unpartitioned decoder stack."""
+    x = np.asarray(x, np.float64)
+    for p in layers:
+        h = x + attn_ref(rmsnorm(x, p["g1"], eps), p["Wq"], p["Wk"], p["Wv"], p["Wo"],
+                         B, S, n_heads, d_head)
+        x = h + mlp_ref(rmsnorm(h, p["g2"], eps), p["W1"], p["W2"])
+    return x
+
+
+# ---------------------------------------------------------------------------
+# Parity measure (the elementwise forward-error form)
+# ---------------------------------------------------------------------------
+def normalised_error(got, ref, norm):
+    """max_ij |got - ref|_ij / norm_ij; entries with norm 0 must match exactly
+    (they contribute +inf otherwise)."""
+    got = np.asarray(got, np.float64)
+    ref = np.asarray(ref, np.float64)
+    norm = np.asarray(norm, np.float64)
+    diff = np.abs(got - ref)
+    with np.errstate(divide="ignore", invalid="ignore"):
+        e = np.where(norm > 0, diff / np.where(norm > 0, norm, 1.0),
+                     np.where(diff == 0, 0.0, np.inf))
+    return float(np.max(e)) if e.size else 0.0
