@@ -1,0 +1,284 @@
+#!/usr/bin/env python3
+"""Benchmark: loop-partitioned MLP / attention chains on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+
+A step is one call of the partitioned program over one batch of seeded
+synthetic input already resident in HBM (all virtual shards, every #tile and
+#sum of the nest).  Prints one JSON line with the achieved TFLOP/s, the
+roofline of the dominant kernel (its average launch time measured with HIP
+events on the launch stream during the timed steps) and the CPU oracle timed
+on a bounded sample of the same workload.
+
+--copy-calib BYTES runs only a device-to-device copy of that size (the
+reference kernel for scaling HBM counters) and exits.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2516.6     # 256 CU x 2.4 GHz x 4096 FLOP/clk (dense bf16 MFMA)
+PEAK_F32_TFLOPS = 157.3       # dense fp32 MFMA
+PEAK_HBM_GBS = 8000.0
+METRIC = "TFLOP/s + MFMA util (% bf16 peak) for loop-partitioned MLP/attn chains"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="mlp_megatron")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0, help="target CPU work of the oracle sample")
+    ap.add_argument("--copy-calib", type=int, default=0)
+    return ap.parse_args()
+
+
+# ---------------------------------------------------------------------------
+# workload setup: host inputs -> device; returns a step closure
+# ---------------------------------------------------------------------------
+def setup(w, P, I):
+    import torch
+    from paper_2401_11202_amd import workloads as W
+    x = W.make_inputs(w)
+    dev_t = lambda t: I.transposed(t).to_device()
+    if w.kind == "matmul":
+        A = x["A"].to_device()
+        B = x["B"].to_device()
+        C = torch.empty((w["M"], w["N"]), dtype=torch.float32, device="cuda")
+        tile = {-1: None, 0: "M", 1: "N"}[w["tile"]]
+        summ = {-1: None, 2: "K"}[w["sum"]]
+        ws = torch.empty(max(1, P.lib().partir_loop_matmul_workspace(
+            w["M"], w["N"], w["K"], P.F32, P.F32, P.B_KN, P._axis(tile), P._axis(summ), w["R"], P.SUM_AUTO)),
+            dtype=torch.uint8, device="cuda")
+        step = lambda: P.loop_matmul(A, B, tile=tile, sum=summ, R=w["R"], b_layout="kn", out=C, workspace=ws)
+        roles = {"loop_matmul.f32": 2.0 * w["M"] * w["N"] * w["K"]}
+        return x, step, roles, "mfma_f32"
+    if w.kind == "mlp":
+        T, D, F = w["T"], w["D"], w["F"]
+        X, W1t, W2t = x["X"].to_device(), dev_t(x["W1"]), dev_t(x["W2"])
+        Y = torch.empty((T, D), dtype=torch.float32, device="cuda")
+        ws = torch.empty(P.mlp_block_workspace(T, D, F, P.F32, w["R_batch"], w["R_model"]),
+                         dtype=torch.uint8, device="cuda")
+        step = lambda: P.mlp_block(X, W1t, W2t, R_batch=w["R_batch"], R_model=w["R_model"], out=Y, workspace=ws)
+        roles = {"mlp.up": 2.0 * T * D * F, "mlp.down": 2.0 * T * D * F}
+        return x, step, roles, "mfma_bf16"
+    if w.kind == "attn":
+        B, S, D, H = w["B"], w["S"], w["D"], w["H"]
+        T = B * S
+        X = x["X"].to_device()
+        Ws = [dev_t(x[k]) for k in ("Wq", "Wk", "Wv", "Wo")]
+        Y = torch.empty((T, D), dtype=torch.float32, device="cuda")
+        ws = torch.empty(P.attn_block_workspace(B, S, D, H, w["dh"], w["R_batch"], w["R_model"]),
+                         dtype=torch.uint8, device="cuda")
+        step = lambda: P.attn_block(X, *Ws, B=B, S=S, n_heads=H, d_head=w["dh"], R_batch=w["R_batch"],
+                                    R_model=w["R_model"], out=Y, workspace=ws)
+        roles = {"attn.qkv": 6.0 * T * D * D, "attn.out": 2.0 * T * D * D,
+                 "attn.core": W.attn_core_flops(B, S, H, w["dh"])}
+        return x, step, roles, "mfma_bf16"
+    if w.kind == "decoder":
+        B, S, D, H, F = w["B"], w["S"], w["D"], w["H"], w["F"]
+        T = B * S
+        x0 = x["x"].to_device()
+        xs = torch.empty_like(x0)
+        layers = [dict(g1=p["g1"].to_device(), g2=p["g2"].to_device(),
+                       W=[dev_t(p[k]) for k in ("Wq", "Wk", "Wv", "Wo", "W1", "W2")]) for p in x["layers"]]
+        ws = torch.empty(P.decoder_layer_workspace(B, S, D, H, w["dh"], F, w["R_batch"], w["R_model"]),
+                         dtype=torch.uint8, device="cuda")
+
+        def step():
+            xs.copy_(x0)   # the stack runs in place on the residual stream
+            for l in layers:
+                P.decoder_layer(xs, l["g1"], l["g2"], *l["W"], B=B, S=S, n_heads=H, d_head=w["dh"],
+                                R_batch=w["R_batch"], R_model=w["R_model"], workspace=ws)
+        L = w["L"]
+        roles = {"attn.qkv": L * 6.0 * T * D * D, "attn.out": L * 2.0 * T * D * D,
+                 "attn.core": L * W.attn_core_flops(B, S, H, w["dh"]),
+                 "mlp.up": L * 2.0 * T * D * F, "mlp.down": L * 2.0 * T * D * F}
+        roles = {k: v / L for k, v in roles.items()}   # per launch
+        return x, step, roles, "mfma_bf16"
+    raise ValueError(w.kind)
+
+
+# ---------------------------------------------------------------------------
+# CPU baseline: the oracle on a bounded sample of the same workload
+# ---------------------------------------------------------------------------
+def cpu_baseline(w, x, target_s):
+    import numpy as np
+    from oracle import partir_oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max(i.get("num_threads", 1) for i in threadpool_info()) or 1
+    except Exception:
+        cores = os.cpu_count() or 1
+    if w.kind == "matmul":
+        A, B = x["A"].f64(), x["B"].f64()
+        t0 = time.perf_counter()
+        reps = 0
+        while time.perf_counter() - t0 < min(target_s, 3.0) or reps == 0:
+            O.loop_matmul(A, B, w["tile"], w["sum"], w["R"])
+            reps += 1
+        dt = time.perf_counter() - t0
+        return dict(value=reps * 2.0 * w["M"] * w["N"] * w["K"] / dt / 1e12, unit="TFLOP/s", cores=cores,
+                    kind="oracle", sample=f"full output, {reps} evaluations, {dt:.2f} s")
+    if w.kind == "mlp":
+        X, W1, W2 = x["X"].f64(), x["W1"].f64(), x["W2"].f64()
+        per_row = 4.0 * w["D"] * w["F"]
+        n = 64
+        rng = np.random.default_rng(0)
+        total_rows, total_t = 0, 0.0
+        while True:
+            rows = np.sort(rng.choice(w["T"], size=min(n, w["T"]), replace=False))
+            t0 = time.perf_counter()
+            O.mlp_block(X, W1, W2, act="gelu", R_batch=w["R_batch"], R_model=w["R_model"], rows=rows)
+            dt = time.perf_counter() - t0
+            total_rows += len(rows)
+            total_t += dt
+            if total_t >= target_s or n >= w["T"]:
+                break
+            n = int(min(w["T"], max(2 * n, len(rows) * (target_s - total_t) / max(dt, 1e-3))))
+        return dict(value=total_rows * per_row / total_t / 1e12, unit="TFLOP/s", cores=cores, kind="oracle",
+                    sample=f"{total_rows} sampled output rows of the {w['T']}-row block "
+                           f"(all {w['R_model']} model shards each), {total_t:.1f} s")
+    if w.kind == "attn":
+        S, D = w["S"], w["D"]
+        Xf = x["X"].f64()
+        Ws = [x[k].f64() for k in ("Wq", "Wk", "Wv", "Wo")]
+        nq = 64
+        rows = [S - 1 - i for i in range(nq)]      # last positions of sequence 0: full key prefix
+        t0 = time.perf_counter()
+        O.attn_block(Xf, *Ws, w["B"], S, w["H"], w["dh"], True, None, w["R_batch"], w["R_model"], rows=rows)
+        dt = time.perf_counter() - t0
+        flops = 2.0 * S * D * D * 2 + nq * 2.0 * D * D * 2 + 4.0 * nq * S * D
+        return dict(value=flops / dt / 1e12, unit="TFLOP/s", cores=cores, kind="oracle",
+                    sample=f"{nq} output rows at the end of one {S}-token sequence (K/V of the whole "
+                           f"sequence), {dt:.1f} s")
+    if w.kind == "decoder":
+        S, D, F = w["S"], w["D"], w["F"]
+        layers = [{k: v.f64() for k, v in p.items()} for p in x["layers"]]
+        pos = 256
+        rows = [pos - 1 - i for i in range(16)]
+        t0 = time.perf_counter()
+        O.decoder(x["x"].f64(), layers, w["B"], S, w["H"], w["dh"], 1e-6, w["R_batch"], w["R_model"], rows=rows)
+        dt = time.perf_counter() - t0
+        per_tok = 8.0 * D * D + 4.0 * D * F
+        flops = pos * per_tok * (w["L"] - 1) + 2 * pos * 2.0 * D * D + len(rows) * per_tok
+        return dict(value=flops / dt / 1e12, unit="TFLOP/s", cores=cores, kind="oracle",
+                    sample=f"{len(rows)} rows of a {pos}-token prefix through {w['L']} layers, {dt:.1f} s")
+    raise ValueError(w.kind)
+
+
+def traffic_from_profile(workload, role):
+    """HBM bytes per launch of `role` from a committed rocprofv3 counter summary,
+    valid only while the kernel source is unchanged."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{role.replace('.', '_')}_{workload}.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    m = re.search(r"traffic_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    h = re.search(r"kernel_source_sha256:\s*([0-9a-f]+)", text)
+    if not m or not h or h.group(1) != kernel_source_hash():
+        return None
+    return float(m.group(1))
+
+
+def kernel_source_hash():
+    d = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2401_11202_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        if f.endswith((".hip", ".h", ".cpp")):
+            d.update(open(os.path.join(csrc, f), "rb").read())
+    return d.hexdigest()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on exactly one GPU; --gpus must be 1",
+                          "n_gpus": args.gpus}))
+        log("bench.py: only --gpus 1 is supported (a single MI355X evaluates every virtual shard)")
+        sys.exit(2)
+    import torch
+    from paper_2401_11202_amd import inputs as I
+    from paper_2401_11202_amd import partir as P
+    from paper_2401_11202_amd import workloads as W
+
+    if args.copy_calib:
+        n = args.copy_calib // 4
+        a = torch.ones(n, dtype=torch.float32, device="cuda")
+        b = torch.empty_like(a)
+        for _ in range(3):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        log(f"copied {n * 4} bytes x3")
+        return
+
+    w = W.WORKLOADS[args.workload]
+    log(f"bench: {w.name} {w.dims}")
+    x, step, roles, unit_kind = setup(w, P, I)
+    torch.cuda.synchronize()
+    log("bench: inputs resident, warming up")
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    P.trace_reset()
+    P.trace_enable(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    P.trace_enable(False)
+    trace = P.trace_read()
+    log(f"bench: {args.steps} steps in {elapsed * 1e3:.2f} ms; trace {trace}")
+
+    flops = W.flops(w)
+    value = flops * args.steps / elapsed / 1e12
+    peak = PEAK_F32_TFLOPS if unit_kind == "mfma_f32" else PEAK_BF16_TFLOPS
+    # dominant kernel: the role with the most GPU time
+    dom = max((k for k in trace if k in roles), key=lambda k: trace[k][1])
+    launches, total_ms = trace[dom]
+    avg_s = total_ms / launches / 1e3
+    achieved = roles[dom] / avg_s / 1e12
+    roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
+                "frac": round(achieved / peak, 4), "traffic": traffic_from_profile(w.name, dom),
+                "kernel": dom, "avg_launch_ms": round(avg_s * 1e3, 4),
+                "flops_per_launch": roles[dom]}
+    kernels = {k: {"launches": v[0], "avg_ms": round(v[1] / v[0], 4),
+                   "tflops": round(roles[k] / (v[1] / v[0] / 1e3) / 1e12, 1) if k in roles else None}
+               for k, v in trace.items()}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("bench: timing the CPU oracle on a sample")
+        cpu = cpu_baseline(w, x, args.cpu_seconds)
+
+    out = {"metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1,
+           "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(elapsed / args.steps * 1e3, 4),
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+           "dtype": "f32" if unit_kind == "mfma_f32" else "bf16",
+           "data": "synthetic (seeded Gaussian, weights scaled 1/sqrt(fan_in))",
+           "config": {"workload": w.name, **w.dims, "parallelism": "virtual shards on 1 GPU"},
+           "mfma_util_pct_of_peak": round(100.0 * value / peak, 2),
+           "roofline": roofline, "kernels": kernels, "cpu_baseline": cpu}
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

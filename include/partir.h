@@ -1,0 +1,277 @@
+/*
+ * partir.h -- C ABI of libpartir: executing PartIR:Core loops on one MI355X.
+ *
+ * PartIR:Core (arXiv 2401.11202, Sec. 5) expresses a partitioned tensor
+ * program with a pure loop over a mesh axis of size R whose action is either
+ *   #tile<d>  -- the iteration results are concatenated along dim d, or
+ *   #sum      -- the iteration results are summed,
+ * and with `slice d x[r]`, the r-th of R equal contiguous chunks of x along
+ * dim d (semantics: App. C, figure "Interpretation of PartIR:Core"; typing
+ * rules TTile / TSum / TSlice in the figure "abstract syntax and typing
+ * rules").  Every entry point below evaluates all R virtual shards of such a
+ * loop nest on the calling GPU:
+ *   - a slice is a zero-copy view (base pointer + offset, same leading dim);
+ *   - a #tile result is written by each shard straight into its slice of the
+ *     output (the all_gather of the SPMD lowering, Sec. 6.1, becomes an
+ *     offset store);
+ *   - a #sum is reduced on the device, in shard order r = 0..R-1, either in
+ *     the MFMA accumulators of one output tile or through fp32 partials (the
+ *     all_reduce of the lowering becomes an in-device reduction).
+ *
+ * Conventions shared by all entry points
+ * --------------------------------------
+ * Layout.  Every matrix is row-major with an explicit leading dimension
+ *   (elements between consecutive rows).  Weight matrices of the blocks are
+ *   passed "output-major": a logical weight W of shape [fan_in, fan_out] is
+ *   stored as its transpose W^T, a row-major [fan_out, fan_in] array (the
+ *   nn.Linear layout), so that every MFMA operand is a contiguous run along
+ *   the contraction dim.  `slice 1 W[m]` is then a block of rows of W^T and
+ *   `slice 0 W[m]` a block of its columns; both are views.
+ * Memory.  All tensor pointers are device pointers owned by the caller, which
+ *   also allocates the workspace (size from the matching *_workspace query;
+ *   may be NULL when the query returns 0).  The library allocates no device
+ *   memory in these calls and keeps no pointer after a call returns.
+ * Alignment.  Base pointers and every row must be 16-byte aligned (leading
+ *   dims multiple of 8 for bf16, of 4 for f32), and so must every shard view
+ *   (the sliced extent times the element size is a multiple of 16 bytes).
+ * Execution.  Work is enqueued on `stream` (a hipStream_t; NULL = the
+ *   default stream) and the call returns without waiting.  Results of a
+ *   #sum are deterministic: the same inputs give the same bits on every run.
+ * Errors.  Argument errors are detected before anything is enqueued; the
+ *   call then returns the status and leaves every output untouched.  A failed
+ *   launch returns PARTIR_E_HIP.  Faults during execution surface at the
+ *   caller's next synchronisation.  partir_last_error() gives a thread-local
+ *   message for the last failing call on this thread.  No C++ exception
+ *   crosses this interface; the library's only mutable global state is that
+ *   message, the trace buffer and a per-device property cache.
+ */
+#ifndef PARTIR_H
+#define PARTIR_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum partir_status {
+  PARTIR_OK = 0,
+  PARTIR_E_NULL = 1,         /* a required pointer is NULL                       */
+  PARTIR_E_SHAPE = 2,        /* a size is <= 0 / too large, or sizes disagree    */
+  PARTIR_E_DIVISIBILITY = 3, /* R does not divide the sliced dim (rule TSlice)   */
+  PARTIR_E_AXIS = 4,         /* invalid axis, or one axis both tiled and summed  */
+  PARTIR_E_DTYPE = 5,        /* unsupported dtype combination                    */
+  PARTIR_E_LAYOUT = 6,       /* leading dim < cols, or 16-byte misalignment      */
+  PARTIR_E_WORKSPACE = 7,    /* workspace smaller than the query returns         */
+  PARTIR_E_HIP = 8,          /* a HIP runtime call or kernel launch failed       */
+  PARTIR_E_UNSUPPORTED = 9   /* R < 1, or an option this build does not provide  */
+} partir_status;
+
+typedef enum partir_dtype { PARTIR_F32 = 0, PARTIR_BF16 = 1 } partir_dtype;
+
+/* Loop axes of a single matmul C[M,N] = A[M,K] B[K,N]. */
+typedef enum partir_axis {
+  PARTIR_AXIS_NONE = -1,
+  PARTIR_AXIS_M = 0,   /* #tile<0>: slice 0 A[r], result rows concatenated    */
+  PARTIR_AXIS_N = 1,   /* #tile<1>: slice 1 B[r], result columns concatenated */
+  PARTIR_AXIS_K = 2    /* #sum: slice 1 A[r] and slice 0 B[r], results summed */
+} partir_axis;
+
+/* How B is stored for partir_loop_matmul. */
+typedef enum partir_b_layout {
+  PARTIR_B_KN = 0,     /* B as a row-major [K, N] array (leading dim ldb >= N)          */
+  PARTIR_B_NK = 1      /* B given by its transpose, row-major [N, K] (ldb >= K)         */
+} partir_b_layout;
+
+/* Realisation of a #sum loop on the device. */
+typedef enum partir_sum_impl {
+  PARTIR_SUM_AUTO = 0,   /* chosen by the planner from the output tile count              */
+  PARTIR_SUM_FUSED = 1,  /* shard K-ranges accumulate, r ascending, in one MFMA accumulator */
+  PARTIR_SUM_SPLITK = 2  /* each shard writes an fp32 partial; an ordered reduce sums them  */
+} partir_sum_impl;
+
+typedef enum partir_act { PARTIR_ACT_NONE = 0, PARTIR_ACT_GELU_ERF = 1 } partir_act;
+
+/* ------------------------------------------------------------------------ */
+/* Single partitioned matmul: the three tile-mapping entries of matmul       */
+/* (Sec. 5.2.1, figure matmul-examples).                                      */
+/* ------------------------------------------------------------------------ */
+/*
+ * C[M,N] = A[M,K] @ B[K,N], written as a loop over R virtual shards:
+ *   tile_axis = M  : loop [#tile<0>] { matmul(slice 0 A[r], B) }
+ *   tile_axis = N  : loop [#tile<1>] { matmul(A, slice 1 B[r]) }
+ *   sum_axis  = K  : loop [#sum]     { matmul(slice 1 A[r], slice 0 B[r]) }
+ * With both set, the tile loop is outside and the sum loop inside, over two
+ * distinct axes of size R each (nesting one axis twice is forbidden,
+ * Sec. 5.2.3).  R = 1 is the unpartitioned product.
+ *
+ * A: [M, K] row-major, leading dim lda >= K.   B: per b_layout, leading dim ldb.
+ * C: [M, N] row-major, leading dim ldc >= N, overwritten.
+ * ab_dtype: PARTIR_F32 or PARTIR_BF16 (A and B alike); c_dtype: PARTIR_F32,
+ * or PARTIR_BF16 when ab_dtype is bf16.  Accumulation is fp32.
+ * b_layout: partir_b_layout.  sum_impl: partir_sum_impl (ignored without a
+ * #sum).  ws / ws_bytes: workspace of at least partir_loop_matmul_workspace().
+ * Errors: E_NULL (A, B or C NULL, or ws NULL with ws_bytes short), E_SHAPE,
+ * E_DIVISIBILITY (R does not divide the tiled or summed dim), E_AXIS,
+ * E_DTYPE, E_LAYOUT, E_WORKSPACE, E_UNSUPPORTED (R < 1), E_HIP.
+ */
+int partir_loop_matmul(const void* A, const void* B, void* C,
+                       int64_t M, int64_t N, int64_t K,
+                       int64_t lda, int64_t ldb, int64_t ldc,
+                       int ab_dtype, int c_dtype, int b_layout,
+                       int tile_axis, int sum_axis, int R, int sum_impl,
+                       void* ws, size_t ws_bytes, void* stream);
+
+/* Workspace bytes partir_loop_matmul needs for these arguments (0 if none);
+ * returns (size_t)-1 if the arguments are invalid. */
+size_t partir_loop_matmul_workspace(int64_t M, int64_t N, int64_t K,
+                                    int ab_dtype, int c_dtype, int b_layout,
+                                    int tile_axis, int sum_axis, int R, int sum_impl);
+
+/* ------------------------------------------------------------------------ */
+/* Megatron MLP block nested in a batch #tile (Sec. 5.2.2 final listing,      */
+/* Sec. 2.3 on model parallelism).                                            */
+/* ------------------------------------------------------------------------ */
+/*
+ * Y = loop b [#tile<0>](R_batch) {
+ *       loop m [#sum](R_model) {
+ *         act(slice 0 X[b] @ slice 1 W1[m] + slice 0 b1[m]) @ slice 0 W2[m] }
+ *       + b2 }
+ * X: [T, D] bf16 row-major (ld = D).  W1t: W1^T, [F, D] bf16.  W2t: W2^T,
+ * [D, F] bf16.  b1: [F] f32 or NULL (tiled with W1's columns).  b2: [D] f32
+ * or NULL, added once after the #sum.  Y: [T, D], out_dtype F32 or BF16.
+ * act: partir_act applied to the first product.  The intermediate
+ * H = act(X W1 + b1) ([T, F], stored bf16) lives in the workspace; each model
+ * shard m writes its columns [m F/R_model, (m+1) F/R_model) and the second
+ * product sums the shards' K-ranges in order.
+ * Errors: E_NULL, E_SHAPE, E_DIVISIBILITY (R_batch does not divide T or
+ * R_model does not divide F), E_DTYPE (in_dtype other than BF16), E_LAYOUT,
+ * E_WORKSPACE, E_UNSUPPORTED (R < 1), E_HIP.
+ */
+int partir_mlp_block(const void* X, const void* W1t, const void* b1,
+                     const void* W2t, const void* b2, void* Y,
+                     int64_t T, int64_t D, int64_t F,
+                     int in_dtype, int out_dtype, int act,
+                     int R_batch, int R_model,
+                     void* ws, size_t ws_bytes, void* stream);
+
+size_t partir_mlp_block_workspace(int64_t T, int64_t D, int64_t F, int out_dtype,
+                                  int R_batch, int R_model);
+
+/* ------------------------------------------------------------------------ */
+/* Attention block: heads #tile inside a Megatron #sum, in a batch #tile.     */
+/* ------------------------------------------------------------------------ */
+/*
+ * Y = loop b [#tile<0>](R_batch) {
+ *       loop m [#sum](R_model) {
+ *         (loop h [#tile<1>](n_heads/R_model) {
+ *             attn(Q_h, K_h, V_h) }) @ slice 0 Wo[m] } }
+ * with Q = slice 0 X[b] @ slice 1 Wq[m] (K, V likewise) and, per sequence
+ * and head, attn = softmax(scale * Q K^T, keys j <= query i when causal) V.
+ * X: [B*S, D] bf16, sequence-major (token t = s*S + position).  Wq_t, Wk_t,
+ * Wv_t, Wo_t: transposed [D, D] bf16 weights; head h owns columns
+ * [h*d_head, (h+1)*d_head) of Q, K and V.  Batch shards hold whole sequences.
+ * scale <= 0 selects 1/sqrt(d_head).  Y: [B*S, D], out_dtype F32 or BF16.
+ * The workspace holds Q, K, V and the attention output (bf16, [B*S, D] each).
+ * Constraints: d_head == 128, S a multiple of 64.
+ * Errors: E_NULL, E_SHAPE (n_heads*d_head != D, or d_head / S outside the
+ * constraints), E_DIVISIBILITY (R_batch does not divide B or R_model does not
+ * divide n_heads), E_DTYPE, E_LAYOUT, E_WORKSPACE, E_UNSUPPORTED, E_HIP.
+ */
+int partir_attn_block(const void* X, const void* Wq_t, const void* Wk_t,
+                      const void* Wv_t, const void* Wo_t, void* Y,
+                      int64_t B, int64_t S, int64_t D, int64_t n_heads, int64_t d_head,
+                      int causal, float scale, int in_dtype, int out_dtype,
+                      int R_batch, int R_model,
+                      void* ws, size_t ws_bytes, void* stream);
+
+size_t partir_attn_block_workspace(int64_t B, int64_t S, int64_t D, int64_t n_heads,
+                                   int64_t d_head, int R_batch, int R_model);
+
+/* ------------------------------------------------------------------------ */
+/* Pre-norm decoder layer on an fp32 residual stream, in place.               */
+/* ------------------------------------------------------------------------ */
+/*
+ * x = loop b [#tile<0>](R_batch) { xb = slice 0 x[b];
+ *       h  = xb + loop m [#sum](R_model) { attn_m(rmsnorm(xb, g1)) @ slice 0 Wo[m] };
+ *       h  + loop m [#sum](R_model) { gelu(rmsnorm(h, g2) @ slice 1 W1[m]) @ slice 0 W2[m] } }
+ * rmsnorm(x, g) = g * x / sqrt(mean(x^2) + eps) over the D features of a row;
+ * attention is causal with scale 1/sqrt(d_head).
+ * x: [B*S, D] f32, updated in place.  g1, g2: [D] f32.  Wq_t..Wo_t as in
+ * partir_attn_block; W1t: [F, D] bf16; W2t: [D, F] bf16.
+ * Workspace: normalised activations, Q, K, V, attention output and the
+ * [B*S, F] FFN intermediate, all bf16.
+ * Errors: as partir_attn_block, plus E_DIVISIBILITY when R_model does not
+ * divide F.
+ */
+int partir_decoder_layer(void* x, const void* g1, const void* g2, float eps,
+                         const void* Wq_t, const void* Wk_t, const void* Wv_t,
+                         const void* Wo_t, const void* W1t, const void* W2t,
+                         int64_t B, int64_t S, int64_t D, int64_t n_heads,
+                         int64_t d_head, int64_t F, int R_batch, int R_model,
+                         void* ws, size_t ws_bytes, void* stream);
+
+size_t partir_decoder_layer_workspace(int64_t B, int64_t S, int64_t D, int64_t n_heads,
+                                      int64_t d_head, int64_t F, int R_batch, int R_model);
+
+/* ------------------------------------------------------------------------ */
+/* Plans: what a call will do, without doing it (host only, no GPU needed).  */
+/* ------------------------------------------------------------------------ */
+typedef struct partir_plan_info {
+  int n_virtual_shards;     /* product of the loop sizes of the nest               */
+  int n_tile_loops;         /* #tile loops in the nest (incl. the heads loop)       */
+  int n_sum_loops;          /* #sum loops: the in-device stand-ins for all_reduce   */
+  int n_sum_splitk;         /* of those, realised through fp32 partials in HBM      */
+  int n_launches;           /* kernel launches the call enqueues                    */
+  int reserved;
+  size_t workspace_bytes;   /* what the matching *_workspace query returns          */
+  double flops;             /* algorithmic FLOPs (causal attention: unmasked pairs)  */
+} partir_plan_info;
+
+/* Fill *info for the call with these arguments; returns a partir_status. */
+int partir_plan_loop_matmul(int64_t M, int64_t N, int64_t K, int ab_dtype, int c_dtype,
+                            int b_layout, int tile_axis, int sum_axis, int R, int sum_impl,
+                            partir_plan_info* info);
+int partir_plan_mlp_block(int64_t T, int64_t D, int64_t F, int out_dtype,
+                          int R_batch, int R_model, partir_plan_info* info);
+int partir_plan_attn_block(int64_t B, int64_t S, int64_t D, int64_t n_heads, int64_t d_head,
+                           int R_batch, int R_model, partir_plan_info* info);
+int partir_plan_decoder_layer(int64_t B, int64_t S, int64_t D, int64_t n_heads,
+                              int64_t d_head, int64_t F, int R_batch, int R_model,
+                              partir_plan_info* info);
+
+/* Human-readable shard table of the last plan built on this thread
+ * (views, offsets, tile grid and #sum realisation per launch).  The string is
+ * owned by the library and valid until the next call on this thread. */
+const char* partir_last_plan_text(void);
+
+/* ------------------------------------------------------------------------ */
+/* Kernel trace: per-kernel GPU time measured with HIP events.                */
+/* ------------------------------------------------------------------------ */
+typedef struct partir_trace_entry {
+  char name[48];            /* kernel family name                               */
+  int64_t launches;         /* launches recorded since the last reset           */
+  double total_ms;          /* summed GPU time between the events bracketing it */
+} partir_trace_entry;
+
+/* While enabled, every launch is bracketed by two events on its stream.
+ * Enabling creates events (a host-side resource), so it is meant for
+ * measurement runs, not for callers that must not allocate. */
+int partir_trace_enable(int on);
+/* Synchronises the recorded events and folds them into per-name totals;
+ * writes up to max entries and returns how many kernel names exist (or a
+ * negative status). */
+int partir_trace_read(partir_trace_entry* out, int max);
+void partir_trace_reset(void);
+
+/* ------------------------------------------------------------------------ */
+const char* partir_status_string(int status);
+const char* partir_last_error(void);
+const char* partir_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PARTIR_H */

@@ -1,0 +1,196 @@
+// Softmax attention forward for gfx950, d_head = 128, bf16 in / bf16 out.
+//
+// One workgroup = one (sequence, head, 128-query block); four waves own 32
+// queries each.  Keys and values stream through a double-buffered LDS stage
+// 64 keys at a time.  Per key block each wave computes
+//     S^T[64 keys x 32 queries] = K_blk . Q^T       (v_mfma_f32_32x32x16_bf16)
+// so that every lane owns one query column: the running max and sum of the
+// online softmax are per-lane registers, and exp(S^T - max) converted to bf16
+// is directly the B operand of
+//     O^T[128 d x 32 queries] += V_blk^T . P^T
+// The V^T operand is read from the row-major V tile with ds_read_b64_tr_b16;
+// the key order inside each 16-key MFMA step is permuted identically on the P
+// and V sides (any order is exact for the contraction).
+// With causal masking a query sees keys at positions <= its own.
+#include "kernels.h"
+
+namespace partir {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef short i16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int DH = 128, BQ = 128, BKV = 64, NT = 256;
+constexpr int KP = 256;                 // K tile row pitch (bytes), chunk-swizzled
+constexpr int VP = 288;                 // V tile row pitch (bytes), padded
+constexpr int KT_BYTES = BKV * KP;
+constexpr int VT_BYTES = BKV * VP;
+constexpr int STAGE = KT_BYTES + VT_BYTES;
+
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+
+__global__ __launch_bounds__(NT, 2)
+void attention_kernel(AttnParams p) {
+  __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
+
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int h = lane >> 5, col = lane & 31;
+
+  // heaviest (latest) query blocks first: causal work grows with the block index
+  const int nqb = p.S / BQ;
+  const int nbh = p.B * p.H;
+  const int qb = nqb - 1 - (int)(blockIdx.x / nbh);
+  const int bh = blockIdx.x % nbh;
+  const int b = bh / p.H, head = bh - b * p.H;
+  const int q0 = qb * BQ;
+  const int64_t tok0 = (int64_t)b * p.S;
+
+  // ---- this lane's query fragments (B operand of S^T = K Q^T), kept in VGPRs
+  const int qi = q0 + 32 * w + col;      // query position of this lane's column
+  bf16x8 qf[8];
+  {
+    const uint16_t* qrow = p.Q + (tok0 + qi) * p.ldq + head * DH + 8 * h;
+#pragma unroll
+    for (int ds = 0; ds < 8; ++ds) qf[ds] = *(const bf16x8*)(qrow + 16 * ds);
+  }
+
+  // ---- K / V tile loads: 64 rows x 256 B each, 4 + 4 chunks of 16 B per thread
+  const int lr = tid >> 4, lc = tid & 15;
+  const uint16_t* kbase = p.K + tok0 * p.ldk + head * DH + lc * 8;
+  const uint16_t* vbase = p.V + tok0 * p.ldv + head * DH + lc * 8;
+  i32x4 rk[4], rv[4];
+  auto gload = [&](int kb) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int64_t key = (int64_t)kb * BKV + lr + 16 * i;
+      rk[i] = *(const i32x4*)(kbase + key * p.ldk);
+      rv[i] = *(const i32x4*)(vbase + key * p.ldv);
+    }
+  };
+  auto lstore = [&](int buf) {
+    char* ks = smem + buf * STAGE;
+    char* vs = ks + KT_BYTES;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = lr + 16 * i;
+      *(i32x4*)(ks + r * KP + ((lc ^ (r & 15)) << 4)) = rk[i];
+      *(i32x4*)(vs + r * VP + (lc << 4)) = rv[i];
+    }
+  };
+
+  f32x16 oacc[4];
+#pragma unroll
+  for (int d = 0; d < 4; ++d)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) oacc[d][v] = 0.0f;
+  float m_run = -1e30f, l_run = 0.0f;
+
+  // ds_read_b64_tr_b16 addressing for the V^T operand (see header comment)
+  const int j16 = lane & 15, G = lane >> 4, hh = G >> 1;
+  const int v_row = 4 * hh + (j16 >> 2);
+  const int v_colb = 2 * (16 * (G & 1) + 4 * (j16 & 3));
+
+  const int nkb = p.causal ? (q0 + BQ + BKV - 1) / BKV : p.S / BKV;
+  const int wave_last_q = q0 + 32 * w + 31;
+
+  gload(0);
+  lstore(0);
+  __syncthreads();
+  for (int kb = 0; kb < nkb; ++kb) {
+    const int cur = kb & 1;
+    if (kb + 1 < nkb) gload(kb + 1);
+    const int k0 = kb * BKV;
+    if (!p.causal || k0 <= wave_last_q) {
+      const char* ks = smem + cur * STAGE;
+      const char* vs = ks + KT_BYTES;
+      // S^T = K Q^T for two 32-key sub-tiles
+      f32x16 sacc[2];
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+#pragma unroll
+        for (int v = 0; v < 16; ++v) sacc[t][v] = 0.0f;
+        const int r = 32 * t + col;
+#pragma unroll
+        for (int ds = 0; ds < 8; ++ds) {
+          const bf16x8 kf = *(const bf16x8*)(ks + r * KP + (((2 * ds + h) ^ (r & 15)) << 4));
+          sacc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ds], sacc[t], 0, 0, 0);
+        }
+      }
+      // scale (log2 domain), causal mask, block max
+      float mloc = -1e30f;
+      const bool need_mask = p.causal && (k0 + BKV - 1 > q0 + 32 * w);
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          float s = sacc[t][v] * p.scale_log2;
+          if (need_mask) {
+            const int key = k0 + 32 * t + 8 * (v >> 2) + 4 * h + (v & 3);
+            if (key > qi) s = -__builtin_inff();
+          }
+          sacc[t][v] = s;
+          mloc = fmaxf(mloc, s);
+        }
+      // the partner lane (lane ^ 32) holds the other keys of this query
+      mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
+      const float m_new = fmaxf(m_run, mloc);
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      m_run = m_new;
+      float lsum = 0.0f;
+      bf16x8 pf[4];
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const float e = __builtin_amdgcn_exp2f(sacc[t][v] - m_new);
+          lsum += e;
+          pf[2 * t + (v >> 3)][v & 7] = (__bf16)e;
+        }
+      l_run = l_run * alpha + lsum;
+#pragma unroll
+      for (int d = 0; d < 4; ++d) oacc[d] *= alpha;
+      // O^T += V^T P^T, 4 steps of 16 keys
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+#pragma unroll
+        for (int d = 0; d < 4; ++d) {
+          const char* base = vs + (16 * u + v_row) * VP + 64 * d + v_colb;
+          const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(base));
+          const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(base + 8 * VP));
+          // whole-vector reinterpretation (per-element casts were lowered to
+          // reads of the first dword only)
+          const bf16x8 vf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+          oacc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[u], oacc[d], 0, 0, 0);
+        }
+      }
+    }
+    if (kb + 1 < nkb) lstore(cur ^ 1);
+    __syncthreads();
+  }
+
+  // ---- normalise and store O[query][head*128 + d] ------------------------------
+  const float inv = 1.0f / (l_run + __shfl_xor(l_run, 32));
+  uint16_t* orow = p.O + (tok0 + qi) * p.ldo + head * DH;
+#pragma unroll
+  for (int d = 0; d < 4; ++d)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      bf16x4 o = {(__bf16)(oacc[d][4 * g + 0] * inv), (__bf16)(oacc[d][4 * g + 1] * inv),
+                  (__bf16)(oacc[d][4 * g + 2] * inv), (__bf16)(oacc[d][4 * g + 3] * inv)};
+      *(bf16x4*)(orow + 32 * d + 8 * g + 4 * h) = o;
+    }
+}
+
+}  // namespace
+
+hipError_t launch_attention(const AttnParams& p, hipStream_t s) {
+  const unsigned nwg = (unsigned)(p.S / BQ) * p.B * p.H;
+  hipLaunchKernelGGL(attention_kernel, dim3(nwg), dim3(NT), 0, s, p);
+  return hipGetLastError();
+}
+
+}  // namespace partir

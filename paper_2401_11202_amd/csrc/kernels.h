@@ -1,0 +1,106 @@
+// Internal launch interface between the host planner (partir_api.cpp) and the
+// HIP kernels.  Plain structs passed by value as kernel arguments.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace partir {
+
+// Epilogue of a GEMM output tile.
+enum GemmEpi : int {
+  EPI_BF16 = 0,      // C (bf16) = act(acc + bias)
+  EPI_F32 = 1,       // C (f32)  = act(acc + bias)
+  EPI_PARTIAL = 2,   // partial[split] (f32) = acc        (split-K #sum)
+  EPI_RESID_F32 = 3  // C (f32)  = resid + act(acc + bias) (resid may alias C)
+};
+
+// C = A . B^T over a grid of virtual shards.
+//   A : [M, K] bf16 row-major, leading dim lda.
+//   B : per group g, B_g^T stored [N, K] bf16 row-major (leading dim ldb).
+//   C : per group g, [M, N] row-major (leading dim ldc).
+// Shards: rm #tile shards along M (extent ms each), rn along N (extent ns),
+// rk #sum shards along K (extent ks).  Output tiles never straddle a shard:
+// tpm / tpn tiles per shard (the last one may be partial).
+struct GemmParams {
+  const uint16_t* A;
+  const uint16_t* B[3];
+  void* C[3];
+  const float* bias[3];
+  const float* resid;
+  float* partial;
+  int64_t lda, ldb, ldc, ldr, part_ld, part_stride;
+  int M, N, K, ngroups;
+  int rm, ms, tpm;
+  int rn, ns, tpn;
+  int rk, ks;
+  int tiles_m, tiles_n;
+  int nsplit;      // 1: the rk shards accumulate in order in one accumulator
+  int group_m;     // tile-order grouping for L2 reuse
+  int act;         // 0 none, 1 gelu-erf
+  int epi;         // GemmEpi
+};
+
+hipError_t launch_gemm_bf16(const GemmParams& p, hipStream_t s);
+int gemm_bf16_tile_m();
+int gemm_bf16_tile_n();
+
+// fp32 GEMM: C = A . B with B [K, N] (b_nk = 0) or B^T [N, K] (b_nk = 1).
+struct GemmF32Params {
+  const float* A;
+  const float* B;
+  float* C;          // EPI_F32 output, or partial buffer base for EPI_PARTIAL
+  int64_t lda, ldb, ldc, part_stride;
+  int M, N, K;
+  int b_nk;
+  int rm, ms, tpm;
+  int rn, ns, tpn;
+  int rk, ks;
+  int tiles_m, tiles_n;
+  int nsplit;
+  int epi;           // EPI_F32 or EPI_PARTIAL
+};
+hipError_t launch_gemm_f32(const GemmF32Params& p, hipStream_t s);
+int gemm_f32_tile();
+
+// Ordered split-K reduction: out = epilogue(sum_{r=0..R-1} partial[r]).
+struct ReduceParams {
+  const float* partial;
+  int64_t part_ld, part_stride;
+  int R, M, N;
+  void* C;
+  int64_t ldc;
+  const float* bias;
+  const float* resid;
+  int64_t ldr;
+  int act;
+  int out_bf16;
+  int resid_add;
+};
+hipError_t launch_splitk_reduce(const ReduceParams& p, hipStream_t s);
+
+// Causal (or full) softmax attention, one head of d_head = 128 per block row.
+//   Q, K, V, O: [B*S, ld] bf16 row-major; head h uses columns [h*128, h*128+128).
+struct AttnParams {
+  const uint16_t* Q;
+  const uint16_t* K;
+  const uint16_t* V;
+  uint16_t* O;
+  int64_t ldq, ldk, ldv, ldo;
+  int B, S, H;       // sequences, length, heads (over all shards)
+  int causal;
+  float scale_log2;  // scale * log2(e)
+};
+hipError_t launch_attention(const AttnParams& p, hipStream_t s);
+
+// y (bf16) = g * x / sqrt(mean(x^2) + eps), one row of D fp32 per wave.
+struct RmsParams {
+  const float* x;
+  const float* g;
+  uint16_t* y;
+  int64_t ldx, ldy;
+  int rows, D;
+  float eps;
+};
+hipError_t launch_rmsnorm(const RmsParams& p, hipStream_t s);
+
+}  // namespace partir

@@ -1,0 +1,838 @@
+// libpartir host side: argument validation, the loop-nest planner and launch.
+//
+// Every entry point follows the same three steps:
+//  1. validate the call against PartIR:Core's typing rules (TSlice needs the
+//     axis size to divide the sliced dim exactly; TTile / TSum fix the result
+//     shapes; one axis may not be nested in itself, Sec. 5.2.3) and against
+//     the layout contract of the kernels, returning a status before anything
+//     is enqueued;
+//  2. plan: enumerate the virtual shards of the nest and turn them into a
+//     short list of kernel launches whose grids span all shards at once
+//     (slices become base offsets, #tile results offset stores, #sum either a
+//     fused accumulator or fp32 partials plus an ordered reduction);
+//  3. enqueue the launches on the caller's stream.
+// The plan-query entry points run steps 1-2 only and need no GPU.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "../../include/partir.h"
+#include "kernels.h"
+
+namespace partir {
+namespace {
+
+constexpr int kNumCU = 256;           // MI355X compute units: a grid below this underfills
+constexpr int kGroupM = 8;            // tile-order grouping for L2 reuse
+constexpr size_t kWsAlign = 256;
+
+thread_local std::string g_error;
+thread_local std::string g_plan_text;
+
+int fail(int status, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_error = std::string(partir_status_string(status)) + ": " + buf;
+  return status;
+}
+
+size_t align_up(size_t x) { return (x + kWsAlign - 1) / kWsAlign * kWsAlign; }
+int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
+int elem_bytes(int dt) { return dt == PARTIR_BF16 ? 2 : 4; }
+bool valid_dtype(int dt) { return dt == PARTIR_F32 || dt == PARTIR_BF16; }
+
+// ---------------------------------------------------------------------------
+// Plans
+// ---------------------------------------------------------------------------
+enum LaunchKind { L_GEMM_BF16, L_GEMM_F32, L_REDUCE, L_ATTN, L_RMS };
+
+struct Launch {
+  LaunchKind kind;
+  std::string name;
+  std::string text;
+  GemmParams gemm{};
+  GemmF32Params gemm32{};
+  ReduceParams reduce{};
+  AttnParams attn{};
+  RmsParams rms{};
+};
+
+struct Plan {
+  std::vector<Launch> launches;
+  int n_shards = 1;
+  int n_tile_loops = 0;
+  int n_sum_loops = 0;
+  int n_sum_splitk = 0;
+  size_t ws_bytes = 0;
+  double flops = 0;
+};
+
+// ---------------------------------------------------------------------------
+// Tracing
+// ---------------------------------------------------------------------------
+struct TraceRec {
+  std::string name;
+  hipEvent_t start, stop;
+};
+std::mutex g_trace_mu;
+bool g_trace_on = false;
+std::vector<TraceRec> g_trace_pending;
+std::map<std::string, std::pair<int64_t, double>> g_trace_totals;
+
+// ---------------------------------------------------------------------------
+// GEMM planning
+// ---------------------------------------------------------------------------
+struct GemmSpec {
+  // operands (NULL while only planning)
+  const void* A = nullptr;
+  const void* B[3] = {nullptr, nullptr, nullptr};
+  void* C[3] = {nullptr, nullptr, nullptr};
+  const float* bias[3] = {nullptr, nullptr, nullptr};
+  const float* resid = nullptr;
+  int64_t lda = 0, ldb = 0, ldc = 0, ldr = 0;
+  int64_t M = 0, N = 0, K = 0;
+  int ngroups = 1;
+  int ab_dtype = PARTIR_BF16, c_dtype = PARTIR_BF16;
+  int b_nk = 1;
+  int rm = 1, rn = 1, rk = 1;   // #tile shards on M, N; #sum shards on K
+  int act = 0;
+  bool resid_add = false;
+  int sum_impl = PARTIR_SUM_AUTO;
+  const char* name = "gemm";    // role, used as the trace name
+  const char* label = "gemm";   // loop nest, for the plan text
+};
+
+int64_t gemm_tiles(const GemmSpec& g) {
+  const int64_t tile = g.ab_dtype == PARTIR_BF16 ? gemm_bf16_tile_m() : gemm_f32_tile();
+  return g.rm * cdiv(g.M / g.rm, tile) * g.ngroups * g.rn * cdiv(g.N / g.rn, tile);
+}
+
+bool gemm_uses_splitk(const GemmSpec& g) {
+  if (g.rk <= 1) return false;
+  if (g.sum_impl == PARTIR_SUM_SPLITK) return true;
+  if (g.sum_impl == PARTIR_SUM_FUSED) return false;
+  return gemm_tiles(g) < kNumCU;   // too few output tiles: spread the K shards too
+}
+
+size_t gemm_ws_bytes(const GemmSpec& g) {
+  return gemm_uses_splitk(g) ? align_up((size_t)g.rk * g.M * g.N * sizeof(float)) : 0;
+}
+
+std::string describe_gemm(const GemmSpec& g, int64_t grid, bool split) {
+  char buf[512];
+  snprintf(buf, sizeof buf,
+           "%s: C[%lld,%lld]%s = A[%lld,%lld] . B[%lld,%lld]; #tile M x%d (rows %lld/shard), "
+           "#tile N x%d (cols %lld/shard)%s; #sum K x%d (%lld/shard) %s; grid %lld WGs",
+           g.label, (long long)g.M, (long long)(g.N * g.ngroups), g.ngroups > 1 ? " (groups)" : "",
+           (long long)g.M, (long long)g.K, (long long)g.K, (long long)(g.N * g.ngroups), g.rm,
+           (long long)(g.M / g.rm), g.rn, (long long)(g.N / g.rn),
+           g.ngroups > 1 ? " per group" : "", g.rk, (long long)(g.K / g.rk),
+           g.rk <= 1 ? "(none)" : (split ? "split-K fp32 partials + ordered reduce" : "fused in accumulator, r ascending"),
+           (long long)grid);
+  return buf;
+}
+
+// Appends the launches of one GEMM to the plan.  `ws` points at this GEMM's
+// partial-buffer region (used only for split-K).
+void plan_gemm(const GemmSpec& g, void* ws, Plan& plan) {
+  const bool split = gemm_uses_splitk(g);
+  if (g.rk > 1) {
+    plan.n_sum_loops += 1;
+    if (split) plan.n_sum_splitk += 1;
+  }
+  const int epi_store = g.resid_add ? EPI_RESID_F32 : (g.c_dtype == PARTIR_BF16 ? EPI_BF16 : EPI_F32);
+  Launch L;
+  if (g.ab_dtype == PARTIR_BF16) {
+    const int tile = gemm_bf16_tile_m();
+    GemmParams& p = L.gemm;
+    p.A = (const uint16_t*)g.A;
+    for (int i = 0; i < 3; ++i) {
+      p.B[i] = (const uint16_t*)g.B[i];
+      p.C[i] = g.C[i];
+      p.bias[i] = split ? nullptr : g.bias[i];
+    }
+    p.resid = g.resid;
+    p.partial = (float*)ws;
+    p.lda = g.lda; p.ldb = g.ldb; p.ldc = g.ldc; p.ldr = g.ldr;
+    p.part_ld = g.N; p.part_stride = g.M * g.N;
+    p.M = (int)g.M; p.N = (int)g.N; p.K = (int)g.K; p.ngroups = g.ngroups;
+    p.rm = g.rm; p.ms = (int)(g.M / g.rm); p.tpm = (int)cdiv(p.ms, tile);
+    p.rn = g.rn; p.ns = (int)(g.N / g.rn); p.tpn = (int)cdiv(p.ns, tile);
+    p.rk = g.rk; p.ks = (int)(g.K / g.rk);
+    p.tiles_m = p.rm * p.tpm;
+    p.tiles_n = g.ngroups * p.rn * p.tpn;
+    p.nsplit = split ? g.rk : 1;
+    p.group_m = kGroupM;
+    p.act = split ? 0 : g.act;
+    p.epi = split ? EPI_PARTIAL : epi_store;
+    L.kind = L_GEMM_BF16;
+    L.name = g.name;
+    L.text = describe_gemm(g, (int64_t)p.tiles_m * p.tiles_n * p.nsplit, split);
+  } else {
+    const int tile = gemm_f32_tile();
+    GemmF32Params& p = L.gemm32;
+    p.A = (const float*)g.A;
+    p.B = (const float*)g.B[0];
+    p.C = split ? (float*)ws : (float*)g.C[0];
+    p.lda = g.lda; p.ldb = g.ldb;
+    p.ldc = split ? g.N : g.ldc;
+    p.part_stride = g.M * g.N;
+    p.M = (int)g.M; p.N = (int)g.N; p.K = (int)g.K; p.b_nk = g.b_nk;
+    p.rm = g.rm; p.ms = (int)(g.M / g.rm); p.tpm = (int)cdiv(p.ms, tile);
+    p.rn = g.rn; p.ns = (int)(g.N / g.rn); p.tpn = (int)cdiv(p.ns, tile);
+    p.rk = g.rk; p.ks = (int)(g.K / g.rk);
+    p.tiles_m = p.rm * p.tpm; p.tiles_n = p.rn * p.tpn;
+    p.nsplit = split ? g.rk : 1;
+    p.epi = split ? EPI_PARTIAL : EPI_F32;
+    L.kind = L_GEMM_F32;
+    L.name = g.name;
+    L.text = describe_gemm(g, (int64_t)p.tiles_m * p.tiles_n * p.nsplit, split);
+  }
+  plan.launches.push_back(L);
+  if (split) {
+    Launch R;
+    R.kind = L_REDUCE;
+    R.name = std::string(g.name) + ".reduce";
+    ReduceParams& r = R.reduce;
+    r.partial = (const float*)ws;
+    r.part_ld = g.N; r.part_stride = g.M * g.N;
+    r.R = g.rk; r.M = (int)g.M; r.N = (int)g.N;
+    r.C = g.C[0]; r.ldc = g.ldc;
+    r.bias = g.bias[0];
+    r.resid = g.resid; r.ldr = g.ldr;
+    r.act = g.act;
+    r.out_bf16 = (!g.resid_add && g.c_dtype == PARTIR_BF16);
+    r.resid_add = g.resid_add;
+    char buf[256];
+    snprintf(buf, sizeof buf, "splitk_reduce: C[%lld,%lld] = sum_{r=0..%d} partial[r] (in-device all_reduce)%s%s",
+             (long long)g.M, (long long)g.N, g.rk - 1, g.bias[0] ? " + bias" : "",
+             g.resid_add ? " + residual" : "");
+    R.text = buf;
+    plan.launches.push_back(R);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Launch
+// ---------------------------------------------------------------------------
+hipError_t run_one(const Launch& L, hipStream_t s) {
+  switch (L.kind) {
+    case L_GEMM_BF16: return launch_gemm_bf16(L.gemm, s);
+    case L_GEMM_F32: return launch_gemm_f32(L.gemm32, s);
+    case L_REDUCE: return launch_splitk_reduce(L.reduce, s);
+    case L_ATTN: return launch_attention(L.attn, s);
+    case L_RMS: return launch_rmsnorm(L.rms, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+void keep_plan_text(const Plan& plan, const char* what) {
+  std::string t = std::string(what) + ": " + std::to_string(plan.n_shards) + " virtual shards, " +
+                  std::to_string(plan.n_tile_loops) + " #tile loops, " + std::to_string(plan.n_sum_loops) +
+                  " #sum loops (" + std::to_string(plan.n_sum_splitk) + " split-K), workspace " +
+                  std::to_string(plan.ws_bytes) + " B\n";
+  for (size_t i = 0; i < plan.launches.size(); ++i)
+    t += "  [" + std::to_string(i) + "] " + plan.launches[i].text + "\n";
+  g_plan_text = t;
+  const char* dump = getenv("PARTIR_DUMP_PLAN");
+  if (dump && dump[0] == '1') fputs(t.c_str(), stderr);
+}
+
+int execute(const Plan& plan, void* stream) {
+  const char* force = getenv("PARTIR_FAIL_LAUNCH");
+  if (force && force[0] == '1') return fail(PARTIR_E_HIP, "launch failure forced by PARTIR_FAIL_LAUNCH");
+  hipStream_t s = (hipStream_t)stream;
+  (void)hipGetLastError();
+  for (const Launch& L : plan.launches) {
+    bool traced = false;
+    TraceRec rec;
+    {
+      std::lock_guard<std::mutex> lk(g_trace_mu);
+      traced = g_trace_on;
+    }
+    if (traced) {
+      rec.name = L.name;
+      if (hipEventCreate(&rec.start) != hipSuccess || hipEventCreate(&rec.stop) != hipSuccess)
+        return fail(PARTIR_E_HIP, "hipEventCreate failed");
+      if (hipEventRecord(rec.start, s) != hipSuccess) return fail(PARTIR_E_HIP, "hipEventRecord failed");
+    }
+    const hipError_t e = run_one(L, s);
+    if (e != hipSuccess) return fail(PARTIR_E_HIP, "launch of %s failed: %s", L.name.c_str(), hipGetErrorString(e));
+    if (traced) {
+      if (hipEventRecord(rec.stop, s) != hipSuccess) return fail(PARTIR_E_HIP, "hipEventRecord failed");
+      std::lock_guard<std::mutex> lk(g_trace_mu);
+      g_trace_pending.push_back(rec);
+    }
+  }
+  return PARTIR_OK;
+}
+
+int check_ws(const Plan& plan, void* ws, size_t ws_bytes) {
+  if (ws_bytes < plan.ws_bytes)
+    return fail(PARTIR_E_WORKSPACE, "workspace of %zu bytes, need %zu", ws_bytes, plan.ws_bytes);
+  if (plan.ws_bytes > 0 && ws == nullptr) return fail(PARTIR_E_NULL, "workspace pointer is NULL");
+  if (plan.ws_bytes > 0 && !aligned16(ws)) return fail(PARTIR_E_LAYOUT, "workspace not 16-byte aligned");
+  return PARTIR_OK;
+}
+
+// ---------------------------------------------------------------------------
+// partir_loop_matmul
+// ---------------------------------------------------------------------------
+struct MatmulArgs {
+  const void *A = nullptr, *B = nullptr;
+  void* C = nullptr;
+  int64_t M, N, K, lda, ldb, ldc;
+  int ab, c, b_layout, tile_axis, sum_axis, R, sum_impl;
+};
+
+int validate_matmul(const MatmulArgs& a, bool with_ptrs) {
+  if (with_ptrs && (!a.A || !a.B || !a.C)) return fail(PARTIR_E_NULL, "A, B and C must be non-NULL");
+  if (a.M < 1 || a.N < 1 || a.K < 1) return fail(PARTIR_E_SHAPE, "M, N, K must be >= 1");
+  if (a.M > (1 << 30) || a.N > (1 << 30) || a.K > (1 << 30)) return fail(PARTIR_E_SHAPE, "dims above 2^30");
+  if (a.R < 1) return fail(PARTIR_E_UNSUPPORTED, "R = %d: a loop needs at least one shard", a.R);
+  if (a.tile_axis != PARTIR_AXIS_NONE && a.tile_axis != PARTIR_AXIS_M && a.tile_axis != PARTIR_AXIS_N) {
+    if (a.tile_axis == PARTIR_AXIS_K)
+      return fail(PARTIR_E_AXIS, "#tile over K: K is contracted, so its shards must be summed, not concatenated");
+    return fail(PARTIR_E_AXIS, "tile_axis %d is not NONE, M or N", a.tile_axis);
+  }
+  if (a.sum_axis != PARTIR_AXIS_NONE && a.sum_axis != PARTIR_AXIS_K) {
+    if (a.sum_axis == a.tile_axis)
+      return fail(PARTIR_E_AXIS, "axis %d is both tiled and summed", a.sum_axis);
+    return fail(PARTIR_E_AXIS, "sum_axis %d: only the contracted dim K can carry #sum", a.sum_axis);
+  }
+  if (!valid_dtype(a.ab) || !valid_dtype(a.c)) return fail(PARTIR_E_DTYPE, "dtype must be F32 or BF16");
+  if (a.ab == PARTIR_F32 && a.c != PARTIR_F32) return fail(PARTIR_E_DTYPE, "f32 inputs need an f32 output");
+  if (a.b_layout != PARTIR_B_KN && a.b_layout != PARTIR_B_NK) return fail(PARTIR_E_LAYOUT, "b_layout %d", a.b_layout);
+  if (a.ab == PARTIR_BF16 && a.b_layout != PARTIR_B_NK)
+    return fail(PARTIR_E_UNSUPPORTED, "bf16 B must be given transposed (PARTIR_B_NK) in this build");
+  if (a.sum_impl < PARTIR_SUM_AUTO || a.sum_impl > PARTIR_SUM_SPLITK)
+    return fail(PARTIR_E_UNSUPPORTED, "sum_impl %d", a.sum_impl);
+  if (a.tile_axis == PARTIR_AXIS_M && a.M % a.R) return fail(PARTIR_E_DIVISIBILITY, "R=%d does not divide M=%lld", a.R, (long long)a.M);
+  if (a.tile_axis == PARTIR_AXIS_N && a.N % a.R) return fail(PARTIR_E_DIVISIBILITY, "R=%d does not divide N=%lld", a.R, (long long)a.N);
+  if (a.sum_axis == PARTIR_AXIS_K && a.K % a.R) return fail(PARTIR_E_DIVISIBILITY, "R=%d does not divide K=%lld", a.R, (long long)a.K);
+  const int eb = elem_bytes(a.ab), vec = 16 / eb;
+  const int64_t ldb_min = a.b_layout == PARTIR_B_KN ? a.N : a.K;
+  if (a.lda < a.K || a.ldb < ldb_min || a.ldc < a.N) return fail(PARTIR_E_LAYOUT, "leading dim smaller than the row length");
+  if (a.lda % vec || a.ldb % vec || a.ldc % (16 / elem_bytes(a.c)))
+    return fail(PARTIR_E_LAYOUT, "leading dims must keep rows 16-byte aligned");
+  if (a.K % vec) return fail(PARTIR_E_LAYOUT, "K must be a multiple of %d", vec);
+  if (a.N % 4) return fail(PARTIR_E_LAYOUT, "N must be a multiple of 4");
+  const int rk = a.sum_axis == PARTIR_AXIS_K ? a.R : 1;
+  const int rn = a.tile_axis == PARTIR_AXIS_N ? a.R : 1;
+  if ((a.K / rk) % vec) return fail(PARTIR_E_LAYOUT, "K/R must be a multiple of %d (16-byte shard views)", vec);
+  if ((a.N / rn) % 4) return fail(PARTIR_E_LAYOUT, "N/R must be a multiple of 4 (16-byte shard views)");
+  if (with_ptrs && (!aligned16(a.A) || !aligned16(a.B) || !aligned16(a.C)))
+    return fail(PARTIR_E_LAYOUT, "A, B and C must be 16-byte aligned");
+  return PARTIR_OK;
+}
+
+GemmSpec matmul_spec(const MatmulArgs& a) {
+  GemmSpec g;
+  g.A = a.A; g.B[0] = a.B; g.C[0] = a.C;
+  g.lda = a.lda; g.ldb = a.ldb; g.ldc = a.ldc;
+  g.M = a.M; g.N = a.N; g.K = a.K;
+  g.ab_dtype = a.ab; g.c_dtype = a.c; g.b_nk = a.b_layout == PARTIR_B_NK;
+  g.rm = a.tile_axis == PARTIR_AXIS_M ? a.R : 1;
+  g.rn = a.tile_axis == PARTIR_AXIS_N ? a.R : 1;
+  g.rk = a.sum_axis == PARTIR_AXIS_K ? a.R : 1;
+  g.sum_impl = a.sum_impl;
+  g.name = a.ab == PARTIR_BF16 ? "loop_matmul.bf16" : "loop_matmul.f32";
+  g.label = "loop_matmul";
+  return g;
+}
+
+void plan_matmul(const MatmulArgs& a, void* ws, Plan& plan) {
+  GemmSpec g = matmul_spec(a);
+  plan.ws_bytes = gemm_ws_bytes(g);
+  plan.n_shards = g.rm * g.rn * g.rk;
+  plan.n_tile_loops = a.tile_axis != PARTIR_AXIS_NONE;
+  plan.flops = 2.0 * a.M * a.N * a.K;
+  plan_gemm(g, ws, plan);
+}
+
+// ---------------------------------------------------------------------------
+// partir_mlp_block
+// ---------------------------------------------------------------------------
+struct MlpArgs {
+  const void *X = nullptr, *W1t = nullptr, *b1 = nullptr, *W2t = nullptr, *b2 = nullptr;
+  void* Y = nullptr;
+  int64_t T, D, F;
+  int in, out, act, Rb, Rm;
+};
+
+int validate_mlp(const MlpArgs& a, bool with_ptrs) {
+  if (with_ptrs && (!a.X || !a.W1t || !a.W2t || !a.Y)) return fail(PARTIR_E_NULL, "X, W1t, W2t and Y must be non-NULL");
+  if (a.T < 1 || a.D < 1 || a.F < 1) return fail(PARTIR_E_SHAPE, "T, D, F must be >= 1");
+  if (a.T > (1 << 30) || a.D > (1 << 20) || a.F > (1 << 22)) return fail(PARTIR_E_SHAPE, "dims too large");
+  if (a.Rb < 1 || a.Rm < 1) return fail(PARTIR_E_UNSUPPORTED, "R_batch and R_model must be >= 1");
+  if (a.in != PARTIR_BF16) return fail(PARTIR_E_DTYPE, "in_dtype must be BF16");
+  if (!valid_dtype(a.out)) return fail(PARTIR_E_DTYPE, "out_dtype must be F32 or BF16");
+  if (a.act != PARTIR_ACT_NONE && a.act != PARTIR_ACT_GELU_ERF) return fail(PARTIR_E_UNSUPPORTED, "act %d", a.act);
+  if (a.T % a.Rb) return fail(PARTIR_E_DIVISIBILITY, "R_batch=%d does not divide T=%lld", a.Rb, (long long)a.T);
+  if (a.F % a.Rm) return fail(PARTIR_E_DIVISIBILITY, "R_model=%d does not divide F=%lld", a.Rm, (long long)a.F);
+  if (a.D % 8 || (a.F / a.Rm) % 8) return fail(PARTIR_E_LAYOUT, "D and F/R_model must be multiples of 8");
+  if (with_ptrs && (!aligned16(a.X) || !aligned16(a.W1t) || !aligned16(a.W2t) || !aligned16(a.Y) ||
+                    !aligned16(a.b1) || !aligned16(a.b2)))
+    return fail(PARTIR_E_LAYOUT, "tensors must be 16-byte aligned");
+  return PARTIR_OK;
+}
+
+void plan_mlp(const MlpArgs& a, void* ws, Plan& plan) {
+  const size_t h_bytes = align_up((size_t)a.T * a.F * 2);
+  char* base = (char*)ws;
+  void* H = base;
+  GemmSpec g1;
+  g1.A = a.X; g1.B[0] = a.W1t; g1.C[0] = H; g1.bias[0] = (const float*)a.b1;
+  g1.lda = a.D; g1.ldb = a.D; g1.ldc = a.F;
+  g1.M = a.T; g1.N = a.F; g1.K = a.D;
+  g1.c_dtype = PARTIR_BF16; g1.rm = a.Rb; g1.rn = a.Rm; g1.act = a.act;
+  g1.name = "mlp.up";
+  g1.label = "mlp.up   H = act(slice 0 X[b] . slice 1 W1[m])";
+  GemmSpec g2;
+  g2.A = H; g2.B[0] = a.W2t; g2.C[0] = a.Y; g2.bias[0] = (const float*)a.b2;
+  g2.lda = a.F; g2.ldb = a.F; g2.ldc = a.D;
+  g2.M = a.T; g2.N = a.D; g2.K = a.F;
+  g2.c_dtype = a.out; g2.rm = a.Rb; g2.rk = a.Rm;
+  g2.name = "mlp.down";
+  g2.label = "mlp.down Y = sum_m H[:, m] . slice 0 W2[m]";
+  plan.ws_bytes = h_bytes + gemm_ws_bytes(g2);
+  plan.n_shards = a.Rb * a.Rm;
+  plan.n_tile_loops = (a.Rb > 1) + 1;
+  plan.flops = 4.0 * a.T * a.D * a.F;
+  plan_gemm(g1, nullptr, plan);
+  plan_gemm(g2, ws ? base + h_bytes : nullptr, plan);
+}
+
+// ---------------------------------------------------------------------------
+// attention block and decoder layer
+// ---------------------------------------------------------------------------
+struct AttnArgs {
+  const void *X = nullptr, *Wq = nullptr, *Wk = nullptr, *Wv = nullptr, *Wo = nullptr;
+  void* Y = nullptr;
+  int64_t B, S, D, H, dh;
+  int causal;
+  float scale;
+  int in, out, Rb, Rm;
+};
+
+int validate_attn_shapes(int64_t B, int64_t S, int64_t D, int64_t H, int64_t dh, int Rb, int Rm) {
+  if (B < 1 || S < 1 || D < 1 || H < 1 || dh < 1) return fail(PARTIR_E_SHAPE, "sizes must be >= 1");
+  if (B * S > (1 << 28) || D > (1 << 20)) return fail(PARTIR_E_SHAPE, "sizes too large");
+  if (H * dh != D) return fail(PARTIR_E_SHAPE, "n_heads*d_head = %lld != D = %lld", (long long)(H * dh), (long long)D);
+  if (dh != 128) return fail(PARTIR_E_SHAPE, "d_head must be 128 (got %lld)", (long long)dh);
+  if (S % 128) return fail(PARTIR_E_SHAPE, "S must be a multiple of 128 (got %lld)", (long long)S);
+  if (Rb < 1 || Rm < 1) return fail(PARTIR_E_UNSUPPORTED, "R_batch and R_model must be >= 1");
+  if (B % Rb) return fail(PARTIR_E_DIVISIBILITY, "R_batch=%d does not divide B=%lld (batch shards hold whole sequences)", Rb, (long long)B);
+  if (H % Rm) return fail(PARTIR_E_DIVISIBILITY, "R_model=%d does not divide n_heads=%lld", Rm, (long long)H);
+  return PARTIR_OK;
+}
+
+int validate_attn(const AttnArgs& a, bool with_ptrs) {
+  if (with_ptrs && (!a.X || !a.Wq || !a.Wk || !a.Wv || !a.Wo || !a.Y)) return fail(PARTIR_E_NULL, "X, W* and Y must be non-NULL");
+  int st = validate_attn_shapes(a.B, a.S, a.D, a.H, a.dh, a.Rb, a.Rm);
+  if (st) return st;
+  if (a.in != PARTIR_BF16) return fail(PARTIR_E_DTYPE, "in_dtype must be BF16");
+  if (!valid_dtype(a.out)) return fail(PARTIR_E_DTYPE, "out_dtype must be F32 or BF16");
+  if (with_ptrs && (!aligned16(a.X) || !aligned16(a.Wq) || !aligned16(a.Wk) || !aligned16(a.Wv) ||
+                    !aligned16(a.Wo) || !aligned16(a.Y)))
+    return fail(PARTIR_E_LAYOUT, "tensors must be 16-byte aligned");
+  return PARTIR_OK;
+}
+
+// QKV projection + attention core into (Q, K, V, O) inside the workspace.
+void plan_attention_core(const void* Xn, const void* Wq, const void* Wk, const void* Wv, char* qkvo,
+                         int64_t B, int64_t S, int64_t D, int64_t H, int64_t dh, int causal, float scale,
+                         int Rb, int Rm, Plan& plan) {
+  const int64_t T = B * S;
+  const size_t one = align_up((size_t)T * D * 2);
+  void* Q = qkvo ? qkvo : nullptr;
+  void* K = qkvo ? qkvo + one : nullptr;
+  void* V = qkvo ? qkvo + 2 * one : nullptr;
+  void* O = qkvo ? qkvo + 3 * one : nullptr;
+  GemmSpec g;
+  g.A = Xn; g.B[0] = Wq; g.B[1] = Wk; g.B[2] = Wv; g.C[0] = Q; g.C[1] = K; g.C[2] = V;
+  g.ngroups = 3;
+  g.lda = D; g.ldb = D; g.ldc = D;
+  g.M = T; g.N = D; g.K = D;
+  g.c_dtype = PARTIR_BF16; g.rm = Rb; g.rn = Rm;
+  g.name = "attn.qkv";
+  g.label = "attn.qkv Q|K|V = slice 0 X[b] . slice 1 W{q,k,v}[m]";
+  plan_gemm(g, nullptr, plan);
+  Launch L;
+  L.kind = L_ATTN;
+  L.name = "attn.core";
+  AttnParams& p = L.attn;
+  p.Q = (const uint16_t*)Q; p.K = (const uint16_t*)K; p.V = (const uint16_t*)V; p.O = (uint16_t*)O;
+  p.ldq = p.ldk = p.ldv = p.ldo = D;
+  p.B = (int)B; p.S = (int)S; p.H = (int)H; p.causal = causal;
+  const float sc = scale > 0 ? scale : 1.0f / std::sqrt((float)dh);
+  p.scale_log2 = sc * 1.4426950408889634f;
+  char buf[256];
+  snprintf(buf, sizeof buf, "attention: loop h [#tile<1>](%lld heads/shard) over %lld sequences x %lld heads, "
+           "S=%lld, %s, %lld WGs", (long long)(H / Rm), (long long)B, (long long)H, (long long)S,
+           causal ? "causal" : "full", (long long)(S / 128 * B * H));
+  L.text = buf;
+  plan.launches.push_back(L);
+}
+
+size_t attn_core_bytes(int64_t T, int64_t D) { return 4 * align_up((size_t)T * D * 2); }
+
+void plan_attn(const AttnArgs& a, void* ws, Plan& plan) {
+  const int64_t T = a.B * a.S;
+  char* base = (char*)ws;
+  const size_t core = attn_core_bytes(T, a.D);
+  plan_attention_core(a.X, a.Wq, a.Wk, a.Wv, base, a.B, a.S, a.D, a.H, a.dh, a.causal, a.scale, a.Rb, a.Rm, plan);
+  GemmSpec g;
+  g.A = base ? base + 3 * align_up((size_t)T * a.D * 2) : nullptr;
+  g.B[0] = a.Wo; g.C[0] = a.Y;
+  g.lda = a.D; g.ldb = a.D; g.ldc = a.D;
+  g.M = T; g.N = a.D; g.K = a.D;
+  g.c_dtype = a.out; g.rm = a.Rb; g.rk = a.Rm;
+  g.name = "attn.out";
+  g.label = "attn.out Y = sum_m O[:, m heads] . slice 0 Wo[m]";
+  plan.ws_bytes = core + gemm_ws_bytes(g);
+  plan.n_shards = a.Rb * a.Rm;
+  plan.n_tile_loops = (a.Rb > 1) + 1;
+  const double pairs = a.causal ? (double)a.S * (a.S + 1) / 2 : (double)a.S * a.S;
+  plan.flops = 8.0 * T * a.D * a.D + 4.0 * a.B * a.H * pairs * a.dh;
+  plan_gemm(g, base ? base + core : nullptr, plan);
+}
+
+struct DecArgs {
+  void* x = nullptr;
+  const void *g1 = nullptr, *g2 = nullptr, *Wq = nullptr, *Wk = nullptr, *Wv = nullptr, *Wo = nullptr,
+             *W1 = nullptr, *W2 = nullptr;
+  float eps;
+  int64_t B, S, D, H, dh, F;
+  int Rb, Rm;
+};
+
+int validate_dec(const DecArgs& a, bool with_ptrs) {
+  if (with_ptrs && (!a.x || !a.g1 || !a.g2 || !a.Wq || !a.Wk || !a.Wv || !a.Wo || !a.W1 || !a.W2))
+    return fail(PARTIR_E_NULL, "all tensors must be non-NULL");
+  int st = validate_attn_shapes(a.B, a.S, a.D, a.H, a.dh, a.Rb, a.Rm);
+  if (st) return st;
+  if (a.F < 1 || a.F > (1 << 22)) return fail(PARTIR_E_SHAPE, "F out of range");
+  if (a.F % a.Rm) return fail(PARTIR_E_DIVISIBILITY, "R_model=%d does not divide F=%lld", a.Rm, (long long)a.F);
+  if ((a.F / a.Rm) % 8) return fail(PARTIR_E_LAYOUT, "F/R_model must be a multiple of 8");
+  if (!(a.eps >= 0.0f)) return fail(PARTIR_E_SHAPE, "eps must be >= 0");
+  if (with_ptrs && (!aligned16(a.x) || !aligned16(a.g1) || !aligned16(a.g2) || !aligned16(a.Wq) ||
+                    !aligned16(a.Wk) || !aligned16(a.Wv) || !aligned16(a.Wo) || !aligned16(a.W1) || !aligned16(a.W2)))
+    return fail(PARTIR_E_LAYOUT, "tensors must be 16-byte aligned");
+  return PARTIR_OK;
+}
+
+void plan_rmsnorm(const float* x, const float* g, void* y, int64_t rows, int64_t D, float eps, int Rb, Plan& plan) {
+  Launch L;
+  L.kind = L_RMS;
+  L.name = "rmsnorm";
+  RmsParams& p = L.rms;
+  p.x = x; p.g = g; p.y = (uint16_t*)y; p.ldx = D; p.ldy = D; p.rows = (int)rows; p.D = (int)D; p.eps = eps;
+  char buf[160];
+  snprintf(buf, sizeof buf, "rmsnorm: %lld rows x %lld (replicated across model shards, %d batch shards)",
+           (long long)rows, (long long)D, Rb);
+  L.text = buf;
+  plan.launches.push_back(L);
+}
+
+void plan_dec(const DecArgs& a, void* ws, Plan& plan) {
+  const int64_t T = a.B * a.S;
+  char* base = (char*)ws;
+  const size_t xn_bytes = align_up((size_t)T * a.D * 2);
+  const size_t core = attn_core_bytes(T, a.D);
+  const size_t h_bytes = align_up((size_t)T * a.F * 2);
+  char* xn = base;
+  char* qkvo = base ? base + xn_bytes : nullptr;
+  char* Hf = base ? base + xn_bytes + core : nullptr;
+  char* part = base ? base + xn_bytes + core + h_bytes : nullptr;
+
+  plan_rmsnorm((const float*)a.x, (const float*)a.g1, xn, T, a.D, a.eps, a.Rb, plan);
+  plan_attention_core(xn, a.Wq, a.Wk, a.Wv, qkvo, a.B, a.S, a.D, a.H, a.dh, 1, 0.0f, a.Rb, a.Rm, plan);
+  GemmSpec go;
+  go.A = qkvo ? qkvo + 3 * align_up((size_t)T * a.D * 2) : nullptr;
+  go.B[0] = a.Wo; go.C[0] = a.x; go.resid = (const float*)a.x; go.resid_add = true;
+  go.lda = a.D; go.ldb = a.D; go.ldc = a.D; go.ldr = a.D;
+  go.M = T; go.N = a.D; go.K = a.D;
+  go.c_dtype = PARTIR_F32; go.rm = a.Rb; go.rk = a.Rm;
+  go.name = "attn.out";
+  go.label = "dec.attn_out x += sum_m O[:, m heads] . slice 0 Wo[m]";
+  plan_gemm(go, part, plan);
+  plan_rmsnorm((const float*)a.x, (const float*)a.g2, xn, T, a.D, a.eps, a.Rb, plan);
+  GemmSpec g1;
+  g1.A = xn; g1.B[0] = a.W1; g1.C[0] = Hf;
+  g1.lda = a.D; g1.ldb = a.D; g1.ldc = a.F;
+  g1.M = T; g1.N = a.F; g1.K = a.D;
+  g1.c_dtype = PARTIR_BF16; g1.rm = a.Rb; g1.rn = a.Rm; g1.act = 1;
+  g1.name = "mlp.up";
+  g1.label = "dec.ffn_up H = gelu(slice 0 xn[b] . slice 1 W1[m])";
+  plan_gemm(g1, nullptr, plan);
+  GemmSpec g2;
+  g2.A = Hf; g2.B[0] = a.W2; g2.C[0] = a.x; g2.resid = (const float*)a.x; g2.resid_add = true;
+  g2.lda = a.F; g2.ldb = a.F; g2.ldc = a.D; g2.ldr = a.D;
+  g2.M = T; g2.N = a.D; g2.K = a.F;
+  g2.c_dtype = PARTIR_F32; g2.rm = a.Rb; g2.rk = a.Rm;
+  g2.name = "mlp.down";
+  g2.label = "dec.ffn_down x += sum_m H[:, m] . slice 0 W2[m]";
+  plan_gemm(g2, part, plan);
+  plan.ws_bytes = xn_bytes + core + h_bytes + std::max(gemm_ws_bytes(go), gemm_ws_bytes(g2));
+  plan.n_shards = a.Rb * a.Rm;
+  plan.n_tile_loops = (a.Rb > 1) + 2;
+  plan.flops = 8.0 * T * a.D * a.D + 4.0 * a.B * a.H * ((double)a.S * (a.S + 1) / 2) * a.dh + 4.0 * T * a.D * a.F;
+}
+
+void fill_info(const Plan& plan, partir_plan_info* info) {
+  if (!info) return;
+  info->n_virtual_shards = plan.n_shards;
+  info->n_tile_loops = plan.n_tile_loops;
+  info->n_sum_loops = plan.n_sum_loops;
+  info->n_sum_splitk = plan.n_sum_splitk;
+  info->n_launches = (int)plan.launches.size();
+  info->reserved = 0;
+  info->workspace_bytes = plan.ws_bytes;
+  info->flops = plan.flops;
+}
+
+}  // namespace
+}  // namespace partir
+
+using namespace partir;
+
+// ===========================================================================
+// C ABI
+// ===========================================================================
+extern "C" {
+
+const char* partir_status_string(int status) {
+  switch (status) {
+    case PARTIR_OK: return "PARTIR_OK";
+    case PARTIR_E_NULL: return "PARTIR_E_NULL";
+    case PARTIR_E_SHAPE: return "PARTIR_E_SHAPE";
+    case PARTIR_E_DIVISIBILITY: return "PARTIR_E_DIVISIBILITY";
+    case PARTIR_E_AXIS: return "PARTIR_E_AXIS";
+    case PARTIR_E_DTYPE: return "PARTIR_E_DTYPE";
+    case PARTIR_E_LAYOUT: return "PARTIR_E_LAYOUT";
+    case PARTIR_E_WORKSPACE: return "PARTIR_E_WORKSPACE";
+    case PARTIR_E_HIP: return "PARTIR_E_HIP";
+    case PARTIR_E_UNSUPPORTED: return "PARTIR_E_UNSUPPORTED";
+    default: return "PARTIR_E_UNKNOWN";
+  }
+}
+
+const char* partir_last_error(void) { return g_error.c_str(); }
+const char* partir_version(void) { return "libpartir 0.1 (gfx950)"; }
+const char* partir_last_plan_text(void) { return g_plan_text.c_str(); }
+
+// ---- loop_matmul ----------------------------------------------------------------
+size_t partir_loop_matmul_workspace(int64_t M, int64_t N, int64_t K, int ab_dtype, int c_dtype,
+                                    int b_layout, int tile_axis, int sum_axis, int R, int sum_impl) {
+  MatmulArgs a{nullptr, nullptr, nullptr, M, N, K,
+               K, b_layout == PARTIR_B_KN ? N : K, N, ab_dtype, c_dtype, b_layout, tile_axis, sum_axis, R, sum_impl};
+  a.lda = ((K + 7) / 8) * 8;
+  a.ldb = b_layout == PARTIR_B_KN ? ((N + 7) / 8) * 8 : a.lda;
+  a.ldc = ((N + 7) / 8) * 8;
+  if (validate_matmul(a, false) != PARTIR_OK) return (size_t)-1;
+  return gemm_ws_bytes(matmul_spec(a));
+}
+
+int partir_plan_loop_matmul(int64_t M, int64_t N, int64_t K, int ab_dtype, int c_dtype, int b_layout,
+                            int tile_axis, int sum_axis, int R, int sum_impl, partir_plan_info* info) {
+  MatmulArgs a{nullptr, nullptr, nullptr, M, N, K, 0, 0, 0, ab_dtype, c_dtype, b_layout, tile_axis, sum_axis, R, sum_impl};
+  a.lda = ((K + 7) / 8) * 8;
+  a.ldb = b_layout == PARTIR_B_KN ? ((N + 7) / 8) * 8 : a.lda;
+  a.ldc = ((N + 7) / 8) * 8;
+  int st = validate_matmul(a, false);
+  if (st) return st;
+  Plan plan;
+  plan_matmul(a, nullptr, plan);
+  keep_plan_text(plan, "loop_matmul");
+  fill_info(plan, info);
+  return PARTIR_OK;
+}
+
+int partir_loop_matmul(const void* A, const void* B, void* C, int64_t M, int64_t N, int64_t K,
+                       int64_t lda, int64_t ldb, int64_t ldc, int ab_dtype, int c_dtype, int b_layout,
+                       int tile_axis, int sum_axis, int R, int sum_impl, void* ws, size_t ws_bytes, void* stream) {
+  MatmulArgs a{A, B, C, M, N, K, lda, ldb, ldc, ab_dtype, c_dtype, b_layout, tile_axis, sum_axis, R, sum_impl};
+  int st = validate_matmul(a, true);
+  if (st) return st;
+  Plan plan;
+  plan_matmul(a, ws, plan);
+  if ((st = check_ws(plan, ws, ws_bytes))) return st;
+  keep_plan_text(plan, "loop_matmul");
+  return execute(plan, stream);
+}
+
+// ---- mlp_block -------------------------------------------------------------------
+size_t partir_mlp_block_workspace(int64_t T, int64_t D, int64_t F, int out_dtype, int R_batch, int R_model) {
+  MlpArgs a{nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, T, D, F, PARTIR_BF16, out_dtype, PARTIR_ACT_GELU_ERF, R_batch, R_model};
+  if (validate_mlp(a, false) != PARTIR_OK) return (size_t)-1;
+  Plan plan;
+  plan_mlp(a, nullptr, plan);
+  return plan.ws_bytes;
+}
+
+int partir_plan_mlp_block(int64_t T, int64_t D, int64_t F, int out_dtype, int R_batch, int R_model,
+                          partir_plan_info* info) {
+  MlpArgs a{nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, T, D, F, PARTIR_BF16, out_dtype, PARTIR_ACT_GELU_ERF, R_batch, R_model};
+  int st = validate_mlp(a, false);
+  if (st) return st;
+  Plan plan;
+  plan_mlp(a, nullptr, plan);
+  keep_plan_text(plan, "mlp_block");
+  fill_info(plan, info);
+  return PARTIR_OK;
+}
+
+int partir_mlp_block(const void* X, const void* W1t, const void* b1, const void* W2t, const void* b2, void* Y,
+                     int64_t T, int64_t D, int64_t F, int in_dtype, int out_dtype, int act,
+                     int R_batch, int R_model, void* ws, size_t ws_bytes, void* stream) {
+  MlpArgs a{X, W1t, b1, W2t, b2, Y, T, D, F, in_dtype, out_dtype, act, R_batch, R_model};
+  int st = validate_mlp(a, true);
+  if (st) return st;
+  Plan probe;
+  plan_mlp(a, nullptr, probe);
+  if ((st = check_ws(probe, ws, ws_bytes))) return st;
+  Plan plan;
+  plan_mlp(a, ws, plan);
+  keep_plan_text(plan, "mlp_block");
+  return execute(plan, stream);
+}
+
+// ---- attn_block ------------------------------------------------------------------
+size_t partir_attn_block_workspace(int64_t B, int64_t S, int64_t D, int64_t n_heads, int64_t d_head,
+                                   int R_batch, int R_model) {
+  AttnArgs a{nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, B, S, D, n_heads, d_head, 1, 0.f,
+             PARTIR_BF16, PARTIR_F32, R_batch, R_model};
+  if (validate_attn(a, false) != PARTIR_OK) return (size_t)-1;
+  Plan plan;
+  plan_attn(a, nullptr, plan);
+  return plan.ws_bytes;
+}
+
+int partir_plan_attn_block(int64_t B, int64_t S, int64_t D, int64_t n_heads, int64_t d_head,
+                           int R_batch, int R_model, partir_plan_info* info) {
+  AttnArgs a{nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, B, S, D, n_heads, d_head, 1, 0.f,
+             PARTIR_BF16, PARTIR_F32, R_batch, R_model};
+  int st = validate_attn(a, false);
+  if (st) return st;
+  Plan plan;
+  plan_attn(a, nullptr, plan);
+  keep_plan_text(plan, "attn_block");
+  fill_info(plan, info);
+  return PARTIR_OK;
+}
+
+int partir_attn_block(const void* X, const void* Wq_t, const void* Wk_t, const void* Wv_t, const void* Wo_t, void* Y,
+                      int64_t B, int64_t S, int64_t D, int64_t n_heads, int64_t d_head, int causal, float scale,
+                      int in_dtype, int out_dtype, int R_batch, int R_model, void* ws, size_t ws_bytes, void* stream) {
+  AttnArgs a{X, Wq_t, Wk_t, Wv_t, Wo_t, Y, B, S, D, n_heads, d_head, causal ? 1 : 0, scale,
+             in_dtype, out_dtype, R_batch, R_model};
+  int st = validate_attn(a, true);
+  if (st) return st;
+  Plan probe;
+  plan_attn(a, nullptr, probe);
+  if ((st = check_ws(probe, ws, ws_bytes))) return st;
+  Plan plan;
+  plan_attn(a, ws, plan);
+  keep_plan_text(plan, "attn_block");
+  return execute(plan, stream);
+}
+
+// ---- decoder_layer ---------------------------------------------------------------
+size_t partir_decoder_layer_workspace(int64_t B, int64_t S, int64_t D, int64_t n_heads, int64_t d_head,
+                                      int64_t F, int R_batch, int R_model) {
+  DecArgs a;
+  a.eps = 1e-6f; a.B = B; a.S = S; a.D = D; a.H = n_heads; a.dh = d_head; a.F = F; a.Rb = R_batch; a.Rm = R_model;
+  if (validate_dec(a, false) != PARTIR_OK) return (size_t)-1;
+  Plan plan;
+  plan_dec(a, nullptr, plan);
+  return plan.ws_bytes;
+}
+
+int partir_plan_decoder_layer(int64_t B, int64_t S, int64_t D, int64_t n_heads, int64_t d_head, int64_t F,
+                              int R_batch, int R_model, partir_plan_info* info) {
+  DecArgs a;
+  a.eps = 1e-6f; a.B = B; a.S = S; a.D = D; a.H = n_heads; a.dh = d_head; a.F = F; a.Rb = R_batch; a.Rm = R_model;
+  int st = validate_dec(a, false);
+  if (st) return st;
+  Plan plan;
+  plan_dec(a, nullptr, plan);
+  keep_plan_text(plan, "decoder_layer");
+  fill_info(plan, info);
+  return PARTIR_OK;
+}
+
+int partir_decoder_layer(void* x, const void* g1, const void* g2, float eps, const void* Wq_t, const void* Wk_t,
+                         const void* Wv_t, const void* Wo_t, const void* W1t, const void* W2t, int64_t B, int64_t S,
+                         int64_t D, int64_t n_heads, int64_t d_head, int64_t F, int R_batch, int R_model,
+                         void* ws, size_t ws_bytes, void* stream) {
+  DecArgs a;
+  a.x = x; a.g1 = g1; a.g2 = g2; a.Wq = Wq_t; a.Wk = Wk_t; a.Wv = Wv_t; a.Wo = Wo_t; a.W1 = W1t; a.W2 = W2t;
+  a.eps = eps; a.B = B; a.S = S; a.D = D; a.H = n_heads; a.dh = d_head; a.F = F; a.Rb = R_batch; a.Rm = R_model;
+  int st = validate_dec(a, true);
+  if (st) return st;
+  Plan probe;
+  plan_dec(a, nullptr, probe);
+  if ((st = check_ws(probe, ws, ws_bytes))) return st;
+  Plan plan;
+  plan_dec(a, ws, plan);
+  keep_plan_text(plan, "decoder_layer");
+  return execute(plan, stream);
+}
+
+// ---- trace ------------------------------------------------------------------------
+int partir_trace_enable(int on) {
+  std::lock_guard<std::mutex> lk(g_trace_mu);
+  g_trace_on = on != 0;
+  return PARTIR_OK;
+}
+
+void partir_trace_reset(void) {
+  std::lock_guard<std::mutex> lk(g_trace_mu);
+  for (auto& r : g_trace_pending) {
+    (void)hipEventDestroy(r.start);
+    (void)hipEventDestroy(r.stop);
+  }
+  g_trace_pending.clear();
+  g_trace_totals.clear();
+}
+
+int partir_trace_read(partir_trace_entry* out, int max) {
+  std::lock_guard<std::mutex> lk(g_trace_mu);
+  for (auto& r : g_trace_pending) {
+    if (hipEventSynchronize(r.stop) != hipSuccess) return -fail(PARTIR_E_HIP, "hipEventSynchronize failed");
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, r.start, r.stop) != hipSuccess) return -fail(PARTIR_E_HIP, "hipEventElapsedTime failed");
+    auto& t = g_trace_totals[r.name];
+    t.first += 1;
+    t.second += ms;
+    (void)hipEventDestroy(r.start);
+    (void)hipEventDestroy(r.stop);
+  }
+  g_trace_pending.clear();
+  int i = 0;
+  for (auto& kv : g_trace_totals) {
+    if (out && i < max) {
+      memset(out[i].name, 0, sizeof out[i].name);
+      strncpy(out[i].name, kv.first.c_str(), sizeof out[i].name - 1);
+      out[i].launches = kv.second.first;
+      out[i].total_ms = kv.second.second;
+    }
+    ++i;
+  }
+  return i;
+}
+
+}  // extern "C"

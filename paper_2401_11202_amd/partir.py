@@ -1,0 +1,273 @@
+"""Python binding of libpartir (ctypes).
+
+Argument marshalling only: every step of the computation runs in the HIP
+library.  PyTorch supplies device memory (outputs and workspaces are
+allocated with ``torch.empty``) and the current HIP stream.  If the built
+library is missing, every call raises ``PartirError`` -- there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libpartir.so")
+
+F32, BF16 = 0, 1
+AXIS_NONE, AXIS_M, AXIS_N, AXIS_K = -1, 0, 1, 2
+B_KN, B_NK = 0, 1
+SUM_AUTO, SUM_FUSED, SUM_SPLITK = 0, 1, 2
+ACT_NONE, ACT_GELU = 0, 1
+
+STATUS = {0: "PARTIR_OK", 1: "PARTIR_E_NULL", 2: "PARTIR_E_SHAPE", 3: "PARTIR_E_DIVISIBILITY",
+          4: "PARTIR_E_AXIS", 5: "PARTIR_E_DTYPE", 6: "PARTIR_E_LAYOUT", 7: "PARTIR_E_WORKSPACE",
+          8: "PARTIR_E_HIP", 9: "PARTIR_E_UNSUPPORTED"}
+ERR = {v: k for k, v in STATUS.items()}
+
+EXPORTS = ("partir_loop_matmul", "partir_loop_matmul_workspace", "partir_mlp_block",
+           "partir_mlp_block_workspace", "partir_attn_block", "partir_attn_block_workspace",
+           "partir_decoder_layer", "partir_decoder_layer_workspace", "partir_plan_loop_matmul",
+           "partir_plan_mlp_block", "partir_plan_attn_block", "partir_plan_decoder_layer",
+           "partir_last_plan_text", "partir_trace_enable", "partir_trace_read", "partir_trace_reset",
+           "partir_status_string", "partir_last_error", "partir_version")
+
+
+class PartirError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{STATUS.get(status, status)}: {msg}")
+        self.status = status
+
+
+class PlanInfo(ctypes.Structure):
+    _fields_ = [("n_virtual_shards", ctypes.c_int), ("n_tile_loops", ctypes.c_int),
+                ("n_sum_loops", ctypes.c_int), ("n_sum_splitk", ctypes.c_int),
+                ("n_launches", ctypes.c_int), ("reserved", ctypes.c_int),
+                ("workspace_bytes", ctypes.c_size_t), ("flops", ctypes.c_double)]
+
+    def as_dict(self):
+        return {f: getattr(self, f) for f, _ in self._fields_ if f != "reserved"}
+
+
+class TraceEntry(ctypes.Structure):
+    _fields_ = [("name", ctypes.c_char * 48), ("launches", ctypes.c_int64), ("total_ms", ctypes.c_double)]
+
+
+_lib = None
+I64, I32, P, SZ, F = ctypes.c_int64, ctypes.c_int, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_float
+
+
+def lib():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise PartirError(-1, f"{LIB_PATH} is not built; run `python -m paper_2401_11202_amd.build`")
+    L = ctypes.CDLL(LIB_PATH)
+    sig = {
+        "partir_loop_matmul": (I32, [P, P, P, I64, I64, I64, I64, I64, I64, I32, I32, I32, I32, I32, I32, I32, P, SZ, P]),
+        "partir_loop_matmul_workspace": (SZ, [I64, I64, I64, I32, I32, I32, I32, I32, I32, I32]),
+        "partir_mlp_block": (I32, [P, P, P, P, P, P, I64, I64, I64, I32, I32, I32, I32, I32, P, SZ, P]),
+        "partir_mlp_block_workspace": (SZ, [I64, I64, I64, I32, I32, I32]),
+        "partir_attn_block": (I32, [P, P, P, P, P, P, I64, I64, I64, I64, I64, I32, F, I32, I32, I32, I32, P, SZ, P]),
+        "partir_attn_block_workspace": (SZ, [I64, I64, I64, I64, I64, I32, I32]),
+        "partir_decoder_layer": (I32, [P, P, P, F, P, P, P, P, P, P, I64, I64, I64, I64, I64, I64, I32, I32, P, SZ, P]),
+        "partir_decoder_layer_workspace": (SZ, [I64, I64, I64, I64, I64, I64, I32, I32]),
+        "partir_plan_loop_matmul": (I32, [I64, I64, I64, I32, I32, I32, I32, I32, I32, I32, ctypes.POINTER(PlanInfo)]),
+        "partir_plan_mlp_block": (I32, [I64, I64, I64, I32, I32, I32, ctypes.POINTER(PlanInfo)]),
+        "partir_plan_attn_block": (I32, [I64, I64, I64, I64, I64, I32, I32, ctypes.POINTER(PlanInfo)]),
+        "partir_plan_decoder_layer": (I32, [I64, I64, I64, I64, I64, I64, I32, I32, ctypes.POINTER(PlanInfo)]),
+        "partir_last_plan_text": (ctypes.c_char_p, []),
+        "partir_trace_enable": (I32, [I32]),
+        "partir_trace_read": (I32, [ctypes.POINTER(TraceEntry), I32]),
+        "partir_trace_reset": (None, []),
+        "partir_status_string": (ctypes.c_char_p, [I32]),
+        "partir_last_error": (ctypes.c_char_p, []),
+        "partir_version": (ctypes.c_char_p, []),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(L, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = L
+    return L
+
+
+def _check(status: int):
+    if status != 0:
+        raise PartirError(status, lib().partir_last_error().decode())
+
+
+def _stream(stream):
+    import torch
+    if stream is None:
+        return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    if isinstance(stream, int):
+        return ctypes.c_void_p(stream)
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _dt(t) -> int:
+    import torch
+    if t.dtype == torch.bfloat16:
+        return BF16
+    if t.dtype == torch.float32:
+        return F32
+    raise PartirError(ERR["PARTIR_E_DTYPE"], f"unsupported tensor dtype {t.dtype}")
+
+
+def _tdt(code: int):
+    import torch
+    return torch.bfloat16 if code == BF16 else torch.float32
+
+
+def _rowmajor(t, name):
+    if t.dim() != 2 or t.stride(1) != 1:
+        raise PartirError(ERR["PARTIR_E_LAYOUT"], f"{name} must be a 2-D row-major tensor")
+    return t.stride(0)
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _workspace(nbytes: int, device, ws):
+    import torch
+    if nbytes == ctypes.c_size_t(-1).value:
+        # invalid arguments: the entry point itself reports the precise status
+        return None, 0
+    if nbytes == 0:
+        return None, 0
+    if ws is None:
+        ws = torch.empty(nbytes, dtype=torch.uint8, device=device)
+    return ws, ws.numel() * ws.element_size()
+
+
+def _axis(name):
+    return {None: AXIS_NONE, "M": AXIS_M, "N": AXIS_N, "K": AXIS_K}[name]
+
+
+# ---------------------------------------------------------------------------
+def loop_matmul(A, B, *, tile: Optional[str] = None, sum: Optional[str] = None, R: int = 1,
+                b_layout: str = "kn", out_dtype=None, sum_impl: str = "auto", out=None,
+                workspace=None, stream=None):
+    """C = A @ B as a loop over R virtual shards.  tile in {None, 'M', 'N'},
+    sum in {None, 'K'}.  b_layout 'kn': B is [K, N]; 'nk': B is given as B^T
+    [N, K]."""
+    import torch
+    M, K = A.shape
+    bl = B_KN if b_layout == "kn" else B_NK
+    N = B.shape[1] if bl == B_KN else B.shape[0]
+    ab = _dt(A)
+    cd = ab if out_dtype is None else (BF16 if out_dtype == torch.bfloat16 else F32)
+    if ab == F32:
+        cd = F32 if out_dtype is None else cd
+    si = {"auto": SUM_AUTO, "fused": SUM_FUSED, "splitk": SUM_SPLITK}[sum_impl]
+    if out is None:
+        out = torch.empty((M, N), dtype=_tdt(cd), device=A.device)
+    nbytes = lib().partir_loop_matmul_workspace(M, N, K, ab, cd, bl, _axis(tile), _axis(sum), R, si)
+    ws, wsb = _workspace(nbytes, A.device, workspace)
+    _check(lib().partir_loop_matmul(_ptr(A), _ptr(B), _ptr(out), M, N, K, _rowmajor(A, "A"), _rowmajor(B, "B"),
+                                    _rowmajor(out, "C"), ab, cd, bl, _axis(tile), _axis(sum), R, si,
+                                    _ptr(ws), wsb, _stream(stream)))
+    return out
+
+
+def mlp_block_workspace(T, D, F, out_dtype=F32, R_batch=1, R_model=1) -> int:
+    return lib().partir_mlp_block_workspace(T, D, F, out_dtype, R_batch, R_model)
+
+
+def mlp_block(X, W1t, W2t, *, b1=None, b2=None, R_batch: int = 1, R_model: int = 1, act: str = "gelu",
+              out_dtype=None, out=None, workspace=None, stream=None):
+    """Y = loop b[#tile<0>](R_batch){ loop m[#sum](R_model){ act(X_b W1[:, m] + b1_m) W2[m, :] } + b2 }.
+    W1t = W1^T [F, D], W2t = W2^T [D, F], all bf16."""
+    import torch
+    T, D = X.shape
+    F = W1t.shape[0]
+    od = F32 if out_dtype in (None, torch.float32) else BF16
+    if out is None:
+        out = torch.empty((T, D), dtype=_tdt(od), device=X.device)
+    ws, wsb = _workspace(mlp_block_workspace(T, D, F, od, R_batch, R_model), X.device, workspace)
+    _check(lib().partir_mlp_block(_ptr(X), _ptr(W1t), _ptr(b1), _ptr(W2t), _ptr(b2), _ptr(out), T, D, F,
+                                  _dt(X), od, ACT_GELU if act == "gelu" else ACT_NONE, R_batch, R_model,
+                                  _ptr(ws), wsb, _stream(stream)))
+    return out
+
+
+def attn_block_workspace(B, S, D, n_heads, d_head=128, R_batch=1, R_model=1) -> int:
+    return lib().partir_attn_block_workspace(B, S, D, n_heads, d_head, R_batch, R_model)
+
+
+def attn_block(X, Wq_t, Wk_t, Wv_t, Wo_t, *, B: int, S: int, n_heads: int, d_head: int = 128,
+               causal: bool = True, scale: float = 0.0, R_batch: int = 1, R_model: int = 1,
+               out_dtype=None, out=None, workspace=None, stream=None):
+    import torch
+    T, D = X.shape
+    od = F32 if out_dtype in (None, torch.float32) else BF16
+    if out is None:
+        out = torch.empty((T, D), dtype=_tdt(od), device=X.device)
+    ws, wsb = _workspace(attn_block_workspace(B, S, D, n_heads, d_head, R_batch, R_model), X.device, workspace)
+    _check(lib().partir_attn_block(_ptr(X), _ptr(Wq_t), _ptr(Wk_t), _ptr(Wv_t), _ptr(Wo_t), _ptr(out),
+                                   B, S, D, n_heads, d_head, int(causal), float(scale), _dt(X), od,
+                                   R_batch, R_model, _ptr(ws), wsb, _stream(stream)))
+    return out
+
+
+def decoder_layer_workspace(B, S, D, n_heads, d_head, F, R_batch=1, R_model=1) -> int:
+    return lib().partir_decoder_layer_workspace(B, S, D, n_heads, d_head, F, R_batch, R_model)
+
+
+def decoder_layer(x, g1, g2, Wq_t, Wk_t, Wv_t, Wo_t, W1t, W2t, *, B: int, S: int, n_heads: int,
+                  d_head: int = 128, eps: float = 1e-6, R_batch: int = 1, R_model: int = 1,
+                  workspace=None, stream=None):
+    """In place on the fp32 residual stream x [B*S, D]."""
+    T, D = x.shape
+    F = W1t.shape[0]
+    ws, wsb = _workspace(decoder_layer_workspace(B, S, D, n_heads, d_head, F, R_batch, R_model), x.device, workspace)
+    _check(lib().partir_decoder_layer(_ptr(x), _ptr(g1), _ptr(g2), float(eps), _ptr(Wq_t), _ptr(Wk_t), _ptr(Wv_t),
+                                      _ptr(Wo_t), _ptr(W1t), _ptr(W2t), B, S, D, n_heads, d_head, F,
+                                      R_batch, R_model, _ptr(ws), wsb, _stream(stream)))
+    return x
+
+
+# ---------------------------------------------------------------------------
+def _plan(fn, *args):
+    info = PlanInfo()
+    _check(fn(*args, ctypes.byref(info)))
+    d = info.as_dict()
+    d["text"] = lib().partir_last_plan_text().decode()
+    return d
+
+
+def plan_loop_matmul(M, N, K, ab=BF16, c=F32, b_layout=B_NK, tile=None, sum=None, R=1, sum_impl=SUM_AUTO):
+    return _plan(lib().partir_plan_loop_matmul, M, N, K, ab, c, b_layout, _axis(tile), _axis(sum), R, sum_impl)
+
+
+def plan_mlp_block(T, D, F, out_dtype=F32, R_batch=1, R_model=1):
+    return _plan(lib().partir_plan_mlp_block, T, D, F, out_dtype, R_batch, R_model)
+
+
+def plan_attn_block(B, S, D, n_heads, d_head=128, R_batch=1, R_model=1):
+    return _plan(lib().partir_plan_attn_block, B, S, D, n_heads, d_head, R_batch, R_model)
+
+
+def plan_decoder_layer(B, S, D, n_heads, d_head, F, R_batch=1, R_model=1):
+    return _plan(lib().partir_plan_decoder_layer, B, S, D, n_heads, d_head, F, R_batch, R_model)
+
+
+def trace_enable(on: bool = True):
+    _check(lib().partir_trace_enable(int(on)))
+
+
+def trace_reset():
+    lib().partir_trace_reset()
+
+
+def trace_read():
+    """{kernel name: (launches, total_ms)} since the last reset."""
+    n = lib().partir_trace_read(None, 0)
+    if n < 0:
+        raise PartirError(-n, lib().partir_last_error().decode())
+    buf = (TraceEntry * max(n, 1))()
+    n = lib().partir_trace_read(buf, n)
+    return {buf[i].name.decode(): (buf[i].launches, buf[i].total_ms) for i in range(n)}

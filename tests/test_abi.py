@@ -1,0 +1,238 @@
+"""Host-side tests of the C ABI: exports, validation, plans (no GPU needed).
+
+No call here passes validation without PARTIR_FAIL_LAUNCH=1, which makes the
+library return PARTIR_E_HIP before touching the GPU; pointers are dummies that
+are never dereferenced.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2401_11202_amd import partir as P
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+DUMMY = ctypes.c_void_p(0x10000)      # 16-byte aligned, never dereferenced
+DUMMY_ODD = ctypes.c_void_p(0x10004)  # misaligned
+NULL = None
+
+
+@pytest.fixture(autouse=True)
+def _never_launch(monkeypatch):
+    """Should a case pass validation by mistake, it still stops before the GPU."""
+    monkeypatch.setenv("PARTIR_FAIL_LAUNCH", "1")
+
+
+def declared_functions():
+    text = open(os.path.join(ROOT, "include", "partir.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(partir_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    L = P.lib()
+    names = declared_functions()
+    assert len(names) >= 19
+    for n in names:
+        assert hasattr(L, n), n
+    assert set(P.EXPORTS) == set(names)
+
+
+def test_status_strings():
+    L = P.lib()
+    for code, name in P.STATUS.items():
+        assert L.partir_status_string(code).decode() == name
+    assert P.lib().partir_version().decode().startswith("libpartir")
+
+
+# ---------------------------------------------------------------------------
+# loop_matmul validation
+# ---------------------------------------------------------------------------
+def mm(M=256, N=256, K=512, lda=None, ldb=None, ldc=None, ab=P.F32, c=P.F32, bl=P.B_KN,
+       tile=P.AXIS_NONE, summ=P.AXIS_K, R=4, impl=P.SUM_AUTO, A=DUMMY, B=DUMMY, C=DUMMY,
+       ws=DUMMY, ws_bytes=1 << 30):
+    lda = K if lda is None else lda
+    ldb = (N if bl == P.B_KN else K) if ldb is None else ldb
+    ldc = N if ldc is None else ldc
+    return P.lib().partir_loop_matmul(A, B, C, M, N, K, lda, ldb, ldc, ab, c, bl, tile, summ, R, impl,
+                                      ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kwargs,status", [
+    (dict(A=NULL), "PARTIR_E_NULL"),
+    (dict(C=NULL), "PARTIR_E_NULL"),
+    (dict(M=0), "PARTIR_E_SHAPE"),
+    (dict(K=-4), "PARTIR_E_SHAPE"),
+    (dict(R=0), "PARTIR_E_UNSUPPORTED"),
+    (dict(R=3), "PARTIR_E_DIVISIBILITY"),                          # 3 does not divide K = 512
+    (dict(tile=P.AXIS_M, summ=P.AXIS_NONE, M=250, R=4), "PARTIR_E_DIVISIBILITY"),
+    (dict(tile=P.AXIS_N, summ=P.AXIS_NONE, N=100, R=8), "PARTIR_E_DIVISIBILITY"),
+    (dict(tile=P.AXIS_K, summ=P.AXIS_NONE), "PARTIR_E_AXIS"),       # a contracted dim cannot be tiled
+    (dict(tile=P.AXIS_M, summ=P.AXIS_M), "PARTIR_E_AXIS"),          # one axis tiled and summed
+    (dict(summ=P.AXIS_N), "PARTIR_E_AXIS"),
+    (dict(tile=7), "PARTIR_E_AXIS"),
+    (dict(ab=5), "PARTIR_E_DTYPE"),
+    (dict(ab=P.F32, c=P.BF16), "PARTIR_E_DTYPE"),
+    (dict(lda=500), "PARTIR_E_LAYOUT"),                              # lda < K
+    (dict(ldc=258), "PARTIR_E_LAYOUT"),                              # rows not 16-byte aligned
+    (dict(A=DUMMY_ODD), "PARTIR_E_LAYOUT"),
+    (dict(K=510, R=2, lda=512), "PARTIR_E_LAYOUT"),                  # K not a whole 16-byte run
+    (dict(ab=P.BF16, c=P.BF16, bl=P.B_NK, K=520, R=4, lda=520), "PARTIR_E_LAYOUT"),  # K/R = 130
+    (dict(ws_bytes=16), "PARTIR_E_WORKSPACE"),
+    (dict(ws=NULL), "PARTIR_E_NULL"),
+    (dict(impl=9), "PARTIR_E_UNSUPPORTED"),
+    (dict(ab=P.BF16, bl=P.B_KN), "PARTIR_E_UNSUPPORTED"),
+])
+def test_loop_matmul_validation(kwargs, status):
+    st = mm(**kwargs)
+    assert P.STATUS[st] == status, P.lib().partir_last_error().decode()
+    assert P.lib().partir_last_error().decode().startswith(status)
+
+
+def test_valid_call_reaches_launch(monkeypatch):
+    monkeypatch.setenv("PARTIR_FAIL_LAUNCH", "1")
+    assert P.STATUS[mm()] == "PARTIR_E_HIP"
+    assert "PARTIR_FAIL_LAUNCH" in P.lib().partir_last_error().decode()
+    assert P.STATUS[mm(ab=P.BF16, c=P.BF16, bl=P.B_NK, tile=P.AXIS_N, summ=P.AXIS_NONE, R=8)] == "PARTIR_E_HIP"
+
+
+def test_error_message_is_thread_local():
+    import threading
+    mm(R=3)
+    msg = {}
+
+    def other():
+        mm(M=0)
+        msg["t"] = P.lib().partir_last_error().decode()
+
+    t = threading.Thread(target=other)
+    t.start()
+    t.join()
+    assert msg["t"].startswith("PARTIR_E_SHAPE")
+    assert P.lib().partir_last_error().decode().startswith("PARTIR_E_DIVISIBILITY")
+
+
+# ---------------------------------------------------------------------------
+# block validation
+# ---------------------------------------------------------------------------
+def mlp(T=512, D=256, F=1024, ind=P.BF16, out=P.F32, act=P.ACT_GELU, Rb=1, Rm=8, X=DUMMY, Y=DUMMY,
+        ws=DUMMY, ws_bytes=1 << 30):
+    return P.lib().partir_mlp_block(X, DUMMY, None, DUMMY, None, Y, T, D, F, ind, out, act, Rb, Rm,
+                                    ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kwargs,status", [
+    (dict(X=NULL), "PARTIR_E_NULL"),
+    (dict(T=0), "PARTIR_E_SHAPE"),
+    (dict(Rm=0), "PARTIR_E_UNSUPPORTED"),
+    (dict(Rm=3), "PARTIR_E_DIVISIBILITY"),
+    (dict(Rb=3), "PARTIR_E_DIVISIBILITY"),
+    (dict(ind=P.F32), "PARTIR_E_DTYPE"),
+    (dict(out=4), "PARTIR_E_DTYPE"),
+    (dict(act=5), "PARTIR_E_UNSUPPORTED"),
+    (dict(D=252), "PARTIR_E_LAYOUT"),
+    (dict(F=1024 + 32, Rm=8), "PARTIR_E_LAYOUT"),   # F/R = 132 is not a multiple of 8
+    (dict(ws_bytes=100), "PARTIR_E_WORKSPACE"),
+])
+def test_mlp_validation(kwargs, status):
+    assert P.STATUS[mlp(**kwargs)] == status, P.lib().partir_last_error().decode()
+
+
+def attn(B=2, S=256, D=1024, H=8, dh=128, Rb=1, Rm=8, out=P.F32, ws_bytes=1 << 30, X=DUMMY):
+    return P.lib().partir_attn_block(X, DUMMY, DUMMY, DUMMY, DUMMY, DUMMY, B, S, D, H, dh, 1, 0.0,
+                                     P.BF16, out, Rb, Rm, DUMMY, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kwargs,status", [
+    (dict(X=NULL), "PARTIR_E_NULL"),
+    (dict(H=6), "PARTIR_E_SHAPE"),               # 6 * 128 != 1024
+    (dict(D=512, H=8, dh=64), "PARTIR_E_SHAPE"),  # d_head must be 128
+    (dict(S=200), "PARTIR_E_SHAPE"),
+    (dict(Rm=3), "PARTIR_E_DIVISIBILITY"),
+    (dict(Rb=4, B=2), "PARTIR_E_DIVISIBILITY"),   # batch shards hold whole sequences
+    (dict(ws_bytes=0), "PARTIR_E_WORKSPACE"),
+])
+def test_attn_validation(kwargs, status):
+    assert P.STATUS[attn(**kwargs)] == status, P.lib().partir_last_error().decode()
+
+
+def test_decoder_validation():
+    L = P.lib()
+    st = L.partir_decoder_layer(DUMMY, DUMMY, DUMMY, 1e-6, DUMMY, DUMMY, DUMMY, DUMMY, DUMMY, DUMMY,
+                                2, 256, 1024, 8, 128, 1002, 2, 4, DUMMY, 1 << 34, None)
+    assert P.STATUS[st] == "PARTIR_E_DIVISIBILITY"   # 4 does not divide F = 1002
+    st = L.partir_decoder_layer(DUMMY, DUMMY, DUMMY, 1e-6, DUMMY, DUMMY, DUMMY, DUMMY, DUMMY, DUMMY,
+                                2, 256, 1024, 8, 128, 1000, 2, 4, DUMMY, 1 << 34, None)
+    assert P.STATUS[st] == "PARTIR_E_LAYOUT"         # F/R = 250 is not a whole 16-byte run
+    st = L.partir_decoder_layer(DUMMY, DUMMY, DUMMY, -1.0, DUMMY, DUMMY, DUMMY, DUMMY, DUMMY, DUMMY,
+                                2, 256, 1024, 8, 128, 1728, 2, 4, DUMMY, 1 << 34, None)
+    assert P.STATUS[st] == "PARTIR_E_SHAPE"
+    st = L.partir_decoder_layer(None, DUMMY, DUMMY, 1e-6, DUMMY, DUMMY, DUMMY, DUMMY, DUMMY, DUMMY,
+                                2, 256, 1024, 8, 128, 1728, 2, 4, DUMMY, 1 << 34, None)
+    assert P.STATUS[st] == "PARTIR_E_NULL"
+
+
+def test_blocks_reach_launch(monkeypatch):
+    monkeypatch.setenv("PARTIR_FAIL_LAUNCH", "1")
+    assert P.STATUS[mlp()] == "PARTIR_E_HIP"
+    assert P.STATUS[attn()] == "PARTIR_E_HIP"
+    st = P.lib().partir_decoder_layer(DUMMY, DUMMY, DUMMY, 1e-6, DUMMY, DUMMY, DUMMY, DUMMY, DUMMY, DUMMY,
+                                      2, 256, 1024, 8, 128, 1728, 2, 4, DUMMY, 1 << 34, None)
+    assert P.STATUS[st] == "PARTIR_E_HIP"
+
+
+# ---------------------------------------------------------------------------
+# plans: the in-device stand-ins of the lowering's collectives
+# ---------------------------------------------------------------------------
+def test_megatron_mlp_has_exactly_one_sum_per_block():
+    """Megatron: one all_reduce per MLP block in the forward pass (Sec. 2.3;
+    Sec. 6.1 lowered program) -> exactly one in-device #sum."""
+    p = P.plan_mlp_block(8192, 4096, 16384, R_batch=1, R_model=8)
+    assert p["n_sum_loops"] == 1 and p["n_virtual_shards"] == 8 and p["n_launches"] == 2
+    assert p["n_sum_splitk"] == 0          # 512 output tiles: fused accumulation, no partials
+    assert p["workspace_bytes"] == 8192 * 16384 * 2
+    assert p["flops"] == 4.0 * 8192 * 4096 * 16384
+
+
+def test_batch_only_mlp_has_no_reduction_across_shards():
+    p = P.plan_mlp_block(16384, 8192, 32768, R_batch=4, R_model=1)
+    assert p["n_sum_loops"] == 0 and p["n_virtual_shards"] == 4
+
+
+def test_two_axis_nest_plans():
+    p = P.plan_mlp_block(16384, 8192, 32768, R_batch=4, R_model=8)
+    assert p["n_virtual_shards"] == 32 and p["n_sum_loops"] == 1 and p["n_tile_loops"] == 2
+    assert "#tile M x4" in p["text"] and "#sum K x8" in p["text"]
+
+
+def test_attention_and_decoder_sums():
+    a = P.plan_attn_block(4, 2048, 4096, 32, 128, 1, 8)
+    assert a["n_sum_loops"] == 1 and a["n_launches"] == 3 and a["n_virtual_shards"] == 8
+    d = P.plan_decoder_layer(4, 2048, 5120, 40, 128, 13824, 2, 4)
+    # two #sum loops per layer (attention out-projection and FFN down): Megatron's 2 all_reduces
+    assert d["n_sum_loops"] == 2 and d["n_virtual_shards"] == 8 and d["n_launches"] == 7
+
+
+def test_small_output_uses_split_partials():
+    p = P.plan_loop_matmul(256, 256, 512, ab=P.F32, c=P.F32, b_layout=P.B_KN, sum="K", R=4)
+    assert p["n_sum_splitk"] == 1 and p["n_launches"] == 2 and p["workspace_bytes"] == 4 * 256 * 256 * 4
+    f = P.plan_loop_matmul(256, 256, 512, ab=P.F32, c=P.F32, b_layout=P.B_KN, sum="K", R=4,
+                           sum_impl=P.SUM_FUSED)
+    assert f["n_sum_splitk"] == 0 and f["n_launches"] == 1 and f["workspace_bytes"] == 0
+
+
+def test_workspace_queries_match_plans():
+    L = P.lib()
+    assert L.partir_mlp_block_workspace(8192, 4096, 16384, P.F32, 1, 8) == \
+        P.plan_mlp_block(8192, 4096, 16384, R_model=8)["workspace_bytes"]
+    assert L.partir_attn_block_workspace(4, 2048, 4096, 32, 128, 1, 8) == \
+        P.plan_attn_block(4, 2048, 4096, 32, 128, 1, 8)["workspace_bytes"]
+    assert L.partir_mlp_block_workspace(8192, 4096, 16383, P.F32, 1, 8) == ctypes.c_size_t(-1).value
+
+
+def test_plan_text_names_every_shard_loop():
+    p = P.plan_decoder_layer(4, 2048, 5120, 40, 128, 13824, 2, 4)
+    t = p["text"]
+    assert t.count("rmsnorm") == 2 and "attention" in t and t.count("fused in accumulator") == 2
+    assert "#tile N x4 (cols 3456/shard)" in t

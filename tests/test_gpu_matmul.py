@@ -1,0 +1,144 @@
+"""GPU parity of partir_loop_matmul against the oracle (fp32 and bf16 paths).
+
+Every call goes through the C ABI (ctypes binding).  Element-by-element
+comparison with the oracle's shard interpreter on the same seeded inputs; the
+measure is max |C_gpu - C_ref| / (|A|.|B|).
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import partir_oracle as O
+from paper_2401_11202_amd import inputs as I
+from paper_2401_11202_amd import partir as P
+from paper_2401_11202_amd import workloads as W
+from tests.gpu_common import TOL_BF16, TOL_F32, accum_bound, host, say
+
+pytestmark = pytest.mark.gpu
+
+AX = {None: O.AXIS_NONE, "M": O.AXIS_M, "N": O.AXIS_N, "K": O.AXIS_K}
+
+
+def run(A, B, tile, summ, R, b_layout, out_dtype=None, sum_impl="auto"):
+    Ad = A.to_device()
+    Bd = (B if b_layout == "kn" else I.transposed(B)).to_device()
+    C = P.loop_matmul(Ad, Bd, tile=tile, sum=summ, R=R, b_layout=b_layout, out_dtype=out_dtype,
+                      sum_impl=sum_impl)
+    torch.cuda.synchronize()
+    return C
+
+
+def check(A, B, C, tile, summ, R, tol):
+    ref = O.loop_matmul(A.f64(), B.f64(), AX[tile], AX[summ], R)
+    norm = O.abs_product(A.f64(), B.f64())
+    err = O.normalised_error(host(C), ref, norm)
+    say(f"    max normalised error {err:.3e} (tol {tol:g})")
+    assert err <= tol
+    return err
+
+
+# ---------------------------------------------------------------------------
+def test_f32_sum_over_K_R4_full_size():
+    """C[256,256] = A[256,512] B[512,256], #sum over K with 4 shards of 128."""
+    w = W.WORKLOADS["matmul_f32_sumK"]
+    x = W.make_inputs(w)
+    for impl in ("auto", "fused", "splitk"):
+        say(f"f32 256x256x512 sum K R=4 impl={impl}")
+        C = run(x["A"], x["B"], None, "K", 4, "kn", sum_impl=impl)
+        err = check(x["A"], x["B"], C, None, "K", 4, TOL_F32)
+        assert err <= accum_bound(512)
+
+
+@pytest.mark.parametrize("b_layout", ["kn", "nk"])
+@pytest.mark.parametrize("tile,summ,R", [(None, None, 1), ("M", None, 4), ("N", None, 4), (None, "K", 4),
+                                         ("M", "K", 2), ("N", "K", 4), (None, "K", 1)])
+def test_f32_modes_ragged(tile, summ, R, b_layout):
+    M, N, K = 200, 144, 80          # ragged against the 64-wide tiles
+    A = I.gaussian(101, 0, (M, K), 1.0, "f32")
+    B = I.gaussian(101, 1, (K, N), 1.0, "f32")
+    for impl in ("fused", "splitk"):
+        say(f"f32 {M}x{N}x{K} tile={tile} sum={summ} R={R} {b_layout} {impl}")
+        C = run(A, B, tile, summ, R, b_layout, sum_impl=impl)
+        check(A, B, C, tile, summ, R, TOL_F32)
+
+
+@pytest.mark.parametrize("out", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("tile,summ,R", [(None, None, 1), ("M", None, 4), ("N", None, 4), (None, "K", 4),
+                                         ("M", "K", 4), ("N", "K", 2), (None, "K", 8)])
+def test_bf16_modes_ragged(tile, summ, R, out):
+    M, N, K = 600, 528, 448         # several 256-wide tiles with ragged tails
+    A = I.gaussian(102, 0, (M, K), 1.0, "bf16")
+    B = I.gaussian(102, 1, (K, N), K ** -0.5, "bf16")
+    for impl in ("fused", "splitk"):
+        say(f"bf16 {M}x{N}x{K} tile={tile} sum={summ} R={R} out={out} {impl}")
+        C = run(A, B, tile, summ, R, "nk", out_dtype=out, sum_impl=impl)
+        err = check(A, B, C, tile, summ, R, TOL_BF16)
+        # fp32 accumulation of exact bf16 products (+ one bf16 rounding of the output)
+        bound = accum_bound(K) + (2.0 ** -8 if out == torch.bfloat16 else 0.0)
+        assert err <= bound
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_integer_inputs_are_bitwise_exact(dtype):
+    """Products and partial sums of small integers are exact in fp32, so every
+    shard decomposition must reproduce the unpartitioned product bit for bit."""
+    M, N, K = 320, 272, 512
+    A = I.small_ints(103, 0, (M, K), dtype=dtype)
+    B = I.small_ints(103, 1, (K, N), dtype=dtype)
+    ref = O.matmul(A.f64(), B.f64())
+    bl = "kn" if dtype == "f32" else "nk"
+    for tile, summ, R in [(None, None, 1), ("M", None, 4), ("N", None, 4), (None, "K", 8), ("M", "K", 4)]:
+        for impl in ("fused", "splitk"):
+            say(f"integer {dtype} tile={tile} sum={summ} R={R} {impl}")
+            C = run(A, B, tile, summ, R, bl, out_dtype=torch.float32, sum_impl=impl)
+            assert np.array_equal(host(C), ref)
+
+
+def test_results_are_deterministic():
+    A = I.gaussian(104, 0, (512, 1024), 1.0, "bf16")
+    B = I.gaussian(104, 1, (1024, 512), 1.0 / 32, "bf16")
+    for impl in ("fused", "splitk"):
+        c1 = run(A, B, None, "K", 8, "nk", out_dtype=torch.float32, sum_impl=impl)
+        c2 = run(A, B, None, "K", 8, "nk", out_dtype=torch.float32, sum_impl=impl)
+        assert torch.equal(c1, c2)
+
+
+def test_shards_write_only_their_slices():
+    """Guard bands: C is a view into a larger canary-filled buffer; nothing
+    outside the [M, N] window may change."""
+    M, N, K = 300, 272, 128
+    A = I.gaussian(105, 0, (M, K), 1.0, "bf16")
+    B = I.gaussian(105, 1, (K, N), 0.1, "bf16")
+    Ad, Bt = A.to_device(), I.transposed(B).to_device()
+    for tile, summ, R in [("M", None, 4), ("N", None, 4), (None, "K", 4)]:
+        for impl in ("fused", "splitk"):
+            big = torch.full((M + 40, N + 48), 1234.5, dtype=torch.float32, device="cuda")
+            view = big[16:16 + M, 8:8 + N]
+            P.loop_matmul(Ad, Bt, tile=tile, sum=summ, R=R, b_layout="nk", out_dtype=torch.float32,
+                          sum_impl=impl, out=view)
+            torch.cuda.synchronize()
+            mask = torch.ones_like(big, dtype=torch.bool)
+            mask[16:16 + M, 8:8 + N] = False
+            assert torch.all(big[mask] == 1234.5), (tile, summ, impl)
+            err = O.normalised_error(host(view), O.matmul(A.f64(), B.f64()), O.abs_product(A.f64(), B.f64()))
+            assert err <= TOL_BF16
+
+
+def test_fused_and_split_sum_agree():
+    A = I.gaussian(106, 0, (512, 2048), 1.0, "bf16")
+    B = I.gaussian(106, 1, (2048, 768), 2048 ** -0.5, "bf16")
+    f = run(A, B, None, "K", 8, "nk", out_dtype=torch.float32, sum_impl="fused")
+    s = run(A, B, None, "K", 8, "nk", out_dtype=torch.float32, sum_impl="splitk")
+    norm = O.abs_product(A.f64(), B.f64())
+    assert O.normalised_error(host(f), host(s), norm) <= 2 * accum_bound(2048)
+
+
+def test_validation_errors_leave_output_untouched():
+    A = torch.ones((64, 96), dtype=torch.float32, device="cuda")
+    B = torch.ones((96, 64), dtype=torch.float32, device="cuda")
+    C = torch.full((64, 64), 7.0, device="cuda")
+    with pytest.raises(P.PartirError) as e:
+        P.loop_matmul(A, B, sum="K", R=5, out=C)
+    assert e.value.status == P.ERR["PARTIR_E_DIVISIBILITY"]
+    torch.cuda.synchronize()
+    assert torch.all(C == 7.0)
