@@ -1,11 +1,15 @@
 // bf16 MFMA GEMM for gfx950: C = A . B^T with both operands K-contiguous.
 //
-// One workgroup computes a 256x256 output tile of one virtual shard with four
-// waves (2 x 2), each owning a 128x128 sub-tile as 4 x 4 accumulators of
-// v_mfma_f32_32x32x16_bf16.  K advances in 64-wide steps through a
-// double-buffered LDS stage (A and B tiles, 32 KiB each) filled from
-// registers; global loads are raw buffer loads whose out-of-range lanes read
-// zero, which covers ragged M / N / K edges without branches.
+// One workgroup computes a 256x256 output tile of one virtual shard with eight
+// waves (2 x 4, two per SIMD), each owning a 128x64 sub-tile as 4 x 2
+// accumulators of v_mfma_f32_32x32x16_bf16; while one wave of a SIMD waits on
+// memory the other keeps the matrix core busy.  K advances in 64-wide tiles
+// through two LDS stages of 64 KiB filled by buffer loads that write LDS
+// directly (no register staging): the loads for tile t+2 are issued in the
+// middle of tile t, after every wave has finished reading the stage they
+// overwrite.  Out-of-range lanes (ragged M / N / K edges, tiles past the end)
+// read as zeros.  The 256x256 tile is the largest whose fp32 accumulators fit
+// the register file, which keeps L2 -> LDS traffic per FLOP minimal.
 //
 // Loop semantics realised here (PartIR:Core, Sec. 5 / App. C):
 //  * #tile over M or N: the grid enumerates every shard's tiles; a tile never
@@ -13,7 +17,7 @@
 //  * #sum over K, fused: the shards' K-ranges are consecutive, so one tile's
 //    K loop walks shard 0, 1, ..., R-1 in order into one accumulator.
 //  * #sum over K, split: the grid also enumerates the K shards and each writes
-//    its own fp32 partial; an ordered reduction (splitk_reduce.hip) sums them.
+//    its own fp32 partial; an ordered reduction (elementwise.hip) sums them.
 #include "kernels.h"
 
 namespace partir {
@@ -25,27 +29,47 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int BM = 256, BN = 256, BK = 64, NT = 256;
-constexpr int STAGE = (BM + BN) * BK * 2;       // bytes of one LDS stage
+constexpr int BM = 256, BN = 256, NT = 512;
+constexpr int BK = 64, NS = 2;
 constexpr uint32_t OOB = 0x80000000u;          // offset that reads as zero
+typedef __attribute__((address_space(3))) void lds_void;
 
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)OOB, 0x00020000);
+// Buffer descriptor of a workgroup-uniform base pointer (kept in SGPRs); any
+// offset at or beyond `bytes` reads as zero.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint32_t bytes) {
+  const uint64_t a = (uint64_t)p;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)a);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(a >> 32));
+  void* u = (void*)(((uint64_t)hi << 32) | lo);
+  return __builtin_amdgcn_make_buffer_rsrc(u, (short)0, (int)__builtin_amdgcn_readfirstlane(bytes), 0x00020000);
 }
+
+template <typename T>
+__device__ __forceinline__ T pick3(int g, T a, T b, T c) { return g == 0 ? a : (g == 1 ? b : c); }
 
 __device__ __forceinline__ float gelu_erf(float x) {
   return 0.5f * x * (1.0f + erff(x * 0.70710678118654752f));
 }
 
+// LDS tile layout: [row][64 k] = 128-byte rows of eight 16-byte chunks; chunk
+// c of row r sits at position c ^ swz(r), swz(r) = (r & 7) ^ ((r >> 3) & 1),
+// which spreads the 32 rows one MFMA operand read touches over all banks.
+__device__ __forceinline__ int swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
+
+// s_waitcnt with only the vector-memory counter constrained (gfx9 encoding)
+#define WAIT_VMCNT(n) __builtin_amdgcn_s_waitcnt((((n) & 15) | (((n) >> 4) << 14)) | (0x7 << 4) | (0xF << 8))
+
 template <int EPI, int ACT>
-__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(1, 1)))
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void gemm_bf16_kernel(GemmParams p) {
-  __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
+  constexpr int OPB = BM * BK * 2, STAGE = 2 * OPB, KK = BK / 16, RB = 1024 / (BK * 2) /* rows per 1 KiB */;
+  constexpr int CPR = BK / 8;   // 16-byte chunks per row
+  __shared__ __attribute__((aligned(1024))) char smem[NS * STAGE];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave >> 2, wn = wave & 3;
 
   // ---- which tile of which virtual shard ----------------------------------
   const int ntiles = p.tiles_m * p.tiles_n;
@@ -75,108 +99,124 @@ void gemm_bf16_kernel(GemmParams p) {
   const int k_begin = (p.nsplit > 1) ? split * p.ks : 0;
   const int k_end = (p.nsplit > 1) ? k_begin + p.ks : p.K;
 
-  // ---- global -> register loads (8 x 16 B of A and of B per thread) -----------
-  const __amdgpu_buffer_rsrc_t ra = make_rsrc(p.A + (int64_t)row0 * p.lda);
-  const __amdgpu_buffer_rsrc_t rb = make_rsrc(p.B[grp] + (int64_t)col0 * p.ldb);
-  const int lr = tid >> 3;   // tile row 0..31 (+32 i)
-  const int lc = tid & 7;    // 16-byte chunk of the 64-wide K step
-  uint32_t a_off[8], b_off[8];
-  uint32_t a_ok = 0, b_ok = 0;
+  // ---- global -> LDS loads ----------------------------------------------------
+  // Per k tile each wave issues 4 + 4 wave-wide 16-byte loads; load j of wave
+  // w fills rows 64 j + 8 w .. +8 of the operand tile (1 KiB of LDS written
+  // lane by lane).  Lane L takes row +L/8, LDS chunk L%8, i.e. global chunk
+  // (L%8) ^ swz(row).  One descriptor per 64-row block bounds the valid rows.
+  const uint16_t* Bg = pick3(grp, p.B[0], p.B[1], p.B[2]);
+  const uint16_t* At = p.A + (int64_t)row0 * p.lda;
+  const uint16_t* Btile = Bg + (int64_t)col0 * p.ldb;
+  constexpr int NJ = BM / (8 * RB);   // wave loads per operand per k tile
+  constexpr int BLK = 8 * RB;          // rows covered by one load of all 8 waves
+  __amdgpu_buffer_rsrc_t ra[NJ], rb[NJ];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const int r = lr + 32 * i;
-    a_off[i] = (uint32_t)(r * p.lda * 2 + lc * 16);
-    b_off[i] = (uint32_t)(r * p.ldb * 2 + lc * 16);
-    a_ok |= (uint32_t)(r < rows) << i;
-    b_ok |= (uint32_t)(r < cols) << i;
+  for (int j = 0; j < NJ; ++j) {
+    const int va = min(max(rows - BLK * j, 0), BLK), vb = min(max(cols - BLK * j, 0), BLK);
+    ra[j] = make_rsrc(At + (int64_t)BLK * j * p.lda, (uint32_t)(va * p.lda * 2));
+    rb[j] = make_rsrc(Btile + (int64_t)BLK * j * p.ldb, (uint32_t)(vb * p.ldb * 2));
   }
-  // LDS tiles are [row][64 k] with the 16-byte chunk index XOR-swizzled by
-  // swz(row) = (row & 7) ^ ((row >> 3) & 1), so the 32 rows one MFMA operand
-  // read touches spread over all banks.
-  const int st_off = lr * 128 + ((lc ^ ((lr & 7) ^ ((lr >> 3) & 1))) << 4);
-
-  i32x4 sa[8], sb[8];
-  auto gload = [&](int kt) {
+  const int lrow = RB * wave + lane / CPR;
+  const int lchunk = (lane % CPR) ^ swz(lrow);
+  const uint32_t a_voff = (uint32_t)(lrow * p.lda * 2 + lchunk * 16);
+  const uint32_t b_voff = (uint32_t)(lrow * p.ldb * 2 + lchunk * 16);
+  const int lds_w = wave * 1024;
+  const int nk = (k_end - k_begin + BK - 1) / BK;
+  auto gload = [&](int kt, int stage) {
     const int kb = k_begin + kt * BK;
-    const bool kv = kb + lc * 8 < k_end;
+    const uint32_t kmask = (kb + lchunk * 8 < k_end) ? 0u : OOB;   // ragged K tail / past the end
     const uint32_t so = (uint32_t)kb * 2;
+    char* base = smem + stage * STAGE + lds_w;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const uint32_t va = (kv && ((a_ok >> i) & 1)) ? a_off[i] : OOB;
-      const uint32_t vb = (kv && ((b_ok >> i) & 1)) ? b_off[i] : OOB;
-      sa[i] = __builtin_amdgcn_raw_buffer_load_b128(ra, va, so, 0);
-      sb[i] = __builtin_amdgcn_raw_buffer_load_b128(rb, vb, so, 0);
-    }
-  };
-  auto lstore = [&](int buf) {
-    char* as = smem + buf * STAGE;
-    char* bs = as + BM * BK * 2;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      *(i32x4*)(as + st_off + i * 4096) = sa[i];
-      *(i32x4*)(bs + st_off + i * 4096) = sb[i];
+    for (int j = 0; j < NJ; ++j) {
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(ra[j], (lds_void*)(base + j * 8192), 16, a_voff | kmask, so, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rb[j], (lds_void*)(base + OPB + j * 8192), 16, b_voff | kmask, so, 0, 0);
     }
   };
 
   // ---- MFMA operand reads -----------------------------------------------------
   const int h = lane >> 5;
-  const int swz = (lane & 7) ^ ((lane >> 3) & 1);
-  const int a_rd = (wm * 128 + (lane & 31)) * 128;
-  const int b_rd = (wn * 128 + (lane & 31)) * 128;
+  const int fsw = swz(lane & 31);
+  const int a_rd = (wm * 128 + (lane & 31)) * BK * 2;
+  const int b_rd = OPB + (wn * 64 + (lane & 31)) * BK * 2;
 
-  f32x16 acc[4][4];
+  f32x16 acc[4][2];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < 2; ++j)
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
 
-  auto compute = [&](int buf) {
-    const char* as = smem + buf * STAGE;
-    const char* bs = as + BM * BK * 2;
+  // fragments of one 16-wide k step: 4 A row blocks and 2 B row blocks
+  bf16x8 fa0[4], fb0[2], fa1[4], fb1[2];
+  auto ldfrag = [&](int stage, int kk, bf16x8* a, bf16x8* b) {
+    const char* st = smem + stage * STAGE;
+    const int ko = ((2 * kk + h) ^ fsw) << 4;
 #pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
-      const int ko = ((2 * kk + h) ^ swz) << 4;
-      bf16x8 a[4], b[4];
+    for (int i = 0; i < 4; ++i) a[i] = *(const bf16x8*)(st + a_rd + i * 32 * BK * 2 + ko);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) a[i] = *(const bf16x8*)(as + a_rd + i * 4096 + ko);
-#pragma unroll
-      for (int j = 0; j < 4; ++j) b[j] = *(const bf16x8*)(bs + b_rd + j * 4096 + ko);
-      // B as the first operand: each lane ends up holding 4 consecutive
-      // output columns of one output row.
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b[j], a[i], acc[i][j], 0, 0, 0);
-    }
+    for (int j = 0; j < 2; ++j) b[j] = *(const bf16x8*)(st + b_rd + j * 32 * BK * 2 + ko);
   };
+  // B as the first operand: each lane ends up holding 4 consecutive output
+  // columns of one output row.
+  auto mma = [&](const bf16x8* a, const bf16x8* b) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b[j], a[i], acc[i][j], 0, 0, 0);
+  };
+  // instruction interleaving hints: mask bits MFMA 0x8, VMEM read 0x20, DS read 0x100
+#define SGB(mask, n) __builtin_amdgcn_sched_group_barrier(mask, n, 0)
 
-  const int nk = (k_end - k_begin + BK - 1) / BK;
-  gload(0);
-  lstore(0);
+  constexpr int LPS = 2 * NJ;   // wave loads per k tile
+  // prologue: both stages in flight, then wait for tile 0.  In the loop, the
+  // first KK-1 steps of a tile read the next step's fragments while their
+  // MFMAs run; then (tile kt+1 landed, every wave done with this stage) the
+  // stage is refilled with tile kt+2 and the next tile's first fragments are
+  // read during the last step.
+#pragma unroll
+  for (int s = 0; s < NS; ++s) gload(s, s);
+  WAIT_VMCNT(LPS * (NS - 1));
   __syncthreads();
+  ldfrag(0, 0, fa0, fb0);
+  int stage = 0;
   for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < nk) gload(kt + 1);
-    compute(cur);
-    if (kt + 1 < nk) lstore(cur ^ 1);
+    const int next = (stage + 1 == NS) ? 0 : stage + 1;
+#pragma unroll
+    for (int kk = 0; kk < KK - 1; ++kk) {
+      if (kk & 1) { ldfrag(stage, kk + 1, fa0, fb0); mma(fa1, fb1); }
+      else { ldfrag(stage, kk + 1, fa1, fb1); mma(fa0, fb0); }
+#pragma unroll
+      for (int i = 0; i < 6; ++i) { SGB(0x8, 1); SGB(0x100, 1); }
+      SGB(0x8, 2);
+    }
+    WAIT_VMCNT(LPS * (NS - 2));
     __syncthreads();
+    gload(kt + NS, stage);
+    if ((KK - 1) & 1) { ldfrag(next, 0, fa0, fb0); mma(fa1, fb1); }
+    else { ldfrag(next, 0, fa1, fb1); mma(fa0, fb0); }
+#pragma unroll
+    for (int i = 0; i < 6; ++i) { SGB(0x8, 1); SGB(0x100, 1); SGB(0x20, 1); }
+    SGB(0x8, 2);
+    stage = next;
   }
+#undef SGB
 
   // ---- epilogue: lane holds C[m][n..n+3] for each (i, j, g) ---------------------
-  const float* bias = p.bias[grp];
+  const float* bias = pick3(grp, p.bias[0], p.bias[1], p.bias[2]);
+  void* Cg = pick3(grp, p.C[0], p.C[1], p.C[2]);
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int ml = wm * 128 + i * 32 + (lane & 31);
     if (ml >= rows) continue;
     const int64_t m = row0 + ml;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < 2; ++j) {
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        const int nl = wn * 128 + j * 32 + 8 * g + 4 * h;
+        const int nl = wn * 64 + j * 32 + 8 * g + 4 * h;
         if (nl >= cols) continue;
         const int64_t n = col0 + nl;
         f32x4 v = {acc[i][j][4 * g + 0], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]};
@@ -194,12 +234,12 @@ void gemm_bf16_kernel(GemmParams p) {
         }
         if (EPI == EPI_BF16) {
           bf16x4 o = {(__bf16)v[0], (__bf16)v[1], (__bf16)v[2], (__bf16)v[3]};
-          *(bf16x4*)((uint16_t*)p.C[grp] + m * p.ldc + n) = o;
+          *(bf16x4*)((uint16_t*)Cg + m * p.ldc + n) = o;
         } else if (EPI == EPI_F32) {
-          *(f32x4*)((float*)p.C[grp] + m * p.ldc + n) = v;
+          *(f32x4*)((float*)Cg + m * p.ldc + n) = v;
         } else {  // EPI_RESID_F32
           const f32x4 r = *(const f32x4*)(p.resid + m * p.ldr + n);
-          *(f32x4*)((float*)p.C[grp] + m * p.ldc + n) = r + v;
+          *(f32x4*)((float*)Cg + m * p.ldc + n) = r + v;
         }
       }
     }

@@ -19,6 +19,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <algorithm>
 #include <map>
 #include <mutex>
 #include <string>
@@ -31,7 +32,9 @@ namespace partir {
 namespace {
 
 constexpr int kNumCU = 256;           // MI355X compute units: a grid below this underfills
-constexpr int kGroupM = 8;            // tile-order grouping for L2 reuse
+// Tile-order grouping for L2 reuse: consecutive workgroups walk group_m tile
+// rows before the next tile column; wide grids want shorter groups.
+int group_m_for(int tiles_n) { return std::min(8, std::max(2, 128 / std::max(1, tiles_n))); }
 constexpr size_t kWsAlign = 256;
 
 thread_local std::string g_error;
@@ -174,7 +177,7 @@ void plan_gemm(const GemmSpec& g, void* ws, Plan& plan) {
     p.tiles_m = p.rm * p.tpm;
     p.tiles_n = g.ngroups * p.rn * p.tpn;
     p.nsplit = split ? g.rk : 1;
-    p.group_m = kGroupM;
+    p.group_m = group_m_for(p.tiles_n);
     p.act = split ? 0 : g.act;
     p.epi = split ? EPI_PARTIAL : epi_store;
     L.kind = L_GEMM_BF16;
