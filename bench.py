@@ -138,21 +138,20 @@ def cpu_baseline(w, x, target_s):
     if w.kind == "mlp":
         X, W1, W2 = x["X"].f64(), x["W1"].f64(), x["W2"].f64()
         per_row = 4.0 * w["D"] * w["F"]
-        n = 64
         rng = np.random.default_rng(0)
-        total_rows, total_t = 0, 0.0
-        while True:
+        n = 256
+        total_rows, total_t, reps = 0, 0.0, 0
+        while total_t < target_s:
             rows = np.sort(rng.choice(w["T"], size=min(n, w["T"]), replace=False))
             t0 = time.perf_counter()
             O.mlp_block(X, W1, W2, act="gelu", R_batch=w["R_batch"], R_model=w["R_model"], rows=rows)
             dt = time.perf_counter() - t0
             total_rows += len(rows)
             total_t += dt
-            if total_t >= target_s or n >= w["T"]:
-                break
-            n = int(min(w["T"], max(2 * n, len(rows) * (target_s - total_t) / max(dt, 1e-3))))
+            reps += 1
+            n = min(w["T"], 2 * n)
         return dict(value=total_rows * per_row / total_t / 1e12, unit="TFLOP/s", cores=cores, kind="oracle",
-                    sample=f"{total_rows} sampled output rows of the {w['T']}-row block "
+                    sample=f"{total_rows} output rows of the {w['T']}-row block in {reps} seeded samples "
                            f"(all {w['R_model']} model shards each), {total_t:.1f} s")
     if w.kind == "attn":
         S, D = w["S"], w["D"]
