@@ -1,16 +1,13 @@
 // HBM-bound kernels: the ordered split-K reduction that stands in for the
 // all_reduce of a #sum loop, and RMSNorm.
 #include "kernels.h"
+#include "device_math.h"
 
 namespace partir {
 namespace {
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-
-__device__ __forceinline__ float gelu_erf(float x) {
-  return 0.5f * x * (1.0f + erff(x * 0.70710678118654752f));
-}
 
 // out[m][n] = epilogue(sum_{r = 0..R-1} partial[r][m][n]), r ascending, so the
 // result does not depend on scheduling.  One thread per 4 columns.

@@ -19,6 +19,7 @@
 //  * #sum over K, split: the grid also enumerates the K shards and each writes
 //    its own fp32 partial; an ordered reduction (elementwise.hip) sums them.
 #include "kernels.h"
+#include "device_math.h"
 
 namespace partir {
 namespace {
@@ -46,10 +47,6 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint3
 
 template <typename T>
 __device__ __forceinline__ T pick3(int g, T a, T b, T c) { return g == 0 ? a : (g == 1 ? b : c); }
-
-__device__ __forceinline__ float gelu_erf(float x) {
-  return 0.5f * x * (1.0f + erff(x * 0.70710678118654752f));
-}
 
 // LDS tile layout: [row][64 k] = 128-byte rows of eight 16-byte chunks; chunk
 // c of row r sits at position c ^ swz(r), swz(r) = (r & 7) ^ ((r >> 3) & 1),
@@ -181,8 +178,9 @@ void gemm_bf16_kernel(GemmParams p) {
   WAIT_VMCNT(LPS * (NS - 1));
   __syncthreads();
   ldfrag(0, 0, fa0, fb0);
-  int stage = 0;
-  for (int kt = 0; kt < nk; ++kt) {
+  // One k tile; `refill` issues the loads of tile kt+NS (skipped once that
+  // tile lies past the end, so no LDS write is still in flight at exit).
+  auto tile = [&](int kt, int stage, bool refill) {
     const int next = (stage + 1 == NS) ? 0 : stage + 1;
 #pragma unroll
     for (int kk = 0; kk < KK - 1; ++kk) {
@@ -194,14 +192,17 @@ void gemm_bf16_kernel(GemmParams p) {
     }
     WAIT_VMCNT(LPS * (NS - 2));
     __syncthreads();
-    gload(kt + NS, stage);
+    if (refill) gload(kt + NS, stage);
     if ((KK - 1) & 1) { ldfrag(next, 0, fa0, fb0); mma(fa1, fb1); }
     else { ldfrag(next, 0, fa1, fb1); mma(fa0, fb0); }
 #pragma unroll
-    for (int i = 0; i < 6; ++i) { SGB(0x8, 1); SGB(0x100, 1); SGB(0x20, 1); }
+    for (int i = 0; i < 6; ++i) { SGB(0x8, 1); SGB(0x100, 1); if (refill) SGB(0x20, 1); }
     SGB(0x8, 2);
-    stage = next;
-  }
+    return next;
+  };
+  int stage = 0, kt = 0;
+  for (; kt + NS < nk; ++kt) stage = tile(kt, stage, true);
+  for (; kt < nk; ++kt) stage = tile(kt, stage, false);
 #undef SGB
 
   // ---- epilogue: lane holds C[m][n..n+3] for each (i, j, g) ---------------------
