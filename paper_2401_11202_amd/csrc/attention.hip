@@ -33,11 +33,21 @@ constexpr int STAGE = KT_BYTES + VT_BYTES;
 
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
+// Buffer descriptor of a workgroup-uniform base pointer (kept in SGPRs).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint32_t bytes) {
+  const uint64_t a = (uint64_t)p;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)a);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(a >> 32));
+  void* u = (void*)(((uint64_t)hi << 32) | lo);
+  return __builtin_amdgcn_make_buffer_rsrc(u, (short)0, (int)__builtin_amdgcn_readfirstlane(bytes), 0x00020000);
+}
+
 __global__ __launch_bounds__(NT, 2)
 void attention_kernel(AttnParams p) {
   __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
 
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform, so per-wave tests branch
   const int h = lane >> 5, col = lane & 31;
 
   // heaviest (latest) query blocks first: causal work grows with the block index
@@ -58,17 +68,26 @@ void attention_kernel(AttnParams p) {
     for (int ds = 0; ds < 8; ++ds) qf[ds] = *(const bf16x8*)(qrow + 16 * ds);
   }
 
-  // ---- K / V tile loads: 64 rows x 256 B each, 4 + 4 chunks of 16 B per thread
+  // ---- K / V tile loads: 64 rows x 256 B each, 4 + 4 chunks of 16 B per thread.
+  // Buffer loads: the per-thread row offsets are loop-invariant VGPRs and the
+  // key block enters as a scalar offset.
   const int lr = tid >> 4, lc = tid & 15;
-  const uint16_t* kbase = p.K + tok0 * p.ldk + head * DH + lc * 8;
-  const uint16_t* vbase = p.V + tok0 * p.ldv + head * DH + lc * 8;
+  const __amdgpu_buffer_rsrc_t krs = make_rsrc(p.K + tok0 * p.ldk + head * DH, (uint32_t)((p.S - 1) * p.ldk * 2 + DH * 2));
+  const __amdgpu_buffer_rsrc_t vrs = make_rsrc(p.V + tok0 * p.ldv + head * DH, (uint32_t)((p.S - 1) * p.ldv * 2 + DH * 2));
+  uint32_t kvo[4], vvo[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    kvo[i] = (uint32_t)((lr + 16 * i) * p.ldk * 2 + lc * 16);
+    vvo[i] = (uint32_t)((lr + 16 * i) * p.ldv * 2 + lc * 16);
+  }
+  const uint32_t kstep = (uint32_t)(BKV * p.ldk * 2), vstep = (uint32_t)(BKV * p.ldv * 2);
   i32x4 rk[4], rv[4];
   auto gload = [&](int kb) {
+    const uint32_t ks_off = (uint32_t)kb * kstep, vs_off = (uint32_t)kb * vstep;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int64_t key = (int64_t)kb * BKV + lr + 16 * i;
-      rk[i] = *(const i32x4*)(kbase + key * p.ldk);
-      rv[i] = *(const i32x4*)(vbase + key * p.ldv);
+      rk[i] = __builtin_bit_cast(i32x4, __builtin_amdgcn_raw_buffer_load_b128(krs, kvo[i], ks_off, 0));
+      rv[i] = __builtin_bit_cast(i32x4, __builtin_amdgcn_raw_buffer_load_b128(vrs, vvo[i], vs_off, 0));
     }
   };
   auto lstore = [&](int buf) {
@@ -120,25 +139,35 @@ void attention_kernel(AttnParams p) {
           sacc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ds], sacc[t], 0, 0, 0);
         }
       }
-      // scale (log2 domain), causal mask, block max
-      float mloc = -1e30f;
-      const bool need_mask = p.causal && (k0 + BKV - 1 > q0 + 32 * w);
+      // causal mask and block max on the raw scores; the scale (> 0, so it
+      // keeps the order) is folded into the exponent: p = 2^(s c - m), with m
+      // the running max of s c.
+      float mloc = -__builtin_inff();
+      if (p.causal && k0 + BKV - 1 > q0 + 32 * w) {   // wave-uniform: only blocks on the diagonal
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const int key = k0 + 32 * t + 8 * (v >> 2) + 4 * h + (v & 3);
+            if (key > qi) sacc[t][v] = -__builtin_inff();
+          }
+      }
 #pragma unroll
       for (int t = 0; t < 2; ++t)
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          float s = sacc[t][v] * p.scale_log2;
-          if (need_mask) {
-            const int key = k0 + 32 * t + 8 * (v >> 2) + 4 * h + (v & 3);
-            if (key > qi) s = -__builtin_inff();
-          }
-          sacc[t][v] = s;
-          mloc = fmaxf(mloc, s);
-        }
+        for (int v = 0; v < 16; ++v) mloc = fmaxf(mloc, sacc[t][v]);
       // the partner lane (lane ^ 32) holds the other keys of this query
       mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
-      const float m_new = fmaxf(m_run, mloc);
-      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      const float sl2 = p.scale_log2;
+      const float m_new = fmaxf(m_run, mloc * sl2);
+      // rescale O and l only when some lane's max moved (alpha is exactly 1
+      // for the others, so skipping the multiply changes nothing)
+      if (__builtin_amdgcn_ballot_w64(m_new > m_run) != 0) {
+        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+        l_run *= alpha;
+#pragma unroll
+        for (int d = 0; d < 4; ++d) oacc[d] *= alpha;
+      }
       m_run = m_new;
       float lsum = 0.0f;
       bf16x8 pf[4];
@@ -146,13 +175,11 @@ void attention_kernel(AttnParams p) {
       for (int t = 0; t < 2; ++t)
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
-          const float e = __builtin_amdgcn_exp2f(sacc[t][v] - m_new);
+          const float e = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[t][v], sl2, -m_new));
           lsum += e;
           pf[2 * t + (v >> 3)][v & 7] = (__bf16)e;
         }
-      l_run = l_run * alpha + lsum;
-#pragma unroll
-      for (int d = 0; d < 4; ++d) oacc[d] *= alpha;
+      l_run += lsum;
       // O^T += V^T P^T, 4 steps of 16 keys
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
