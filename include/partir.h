@@ -37,6 +37,12 @@
  * Execution.  Work is enqueued on `stream` (a hipStream_t; NULL = the
  *   default stream) and the call returns without waiting.  Results of a
  *   #sum are deterministic: the same inputs give the same bits on every run.
+ * Empty operands.  A size of 0 is legal wherever the method allows it: a
+ *   zero-size dim slices into R empty shards (TSlice with n_d = 0), a #tile
+ *   of empty shards is an empty result (nothing is launched), and a #sum over
+ *   an empty contraction (K = 0, F = 0) is the empty sum, so the output is
+ *   the epilogue applied to 0 (zeros, the bias, or the unchanged residual).
+ *   A pointer may be NULL when its tensor holds no elements or is never read.
  * Errors.  Argument errors are detected before anything is enqueued; the
  *   call then returns the status and leaves every output untouched.  A failed
  *   launch returns PARTIR_E_HIP.  Faults during execution surface at the
@@ -58,7 +64,7 @@ extern "C" {
 typedef enum partir_status {
   PARTIR_OK = 0,
   PARTIR_E_NULL = 1,         /* a required pointer is NULL                       */
-  PARTIR_E_SHAPE = 2,        /* a size is <= 0 / too large, or sizes disagree    */
+  PARTIR_E_SHAPE = 2,        /* a size is < 0 / too large, or sizes disagree     */
   PARTIR_E_DIVISIBILITY = 3, /* R does not divide the sliced dim (rule TSlice)   */
   PARTIR_E_AXIS = 4,         /* invalid axis, or one axis both tiled and summed  */
   PARTIR_E_DTYPE = 5,        /* unsupported dtype combination                    */
@@ -112,7 +118,9 @@ typedef enum partir_act { PARTIR_ACT_NONE = 0, PARTIR_ACT_GELU_ERF = 1 } partir_
  * or PARTIR_BF16 when ab_dtype is bf16.  Accumulation is fp32.
  * b_layout: partir_b_layout.  sum_impl: partir_sum_impl (ignored without a
  * #sum).  ws / ws_bytes: workspace of at least partir_loop_matmul_workspace().
- * Errors: E_NULL (A, B or C NULL, or ws NULL with ws_bytes short), E_SHAPE,
+ * M, N or K may be 0: M = 0 or N = 0 launches nothing; K = 0 writes zeros.
+ * Errors: E_NULL (a non-empty A, B or C NULL, or ws NULL with ws_bytes
+ * short), E_SHAPE (a size < 0 or above 2^30),
  * E_DIVISIBILITY (R does not divide the tiled or summed dim), E_AXIS,
  * E_DTYPE, E_LAYOUT, E_WORKSPACE, E_UNSUPPORTED (R < 1), E_HIP.
  */
@@ -144,7 +152,8 @@ size_t partir_loop_matmul_workspace(int64_t M, int64_t N, int64_t K,
  * act: partir_act applied to the first product.  The intermediate
  * H = act(X W1 + b1) ([T, F], stored bf16) lives in the workspace; each model
  * shard m writes its columns [m F/R_model, (m+1) F/R_model) and the second
- * product sums the shards' K-ranges in order.
+ * product sums the shards' K-ranges in order.  T = 0 or D = 0 launches
+ * nothing; F = 0 (every model shard empty) gives Y = b2 (or 0).
  * Errors: E_NULL, E_SHAPE, E_DIVISIBILITY (R_batch does not divide T or
  * R_model does not divide F), E_DTYPE (in_dtype other than BF16), E_LAYOUT,
  * E_WORKSPACE, E_UNSUPPORTED (R < 1), E_HIP.
@@ -174,7 +183,8 @@ size_t partir_mlp_block_workspace(int64_t T, int64_t D, int64_t F, int out_dtype
  * [h*d_head, (h+1)*d_head) of Q, K and V.  Batch shards hold whole sequences.
  * scale <= 0 selects 1/sqrt(d_head).  Y: [B*S, D], out_dtype F32 or BF16.
  * The workspace holds Q, K, V and the attention output (bf16, [B*S, D] each).
- * Constraints: d_head == 128, S a multiple of 64.
+ * Constraints: d_head == 128, S a multiple of 128.  B = 0 or S = 0 (no
+ * tokens) launches nothing.
  * Errors: E_NULL, E_SHAPE (n_heads*d_head != D, or d_head / S outside the
  * constraints), E_DIVISIBILITY (R_batch does not divide B or R_model does not
  * divide n_heads), E_DTYPE, E_LAYOUT, E_WORKSPACE, E_UNSUPPORTED, E_HIP.
@@ -202,6 +212,8 @@ size_t partir_attn_block_workspace(int64_t B, int64_t S, int64_t D, int64_t n_he
  * partir_attn_block; W1t: [F, D] bf16; W2t: [D, F] bf16.
  * Workspace: normalised activations, Q, K, V, attention output and the
  * [B*S, F] FFN intermediate, all bf16.
+ * F = 0 leaves out the FFN half (it adds the empty sum); B = 0 or S = 0
+ * launches nothing.
  * Errors: as partir_attn_block, plus E_DIVISIBILITY when R_model does not
  * divide F.
  */

@@ -329,7 +329,8 @@ def decoder_layer(x, p, B, S, n_heads, d_head, eps=1e-6, R_batch=1, R_model=1,
     reads the same normalised rows.  ``rows`` restricts the output rows; the
     attention then reads every key position of the touched sequences up to the
     largest requested one.  The normaliser returned with ``return_norm`` is
-    |h| + |gelu(.)|.|W2| of the final residual add."""
+    |h| + |gelu(.)|.|W2| of the final residual add (|x| + |attn|.|Wo| of the
+    attention residual add when the FFN has width 0)."""
     T, D = x.shape
     if T != B * S or B % R_batch or n_heads % R_model or p["W1"].shape[1] % R_model:
         raise ValueError("indivisible partition")
@@ -348,13 +349,14 @@ def decoder_layer(x, p, B, S, n_heads, d_head, eps=1e-6, R_batch=1, R_model=1,
         local = np.array([t for _, t in mine])
         xn = rmsnorm(xb, p["g1"], eps)
 
-        def attn_shard(m):
+        att = []
+        for m in range(R_model):
             a = _attend_shard(xn, slice_(p["Wq"], 1, m, R_model), slice_(p["Wk"], 1, m, R_model),
                               slice_(p["Wv"], 1, m, R_model), B // R_batch, S, hps, d_head,
                               scale, True, local)
-            return matmul(a, slice_(p["Wo"], 0, m, R_model))
-
-        h = xb[local] + loop_sum(R_model, attn_shard)
+            wo = slice_(p["Wo"], 0, m, R_model)
+            att.append((matmul(a, wo), abs_product(a, wo) if return_norm else None))
+        h = xb[local] + loop_sum(R_model, lambda m: att[m][0])
         hn = rmsnorm(h, p["g2"], eps)
         parts = []
         for m in range(R_model):
@@ -364,7 +366,12 @@ def decoder_layer(x, p, B, S, n_heads, d_head, eps=1e-6, R_batch=1, R_model=1,
         idx = np.array([i for i, _ in mine])
         out[idx] = h + loop_sum(R_model, lambda m: parts[m][0])
         if return_norm:
-            norm[idx] = np.abs(h) + loop_sum(R_model, lambda m: parts[m][1])
+            if p["W1"].shape[1] == 0:
+                # an FFN of width 0 contracts over nothing: the last contraction
+                # is the attention out-projection
+                norm[idx] = np.abs(xb[local]) + loop_sum(R_model, lambda m: att[m][1])
+            else:
+                norm[idx] = np.abs(h) + loop_sum(R_model, lambda m: parts[m][1])
     return (out, norm) if return_norm else out
 
 

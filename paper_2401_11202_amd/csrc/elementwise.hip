@@ -10,16 +10,21 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 
 // out[m][n] = epilogue(sum_{r = 0..R-1} partial[r][m][n]), r ascending, so the
-// result does not depend on scheduling.  One thread per 4 columns.
+// result does not depend on scheduling.  R = 0 is the empty sum (a contraction
+// over K = 0): the output is the epilogue applied to zero.  One thread per 4
+// columns.
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(ReduceParams p) {
   const int nq = p.N >> 2;
   const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (idx >= (int64_t)p.M * nq) return;
   const int m = (int)(idx / nq);
   const int n = (int)(idx - (int64_t)m * nq) * 4;
-  const float* src = p.partial + (int64_t)m * p.part_ld + n;
-  f32x4 acc = *(const f32x4*)src;
-  for (int r = 1; r < p.R; ++r) acc += *(const f32x4*)(src + r * p.part_stride);
+  f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+  if (p.R > 0) {
+    const float* src = p.partial + (int64_t)m * p.part_ld + n;
+    acc = *(const f32x4*)src;
+    for (int r = 1; r < p.R; ++r) acc += *(const f32x4*)(src + r * p.part_stride);
+  }
   if (p.bias) acc += *(const f32x4*)(p.bias + n);
   if (p.act) {
 #pragma unroll
@@ -62,6 +67,7 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(RmsParams p) {
 
 hipError_t launch_splitk_reduce(const ReduceParams& p, hipStream_t s) {
   const int64_t n = (int64_t)p.M * (p.N / 4);
+  if (n == 0) return hipSuccess;
   hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, p);
   return hipGetLastError();
 }

@@ -301,8 +301,11 @@ struct MatmulArgs {
 };
 
 int validate_matmul(const MatmulArgs& a, bool with_ptrs) {
-  if (with_ptrs && (!a.A || !a.B || !a.C)) return fail(PARTIR_E_NULL, "A, B and C must be non-NULL");
-  if (a.M < 1 || a.N < 1 || a.K < 1) return fail(PARTIR_E_SHAPE, "M, N, K must be >= 1");
+  // Empty operands are legal: a zero-size dim slices into R empty shards
+  // (n_d = 0 satisfies TSlice), and a #sum over K = 0 is the empty sum.
+  if (a.M < 0 || a.N < 0 || a.K < 0) return fail(PARTIR_E_SHAPE, "M, N, K must be >= 0");
+  if (with_ptrs && ((a.M * a.K > 0 && !a.A) || (a.K * a.N > 0 && !a.B) || (a.M * a.N > 0 && !a.C)))
+    return fail(PARTIR_E_NULL, "A, B and C must be non-NULL (unless empty)");
   if (a.M > (1 << 30) || a.N > (1 << 30) || a.K > (1 << 30)) return fail(PARTIR_E_SHAPE, "dims above 2^30");
   if (a.R < 1) return fail(PARTIR_E_UNSUPPORTED, "R = %d: a loop needs at least one shard", a.R);
   if (a.tile_axis != PARTIR_AXIS_NONE && a.tile_axis != PARTIR_AXIS_M && a.tile_axis != PARTIR_AXIS_N) {
@@ -327,8 +330,11 @@ int validate_matmul(const MatmulArgs& a, bool with_ptrs) {
   if (a.sum_axis == PARTIR_AXIS_K && a.K % a.R) return fail(PARTIR_E_DIVISIBILITY, "R=%d does not divide K=%lld", a.R, (long long)a.K);
   const int eb = elem_bytes(a.ab), vec = 16 / eb;
   const int64_t ldb_min = a.b_layout == PARTIR_B_KN ? a.N : a.K;
-  if (a.lda < a.K || a.ldb < ldb_min || a.ldc < a.N) return fail(PARTIR_E_LAYOUT, "leading dim smaller than the row length");
-  if (a.lda % vec || a.ldb % vec || a.ldc % (16 / elem_bytes(a.c)))
+  // leading dims matter only for operands that hold elements
+  const bool a_used = a.M * a.K > 0, b_used = a.K * a.N > 0, c_used = a.M * a.N > 0;
+  if ((a_used && a.lda < a.K) || (b_used && a.ldb < ldb_min) || (c_used && a.ldc < a.N))
+    return fail(PARTIR_E_LAYOUT, "leading dim smaller than the row length");
+  if ((a_used && a.lda % vec) || (b_used && a.ldb % vec) || (c_used && a.ldc % (16 / elem_bytes(a.c))))
     return fail(PARTIR_E_LAYOUT, "leading dims must keep rows 16-byte aligned");
   if (a.K % vec) return fail(PARTIR_E_LAYOUT, "K must be a multiple of %d", vec);
   if (a.N % 4) return fail(PARTIR_E_LAYOUT, "N must be a multiple of 4");
@@ -339,6 +345,25 @@ int validate_matmul(const MatmulArgs& a, bool with_ptrs) {
   if (with_ptrs && (!aligned16(a.A) || !aligned16(a.B) || !aligned16(a.C)))
     return fail(PARTIR_E_LAYOUT, "A, B and C must be 16-byte aligned");
   return PARTIR_OK;
+}
+
+// C[M, N] = epilogue(0): the #sum over an empty contraction (K = 0), done by
+// the ordered reduction with no partials.
+void plan_empty_sum(void* C, int64_t M, int64_t N, int64_t ldc, bool out_bf16, const float* bias,
+                    const float* resid, int64_t ldr, bool resid_add, const char* name, Plan& plan) {
+  Launch R;
+  R.kind = L_REDUCE;
+  R.name = name;
+  ReduceParams& r = R.reduce;
+  r.partial = nullptr; r.part_ld = 0; r.part_stride = 0;
+  r.R = 0; r.M = (int)M; r.N = (int)N;
+  r.C = C; r.ldc = ldc; r.bias = bias; r.resid = resid; r.ldr = ldr;
+  r.act = 0; r.out_bf16 = out_bf16; r.resid_add = resid_add;
+  char buf[200];
+  snprintf(buf, sizeof buf, "empty_sum: C[%lld,%lld] = sum over K = 0 (zero)%s", (long long)M, (long long)N,
+           bias ? " + bias" : "");
+  R.text = buf;
+  plan.launches.push_back(R);
 }
 
 GemmSpec matmul_spec(const MatmulArgs& a) {
@@ -362,6 +387,14 @@ void plan_matmul(const MatmulArgs& a, void* ws, Plan& plan) {
   plan.n_shards = g.rm * g.rn * g.rk;
   plan.n_tile_loops = a.tile_axis != PARTIR_AXIS_NONE;
   plan.flops = 2.0 * a.M * a.N * a.K;
+  if (a.M == 0 || a.N == 0) return;                 // empty output: nothing to launch
+  if (a.K == 0) {
+    plan.ws_bytes = 0;
+    if (g.rk > 1) plan.n_sum_loops = 1;
+    plan_empty_sum(a.C, a.M, a.N, a.ldc, a.c == PARTIR_BF16, nullptr, nullptr, 0, false,
+                   a.ab == PARTIR_BF16 ? "loop_matmul.bf16" : "loop_matmul.f32", plan);
+    return;
+  }
   plan_gemm(g, ws, plan);
 }
 
@@ -376,8 +409,11 @@ struct MlpArgs {
 };
 
 int validate_mlp(const MlpArgs& a, bool with_ptrs) {
-  if (with_ptrs && (!a.X || !a.W1t || !a.W2t || !a.Y)) return fail(PARTIR_E_NULL, "X, W1t, W2t and Y must be non-NULL");
-  if (a.T < 1 || a.D < 1 || a.F < 1) return fail(PARTIR_E_SHAPE, "T, D, F must be >= 1");
+  if (a.T < 0 || a.D < 0 || a.F < 0) return fail(PARTIR_E_SHAPE, "T, D, F must be >= 0");
+  // an operand must be present only if it will be read (or written)
+  if (with_ptrs && ((a.T * a.D > 0 && a.F > 0 && !a.X) || (a.T * a.D * a.F > 0 && (!a.W1t || !a.W2t)) ||
+                    (a.T * a.D > 0 && !a.Y)))
+    return fail(PARTIR_E_NULL, "X, W1t, W2t and Y must be non-NULL (unless empty)");
   if (a.T > (1 << 30) || a.D > (1 << 20) || a.F > (1 << 22)) return fail(PARTIR_E_SHAPE, "dims too large");
   if (a.Rb < 1 || a.Rm < 1) return fail(PARTIR_E_UNSUPPORTED, "R_batch and R_model must be >= 1");
   if (a.in != PARTIR_BF16) return fail(PARTIR_E_DTYPE, "in_dtype must be BF16");
@@ -414,6 +450,13 @@ void plan_mlp(const MlpArgs& a, void* ws, Plan& plan) {
   plan.n_shards = a.Rb * a.Rm;
   plan.n_tile_loops = (a.Rb > 1) + 1;
   plan.flops = 4.0 * a.T * a.D * a.F;
+  if (a.T == 0 || a.D == 0) { plan.ws_bytes = 0; return; }   // Y is empty
+  if (a.F == 0) {                                              // every model shard is empty: Y = b2
+    plan.ws_bytes = 0;
+    plan.n_sum_loops = 1;
+    plan_empty_sum(a.Y, a.T, a.D, a.D, a.out == PARTIR_BF16, (const float*)a.b2, nullptr, 0, false, "mlp.down", plan);
+    return;
+  }
   plan_gemm(g1, nullptr, plan);
   plan_gemm(g2, ws ? base + h_bytes : nullptr, plan);
 }
@@ -431,7 +474,8 @@ struct AttnArgs {
 };
 
 int validate_attn_shapes(int64_t B, int64_t S, int64_t D, int64_t H, int64_t dh, int Rb, int Rm) {
-  if (B < 1 || S < 1 || D < 1 || H < 1 || dh < 1) return fail(PARTIR_E_SHAPE, "sizes must be >= 1");
+  if (B < 0 || S < 0) return fail(PARTIR_E_SHAPE, "B and S must be >= 0 (zero: no tokens, nothing to do)");
+  if (D < 1 || H < 1 || dh < 1) return fail(PARTIR_E_SHAPE, "D, n_heads and d_head must be >= 1");
   if (B * S > (1 << 28) || D > (1 << 20)) return fail(PARTIR_E_SHAPE, "sizes too large");
   if (H * dh != D) return fail(PARTIR_E_SHAPE, "n_heads*d_head = %lld != D = %lld", (long long)(H * dh), (long long)D);
   if (dh != 128) return fail(PARTIR_E_SHAPE, "d_head must be 128 (got %lld)", (long long)dh);
@@ -443,9 +487,11 @@ int validate_attn_shapes(int64_t B, int64_t S, int64_t D, int64_t H, int64_t dh,
 }
 
 int validate_attn(const AttnArgs& a, bool with_ptrs) {
-  if (with_ptrs && (!a.X || !a.Wq || !a.Wk || !a.Wv || !a.Wo || !a.Y)) return fail(PARTIR_E_NULL, "X, W* and Y must be non-NULL");
   int st = validate_attn_shapes(a.B, a.S, a.D, a.H, a.dh, a.Rb, a.Rm);
   if (st) return st;
+  const bool empty = a.B * a.S == 0;
+  if (with_ptrs && !empty && (!a.X || !a.Wq || !a.Wk || !a.Wv || !a.Wo || !a.Y))
+    return fail(PARTIR_E_NULL, "X, W* and Y must be non-NULL");
   if (a.in != PARTIR_BF16) return fail(PARTIR_E_DTYPE, "in_dtype must be BF16");
   if (!valid_dtype(a.out)) return fail(PARTIR_E_DTYPE, "out_dtype must be F32 or BF16");
   if (with_ptrs && (!aligned16(a.X) || !aligned16(a.Wq) || !aligned16(a.Wk) || !aligned16(a.Wv) ||
@@ -494,6 +540,11 @@ size_t attn_core_bytes(int64_t T, int64_t D) { return 4 * align_up((size_t)T * D
 
 void plan_attn(const AttnArgs& a, void* ws, Plan& plan) {
   const int64_t T = a.B * a.S;
+  if (T == 0) {                                      // no tokens: nothing to do
+    plan.n_shards = a.Rb * a.Rm;
+    plan.n_tile_loops = (a.Rb > 1) + 1;
+    return;
+  }
   char* base = (char*)ws;
   const size_t core = attn_core_bytes(T, a.D);
   plan_attention_core(a.X, a.Wq, a.Wk, a.Wv, base, a.B, a.S, a.D, a.H, a.dh, a.causal, a.scale, a.Rb, a.Rm, plan);
@@ -523,11 +574,13 @@ struct DecArgs {
 };
 
 int validate_dec(const DecArgs& a, bool with_ptrs) {
-  if (with_ptrs && (!a.x || !a.g1 || !a.g2 || !a.Wq || !a.Wk || !a.Wv || !a.Wo || !a.W1 || !a.W2))
-    return fail(PARTIR_E_NULL, "all tensors must be non-NULL");
   int st = validate_attn_shapes(a.B, a.S, a.D, a.H, a.dh, a.Rb, a.Rm);
   if (st) return st;
-  if (a.F < 1 || a.F > (1 << 22)) return fail(PARTIR_E_SHAPE, "F out of range");
+  if (a.F < 0 || a.F > (1 << 22)) return fail(PARTIR_E_SHAPE, "F out of range");
+  const bool empty = a.B * a.S == 0;
+  if (with_ptrs && !empty && (!a.x || !a.g1 || !a.Wq || !a.Wk || !a.Wv || !a.Wo ||
+                              (a.F > 0 && (!a.g2 || !a.W1 || !a.W2))))
+    return fail(PARTIR_E_NULL, "all tensors must be non-NULL");
   if (a.F % a.Rm) return fail(PARTIR_E_DIVISIBILITY, "R_model=%d does not divide F=%lld", a.Rm, (long long)a.F);
   if ((a.F / a.Rm) % 8) return fail(PARTIR_E_LAYOUT, "F/R_model must be a multiple of 8");
   if (!(a.eps >= 0.0f)) return fail(PARTIR_E_SHAPE, "eps must be >= 0");
@@ -552,6 +605,11 @@ void plan_rmsnorm(const float* x, const float* g, void* y, int64_t rows, int64_t
 
 void plan_dec(const DecArgs& a, void* ws, Plan& plan) {
   const int64_t T = a.B * a.S;
+  if (T == 0) {                                      // no tokens: nothing to do
+    plan.n_shards = a.Rb * a.Rm;
+    plan.n_tile_loops = (a.Rb > 1) + 2;
+    return;
+  }
   char* base = (char*)ws;
   const size_t xn_bytes = align_up((size_t)T * a.D * 2);
   const size_t core = attn_core_bytes(T, a.D);
@@ -572,6 +630,11 @@ void plan_dec(const DecArgs& a, void* ws, Plan& plan) {
   go.name = "attn.out";
   go.label = "dec.attn_out x += sum_m O[:, m heads] . slice 0 Wo[m]";
   plan_gemm(go, part, plan);
+  plan.ws_bytes = xn_bytes + core + gemm_ws_bytes(go);
+  plan.n_shards = a.Rb * a.Rm;
+  plan.n_tile_loops = (a.Rb > 1) + 2;
+  plan.flops = 8.0 * T * a.D * a.D + 4.0 * a.B * a.H * ((double)a.S * (a.S + 1) / 2) * a.dh + 4.0 * T * a.D * a.F;
+  if (a.F == 0) return;       // an FFN of width 0 adds the empty sum: x is unchanged
   plan_rmsnorm((const float*)a.x, (const float*)a.g2, xn, T, a.D, a.eps, a.Rb, plan);
   GemmSpec g1;
   g1.A = xn; g1.B[0] = a.W1; g1.C[0] = Hf;

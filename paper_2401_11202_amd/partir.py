@@ -122,7 +122,11 @@ def _tdt(code: int):
 
 
 def _rowmajor(t, name):
-    if t.dim() != 2 or t.stride(1) != 1:
+    if t.dim() != 2:
+        raise PartirError(ERR["PARTIR_E_LAYOUT"], f"{name} must be a 2-D row-major tensor")
+    if t.numel() == 0:
+        return t.shape[1]          # holds no elements: its strides are never used
+    if t.stride(1) != 1:
         raise PartirError(ERR["PARTIR_E_LAYOUT"], f"{name} must be a 2-D row-major tensor")
     return t.stride(0)
 

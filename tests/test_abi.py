@@ -62,8 +62,10 @@ def mm(M=256, N=256, K=512, lda=None, ldb=None, ldc=None, ab=P.F32, c=P.F32, bl=
 @pytest.mark.parametrize("kwargs,status", [
     (dict(A=NULL), "PARTIR_E_NULL"),
     (dict(C=NULL), "PARTIR_E_NULL"),
-    (dict(M=0), "PARTIR_E_SHAPE"),
+    (dict(M=-1), "PARTIR_E_SHAPE"),
     (dict(K=-4), "PARTIR_E_SHAPE"),
+    (dict(M=256, N=256, K=0, A=NULL, lda=0), "PARTIR_E_HIP"),       # empty contraction: valid, reaches launch
+    (dict(M=0, N=256, K=512, C=NULL), "PARTIR_E_HIP"),              # empty output: valid (no launch needed)
     (dict(R=0), "PARTIR_E_UNSUPPORTED"),
     (dict(R=3), "PARTIR_E_DIVISIBILITY"),                          # 3 does not divide K = 512
     (dict(tile=P.AXIS_M, summ=P.AXIS_NONE, M=250, R=4), "PARTIR_E_DIVISIBILITY"),
@@ -103,7 +105,7 @@ def test_error_message_is_thread_local():
     msg = {}
 
     def other():
-        mm(M=0)
+        mm(M=-1)
         msg["t"] = P.lib().partir_last_error().decode()
 
     t = threading.Thread(target=other)
@@ -124,7 +126,7 @@ def mlp(T=512, D=256, F=1024, ind=P.BF16, out=P.F32, act=P.ACT_GELU, Rb=1, Rm=8,
 
 @pytest.mark.parametrize("kwargs,status", [
     (dict(X=NULL), "PARTIR_E_NULL"),
-    (dict(T=0), "PARTIR_E_SHAPE"),
+    (dict(T=-1), "PARTIR_E_SHAPE"),
     (dict(Rm=0), "PARTIR_E_UNSUPPORTED"),
     (dict(Rm=3), "PARTIR_E_DIVISIBILITY"),
     (dict(Rb=3), "PARTIR_E_DIVISIBILITY"),
@@ -149,6 +151,7 @@ def attn(B=2, S=256, D=1024, H=8, dh=128, Rb=1, Rm=8, out=P.F32, ws_bytes=1 << 3
     (dict(H=6), "PARTIR_E_SHAPE"),               # 6 * 128 != 1024
     (dict(D=512, H=8, dh=64), "PARTIR_E_SHAPE"),  # d_head must be 128
     (dict(S=200), "PARTIR_E_SHAPE"),
+    (dict(S=-128), "PARTIR_E_SHAPE"),
     (dict(Rm=3), "PARTIR_E_DIVISIBILITY"),
     (dict(Rb=4, B=2), "PARTIR_E_DIVISIBILITY"),   # batch shards hold whole sequences
     (dict(ws_bytes=0), "PARTIR_E_WORKSPACE"),
@@ -236,3 +239,34 @@ def test_plan_text_names_every_shard_loop():
     t = p["text"]
     assert t.count("rmsnorm") == 2 and "attention" in t and t.count("fused in accumulator") == 2
     assert "#tile N x4 (cols 3456/shard)" in t
+
+
+# ---------------------------------------------------------------------------
+# empty operands: a zero-size dim is a legal TSlice (n_d = 0); #sum over an
+# empty contraction is the empty sum
+# ---------------------------------------------------------------------------
+def test_empty_shapes_plan():
+    e = P.plan_loop_matmul(0, 256, 512, ab=P.BF16, c=P.BF16, b_layout=P.B_NK, tile="M", R=4)
+    assert e["n_launches"] == 0 and e["workspace_bytes"] == 0 and e["flops"] == 0
+    z = P.plan_loop_matmul(256, 256, 0, ab=P.BF16, c=P.F32, b_layout=P.B_NK, sum="K", R=4)
+    assert z["n_launches"] == 1 and z["n_sum_loops"] == 1 and z["workspace_bytes"] == 0
+    assert "empty_sum" in z["text"]
+    m = P.plan_mlp_block(512, 256, 0, R_model=8)        # every model shard is empty: Y = b2
+    assert m["n_launches"] == 1 and m["workspace_bytes"] == 0
+    assert P.plan_mlp_block(0, 256, 1024, R_model=8)["n_launches"] == 0
+    assert P.plan_attn_block(0, 2048, 4096, 32, 128, 1, 8)["n_launches"] == 0
+    d = P.plan_decoder_layer(2, 256, 1024, 8, 128, 0, 2, 4)   # FFN of width 0: attention half only
+    assert d["n_sum_loops"] == 1 and "ffn" not in d["text"] and d["text"].count("rmsnorm") == 1
+    assert P.plan_decoder_layer(0, 256, 1024, 8, 128, 1728, 2, 4)["n_launches"] == 0
+
+
+def test_empty_calls_validate(monkeypatch):
+    monkeypatch.setenv("PARTIR_FAIL_LAUNCH", "1")
+    L = P.lib()
+    # NULL operands are fine when they hold no elements
+    st = L.partir_mlp_block(NULL, NULL, None, NULL, None, NULL, 0, 256, 1024, P.BF16, P.F32, P.ACT_GELU, 1, 8,
+                            NULL, 0, None)
+    assert P.STATUS[st] == "PARTIR_E_HIP"
+    st = L.partir_attn_block(NULL, NULL, NULL, NULL, NULL, NULL, 0, 256, 1024, 8, 128, 1, 0.0,
+                             P.BF16, P.F32, 1, 8, NULL, 0, None)
+    assert P.STATUS[st] == "PARTIR_E_HIP"

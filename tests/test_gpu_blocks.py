@@ -215,3 +215,48 @@ def test_decoder_full_size_sampled_rows():
     err = O.normalised_error(host(out[rows]), ref, norm)
     say(f"    max normalised error {err:.3e}")
     assert err <= TOL_BF16
+
+
+# ---------------------------------------------------------------------------
+# empty operands
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("out", [torch.float32, torch.bfloat16])
+def test_mlp_with_empty_ffn_is_the_output_bias(out):
+    """F = 0: each model shard is empty, the #sum adds nothing, Y = b2."""
+    T, D = 256, 512
+    X = I.gaussian(108, 0, (T, D), 1.0, "bf16").to_device()
+    b2 = I.gaussian(108, 1, (D,), 1.0, "f32")
+    W1t = torch.empty((0, D), dtype=torch.bfloat16, device="cuda")
+    W2t = torch.empty((D, 0), dtype=torch.bfloat16, device="cuda")
+    say(f"mlp F=0 out={out}")
+    Y = P.mlp_block(X, W1t, W2t, b2=b2.to_device(), R_model=4, out_dtype=out)
+    torch.cuda.synchronize()
+    ref = O.mlp_block(np.zeros((T, D)), np.zeros((D, 0)), np.zeros((0, D)), None, b2.f64(), "gelu", 1, 4)
+    if out == torch.bfloat16:
+        ref = I.bf16_to_f32(I.bf16_bits(ref.astype(np.float32))).astype(np.float64)
+    assert np.array_equal(host(Y), ref)
+
+
+def test_decoder_with_empty_ffn_matches_oracle():
+    """F = 0: the FFN half adds the empty sum, so only attention updates x."""
+    w = W.WORKLOADS["decoder_2layer_small"]
+    x = W.make_inputs(w)
+    D = w["D"]
+    for p in x["layers"]:
+        p["W1"] = I.gaussian(w.wid, 300, (D, 0), 1.0, "bf16")
+        p["W2"] = I.gaussian(w.wid, 301, (0, D), 1.0, "bf16")
+    out = run_decoder(w, x)
+    ref, norm = O.decoder(x["x"].f64(), oracle_layers(x), w["B"], w["S"], w["H"], w["dh"], 1e-6,
+                          w["R_batch"], w["R_model"], return_norm=True)
+    err = O.normalised_error(host(out), ref, norm)
+    say(f"decoder F=0: max normalised error {err:.3e}")
+    assert err <= TOL_BF16
+
+
+def test_attention_with_no_tokens_is_a_no_op():
+    X = torch.empty((0, 1024), dtype=torch.bfloat16, device="cuda")
+    W_ = I.gaussian(109, 0, (1024, 1024), 1.0 / 32, "bf16")
+    Wt = dev_t(W_)
+    Y = P.attn_block(X, Wt, Wt, Wt, Wt, B=0, S=256, n_heads=8, R_model=8)
+    torch.cuda.synchronize()
+    assert tuple(Y.shape) == (0, 1024)

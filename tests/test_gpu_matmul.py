@@ -142,3 +142,40 @@ def test_validation_errors_leave_output_untouched():
     assert e.value.status == P.ERR["PARTIR_E_DIVISIBILITY"]
     torch.cuda.synchronize()
     assert torch.all(C == 7.0)
+
+
+# ---------------------------------------------------------------------------
+# empty operands
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("dtype,out", [("bf16", torch.float32), ("bf16", torch.bfloat16), ("f32", torch.float32)])
+def test_empty_contraction_is_the_empty_sum(dtype, out):
+    """K = 0: the sum over no K shards is 0 everywhere (exact), whatever the
+    loop nest; the output window is fully written."""
+    M, N = 300, 272
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    bl = "nk" if dtype == "bf16" else "kn"
+    A = torch.empty((M, 0), dtype=tdt, device="cuda")
+    B = torch.empty((N, 0) if bl == "nk" else (0, N), dtype=tdt, device="cuda")
+    C = torch.empty((M, N), dtype=out, device="cuda")
+    for tile, summ, R in [(None, "K", 4), ("M", None, 4), ("N", "K", 2), (None, None, 1)]:
+        say(f"empty K {dtype} -> {out} tile={tile} sum={summ} R={R}")
+        C.fill_(7.0)
+        P.loop_matmul(A, B, tile=tile, sum=summ, R=R, b_layout=bl, out_dtype=out, out=C)
+        torch.cuda.synchronize()
+        ref = O.loop_matmul(np.zeros((M, 0)), np.zeros((0, N)), AX[tile], AX[summ], R)
+        assert np.array_equal(host(C), ref)
+
+
+def test_empty_output_is_a_no_op():
+    """M = 0 or N = 0: every #tile shard is empty; nothing is launched and the
+    result has the right (empty) shape."""
+    A = I.gaussian(107, 0, (0, 64), 1.0, "bf16").to_device()
+    Bt = I.transposed(I.gaussian(107, 1, (64, 48), 1.0, "bf16")).to_device()
+    C = P.loop_matmul(A, Bt, tile="M", R=4, b_layout="nk", out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    assert tuple(C.shape) == (0, 48)
+    A2 = I.gaussian(107, 2, (32, 64), 1.0, "bf16").to_device()
+    Bt2 = torch.empty((0, 64), dtype=torch.bfloat16, device="cuda")
+    C2 = P.loop_matmul(A2, Bt2, tile="N", R=4, b_layout="nk", out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    assert tuple(C2.shape) == (32, 0)

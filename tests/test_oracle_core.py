@@ -250,3 +250,33 @@ def test_normalised_error_definition():
     norm = np.array([2.0, 4.0, 0.0])
     assert O.normalised_error(np.array([1.5, 2.0, 0.0]), ref, norm) == 0.25
     assert O.normalised_error(np.array([1.0, 2.0, 1e-30]), ref, norm) == np.inf
+
+
+# ---------------------------------------------------------------------------
+# empty operands: TSlice with n_d = 0, and the empty sum
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("tile,summ,R", [(O.AXIS_NONE, O.AXIS_K, 4), (O.AXIS_M, O.AXIS_NONE, 4),
+                                         (O.AXIS_N, O.AXIS_K, 2), (O.AXIS_NONE, O.AXIS_NONE, 1)])
+def test_empty_contraction_is_the_empty_sum(tile, summ, R):
+    """K = 0: each shard's partial is an [M, N] block of empty dot products,
+    and a sum over no terms is 0 (pure-Python brute force agrees)."""
+    A, B = np.zeros((8, 0)), np.zeros((0, 12))
+    C = O.loop_matmul(A, B, tile, summ, R)
+    assert C.shape == (8, 12)
+    brute = [[sum(()) for _ in range(12)] for _ in range(8)]   # sum of an empty sequence
+    assert C.tolist() == brute
+
+
+@pytest.mark.parametrize("tile,R", [(O.AXIS_M, 4), (O.AXIS_N, 4)])
+def test_tiling_an_empty_dim_gives_empty_shards(tile, R):
+    """slice d x[r] of a zero-size dim: R empty chunks whose concatenation is
+    the empty result of the right shape."""
+    rng = np.random.default_rng(5)
+    if tile == O.AXIS_M:
+        A, B = rng.standard_normal((0, 16)), rng.standard_normal((16, 12))
+        assert O.slice_(A, 0, R - 1, R).shape == (0, 16)
+    else:
+        A, B = rng.standard_normal((8, 16)), rng.standard_normal((16, 0))
+        assert O.slice_(B, 1, R - 1, R).shape == (16, 0)
+    C = O.loop_matmul(A, B, tile, O.AXIS_NONE, R)
+    assert C.shape == (A.shape[0], B.shape[1]) and C.size == 0

@@ -197,3 +197,36 @@ def test_decoder_independent_of_model_partition():
     outs = [O.decoder_layer(x, p, B, S, H, dh, 1e-6, Rb, Rm) for Rb in (1, 2) for Rm in (1, 2, 4, 8)]
     for o in outs[1:]:
         assert np.max(np.abs(o - outs[0])) < 1e-12
+
+
+def test_mlp_with_empty_ffn_is_the_output_bias():
+    """F = 0: every model shard holds no hidden units, the #sum over m adds R
+    empty contributions (0), and only the bias added after the loop remains."""
+    rng = np.random.default_rng(7)
+    X = rng.standard_normal((16, 8))
+    b2 = rng.standard_normal(8)
+    for Rm in (1, 4):
+        Y = O.mlp_block(X, np.zeros((8, 0)), np.zeros((0, 8)), None, b2, "gelu", 1, Rm)
+        assert np.array_equal(Y, np.broadcast_to(b2, (16, 8)))
+    assert np.array_equal(O.mlp_block(X, np.zeros((8, 0)), np.zeros((0, 8)), act="gelu", R_model=2),
+                          np.zeros((16, 8)))
+
+
+def test_decoder_with_empty_ffn_equals_zero_down_projection():
+    """F = 0 adds the empty sum; a width-8 FFN whose down-projection is all
+    zeros adds exactly 0 as well, so the two layers agree bit for bit, and
+    the normaliser falls back to the attention residual add (>= |x|)."""
+    rng = np.random.default_rng(11)
+    B, S, H, dh = 2, 8, 2, 4
+    D = H * dh
+    x = rng.standard_normal((B * S, D))
+    p = {"g1": np.ones(D), "g2": np.ones(D)}
+    for k in ("Wq", "Wk", "Wv", "Wo"):
+        p[k] = rng.standard_normal((D, D)) / math.sqrt(D)
+    empty = dict(p, W1=np.zeros((D, 0)), W2=np.zeros((0, D)))
+    zero = dict(p, W1=rng.standard_normal((D, 8)), W2=np.zeros((8, D)))
+    for Rm in (1, 2):
+        a, na = O.decoder_layer(x, empty, B, S, H, dh, R_batch=2, R_model=Rm, return_norm=True)
+        b = O.decoder_layer(x, zero, B, S, H, dh, R_batch=2, R_model=Rm)
+        assert np.array_equal(a, b)
+        assert np.all(na >= np.abs(x) - 1e-15) and np.all(na > 0)
