@@ -179,3 +179,23 @@ def test_empty_output_is_a_no_op():
     C2 = P.loop_matmul(A2, Bt2, tile="N", R=4, b_layout="nk", out_dtype=torch.float32)
     torch.cuda.synchronize()
     assert tuple(C2.shape) == (32, 0)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_degenerate_shard_sizes(dtype):
+    """R as large as the layout allows: single-row M shards, N shards of one
+    16-byte run, K shards of one 16-byte run (64 of them, summed in order)."""
+    vec = 8 if dtype == "bf16" else 4
+    tol = TOL_BF16 if dtype == "bf16" else TOL_F32
+    bl = "nk" if dtype == "bf16" else "kn"
+    cases = [(64, 256, 128, "M", None, 64),            # 64 shards of 1 row
+             (96, 32 * vec, 128, "N", None, 32),       # 32 shards of `vec` columns
+             (128, 256, 64 * vec, None, "K", 64),      # 64 K shards of `vec`
+             (64, 16 * vec, 16 * vec, "M", "K", 16)]   # 16 x 16 nest, 4-row tiles of vec-wide K shards
+    for (M, N, K, tile, summ, R) in cases:
+        A = I.gaussian(110, 0, (M, K), 1.0, dtype)
+        B = I.gaussian(110, 1, (K, N), K ** -0.5, dtype)
+        for impl in ("fused", "splitk"):
+            say(f"degenerate {dtype} {M}x{N}x{K} tile={tile} sum={summ} R={R} {impl}")
+            C = run(A, B, tile, summ, R, bl, out_dtype=torch.float32, sum_impl=impl)
+            check(A, B, C, tile, summ, R, tol)
