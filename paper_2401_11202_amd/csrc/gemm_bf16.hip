@@ -32,6 +32,12 @@ typedef int i32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int BM = 256, BN = 256, NT = 512;
 constexpr int BK = 64, NS = 2;
+// Epilogue staging of the output tile in LDS (reusing the K stages): bf16
+// rows of 256 + 8 elements (528 B, 16-byte aligned rows), fp32 in two halves
+// of 128 rows of 256 + 4 floats (1040 B); the pads spread consecutive rows
+// over the LDS banks.
+constexpr int CPB = BN + 8, CPF = BN + 4;
+constexpr int C_LDS = (BM * CPB * 2 > (BM / 2) * CPF * 4) ? BM * CPB * 2 : (BM / 2) * CPF * 4;
 constexpr uint32_t OOB = 0x80000000u;          // offset that reads as zero
 typedef __attribute__((address_space(3))) void lds_void;
 
@@ -61,7 +67,7 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void gemm_bf16_kernel(GemmParams p) {
   constexpr int OPB = BM * BK * 2, STAGE = 2 * OPB, KK = BK / 16, RB = 1024 / (BK * 2) /* rows per 1 KiB */;
   constexpr int CPR = BK / 8;   // 16-byte chunks per row
-  __shared__ __attribute__((aligned(1024))) char smem[NS * STAGE];
+  __shared__ __attribute__((aligned(1024))) char smem[(NS * STAGE > C_LDS) ? NS * STAGE : C_LDS];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -205,44 +211,95 @@ void gemm_bf16_kernel(GemmParams p) {
   for (; kt < nk; ++kt) stage = tile(kt, stage, false);
 #undef SGB
 
-  // ---- epilogue: lane holds C[m][n..n+3] for each (i, j, g) ---------------------
+  // ---- epilogue ----------------------------------------------------------------
+  // Lane holds C[m][n..n+3] for each (i, j, g): 16-byte pieces of 32 rows per
+  // store, which the memory system would see as partial lines.  The tile is
+  // therefore staged through LDS and written back row by row, each row as
+  // one contiguous run (bf16: 32 lanes x 16 B; fp32: 64 lanes x 16 B).
   const float* bias = pick3(grp, p.bias[0], p.bias[1], p.bias[2]);
   void* Cg = pick3(grp, p.C[0], p.C[1], p.C[2]);
+  __syncthreads();   // every wave is done with the K stages
+  if (EPI == EPI_BF16) {
+    uint16_t* cs = (uint16_t*)smem;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int ml = wm * 128 + i * 32 + (lane & 31);
-    if (ml >= rows) continue;
-    const int64_t m = row0 + ml;
+    for (int i = 0; i < 4; ++i) {
+      const int ml = wm * 128 + i * 32 + (lane & 31);
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
+      for (int j = 0; j < 2; ++j)
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int nl = wn * 64 + j * 32 + 8 * g + 4 * h;
-        if (nl >= cols) continue;
-        const int64_t n = col0 + nl;
-        f32x4 v = {acc[i][j][4 * g + 0], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]};
+        for (int g = 0; g < 4; ++g) {
+          const int nl = wn * 64 + j * 32 + 8 * g + 4 * h;
+          f32x4 v = {acc[i][j][4 * g + 0], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]};
+          if (bias) {
+            if (nl < cols) v += *(const f32x4*)(bias + col0 + nl);
+          }
+          if (ACT) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[e] = gelu_erf(v[e]);
+          }
+          const bf16x4 o = {(__bf16)v[0], (__bf16)v[1], (__bf16)v[2], (__bf16)v[3]};
+          *(bf16x4*)(cs + ml * CPB + nl) = o;
+        }
+    }
+    __syncthreads();
+    // 16 rows per pass: thread t writes 8 columns (16 B) of row t / 32
+    const int cr = tid >> 5, cc = (tid & 31) * 8;
+#pragma unroll 4
+    for (int r0 = 0; r0 < BM; r0 += NT / 32) {
+      const int r = r0 + cr;
+      if (r >= rows || cc >= cols) continue;
+      const i32x4 v = *(const i32x4*)(cs + r * CPB + cc);
+      uint16_t* dst = (uint16_t*)Cg + (row0 + r) * p.ldc + col0 + cc;
+      if (cc + 8 <= cols) *(i32x4*)dst = v;
+      else *(int2*)dst = make_int2(v[0], v[1]);   // a 4-column tail (cols % 8 == 4)
+    }
+  } else {
+    // fp32 results (plain, residual or split partial): two halves of 128 rows
+    float* cs = (float*)smem;
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      if (wm == q) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int ml = i * 32 + (lane & 31);
+#pragma unroll
+          for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+              const int nl = wn * 64 + j * 32 + 8 * g + 4 * h;
+              f32x4 v = {acc[i][j][4 * g + 0], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]};
+              if (EPI != EPI_PARTIAL) {
+                if (bias) {
+                  if (nl < cols) v += *(const f32x4*)(bias + col0 + nl);
+                }
+                if (ACT) {
+#pragma unroll
+                  for (int e = 0; e < 4; ++e) v[e] = gelu_erf(v[e]);
+                }
+              }
+              *(f32x4*)(cs + ml * CPF + nl) = v;
+            }
+        }
+      }
+      __syncthreads();
+      // 8 rows per pass: thread t writes 4 columns (16 B) of row t / 64
+      const int cr = tid >> 6, cc = (tid & 63) * 4;
+#pragma unroll 4
+      for (int r0 = 0; r0 < BM / 2; r0 += NT / 64) {
+        const int rl = r0 + cr, r = q * (BM / 2) + rl;
+        if (r >= rows || cc >= cols) continue;
+        const f32x4 v = *(const f32x4*)(cs + rl * CPF + cc);
+        const int64_t m = row0 + r, n = col0 + cc;
         if (EPI == EPI_PARTIAL) {
           *(f32x4*)(p.partial + split * p.part_stride + m * p.part_ld + n) = v;
-          continue;
-        }
-        if (bias) {
-          const f32x4 bv = *(const f32x4*)(bias + n);
-          v += bv;
-        }
-        if (ACT) {
-#pragma unroll
-          for (int e = 0; e < 4; ++e) v[e] = gelu_erf(v[e]);
-        }
-        if (EPI == EPI_BF16) {
-          bf16x4 o = {(__bf16)v[0], (__bf16)v[1], (__bf16)v[2], (__bf16)v[3]};
-          *(bf16x4*)((uint16_t*)Cg + m * p.ldc + n) = o;
         } else if (EPI == EPI_F32) {
           *(f32x4*)((float*)Cg + m * p.ldc + n) = v;
         } else {  // EPI_RESID_F32
-          const f32x4 r = *(const f32x4*)(p.resid + m * p.ldr + n);
-          *(f32x4*)((float*)Cg + m * p.ldc + n) = r + v;
+          const f32x4 rv = *(const f32x4*)(p.resid + m * p.ldr + n);
+          *(f32x4*)((float*)Cg + m * p.ldc + n) = rv + v;
         }
       }
+      if (q == 0) __syncthreads();   // the second half reuses the buffer
     }
   }
 }
