@@ -259,6 +259,45 @@ int partir_plan_decoder_layer(int64_t B, int64_t S, int64_t D, int64_t n_heads,
 const char* partir_last_plan_text(void);
 
 /* ------------------------------------------------------------------------ */
+/* Planner: ManualPartition tactics, value tiling and propagation on the host */
+/* (Sec. 3 schedules; Sec. 5.1 value tiling; Sec. 5.2 TMR, propagation,       */
+/* inference and conflicts; App. A multi-axis nests).  No GPU needed.         */
+/* ------------------------------------------------------------------------ */
+/*
+ * program: NUL-terminated text, one statement per line (or ';'), '#' comments:
+ *   mesh <axis>=<size> ...            the mesh axes, in order
+ *   arg <name> <rows>x<cols>          a 2-D function argument
+ *   <name> = matmul <a> <b> | add <a> <b> | gelu <a> | rmsnorm <a>
+ *   ret <name> ...
+ * schedule: text, one tactic per line:
+ *   partition <axis> <name>:<dim> ...   ManualPartition({name: dim, ...}, axis):
+ *                                       value-tile each named value, then propagate
+ *   tile <name> <dim> <axis>            a bare value-tiling action
+ *   propagate                           a bare propagation action
+ * TMR: matmul (#tile<0>,_) -> #tile<0>, (_,#tile<1>) -> #tile<1>,
+ * (#tile<1>,#tile<0>) -> #sum; add (#tile<d>,#tile<d>) -> #tile<d>; gelu
+ * #tile<d> -> #tile<d>; rmsnorm #tile<0> -> #tile<0>.  An op never gets a
+ * second loop over an axis it is already nested in; several matching entries
+ * are a conflict, reported and left alone.
+ * out / out_len: caller buffer for the NUL-terminated report; *needed (if
+ * non-NULL) receives its size.  Report lines:
+ *   action <...>                          every action, each rewrite tagged
+ *                                         (forward|backward|inference), conflicts
+ *   loop <op> <kind> <axis>:<tile0|tile1|sum> ... | none   loop nest, outer first
+ *   operand <op> <i> <value> <axis>:<dim> ...     how the op slices operand i
+ *   gather|reshard <op> <value> <axis>    a tiled value used whole / along another dim
+ *   value <name> <axis>:<dim> ... | replicated    tiling after the schedule
+ *   call partir_loop_matmul <op> tile=<M|N|none> sum=<K|none> R=<n>
+ *   call partir_mlp_block <op> R_batch=<n> R_model=<n> ops=<up>,<act>,<down>
+ *   nest <op> (...)                       a nest no single entry point runs
+ * Errors: E_NULL, E_SHAPE (parse error or shape mismatch), E_AXIS (unknown
+ * axis or dim, or a value tiled along two dims on one axis), E_DIVISIBILITY
+ * (TSlice), E_UNSUPPORTED (unknown op), E_WORKSPACE (out too small).
+ */
+int partir_propagate(const char* program, const char* schedule, char* out, size_t out_len,
+                     size_t* needed);
+
+/* ------------------------------------------------------------------------ */
 /* Kernel trace: per-kernel GPU time measured with HIP events.                */
 /* ------------------------------------------------------------------------ */
 typedef struct partir_trace_entry {

@@ -671,6 +671,9 @@ void fill_info(const Plan& plan, partir_plan_info* info) {
 }
 
 }  // namespace
+
+void set_last_error(const std::string& msg) { g_error = msg; }
+
 }  // namespace partir
 
 using namespace partir;

@@ -30,7 +30,7 @@ EXPORTS = ("partir_loop_matmul", "partir_loop_matmul_workspace", "partir_mlp_blo
            "partir_decoder_layer", "partir_decoder_layer_workspace", "partir_plan_loop_matmul",
            "partir_plan_mlp_block", "partir_plan_attn_block", "partir_plan_decoder_layer",
            "partir_last_plan_text", "partir_trace_enable", "partir_trace_read", "partir_trace_reset",
-           "partir_status_string", "partir_last_error", "partir_version")
+           "partir_status_string", "partir_last_error", "partir_version", "partir_propagate")
 
 
 class PartirError(RuntimeError):
@@ -84,6 +84,7 @@ def lib():
         "partir_status_string": (ctypes.c_char_p, [I32]),
         "partir_last_error": (ctypes.c_char_p, []),
         "partir_version": (ctypes.c_char_p, []),
+        "partir_propagate": (I32, [ctypes.c_char_p, ctypes.c_char_p, ctypes.c_char_p, SZ, ctypes.POINTER(SZ)]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(L, name)
@@ -275,3 +276,64 @@ def trace_read():
     buf = (TraceEntry * max(n, 1))()
     n = lib().partir_trace_read(buf, n)
     return {buf[i].name.decode(): (buf[i].launches, buf[i].total_ms) for i in range(n)}
+
+
+# ---------------------------------------------------------------------------
+# planner (host only)
+# ---------------------------------------------------------------------------
+def schedule_text(schedule) -> str:
+    """[(axis, {name: dim, ...}), ...] -> the planner's schedule text: one
+    ManualPartition tactic per line."""
+    return "\n".join("partition " + axis + " " + " ".join(f"{n}:{d}" for n, d in parts.items())
+                     for axis, parts in schedule)
+
+
+def propagate_text(program: str, schedule: str) -> str:
+    """Run partir_propagate and return its report text."""
+    need = SZ(0)
+    buf = ctypes.create_string_buffer(1 << 16)
+    st = lib().partir_propagate(program.encode(), schedule.encode(), buf, len(buf), ctypes.byref(need))
+    if st == ERR["PARTIR_E_WORKSPACE"] and need.value > len(buf):
+        buf = ctypes.create_string_buffer(need.value)
+        st = lib().partir_propagate(program.encode(), schedule.encode(), buf, len(buf), ctypes.byref(need))
+    _check(st)
+    return buf.value.decode()
+
+
+def parse_report(text: str) -> dict:
+    """Report text -> {'actions': [...], 'loops': {op: [(axis, action)]},
+    'operands': {(op, i): {axis: dim}}, 'values': {name: {axis: dim}},
+    'gathers': [(op, value, axis)], 'reshards': [...], 'conflicts': [(op, axis)],
+    'calls': [str], 'nests': [op]}."""
+    r = {"actions": [], "loops": {}, "kinds": {}, "operands": {}, "operand_names": {}, "values": {},
+         "gathers": [], "reshards": [], "conflicts": [], "calls": [], "nests": []}
+    for line in text.splitlines():
+        t = line.split()
+        if not t:
+            continue
+        if t[0] == "action":
+            r["actions"].append(" ".join(t[1:]))
+            if t[1] == "conflict":
+                r["conflicts"].append((t[2], t[3]))
+        elif t[0] == "loop":
+            r["kinds"][t[1]] = t[2]
+            r["loops"][t[1]] = [] if t[3:] == ["none"] else [tuple(x.split(":")) for x in t[3:]]
+        elif t[0] == "operand":
+            r["operands"][(t[1], int(t[2]))] = {a: int(d) for a, d in (x.split(":") for x in t[4:])}
+            r["operand_names"][(t[1], int(t[2]))] = t[3]
+        elif t[0] in ("gather", "reshard"):
+            r[t[0] + "s"].append((t[1], t[2], t[3]))
+        elif t[0] == "value":
+            r["values"][t[1]] = {} if t[2:] == ["replicated"] else {a: int(d) for a, d in (x.split(":") for x in t[2:])}
+        elif t[0] == "call":
+            r["calls"].append(" ".join(t[1:]))
+        elif t[0] == "nest":
+            r["nests"].append(t[1])
+    return r
+
+
+def propagate(program: str, schedule) -> dict:
+    """Partition `program` with a schedule of ManualPartition tactics
+    [(axis, {name: dim})] (or schedule text) and return the parsed report."""
+    text = schedule if isinstance(schedule, str) else schedule_text(schedule)
+    return parse_report(propagate_text(program, text))

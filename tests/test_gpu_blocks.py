@@ -260,3 +260,32 @@ def test_attention_with_no_tokens_is_a_no_op():
     Y = P.attn_block(X, Wt, Wt, Wt, Wt, B=0, S=256, n_heads=8, R_model=8)
     torch.cuda.synchronize()
     assert tuple(Y.shape) == (0, 1024)
+
+
+# ---------------------------------------------------------------------------
+# the planner's emitted entry point, executed
+# ---------------------------------------------------------------------------
+def test_planner_emitted_mlp_call_runs_and_matches_oracle():
+    """BP + MP tactics on the MLP program: the planner names partir_mlp_block
+    with the loop sizes of its nest; running that call reproduces the oracle."""
+    w = W.WORKLOADS["mlp_megatron_small"]
+    x = W.make_inputs(w)
+    T, D, F = w["T"], w["D"], w["F"]
+    prog = (f"mesh B=2 M=8\narg x {T}x{D}\narg w1 {D}x{F}\narg w2 {F}x{D}\n"
+            "h = matmul x w1\ng = gelu h\ny = matmul g w2\nret y")
+    r = P.propagate(prog, [("B", {"x": 0}), ("M", {"w1": 1})])
+    (call,) = r["calls"]
+    name, out, *fields = call.split()
+    assert name == "partir_mlp_block" and out == "y"
+    f = dict(kv.split("=") for kv in fields)
+    Rb, Rm = int(f["R_batch"]), int(f["R_model"])
+    assert (Rb, Rm) == (2, 8)
+    say(f"planner call: {call}")
+    Y = P.mlp_block(x["X"].to_device(), dev_t(x["W1"]), dev_t(x["W2"]), R_batch=Rb, R_model=Rm, act="gelu",
+                    out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    ref, norm = O.mlp_block(x["X"].f64(), x["W1"].f64(), x["W2"].f64(), act="gelu", R_batch=Rb, R_model=Rm,
+                            return_norm=True)
+    err = O.normalised_error(host(Y), ref, norm)
+    say(f"    max normalised error {err:.3e}")
+    assert err <= TOL_BF16
