@@ -111,6 +111,15 @@ def setup(w, P, I):
                  "mlp.up": L * 2.0 * T * D * F, "mlp.down": L * 2.0 * T * D * F}
         roles = {k: v / L for k, v in roles.items()}   # per launch
         return x, step, roles, "mfma_bf16"
+    if w.kind == "attn_core":
+        B, S, H, dh = w["B"], w["S"], w["H"], w["dh"]
+        Q, K, V = (x[n].to_device() for n in ("Q", "K", "V"))
+        O = torch.empty_like(Q)
+        ws = torch.empty(max(1, P.lib().partir_attention_workspace(B, S, H, dh, w["R_kv"])), dtype=torch.uint8,
+                         device="cuda")
+        step = lambda: P.attention(Q, K, V, B=B, S=S, n_heads=H, d_head=dh, R_kv=w["R_kv"], out=O, workspace=ws)
+        roles = {"attn.core": W.attn_core_flops(B, S, H, dh)}
+        return x, step, roles, "mfma_bf16"
     raise ValueError(w.kind)
 
 
@@ -166,6 +175,19 @@ def cpu_baseline(w, x, target_s):
         return dict(value=flops / dt / 1e12, unit="TFLOP/s", cores=cores, kind="oracle",
                     sample=f"{nq} output rows at the end of one {S}-token sequence (K/V of the whole "
                            f"sequence), {dt:.1f} s")
+    if w.kind == "attn_core":
+        S, H, dh = w["S"], w["H"], w["dh"]
+        q, k, v = x["Q"].f64(), x["K"].f64(), x["V"].f64()
+        nq = 1024
+        rows = np.arange(S - nq, S)             # the last positions of sequence 0: the longest key prefixes
+        t0 = time.perf_counter()
+        for h in range(H):
+            cs = slice(h * dh, (h + 1) * dh)
+            O.attention_split_kv(q[rows, cs], k[:S, cs], v[:S, cs], dh ** -0.5, True, w["R_kv"], q_pos=rows)
+        dt = time.perf_counter() - t0
+        flops = 4.0 * H * dh * float(np.sum(rows + 1))
+        return dict(value=flops / dt / 1e12, unit="TFLOP/s", cores=cores, kind="oracle",
+                    sample=f"{nq} query rows x {H} heads at the end of the {S}-token sequence, {dt:.1f} s")
     if w.kind == "decoder":
         S, D, F = w["S"], w["D"], w["F"]
         layers = [{k: v.f64() for k, v in p.items()} for p in x["layers"]]

@@ -200,6 +200,37 @@ size_t partir_attn_block_workspace(int64_t B, int64_t S, int64_t D, int64_t n_he
                                    int64_t d_head, int R_batch, int R_model);
 
 /* ------------------------------------------------------------------------ */
+/* Attention core alone, with the key axis as a loop whose reduction is a     */
+/* custom associative #sum (Sec. 5.2.1 footnote: any associative reduction).  */
+/* ------------------------------------------------------------------------ */
+/*
+ * O = loop h [#tile<1>](n_heads) {
+ *       loop s [#sum softmax](R_kv) { partial(Q_h, slice 0 K_h[s], slice 0 V_h[s]) } }
+ * The key positions of each sequence are split into R_kv contiguous shards.
+ * A shard yields (m, l, o) for every query: m = max_j c s_j over its keys
+ * (log2 domain, c = scale log2 e), l = sum_j 2^(c s_j - m), o = sum_j
+ * 2^(c s_j - m) v_j.  The reduction is (m, l, o) (+) (m', l', o') =
+ * (M, 2^(m-M) l + 2^(m'-M) l', 2^(m-M) o + 2^(m'-M) o'), M = max(m, m'),
+ * which is associative and commutative; the shards are folded in order
+ * s = 0..R_kv-1 and O = o / l.  With causal masking a query sees keys at
+ * positions <= its own, so shards past it contribute (-inf, 0, 0).  R_kv = 1
+ * is plain attention (no workspace).
+ * Q, K, V, O: [B*S, n_heads*d_head] bf16 row-major (ld = n_heads*d_head),
+ * sequence-major; head h owns columns [h*d_head, (h+1)*d_head).
+ * scale <= 0 selects 1/sqrt(d_head).  Constraints: d_head == 128, S a
+ * multiple of 128, R_kv dividing S/64.  Workspace (R_kv > 1): the shards'
+ * fp32 o (R_kv*B*S*n_heads*d_head) and m, l (R_kv*B*S*n_heads each).
+ * Errors: E_NULL, E_SHAPE, E_DIVISIBILITY (R_kv does not divide S/64),
+ * E_LAYOUT, E_WORKSPACE, E_UNSUPPORTED (R_kv < 1), E_HIP.
+ */
+int partir_attention(const void* Q, const void* K, const void* V, void* O,
+                     int64_t B, int64_t S, int64_t n_heads, int64_t d_head,
+                     int causal, float scale, int R_kv,
+                     void* ws, size_t ws_bytes, void* stream);
+
+size_t partir_attention_workspace(int64_t B, int64_t S, int64_t n_heads, int64_t d_head, int R_kv);
+
+/* ------------------------------------------------------------------------ */
 /* Pre-norm decoder layer on an fp32 residual stream, in place.               */
 /* ------------------------------------------------------------------------ */
 /*
@@ -249,6 +280,8 @@ int partir_plan_mlp_block(int64_t T, int64_t D, int64_t F, int out_dtype,
                           int R_batch, int R_model, partir_plan_info* info);
 int partir_plan_attn_block(int64_t B, int64_t S, int64_t D, int64_t n_heads, int64_t d_head,
                            int R_batch, int R_model, partir_plan_info* info);
+int partir_plan_attention(int64_t B, int64_t S, int64_t n_heads, int64_t d_head, int causal, int R_kv,
+                          partir_plan_info* info);
 int partir_plan_decoder_layer(int64_t B, int64_t S, int64_t D, int64_t n_heads,
                               int64_t d_head, int64_t F, int R_batch, int R_model,
                               partir_plan_info* info);

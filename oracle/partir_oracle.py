@@ -135,6 +135,52 @@ def causal_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, scale: float,
 
 
 # ---------------------------------------------------------------------------
+# The key axis as a loop: a custom associative #sum (Sec. 5.2.1 footnote)
+# ---------------------------------------------------------------------------
+def softmax_partial(q: np.ndarray, k: np.ndarray, v: np.ndarray, scale: float, causal: bool,
+                    q_pos: np.ndarray, k_pos: np.ndarray):
+    """One key shard of softmax attention, per query: (m, l, o) with
+    m = max_j s_ij over the keys j of the shard the query may see,
+    l = sum_j exp(s_ij - m), o = sum_j exp(s_ij - m) v_j.  A query that sees
+    no key of the shard gets (-inf, 0, 0), the identity of the combiner."""
+    q = np.asarray(q, np.float64)
+    k = np.asarray(k, np.float64)
+    v = np.asarray(v, np.float64)
+    s = matmul(q, k.T) * scale
+    if causal:
+        s = np.where(np.asarray(k_pos)[None, :] <= np.asarray(q_pos)[:, None], s, -np.inf)
+    m = np.max(s, axis=1) if s.shape[1] else np.full(s.shape[0], -np.inf)
+    seen = np.isfinite(m)
+    e = np.where(seen[:, None], np.exp(s - np.where(seen, m, 0.0)[:, None]), 0.0)
+    return m, e.sum(axis=1), matmul(e, v)
+
+
+def softmax_combine(a, b):
+    """(m, l, o) (+) (m', l', o') = (M, e^(m-M) l + e^(m'-M) l', e^(m-M) o + e^(m'-M) o'),
+    M = max(m, m'); a shard with m = -inf carries weight 0."""
+    (m1, l1, o1), (m2, l2, o2) = a, b
+    M = np.maximum(m1, m2)
+    w1 = np.where(np.isfinite(m1), np.exp(m1 - np.where(np.isfinite(M), M, 0.0)), 0.0)
+    w2 = np.where(np.isfinite(m2), np.exp(m2 - np.where(np.isfinite(M), M, 0.0)), 0.0)
+    return M, w1 * l1 + w2 * l2, w1[:, None] * o1 + w2[:, None] * o2
+
+
+def attention_split_kv(q: np.ndarray, k: np.ndarray, v: np.ndarray, scale: float, causal: bool, R: int,
+                       q_pos: Optional[np.ndarray] = None) -> np.ndarray:
+    """loop s [#sum softmax](R) { softmax_partial(q, slice 0 k[s], slice 0 v[s]) },
+    folded with softmax_combine in shard order, then o / l."""
+    nk = k.shape[0]
+    if q_pos is None:
+        q_pos = np.arange(q.shape[0])
+    acc = None
+    for r in range(R):
+        pos = np.arange(r * (nk // R), (r + 1) * (nk // R))
+        part = softmax_partial(q, slice_(k, 0, r, R), slice_(v, 0, r, R), scale, causal, q_pos, pos)
+        acc = part if acc is None else softmax_combine(acc, part)
+    return acc[2] / acc[1][:, None]
+
+
+# ---------------------------------------------------------------------------
 # Single partitioned matmul: the three TMR forms of matmul (Sec. 5.2.1)
 # ---------------------------------------------------------------------------
 def loop_matmul(A: np.ndarray, B: np.ndarray, tile_axis: int, sum_axis: int, R: int) -> np.ndarray:

@@ -23,6 +23,7 @@ typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef short i16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef int i32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int DH = 128, BQ = 128, BKV = 64, NT = 256;
 constexpr int KP = 256;                 // K tile row pitch (bytes), chunk-swizzled
@@ -50,10 +51,13 @@ void attention_kernel(AttnParams p) {
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform, so per-wave tests branch
   const int h = lane >> 5, col = lane & 31;
 
-  // heaviest (latest) query blocks first: causal work grows with the block index
+  // heaviest (latest) query blocks first: causal work grows with the block
+  // index; with a split key axis, the shards of one query block are adjacent
   const int nqb = p.S / BQ;
   const int nbh = p.B * p.H;
-  const int qb = nqb - 1 - (int)(blockIdx.x / nbh);
+  const int qs = blockIdx.x / nbh;
+  const int qb = nqb - 1 - qs / p.nsplit;
+  const int split = qs % p.nsplit;
   const int bh = blockIdx.x % nbh;
   const int b = bh / p.H, head = bh - b * p.H;
   const int q0 = qb * BQ;
@@ -113,14 +117,18 @@ void attention_kernel(AttnParams p) {
   const int v_row = 4 * hh + (j16 >> 2);
   const int v_colb = 2 * (16 * (G & 1) + 4 * (j16 & 3));
 
-  const int nkb = p.causal ? (q0 + BQ + BKV - 1) / BKV : p.S / BKV;
+  const int nkb_all = p.causal ? (q0 + BQ + BKV - 1) / BKV : p.S / BKV;
+  const int kb_begin = p.nsplit > 1 ? split * p.kb_per : 0;
+  const int nkb = p.nsplit > 1 ? min(nkb_all, kb_begin + p.kb_per) : nkb_all;   // one past the last block
   const int wave_last_q = q0 + 32 * w + 31;
 
-  gload(0);
-  lstore(0);
+  if (kb_begin < nkb) {
+    gload(kb_begin);
+    lstore(0);
+  }
   __syncthreads();
-  for (int kb = 0; kb < nkb; ++kb) {
-    const int cur = kb & 1;
+  for (int kb = kb_begin; kb < nkb; ++kb) {
+    const int cur = (kb - kb_begin) & 1;
     if (kb + 1 < nkb) gload(kb + 1);
     const int k0 = kb * BKV;
     if (!p.causal || k0 <= wave_last_q) {
@@ -199,8 +207,27 @@ void attention_kernel(AttnParams p) {
     __syncthreads();
   }
 
+  const float l_tot = l_run + __shfl_xor(l_run, 32);
+  if (p.nsplit > 1) {
+    // one shard of the key loop: unnormalised output and (m, l) for the combine
+    const int64_t tq = tok0 + qi;
+    float* orow = p.Opart + ((int64_t)split * p.B * p.S + tq) * (p.H * DH) + head * DH;
+#pragma unroll
+    for (int d = 0; d < 4; ++d)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const f32x4 o = {oacc[d][4 * g + 0], oacc[d][4 * g + 1], oacc[d][4 * g + 2], oacc[d][4 * g + 3]};
+        *(f32x4*)(orow + 32 * d + 8 * g + 4 * h) = o;
+      }
+    if (h == 0) {
+      const int64_t st = ((int64_t)split * p.B * p.S + tq) * p.H + head;
+      p.Mpart[st] = m_run;
+      p.Lpart[st] = l_tot;
+    }
+    return;
+  }
   // ---- normalise and store O[query][head*128 + d] ------------------------------
-  const float inv = 1.0f / (l_run + __shfl_xor(l_run, 32));
+  const float inv = 1.0f / l_tot;
   uint16_t* orow = p.O + (tok0 + qi) * p.ldo + head * DH;
 #pragma unroll
   for (int d = 0; d < 4; ++d)
@@ -212,10 +239,42 @@ void attention_kernel(AttnParams p) {
     }
 }
 
+// One thread per (token, head, 4 of the 128 output columns).  The shards are
+// folded in order s = 0..nsplit-1, so the result does not depend on timing.
+__global__ __launch_bounds__(256) void attention_combine_kernel(AttnParams p) {
+  const int64_t T = (int64_t)p.B * p.S;
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= T * p.H * (DH / 4)) return;
+  const int c4 = (int)(idx % (DH / 4));
+  const int64_t th = idx / (DH / 4);          // token * H + head
+  const int64_t t = th / p.H;
+  const int head = (int)(th - t * p.H);
+  const int64_t sstride = T * p.H;
+  float M = -3.0e38f;
+  for (int s = 0; s < p.nsplit; ++s) M = fmaxf(M, p.Mpart[s * sstride + th]);
+  float L = 0.0f;
+  f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+  for (int s = 0; s < p.nsplit; ++s) {
+    const float w = __builtin_amdgcn_exp2f(p.Mpart[s * sstride + th] - M);
+    L += w * p.Lpart[s * sstride + th];
+    acc += w * *(const f32x4*)(p.Opart + (s * T + t) * (int64_t)(p.H * DH) + head * DH + 4 * c4);
+  }
+  const float inv = 1.0f / L;
+  const bf16x4 o = {(__bf16)(acc[0] * inv), (__bf16)(acc[1] * inv), (__bf16)(acc[2] * inv), (__bf16)(acc[3] * inv)};
+  *(bf16x4*)(p.O + t * p.ldo + head * DH + 4 * c4) = o;
+}
+
 }  // namespace
 
+hipError_t launch_attention_combine(const AttnParams& p, hipStream_t s) {
+  const int64_t n = (int64_t)p.B * p.S * p.H * (DH / 4);
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(attention_combine_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, p);
+  return hipGetLastError();
+}
+
 hipError_t launch_attention(const AttnParams& p, hipStream_t s) {
-  const unsigned nwg = (unsigned)(p.S / BQ) * p.B * p.H;
+  const unsigned nwg = (unsigned)(p.S / BQ) * p.B * p.H * p.nsplit;
   hipLaunchKernelGGL(attention_kernel, dim3(nwg), dim3(NT), 0, s, p);
   return hipGetLastError();
 }

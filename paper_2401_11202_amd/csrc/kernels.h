@@ -89,8 +89,19 @@ struct AttnParams {
   int B, S, H;       // sequences, length, heads (over all shards)
   int causal;
   float scale_log2;  // scale * log2(e)
+  // key axis as a loop of nsplit shards (a custom associative #sum): shard s
+  // covers key blocks [s * kb_per, (s + 1) * kb_per) of 64 keys and writes its
+  // unnormalised output and softmax statistics instead of O
+  int nsplit = 1;
+  int kb_per = 0;
+  float* Opart = nullptr;   // [nsplit][B*S][H*128] fp32, sum_j 2^(s_j c - m) v_j
+  float* Mpart = nullptr;   // [nsplit][B*S][H] running max m (log2 domain, scaled)
+  float* Lpart = nullptr;   // [nsplit][B*S][H] sum_j 2^(s_j c - m)
 };
 hipError_t launch_attention(const AttnParams& p, hipStream_t s);
+// O = combine over the shards: M = max m_s, w_s = 2^(m_s - M),
+// O = (sum_s w_s o_s) / (sum_s w_s l_s), s ascending; bf16 into p.O
+hipError_t launch_attention_combine(const AttnParams& p, hipStream_t s);
 
 // y (bf16) = g * x / sqrt(mean(x^2) + eps), one row of D fp32 per wave.
 struct RmsParams {

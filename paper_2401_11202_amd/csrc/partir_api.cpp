@@ -59,7 +59,7 @@ bool valid_dtype(int dt) { return dt == PARTIR_F32 || dt == PARTIR_BF16; }
 // ---------------------------------------------------------------------------
 // Plans
 // ---------------------------------------------------------------------------
-enum LaunchKind { L_GEMM_BF16, L_GEMM_F32, L_REDUCE, L_ATTN, L_RMS };
+enum LaunchKind { L_GEMM_BF16, L_GEMM_F32, L_REDUCE, L_ATTN, L_ATTN_COMBINE, L_RMS };
 
 struct Launch {
   LaunchKind kind;
@@ -236,6 +236,7 @@ hipError_t run_one(const Launch& L, hipStream_t s) {
     case L_GEMM_F32: return launch_gemm_f32(L.gemm32, s);
     case L_REDUCE: return launch_splitk_reduce(L.reduce, s);
     case L_ATTN: return launch_attention(L.attn, s);
+    case L_ATTN_COMBINE: return launch_attention_combine(L.attn, s);
     case L_RMS: return launch_rmsnorm(L.rms, s);
   }
   return hipErrorInvalidValue;
@@ -658,6 +659,75 @@ void plan_dec(const DecArgs& a, void* ws, Plan& plan) {
   plan.flops = 8.0 * T * a.D * a.D + 4.0 * a.B * a.H * ((double)a.S * (a.S + 1) / 2) * a.dh + 4.0 * T * a.D * a.F;
 }
 
+// ---------------------------------------------------------------------------
+// partir_attention: the attention core alone, the key axis as a loop
+// ---------------------------------------------------------------------------
+struct AttnCoreArgs {
+  const void *Q = nullptr, *K = nullptr, *V = nullptr;
+  void* O = nullptr;
+  int64_t B, S, H, dh;
+  int causal;
+  float scale;
+  int Rkv;
+};
+
+int validate_attn_core(const AttnCoreArgs& a, bool with_ptrs) {
+  int st = validate_attn_shapes(a.B, a.S, a.H * a.dh, a.H, a.dh, 1, 1);
+  if (st) return st;
+  if (a.Rkv < 1) return fail(PARTIR_E_UNSUPPORTED, "R_kv = %d: a loop needs at least one shard", a.Rkv);
+  if ((a.S / 64) % a.Rkv)
+    return fail(PARTIR_E_DIVISIBILITY, "R_kv=%d does not divide the %lld key blocks of 64 (S=%lld)", a.Rkv,
+                (long long)(a.S / 64), (long long)a.S);
+  if (with_ptrs && a.B * a.S > 0 && (!a.Q || !a.K || !a.V || !a.O))
+    return fail(PARTIR_E_NULL, "Q, K, V and O must be non-NULL");
+  if (with_ptrs && (!aligned16(a.Q) || !aligned16(a.K) || !aligned16(a.V) || !aligned16(a.O)))
+    return fail(PARTIR_E_LAYOUT, "Q, K, V and O must be 16-byte aligned");
+  return PARTIR_OK;
+}
+
+void plan_attn_core(const AttnCoreArgs& a, void* ws, Plan& plan) {
+  const int64_t T = a.B * a.S, D = a.H * a.dh;
+  plan.n_shards = a.Rkv;
+  plan.n_tile_loops = 1;                 // the heads loop
+  const double pairs = a.causal ? (double)a.S * (a.S + 1) / 2 : (double)a.S * a.S;
+  plan.flops = 4.0 * a.B * a.H * pairs * a.dh;
+  if (T == 0) return;
+  const size_t o_bytes = align_up((size_t)a.Rkv * T * D * 4), ml_bytes = align_up((size_t)a.Rkv * T * a.H * 4);
+  if (a.Rkv > 1) {
+    plan.ws_bytes = o_bytes + 2 * ml_bytes;
+    plan.n_sum_loops = 1;
+    plan.n_sum_splitk = 1;
+  }
+  Launch L;
+  L.kind = L_ATTN;
+  L.name = "attn.core";
+  AttnParams& p = L.attn;
+  p.Q = (const uint16_t*)a.Q; p.K = (const uint16_t*)a.K; p.V = (const uint16_t*)a.V; p.O = (uint16_t*)a.O;
+  p.ldq = p.ldk = p.ldv = p.ldo = D;
+  p.B = (int)a.B; p.S = (int)a.S; p.H = (int)a.H; p.causal = a.causal;
+  const float sc = a.scale > 0 ? a.scale : 1.0f / std::sqrt((float)a.dh);
+  p.scale_log2 = sc * 1.4426950408889634f;
+  p.nsplit = a.Rkv;
+  p.kb_per = (int)(a.S / 64 / a.Rkv);
+  char* base = (char*)ws;
+  p.Opart = base ? (float*)base : nullptr;
+  p.Mpart = base ? (float*)(base + o_bytes) : nullptr;
+  p.Lpart = base ? (float*)(base + o_bytes + ml_bytes) : nullptr;
+  char buf[256];
+  snprintf(buf, sizeof buf, "attention: loop h [#tile<1>](%lld heads) x loop s [#sum softmax](%d key shards of %d) over "
+           "%lld sequences, S=%lld, %s", (long long)a.H, a.Rkv, p.kb_per * 64, (long long)a.B, (long long)a.S,
+           a.causal ? "causal" : "full");
+  L.text = buf;
+  plan.launches.push_back(L);
+  if (a.Rkv > 1) {
+    Launch C = L;
+    C.kind = L_ATTN_COMBINE;
+    C.name = "attn.combine";
+    C.text = "attention_combine: O = sum_s 2^(m_s - M) o_s / sum_s 2^(m_s - M) l_s, s ascending";
+    plan.launches.push_back(C);
+  }
+}
+
 void fill_info(const Plan& plan, partir_plan_info* info) {
   if (!info) return;
   info->n_virtual_shards = plan.n_shards;
@@ -816,6 +886,42 @@ int partir_attn_block(const void* X, const void* Wq_t, const void* Wk_t, const v
   Plan plan;
   plan_attn(a, ws, plan);
   keep_plan_text(plan, "attn_block");
+  return execute(plan, stream);
+}
+
+// ---- attention core ---------------------------------------------------------------
+size_t partir_attention_workspace(int64_t B, int64_t S, int64_t n_heads, int64_t d_head, int R_kv) {
+  AttnCoreArgs a{nullptr, nullptr, nullptr, nullptr, B, S, n_heads, d_head, 1, 0.f, R_kv};
+  if (validate_attn_core(a, false) != PARTIR_OK) return (size_t)-1;
+  Plan plan;
+  plan_attn_core(a, nullptr, plan);
+  return plan.ws_bytes;
+}
+
+int partir_plan_attention(int64_t B, int64_t S, int64_t n_heads, int64_t d_head, int causal, int R_kv,
+                          partir_plan_info* info) {
+  AttnCoreArgs a{nullptr, nullptr, nullptr, nullptr, B, S, n_heads, d_head, causal ? 1 : 0, 0.f, R_kv};
+  int st = validate_attn_core(a, false);
+  if (st) return st;
+  Plan plan;
+  plan_attn_core(a, nullptr, plan);
+  keep_plan_text(plan, "attention");
+  fill_info(plan, info);
+  return PARTIR_OK;
+}
+
+int partir_attention(const void* Q, const void* K, const void* V, void* O, int64_t B, int64_t S,
+                     int64_t n_heads, int64_t d_head, int causal, float scale, int R_kv, void* ws,
+                     size_t ws_bytes, void* stream) {
+  AttnCoreArgs a{Q, K, V, O, B, S, n_heads, d_head, causal ? 1 : 0, scale, R_kv};
+  int st = validate_attn_core(a, true);
+  if (st) return st;
+  Plan probe;
+  plan_attn_core(a, nullptr, probe);
+  if ((st = check_ws(probe, ws, ws_bytes))) return st;
+  Plan plan;
+  plan_attn_core(a, ws, plan);
+  keep_plan_text(plan, "attention");
   return execute(plan, stream);
 }
 

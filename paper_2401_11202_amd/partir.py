@@ -30,7 +30,8 @@ EXPORTS = ("partir_loop_matmul", "partir_loop_matmul_workspace", "partir_mlp_blo
            "partir_decoder_layer", "partir_decoder_layer_workspace", "partir_plan_loop_matmul",
            "partir_plan_mlp_block", "partir_plan_attn_block", "partir_plan_decoder_layer",
            "partir_last_plan_text", "partir_trace_enable", "partir_trace_read", "partir_trace_reset",
-           "partir_status_string", "partir_last_error", "partir_version", "partir_propagate")
+           "partir_status_string", "partir_last_error", "partir_version", "partir_propagate",
+           "partir_attention", "partir_attention_workspace", "partir_plan_attention")
 
 
 class PartirError(RuntimeError):
@@ -85,6 +86,9 @@ def lib():
         "partir_last_error": (ctypes.c_char_p, []),
         "partir_version": (ctypes.c_char_p, []),
         "partir_propagate": (I32, [ctypes.c_char_p, ctypes.c_char_p, ctypes.c_char_p, SZ, ctypes.POINTER(SZ)]),
+        "partir_attention": (I32, [P, P, P, P, I64, I64, I64, I64, I32, F, I32, P, SZ, P]),
+        "partir_attention_workspace": (SZ, [I64, I64, I64, I64, I32]),
+        "partir_plan_attention": (I32, [I64, I64, I64, I64, I32, I32, ctypes.POINTER(PlanInfo)]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(L, name)
@@ -216,6 +220,25 @@ def attn_block(X, Wq_t, Wk_t, Wv_t, Wo_t, *, B: int, S: int, n_heads: int, d_hea
                                    B, S, D, n_heads, d_head, int(causal), float(scale), _dt(X), od,
                                    R_batch, R_model, _ptr(ws), wsb, _stream(stream)))
     return out
+
+
+def attention(Q, K, V, *, B: int, S: int, n_heads: int, d_head: int = 128, causal: bool = True,
+              scale: float = 0.0, R_kv: int = 1, out=None, workspace=None, stream=None):
+    """O = softmax attention per (sequence, head), the key axis a loop of R_kv
+    shards reduced with the (max, sum, output) combiner.  Q, K, V, O: [B*S, n_heads*d_head] bf16."""
+    import torch
+    T, D = Q.shape
+    if out is None:
+        out = torch.empty((T, D), dtype=torch.bfloat16, device=Q.device)
+    nbytes = lib().partir_attention_workspace(B, S, n_heads, d_head, R_kv)
+    ws, wsb = _workspace(nbytes, Q.device, workspace)
+    _check(lib().partir_attention(_ptr(Q), _ptr(K), _ptr(V), _ptr(out), B, S, n_heads, d_head, int(causal),
+                                  float(scale), R_kv, _ptr(ws), wsb, _stream(stream)))
+    return out
+
+
+def plan_attention(B, S, n_heads, d_head=128, causal=True, R_kv=1):
+    return _plan(lib().partir_plan_attention, B, S, n_heads, d_head, int(causal), R_kv)
 
 
 def decoder_layer_workspace(B, S, D, n_heads, d_head, F, R_batch=1, R_model=1) -> int:

@@ -24,7 +24,7 @@ from . import inputs as I
 @dataclass(frozen=True)
 class Workload:
     name: str
-    kind: str                 # matmul | mlp | attn | decoder
+    kind: str                 # matmul | mlp | attn | decoder | attn_core
     wid: int                  # seed id
     dims: Dict[str, int] = field(default_factory=dict)
     dtype: str = "bf16"
@@ -58,6 +58,11 @@ WORKLOADS = {
     "mlp_batch_x_megatron": _mlp("mlp_batch_x_megatron", 4, 16384, 8192, 32768, 4, 8),
     # two-layer pre-norm decoder, batch R = 2 x model R = 4
     "decoder_2layer": _dec("decoder_2layer", 5, 4, 2048, 5120, 40, 128, 13824, 2, 2, 4),
+    # attention core alone over one 8192-token sequence with 2 heads (a device's
+    # share after head tiling): 128 workgroups leave most of the GPU idle unless
+    # the key axis is also a loop, here of R_kv = 4 shards
+    "attn_core_long": Workload("attn_core_long", "attn_core", 6, dict(B=1, S=8192, H=2, dh=128, R_kv=4)),
+    "attn_core_long_R1": Workload("attn_core_long_R1", "attn_core", 6, dict(B=1, S=8192, H=2, dh=128, R_kv=1)),
     # small twins: same structure and partition sizes, scaled down
     "mlp_megatron_small": _mlp("mlp_megatron_small", 12, 512, 256, 1024, 1, 8),
     "attn_block_small": _attn("attn_block_small", 13, 2, 256, 1024, 8, 128, 1, 8),
@@ -106,9 +111,14 @@ def decoder_inputs(w: Workload):
     return dict(x=x, layers=layers)
 
 
+def attn_core_inputs(w: Workload):
+    T, D = w["B"] * w["S"], w["H"] * w["dh"]
+    return {n: I.gaussian(w.wid, i, (T, D), 1.0) for i, n in enumerate(("Q", "K", "V"))}
+
+
 def make_inputs(w: Workload):
     return {"matmul": matmul_inputs, "mlp": mlp_inputs, "attn": attn_inputs,
-            "decoder": decoder_inputs}[w.kind](w)
+            "decoder": decoder_inputs, "attn_core": attn_core_inputs}[w.kind](w)
 
 
 # ---------------------------------------------------------------------------
@@ -133,4 +143,6 @@ def flops(w: Workload) -> float:
         per = 8.0 * T * w["D"] * w["D"] + attn_core_flops(w["B"], w["S"], w["H"], w["dh"]) \
             + 4.0 * T * w["D"] * w["F"]
         return per * w["L"]
+    if w.kind == "attn_core":
+        return attn_core_flops(w["B"], w["S"], w["H"], w["dh"])
     raise ValueError(w.kind)

@@ -270,3 +270,36 @@ def test_empty_calls_validate(monkeypatch):
     st = L.partir_attn_block(NULL, NULL, NULL, NULL, NULL, NULL, 0, 256, 1024, 8, 128, 1, 0.0,
                              P.BF16, P.F32, 1, 8, NULL, 0, None)
     assert P.STATUS[st] == "PARTIR_E_HIP"
+
+
+# ---------------------------------------------------------------------------
+# attention core with the key axis as a loop
+# ---------------------------------------------------------------------------
+def test_attention_core_plans():
+    one = P.plan_attention(2, 2048, 8, 128, True, 1)
+    assert one["n_launches"] == 1 and one["workspace_bytes"] == 0 and one["n_sum_loops"] == 0
+    four = P.plan_attention(2, 2048, 8, 128, True, 4)
+    T, D = 2 * 2048, 8 * 128
+    assert four["n_launches"] == 2 and four["n_sum_loops"] == 1 and four["n_virtual_shards"] == 4
+    assert four["workspace_bytes"] == 4 * T * D * 4 + 2 * 4 * T * 8 * 4
+    assert four["flops"] == one["flops"] == 4.0 * 2 * 8 * (2048 * 2049 / 2) * 128
+    assert "#sum softmax" in four["text"]
+    assert P.lib().partir_attention_workspace(2, 2048, 8, 128, 4) == four["workspace_bytes"]
+
+
+@pytest.mark.parametrize("kwargs,status", [
+    (dict(R=3), "PARTIR_E_DIVISIBILITY"),     # 32 key blocks of 64
+    (dict(R=0), "PARTIR_E_UNSUPPORTED"),
+    (dict(S=200), "PARTIR_E_SHAPE"),
+    (dict(dh=64), "PARTIR_E_SHAPE"),
+    (dict(Q=NULL), "PARTIR_E_NULL"),
+    (dict(Q=DUMMY_ODD), "PARTIR_E_LAYOUT"),
+    (dict(ws_bytes=0), "PARTIR_E_WORKSPACE"),
+    (dict(), "PARTIR_E_HIP"),                  # valid: stops at the forced launch failure
+])
+def test_attention_core_validation(kwargs, status):
+    a = dict(Q=DUMMY, B=2, S=2048, H=8, dh=128, R=4, ws_bytes=1 << 30)
+    a.update(kwargs)
+    st = P.lib().partir_attention(a["Q"], DUMMY, DUMMY, DUMMY, a["B"], a["S"], a["H"], a["dh"], 1, 0.0, a["R"],
+                                  DUMMY, a["ws_bytes"], None)
+    assert P.STATUS[st] == status, P.lib().partir_last_error().decode()

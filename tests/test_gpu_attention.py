@@ -1,0 +1,111 @@
+"""GPU parity of partir_attention: the key axis as a loop of R_kv shards
+folded with the softmax combiner (a custom associative #sum).
+
+Every element is compared with the oracle on small shapes; at a long
+sequence, seeded rows (always including the last position) are compared.
+The error is normalised by sum_j p_ij |v_j| (the |P|.|V| of the last
+contraction), obtained as attention applied to |V|.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import partir_oracle as O
+from paper_2401_11202_amd import inputs as I
+from paper_2401_11202_amd import partir as P
+from tests.gpu_common import TOL_BF16, host, say
+
+pytestmark = pytest.mark.gpu
+DH = 128
+
+
+def make_qkv(seed, B, S, H):
+    D = H * DH
+    return [I.gaussian(seed, i, (B * S, D), 1.0, "bf16") for i in range(3)]
+
+
+def reference(Q, K, V, B, S, H, causal, rows=None):
+    """Oracle output and normaliser at `rows` (all rows by default)."""
+    q, k, v = Q.f64(), K.f64(), V.f64()
+    rows = np.arange(B * S) if rows is None else np.asarray(rows)
+    out = np.zeros((len(rows), H * DH))
+    nrm = np.zeros_like(out)
+    scale = DH ** -0.5
+    for b in range(B):
+        sel = [(i, r - b * S) for i, r in enumerate(rows) if b * S <= r < (b + 1) * S]
+        if not sel:
+            continue
+        idx = np.array([i for i, _ in sel])
+        pos = np.array([p for _, p in sel])
+        for h in range(H):
+            cs = slice(h * DH, (h + 1) * DH)
+            qs = q[b * S + pos, cs]
+            ks, vs = k[b * S:(b + 1) * S, cs], v[b * S:(b + 1) * S, cs]
+            out[idx, cs] = O.causal_attention(qs, ks, vs, scale, causal, q_pos=pos)
+            nrm[idx, cs] = O.causal_attention(qs, ks, np.abs(vs), scale, causal, q_pos=pos)
+    return out, nrm
+
+
+def run(Q, K, V, B, S, H, causal, R):
+    o = P.attention(Q.to_device(), K.to_device(), V.to_device(), B=B, S=S, n_heads=H, causal=causal, R_kv=R)
+    torch.cuda.synchronize()
+    return o
+
+
+@pytest.mark.parametrize("causal", [True, False])
+@pytest.mark.parametrize("R", [1, 2, 4])
+def test_split_kv_small_full_output(causal, R):
+    B, S, H = 2, 256, 4
+    Q, K, V = make_qkv(120, B, S, H)
+    say(f"attention B={B} S={S} H={H} causal={causal} R_kv={R}")
+    o = run(Q, K, V, B, S, H, causal, R)
+    ref, nrm = reference(Q, K, V, B, S, H, causal)
+    err = O.normalised_error(host(o), ref, nrm)
+    say(f"    max normalised error {err:.3e}")
+    assert err <= TOL_BF16
+
+
+def test_split_kv_agrees_with_oracle_split_kv():
+    """The oracle's own split-K/V fold (same shards, same order) as reference."""
+    B, S, H, R = 1, 512, 2, 8
+    Q, K, V = make_qkv(121, B, S, H)
+    o = host(run(Q, K, V, B, S, H, True, R))
+    for h in range(H):
+        cs = slice(h * DH, (h + 1) * DH)
+        ref = O.attention_split_kv(Q.f64()[:, cs], K.f64()[:, cs], V.f64()[:, cs], DH ** -0.5, True, R)
+        nrm = O.attention_split_kv(Q.f64()[:, cs], K.f64()[:, cs], np.abs(V.f64()[:, cs]), DH ** -0.5, True, R)
+        assert O.normalised_error(o[:, cs], ref, nrm) <= TOL_BF16
+
+
+def test_split_kv_long_sequence_sampled_rows():
+    B, S, H, R = 1, 4096, 8, 8
+    Q, K, V = make_qkv(122, B, S, H)
+    rng = np.random.default_rng(122)
+    rows = np.unique(np.concatenate([[0, 63, 64, S - 1], rng.choice(S, 28, replace=False)]))
+    say(f"attention B={B} S={S} H={H} R_kv={R}: {len(rows)} sampled rows")
+    o = host(run(Q, K, V, B, S, H, True, R))[rows]
+    ref, nrm = reference(Q, K, V, B, S, H, True, rows)
+    err = O.normalised_error(o, ref, nrm)
+    say(f"    max normalised error {err:.3e}")
+    assert err <= TOL_BF16
+
+
+def test_split_kv_matches_single_shard_and_is_deterministic():
+    B, S, H = 2, 512, 4
+    Q, K, V = make_qkv(123, B, S, H)
+    one = run(Q, K, V, B, S, H, True, 1)
+    four = run(Q, K, V, B, S, H, True, 4)
+    again = run(Q, K, V, B, S, H, True, 4)
+    assert torch.equal(four, again)
+    _, nrm = reference(Q, K, V, B, S, H, True)
+    assert O.normalised_error(host(four), host(one), nrm) <= TOL_BF16
+
+
+def test_split_kv_validation():
+    Q = torch.zeros((256, 512), dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(P.PartirError) as e:
+        P.attention(Q, Q, Q, B=1, S=256, n_heads=4, R_kv=3)       # 3 does not divide the 4 key blocks
+    assert e.value.status == P.ERR["PARTIR_E_DIVISIBILITY"]
+    with pytest.raises(P.PartirError) as e:
+        P.attention(Q, Q, Q, B=1, S=256, n_heads=4, R_kv=0)
+    assert e.value.status == P.ERR["PARTIR_E_UNSUPPORTED"]

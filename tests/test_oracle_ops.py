@@ -142,3 +142,54 @@ def test_attention_large_scores_stay_finite():
     o = O.causal_attention(q, k, v, 1.0)
     assert np.all(np.isfinite(o))
     assert np.array_equal(o[1], v[1]) and np.array_equal(o[3], v[3])
+
+
+# ---------------------------------------------------------------------------
+# the key axis as a loop with the softmax combiner (custom associative #sum)
+# ---------------------------------------------------------------------------
+def test_split_kv_attention_equals_attention():
+    """Folding the shards' (m, l, o) with the combiner gives softmax
+    attention over all keys, for every shard count and with a causal mask
+    (shards past a query contribute the identity)."""
+    rng = np.random.default_rng(31)
+    q, k, v = (rng.standard_normal((64, 16)) for _ in range(3))
+    for causal in (True, False):
+        ref = O.causal_attention(q, k, v, 0.25, causal)
+        for R in (1, 2, 4, 8, 64):
+            got = O.attention_split_kv(q, k, v, 0.25, causal, R)
+            assert np.abs(got - ref).max() <= 1e-13
+
+
+def test_softmax_combiner_is_associative_and_commutative_with_identity():
+    rng = np.random.default_rng(32)
+    q = rng.standard_normal((8, 4))
+    parts = []
+    for r in range(3):
+        k, v = rng.standard_normal((5, 4)), rng.standard_normal((5, 4))
+        parts.append(O.softmax_partial(q, k, v, 1.3, False, np.arange(8), np.arange(5)))
+    a, b, c = parts
+
+    def close(x, y):
+        return all(np.allclose(u, w, rtol=1e-13, atol=1e-13) for u, w in zip(x, y))
+    assert close(O.softmax_combine(O.softmax_combine(a, b), c), O.softmax_combine(a, O.softmax_combine(b, c)))
+    assert close(O.softmax_combine(a, b), O.softmax_combine(b, a))
+    ident = (np.full(8, -np.inf), np.zeros(8), np.zeros((8, 4)))
+    assert close(O.softmax_combine(a, ident), a) and close(O.softmax_combine(ident, a), a)
+
+
+def test_softmax_partial_brute_force():
+    """(m, l, o) of one shard against pure-Python loops."""
+    rng = np.random.default_rng(33)
+    q, k, v = rng.standard_normal((3, 4)), rng.standard_normal((5, 4)), rng.standard_normal((5, 4))
+    m, l, o = O.softmax_partial(q, k, v, 0.5, True, np.array([1, 3, 9]), np.arange(2, 7))
+    for i, qp in enumerate([1, 3, 9]):
+        s = [0.5 * sum(q[i][t] * k[j][t] for t in range(4)) for j in range(5) if 2 + j <= qp]
+        js = [j for j in range(5) if 2 + j <= qp]
+        if not s:
+            assert m[i] == -np.inf and l[i] == 0 and not o[i].any()
+            continue
+        mm = max(s)
+        assert m[i] == pytest.approx(mm, rel=1e-14)
+        assert l[i] == pytest.approx(sum(math.exp(x - mm) for x in s), rel=1e-13)
+        for t in range(4):
+            assert o[i][t] == pytest.approx(sum(math.exp(x - mm) * v[j][t] for x, j in zip(s, js)), rel=1e-12, abs=1e-14)
