@@ -104,6 +104,19 @@ def activation(x: np.ndarray, act: str) -> np.ndarray:
     raise ValueError(f"unknown activation {act!r}")
 
 
+def activation_grad(x: np.ndarray, act: str) -> np.ndarray:
+    """d act(x) / dx.  GELU-erf is x Phi(x), so by the product rule its
+    derivative is Phi(x) + x phi(x) with phi the standard normal density."""
+    x = np.asarray(x, np.float64)
+    if act == "none":
+        return np.ones_like(x)
+    if act == "gelu":
+        cdf = 0.5 * (1.0 + _erf(x / math.sqrt(2.0)))
+        pdf = np.exp(-0.5 * x * x) / math.sqrt(2.0 * math.pi)
+        return cdf + x * pdf
+    raise ValueError(f"unknown activation {act!r}")
+
+
 def rmsnorm(x: np.ndarray, g: np.ndarray, eps: float) -> np.ndarray:
     x = np.asarray(x, np.float64)
     ms = np.mean(x * x, axis=-1, keepdims=True)
@@ -276,6 +289,104 @@ def mlp_ref(X, W1, W2, b1=None, b2=None, act="gelu"):
     if b2 is not None:
         y = y + b2
     return y
+
+
+def mlp_block_backward(X, W1, W2, dY, b1=None, act="gelu", R_batch=1, R_model=1, return_norm=False):
+    """Gradients of mlp_block for the output cotangent dY, as loop nests over
+    the same batch (b, R_batch) and model (m, R_model) shards as the forward.
+
+    Reverse-mode differentiation of a partitioned program is again a
+    partitioned program (the paper partitions whole training steps, Sec. 7):
+    every product of the backward pass is a matmul whose operands are sliced
+    exactly as the matmul tile-mapping entries of Sec. 5.2.1 demand, so a
+    gradient that contracts over a sliced dimension is a #sum loop:
+
+      Z[b][:, m]  = slice 0 X[b] @ slice 1 W1[m] + slice 0 b1[m]      (recomputed)
+      dH[b][:, m] = slice 0 dY[b] @ (slice 0 W2[m])^T
+      dZ[b][:, m] = dH[b][:, m] * act'(Z[b][:, m])
+      dW2 = loop m [#tile<0>] { loop b [#sum] { act(Z[b][:, m])^T @ slice 0 dY[b] } }
+      dW1 = loop m [#tile<1>] { loop b [#sum] { (slice 0 X[b])^T @ dZ[b][:, m] } }
+      dX  = loop b [#tile<0>] { loop m [#sum] { dZ[b][:, m] @ (slice 1 W1[m])^T } }
+      db1 = loop m [#tile<0>] { loop b [#sum] { column sums of dZ[b][:, m] } }
+      db2 = loop b [#sum] { column sums of slice 0 dY[b] }
+
+    X [T, D], W1 [D, F], W2 [F, D], dY [T, D], b1 [F] or None.  Returns a dict
+    with dX [T, D], dW1 [D, F], dW2 [F, D], db1 [F], db2 [D].  With
+    ``return_norm`` also a dict of elementwise normalisers: each gradient's
+    last contraction with every operand replaced by a first-order bound on
+    its own magnitude and error sensitivity (see mlp_backward_norms).
+    """
+    T = X.shape[0]
+    F = W1.shape[1]
+    if T % R_batch or F % R_model:
+        raise ValueError("indivisible partition")
+    b1v = None if b1 is None else np.asarray(b1, np.float64)
+    shard = {}
+    for b in range(R_batch):
+        xb, dyb = slice_(X, 0, b, R_batch), slice_(dY, 0, b, R_batch)
+        for m in range(R_model):
+            z = matmul(xb, slice_(W1, 1, m, R_model))
+            if b1v is not None:
+                z = z + slice_(b1v, 0, m, R_model)
+            dh = matmul(dyb, slice_(W2, 0, m, R_model).T)
+            dz = dh * activation_grad(z, act)
+            shard[b, m] = dict(x=xb, dy=dyb, z=z, h=activation(z, act), dh=dh, dz=dz)
+    w1 = lambda m: slice_(W1, 1, m, R_model)
+    g = {
+        "dW2": loop_tile(R_model, 0, lambda m: loop_sum(
+            R_batch, lambda b: matmul(shard[b, m]["h"].T, shard[b, m]["dy"]))),
+        "dW1": loop_tile(R_model, 1, lambda m: loop_sum(
+            R_batch, lambda b: matmul(shard[b, m]["x"].T, shard[b, m]["dz"]))),
+        "dX": loop_tile(R_batch, 0, lambda b: loop_sum(
+            R_model, lambda m: matmul(shard[b, m]["dz"], w1(m).T))),
+        "db1": loop_tile(R_model, 0, lambda m: loop_sum(
+            R_batch, lambda b: np.sum(shard[b, m]["dz"], axis=0))),
+        "db2": loop_sum(R_batch, lambda b: np.sum(shard[b, 0]["dy"], axis=0)),
+    }
+    if not return_norm:
+        return g
+    return g, mlp_backward_norms(X, W1, W2, dY, b1, act)
+
+
+def mlp_backward_norms(X, W1, W2, dY, b1=None, act="gelu"):
+    """Elementwise error normalisers for the MLP gradients, by first-order
+    error propagation through the unpartitioned backward pass:
+
+      nZ  = |X| |W1| + |b1|                  (normaliser of Z's contraction)
+      ndH = |dY| |W2|^T
+      ndZ = ndH |act'(Z)| + |dH| nZ          (sup |GELU''| = 2 phi(0) < 1)
+      nH  = |act'(Z)| nZ + |act(Z)|
+      dW2: nH^T |dY|,  dW1: |X|^T ndZ,  dX: ndZ |W1|^T,
+      db1: column sums of ndZ,  db2: column sums of |dY|.
+    For the identity activation ndZ = ndH and nH = nZ.
+    """
+    nz = abs_product(X, W1)
+    z = matmul(X, W1)
+    if b1 is not None:
+        nz = nz + np.abs(np.asarray(b1, np.float64))
+        z = z + np.asarray(b1, np.float64)
+    ndh = abs_product(dY, np.asarray(W2, np.float64).T)
+    dh = matmul(dY, np.asarray(W2, np.float64).T)
+    if act == "none":
+        ndz, nh = ndh, nz
+    else:
+        gp = np.abs(activation_grad(z, act))
+        ndz = ndh * gp + np.abs(dh) * nz
+        nh = gp * nz + np.abs(activation(z, act))
+    return {"dW2": matmul(nh.T, np.abs(dY)), "dW1": matmul(np.abs(X).T, ndz),
+            "dX": matmul(ndz, np.abs(W1).T), "db1": np.sum(ndz, axis=0),
+            "db2": np.sum(np.abs(np.asarray(dY, np.float64)), axis=0)}
+
+
+def mlp_backward_ref(X, W1, W2, dY, b1=None, act="gelu"):
+    """Unpartitioned gradients of act(X W1 + b1) W2 + b2 for cotangent dY."""
+    z = matmul(X, W1)
+    if b1 is not None:
+        z = z + np.asarray(b1, np.float64)
+    dz = matmul(dY, np.asarray(W2, np.float64).T) * activation_grad(z, act)
+    return {"dW2": matmul(activation(z, act).T, dY), "dW1": matmul(np.asarray(X, np.float64).T, dz),
+            "dX": matmul(dz, np.asarray(W1, np.float64).T), "db1": np.sum(dz, axis=0),
+            "db2": np.sum(np.asarray(dY, np.float64), axis=0)}
 
 
 # ---------------------------------------------------------------------------

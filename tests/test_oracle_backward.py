@@ -1,0 +1,175 @@
+"""Pins for the oracle's MLP backward pass (gradients as loop nests).
+
+The gradients are pinned to things other than the oracle's own formulas:
+closed forms of GELU's derivative, central finite differences of the
+(separately pinned) forward shard interpreter, torch's fp64 autograd of the
+same forward, and bitwise integer arithmetic for the identity activation
+across partition sizes.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import partir_oracle as O
+
+KEYS = ("dX", "dW1", "dW2", "db1", "db2")
+
+
+def ints(rng, shape, lo=-2, hi=2):
+    return rng.integers(lo, hi + 1, size=shape).astype(np.float64)
+
+
+def problem(seed, T=16, D=8, F=32, scale=1.0):
+    rng = np.random.default_rng(seed)
+    X = rng.standard_normal((T, D)) * scale
+    W1 = rng.standard_normal((D, F)) / math.sqrt(D)
+    W2 = rng.standard_normal((F, D)) / math.sqrt(F)
+    dY = rng.standard_normal((T, D))
+    b1 = rng.standard_normal(F) * 0.5
+    return X, W1, W2, dY, b1
+
+
+# ---------------------------------------------------------------------------
+# GELU derivative
+# ---------------------------------------------------------------------------
+def test_gelu_grad_closed_forms():
+    assert O.activation_grad(np.array([0.0]), "gelu")[0] == 0.5
+    x = np.linspace(-7, 7, 113)
+    # Phi(x) + Phi(-x) = 1 and x phi(x) is odd: gelu'(x) + gelu'(-x) = 1
+    assert np.max(np.abs(O.activation_grad(x, "gelu") + O.activation_grad(-x, "gelu") - 1)) < 1e-15
+    assert np.all(np.abs(O.activation_grad(np.array([40.0]), "gelu") - 1) < 1e-15)
+    assert np.all(np.abs(O.activation_grad(np.array([-40.0]), "gelu")) < 1e-30)
+    assert np.array_equal(O.activation_grad(x, "none"), np.ones_like(x))
+    # the minimum of gelu' (near x = -1.4142) equals 1 - Phi(sqrt2) - sqrt2 phi(sqrt2)
+    s2 = math.sqrt(2.0)
+    closed = 0.5 * math.erfc(1.0) - s2 * math.exp(-1.0) / math.sqrt(2 * math.pi)
+    assert abs(O.activation_grad(np.array([-s2]), "gelu")[0] - closed) < 1e-16
+
+
+def test_gelu_grad_matches_central_differences_and_torch():
+    x = np.random.default_rng(3).standard_normal(301) * 3
+    h = 1e-5
+    fd = (O.gelu_erf(x + h) - O.gelu_erf(x - h)) / (2 * h)
+    assert np.max(np.abs(O.activation_grad(x, "gelu") - fd)) < 1e-9
+    t = torch.from_numpy(x).requires_grad_(True)
+    torch.nn.functional.gelu(t, approximate="none").sum().backward()
+    assert np.max(np.abs(O.activation_grad(x, "gelu") - t.grad.numpy())) < 1e-15
+
+
+# ---------------------------------------------------------------------------
+# MLP gradients
+# ---------------------------------------------------------------------------
+def torch_grads(X, W1, W2, dY, b1, act):
+    ts = {k: torch.from_numpy(np.array(v)).requires_grad_(True)
+          for k, v in dict(X=X, W1=W1, W2=W2, b1=b1, b2=np.zeros(W2.shape[1])).items()}
+    z = ts["X"] @ ts["W1"] + ts["b1"]
+    h = torch.nn.functional.gelu(z, approximate="none") if act == "gelu" else z
+    y = h @ ts["W2"] + ts["b2"]
+    y.backward(torch.from_numpy(dY))
+    return {"dX": ts["X"].grad.numpy(), "dW1": ts["W1"].grad.numpy(), "dW2": ts["W2"].grad.numpy(),
+            "db1": ts["b1"].grad.numpy(), "db2": ts["b2"].grad.numpy()}
+
+
+@pytest.mark.parametrize("act", ["gelu", "none"])
+@pytest.mark.parametrize("Rb,Rm", [(1, 1), (2, 4), (4, 2), (1, 8)])
+def test_mlp_backward_matches_torch_autograd(act, Rb, Rm):
+    X, W1, W2, dY, b1 = problem(10 + Rb * 8 + Rm)
+    want = torch_grads(X, W1, W2, dY, b1, act)
+    got = O.mlp_block_backward(X, W1, W2, dY, b1, act, Rb, Rm)
+    ref = O.mlp_backward_ref(X, W1, W2, dY, b1, act)
+    for k in KEYS:
+        assert got[k].shape == want[k].shape
+        assert np.max(np.abs(got[k] - want[k])) < 1e-12, k
+        assert np.max(np.abs(ref[k] - want[k])) < 1e-12, k
+
+
+def test_mlp_backward_central_differences_of_the_forward():
+    """dL/dtheta for L = <mlp_block(theta), dY>, entry by entry."""
+    T, D, F = 4, 3, 8
+    X, W1, W2, dY, b1 = problem(5, T, D, F)
+    b2 = np.zeros(D)
+    g = O.mlp_block_backward(X, W1, W2, dY, b1, "gelu", 2, 4)
+    args = dict(X=X, W1=W1, W2=W2, b1=b1, b2=b2)
+    names = {"dX": "X", "dW1": "W1", "dW2": "W2", "db1": "b1", "db2": "b2"}
+    h = 1e-6
+
+    def loss(a):
+        return float(np.sum(O.mlp_block(a["X"], a["W1"], a["W2"], a["b1"], a["b2"], "gelu", 2, 4) * dY))
+
+    for gk, ak in names.items():
+        base = args[ak]
+        for idx in np.ndindex(base.shape):
+            up, dn = base.copy(), base.copy()
+            up[idx] += h
+            dn[idx] -= h
+            fd = (loss(dict(args, **{ak: up})) - loss(dict(args, **{ak: dn}))) / (2 * h)
+            assert abs(g[gk][idx] - fd) < 1e-7 * max(1.0, abs(fd)), (gk, idx)
+
+
+@pytest.mark.parametrize("Rb,Rm", [(1, 1), (2, 2), (4, 8), (8, 1)])
+def test_mlp_backward_integer_exact_bitwise(Rb, Rm):
+    """Identity activation on small integers: every gradient is an integer
+    matrix product, exact in fp64 whatever the partition."""
+    rng = np.random.default_rng(Rb * 16 + Rm)
+    T, D, F = 32, 8, 64
+    X, W1, W2, dY = ints(rng, (T, D)), ints(rng, (D, F)), ints(rng, (F, D)), ints(rng, (T, D))
+    b1 = ints(rng, F)
+    g = O.mlp_block_backward(X, W1, W2, dY, b1, "none", Rb, Rm)
+    dZ = dY @ W2.T
+    assert np.array_equal(g["dX"], dZ @ W1.T)
+    assert np.array_equal(g["dW1"], X.T @ dZ)
+    assert np.array_equal(g["dW2"], (X @ W1 + b1).T @ dY)
+    assert np.array_equal(g["db1"], dZ.sum(axis=0))
+    assert np.array_equal(g["db2"], dY.sum(axis=0))
+
+
+def test_mlp_backward_sum_loops_visit_every_shard():
+    """Each #sum loop adds exactly R terms: with the batch loop of 4 shards,
+    scaling one shard's cotangent by 2 moves dW2 by that shard's term once."""
+    X, W1, W2, dY, b1 = problem(6, T=16)
+    base = O.mlp_block_backward(X, W1, W2, dY, b1, "gelu", 4, 2)
+    dY2 = dY.copy()
+    dY2[4:8] *= 2
+    moved = O.mlp_block_backward(X, W1, W2, dY2, b1, "gelu", 4, 2)
+    h = O.gelu_erf(X[4:8] @ W1 + b1)
+    assert np.max(np.abs(moved["dW2"] - base["dW2"] - h.T @ dY[4:8])) < 1e-12
+    assert np.max(np.abs(moved["db2"] - base["db2"] - dY[4:8].sum(axis=0))) < 1e-12
+
+
+def test_mlp_backward_norms_bound_the_gradients():
+    X, W1, W2, dY, b1 = problem(7)
+    g, n = O.mlp_block_backward(X, W1, W2, dY, b1, "gelu", 2, 4, return_norm=True)
+    for k in KEYS:
+        assert n[k].shape == g[k].shape
+        assert np.all(np.abs(g[k]) <= n[k] * (1 + 1e-12)), k
+    # identity activation: the normalisers are plain |A|.|B| of each product
+    g, n = O.mlp_block_backward(X, W1, W2, dY, b1, "none", 1, 1, return_norm=True)
+    dZa = np.abs(dY) @ np.abs(W2).T
+    assert np.allclose(n["dX"], dZa @ np.abs(W1).T, rtol=1e-13, atol=0)
+    assert np.allclose(n["dW2"], (np.abs(X) @ np.abs(W1) + np.abs(b1)).T @ np.abs(dY), rtol=1e-13, atol=0)
+
+
+def test_mlp_backward_empty_sizes():
+    rng = np.random.default_rng(9)
+    D, F = 8, 16
+    W1, W2 = rng.standard_normal((D, F)), rng.standard_normal((F, D))
+    # no tokens: the weight gradients are empty sums over the batch
+    g = O.mlp_block_backward(np.zeros((0, D)), W1, W2, np.zeros((0, D)), np.ones(F), "gelu", 2, 4)
+    assert g["dX"].shape == (0, D)
+    for k, shape in (("dW1", (D, F)), ("dW2", (F, D)), ("db1", (F,)), ("db2", (D,))):
+        assert g[k].shape == shape and np.array_equal(g[k], np.zeros(shape))
+    # no hidden units: dX is the empty sum over the model loop
+    X, dY = rng.standard_normal((16, D)), rng.standard_normal((16, D))
+    g = O.mlp_block_backward(X, np.zeros((D, 0)), np.zeros((0, D)), dY, None, "gelu", 2, 4)
+    assert np.array_equal(g["dX"], np.zeros((16, D)))
+    assert g["dW1"].shape == (D, 0) and g["dW2"].shape == (0, D) and g["db1"].shape == (0,)
+    assert np.allclose(g["db2"], dY.sum(axis=0), rtol=1e-15, atol=1e-15)
+
+
+def test_mlp_backward_rejects_indivisible():
+    with pytest.raises(ValueError):
+        O.mlp_block_backward(np.zeros((6, 2)), np.zeros((2, 8)), np.zeros((8, 2)), np.zeros((6, 2)), R_batch=4)
+    with pytest.raises(ValueError):
+        O.mlp_block_backward(np.zeros((8, 2)), np.zeros((2, 6)), np.zeros((6, 2)), np.zeros((8, 2)), R_model=4)

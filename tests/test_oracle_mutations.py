@@ -11,6 +11,7 @@ import numpy as np
 import pytest
 
 from oracle import partir_oracle as O
+from tests import test_oracle_backward as BW
 from tests import test_oracle_core as C
 from tests import test_oracle_ops as P
 from tests import test_oracle_programs as G
@@ -87,6 +88,20 @@ def _mlp_bias_inside(X, W1, W2, b1=None, b2=None, act="gelu", R_batch=1, R_model
     return _real["mlp_block"](X, W1, W2, b1, b2, act, R_batch, R_model, rows, return_norm)
 
 
+def _gelu_grad_cdf_only(x, act):
+    from scipy.special import erf
+    x = np.asarray(x, np.float64)
+    return np.ones_like(x) if act == "none" else 0.5 * (1 + erf(x / math.sqrt(2)))
+
+
+def _gelu_grad_minus(x, act):
+    from scipy.special import erf
+    x = np.asarray(x, np.float64)
+    if act == "none":
+        return np.ones_like(x)
+    return 0.5 * (1 + erf(x / math.sqrt(2))) - x * np.exp(-0.5 * x * x) / math.sqrt(2 * math.pi)
+
+
 def _attend_k_from_q(xb, Wq_m, Wk_m, Wv_m, *rest):
     return _real["_attend_shard"](xb, Wq_m, Wq_m, Wv_m, *rest)
 
@@ -107,6 +122,8 @@ def _run(pins, golden):
                 pin(2, 4)
             elif pin.__name__ == "test_mlp_integer_exact_across_partitions":
                 pin(2, 4)
+            elif pin.__name__ == "test_mlp_backward_matches_torch_autograd":
+                pin("gelu", 2, 4)
             else:
                 pin(**kwargs)
         except (AssertionError, ValueError, FloatingPointError):
@@ -135,6 +152,11 @@ CASES = {
     "attention forgets the scale": ("causal_attention", _attn_variant(lambda kp, qp: kp <= qp, scaled=False),
                                     [P.test_attention_brute_force, P.test_attention_matches_torch_sdpa]),
     "bias added inside the #sum": ("mlp_block", _mlp_bias_inside, [G.test_mlp_bias_of_sum_loop_is_added_once]),
+    "gelu derivative drops x phi(x)": ("activation_grad", _gelu_grad_cdf_only,
+                                       [BW.test_gelu_grad_closed_forms, BW.test_mlp_backward_matches_torch_autograd]),
+    "gelu derivative subtracts x phi(x)": ("activation_grad", _gelu_grad_minus,
+                                           [BW.test_gelu_grad_matches_central_differences_and_torch,
+                                            BW.test_mlp_backward_central_differences_of_the_forward]),
     "keys projected with Wq": ("_attend_shard", _attend_k_from_q, [G.test_attn_block_brute_force]),
 }
 
