@@ -77,6 +77,29 @@ def setup(w, P, I):
         step = lambda: P.mlp_block(X, W1t, W2t, R_batch=w["R_batch"], R_model=w["R_model"], out=Y, workspace=ws)
         roles = {"mlp.up": 2.0 * T * D * F, "mlp.down": 2.0 * T * D * F}
         return x, step, roles, "mfma_bf16"
+    if w.kind == "mlp_train":
+        T, D, F, Rb, Rm = w["T"], w["D"], w["F"], w["R_batch"], w["R_model"]
+        X, W1t, W2t, dY, b1 = x["X"].to_device(), dev_t(x["W1"]), dev_t(x["W2"]), x["dY"].to_device(), \
+            x["b1"].to_device()
+        Y = torch.empty((T, D), dtype=torch.float32, device="cuda")
+        wsf = torch.empty(P.mlp_block_workspace(T, D, F, P.F32, Rb, Rm), dtype=torch.uint8, device="cuda")
+        wsb = torch.empty(P.lib().partir_mlp_block_backward_workspace(T, D, F, P.ACT_GELU, 1, Rb, Rm),
+                          dtype=torch.uint8, device="cuda")
+
+        f32 = dict(dtype=torch.float32, device="cuda")
+        grads = (torch.empty((T, D), **f32), torch.empty((F, D), **f32), torch.empty((D, F), **f32),
+                 torch.empty((F,), **f32), torch.empty((D,), **f32))
+
+        def step():
+            # forward, then every gradient of the same nest (a training step
+            # without the optimizer update, which is elementwise)
+            P.mlp_block(X, W1t, W2t, b1=b1, R_batch=Rb, R_model=Rm, out=Y, workspace=wsf)
+            P.mlp_block_backward(X, W1t, W2t, dY, b1=b1, R_batch=Rb, R_model=Rm, bias_grads=True, out=grads,
+                                 workspace=wsb)
+        f = 2.0 * T * D * F
+        roles = {"mlp.up": f, "mlp.down": f, "mlp.bwd.z": f, "mlp.bwd.dh": f, "mlp.bwd.dw2": f,
+                 "mlp.bwd.dw1": f, "mlp.bwd.dx": f}
+        return x, step, roles, "mfma_bf16"
     if w.kind == "attn":
         B, S, D, H = w["B"], w["S"], w["D"], w["H"]
         T = B * S
@@ -162,6 +185,28 @@ def cpu_baseline(w, x, target_s):
         return dict(value=total_rows * per_row / total_t / 1e12, unit="TFLOP/s", cores=cores, kind="oracle",
                     sample=f"{total_rows} output rows of the {w['T']}-row block in {reps} seeded samples "
                            f"(all {w['R_model']} model shards each), {total_t:.1f} s")
+    if w.kind == "mlp_train":
+        T, D, F = w["T"], w["D"], w["F"]
+        X, W1, W2, dY, b1 = (x[k].f64() for k in ("X", "W1", "W2", "dY", "b1"))
+        rng = np.random.default_rng(0)
+        n, total_t, work, done = 8, 0.0, 0.0, [0, 0]
+        while total_t < target_s:
+            rows = np.sort(rng.choice(T, size=min(n, T), replace=False))
+            units = np.sort(rng.choice(F, size=min(n, F), replace=False))
+            t0 = time.perf_counter()
+            O.mlp_block(X, W1, W2, b1, None, "gelu", w["R_batch"], w["R_model"], rows=rows)
+            O.mlp_block_backward_sampled(X, W1, W2, dY, b1, "gelu", w["R_batch"], w["R_model"], rows, units)
+            total_t += time.perf_counter() - t0
+            # forward row 4DF; dX row: its dH row and product 4DF; hidden unit:
+            # its dH column, dW1 column and dW2 row 6TD
+            work += len(rows) * 8.0 * D * F + len(units) * 6.0 * T * D
+            done[0] += len(rows)
+            done[1] += len(units)
+            n *= 2
+        return dict(value=work / total_t / 1e12, unit="TFLOP/s", cores=cores, kind="oracle",
+                    sample=f"{done[0]} token rows (forward output and dX) and {done[1]} hidden units "
+                           f"(dW1 column, dW2 row, db1) in seeded samples, every shard that owns them, "
+                           f"{total_t:.1f} s")
     if w.kind == "attn":
         S, D = w["S"], w["D"]
         Xf = x["X"].f64()

@@ -169,6 +169,41 @@ size_t partir_mlp_block_workspace(int64_t T, int64_t D, int64_t F, int out_dtype
                                   int R_batch, int R_model);
 
 /* ------------------------------------------------------------------------ */
+/* Backward pass of the MLP block (the evaluation trains, Sec. 7; gradient   */
+/* reductions of batch and model parallelism, Sec. 2.3).                      */
+/* ------------------------------------------------------------------------ */
+/*
+ * Given dY = dL/dY of partir_mlp_block's output (Z = X W1 + b1, H = act(Z),
+ * Y = H W2 + b2), computes, with the same batch (R_batch) and model
+ * (R_model) loops:
+ *   dH  = dY W2^T      loop b [#tile<0>] { loop m [#tile<1>] }
+ *   dZ  = dH * act'(Z) (Z recomputed)
+ *   dW2 = H^T dY       loop m [#tile<0>] { loop b [#sum] }   the batch-parallel gradient sum
+ *   dW1 = X^T dZ       loop m [#tile<1>] { loop b [#sum] }
+ *   dX  = dZ W1^T      loop b [#tile<0>] { loop m [#sum] }   the model-parallel sum
+ *   db1 = sum_t dZ, db2 = sum_t dY  (in fixed row-block order)
+ * X, W1t, W2t, b1 as in partir_mlp_block; dY: [T, D] bf16.  Outputs fp32:
+ * dX [T, D]; dW1t = dW1^T [F, D] and dW2t = dW2^T [D, F] (the weights'
+ * stored layout); db1 [F], db2 [D] (either may be NULL: not computed).
+ * Intermediates Z, dH, dZ are bf16 in the workspace, which also holds the
+ * transposes the token-contracting products read (X^T, dY^T, H^T, dZ^T,
+ * W1, W2).  Constraints: D, F/R_model and T/R_batch multiples of 8.  A size
+ * of 0 gives empty sums (zeros) for every non-empty gradient.
+ * Errors: E_NULL, E_SHAPE, E_DIVISIBILITY, E_LAYOUT, E_WORKSPACE,
+ * E_UNSUPPORTED (R < 1, unknown act), E_HIP.
+ */
+int partir_mlp_block_backward(const void* X, const void* W1t, const void* b1,
+                              const void* W2t, const void* dY,
+                              void* dX, void* dW1t, void* db1, void* dW2t, void* db2,
+                              int64_t T, int64_t D, int64_t F, int act,
+                              int R_batch, int R_model,
+                              void* ws, size_t ws_bytes, void* stream);
+
+/* with_bias_grads: nonzero if db1 / db2 will be requested. */
+size_t partir_mlp_block_backward_workspace(int64_t T, int64_t D, int64_t F, int act,
+                                           int with_bias_grads, int R_batch, int R_model);
+
+/* ------------------------------------------------------------------------ */
 /* Attention block: heads #tile inside a Megatron #sum, in a batch #tile.     */
 /* ------------------------------------------------------------------------ */
 /*
@@ -282,6 +317,8 @@ int partir_plan_attn_block(int64_t B, int64_t S, int64_t D, int64_t n_heads, int
                            int R_batch, int R_model, partir_plan_info* info);
 int partir_plan_attention(int64_t B, int64_t S, int64_t n_heads, int64_t d_head, int causal, int R_kv,
                           partir_plan_info* info);
+int partir_plan_mlp_block_backward(int64_t T, int64_t D, int64_t F, int act, int R_batch, int R_model,
+                                   partir_plan_info* info);
 int partir_plan_decoder_layer(int64_t B, int64_t S, int64_t D, int64_t n_heads,
                               int64_t d_head, int64_t F, int R_batch, int R_model,
                               partir_plan_info* info);

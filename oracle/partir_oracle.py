@@ -348,6 +348,84 @@ def mlp_block_backward(X, W1, W2, dY, b1=None, act="gelu", R_batch=1, R_model=1,
     return g, mlp_backward_norms(X, W1, W2, dY, b1, act)
 
 
+def mlp_block_backward_sampled(X, W1, W2, dY, b1=None, act="gelu", R_batch=1, R_model=1,
+                               rows=(), units=()):
+    """The loop nests of mlp_block_backward evaluated only where asked, each
+    entry by the shards that own it: dX at token ``rows`` (batch shard b of
+    the row, #sum over every model shard m) and, at hidden ``units`` f (model
+    shard m of the unit, #sum over every batch shard b), dW1[:, f], dW2[f, :]
+    and db1[f]; db2 in full.  Returns (values, normalisers), both dicts with
+    dX [len(rows), D], dW1 [D, len(units)], dW2 [len(units), D],
+    db1 [len(units)], db2 [D].
+    """
+    T, D = X.shape
+    F = W1.shape[1]
+    if T % R_batch or F % R_model:
+        raise ValueError("indivisible partition")
+    X, W1, W2, dY = (np.asarray(a, np.float64) for a in (X, W1, W2, dY))
+    b1v = np.zeros(F) if b1 is None else np.asarray(b1, np.float64)
+    Tb, Fm = T // R_batch, F // R_model
+    rows, units = np.asarray(rows, int), np.asarray(units, int)
+
+    def unit_grads(x, dy, w1, b1s, w2):
+        """z, h, dz of one shard's tokens x over one shard's hidden units."""
+        z = matmul(x, w1) + b1s
+        dh = matmul(dy, w2.T)
+        return z, activation(z, act), dh, dh * activation_grad(z, act)
+
+    out = {"dX": np.zeros((len(rows), D)), "dW1": np.zeros((D, len(units))),
+           "dW2": np.zeros((len(units), D)), "db1": np.zeros(len(units))}
+    nrm = {k: np.zeros_like(v) for k, v in out.items()}
+    for i, t in enumerate(rows):
+        b = t // Tb
+        x, dy = slice_(X, 0, b, R_batch)[t - b * Tb][None], slice_(dY, 0, b, R_batch)[t - b * Tb][None]
+
+        def shard(m):
+            w1, w2 = slice_(W1, 1, m, R_model), slice_(W2, 0, m, R_model)
+            z, _, dh, dz = unit_grads(x, dy, w1, slice_(b1v, 0, m, R_model), w2)
+            n = _dz_norm(x, dy, w1, slice_(b1v, 0, m, R_model), w2, z, dh, act)
+            return matmul(dz, w1.T)[0], matmul(n, np.abs(w1).T)[0]
+
+        parts = [shard(m) for m in range(R_model)]
+        out["dX"][i] = loop_sum(R_model, lambda m: parts[m][0])
+        nrm["dX"][i] = loop_sum(R_model, lambda m: parts[m][1])
+    for j, f in enumerate(units):
+        m = f // Fm
+        w1, w2 = slice_(W1, 1, m, R_model)[:, [f - m * Fm]], slice_(W2, 0, m, R_model)[[f - m * Fm]]
+        b1s = slice_(b1v, 0, m, R_model)[[f - m * Fm]]
+
+        def shard(b):
+            x, dy = slice_(X, 0, b, R_batch), slice_(dY, 0, b, R_batch)
+            z, h, dh, dz = unit_grads(x, dy, w1, b1s, w2)
+            ndz = _dz_norm(x, dy, w1, b1s, w2, z, dh, act)
+            nh = abs_product(x, w1) + np.abs(b1s)
+            if act != "none":
+                nh = np.abs(activation_grad(z, act)) * nh + np.abs(h)
+            return (matmul(x.T, dz)[:, 0], matmul(h.T, dy)[0], np.sum(dz),
+                    matmul(np.abs(x).T, ndz)[:, 0], matmul(nh.T, np.abs(dy))[0], np.sum(ndz))
+
+        parts = [shard(b) for b in range(R_batch)]
+        for k, key in enumerate(("dW1", "dW2", "db1")):
+            val = loop_sum(R_batch, lambda b: np.asarray(parts[b][k]))
+            nv = loop_sum(R_batch, lambda b: np.asarray(parts[b][k + 3]))
+            if key == "dW1":
+                out[key][:, j], nrm[key][:, j] = val, nv
+            else:
+                out[key][j], nrm[key][j] = val, nv
+    out["db2"] = loop_sum(R_batch, lambda b: np.sum(slice_(dY, 0, b, R_batch), axis=0))
+    nrm["db2"] = loop_sum(R_batch, lambda b: np.sum(np.abs(slice_(dY, 0, b, R_batch)), axis=0))
+    return out, nrm
+
+
+def _dz_norm(x, dy, w1, b1s, w2, z, dh, act):
+    """First-order normaliser of dZ for one shard (mlp_backward_norms)."""
+    ndh = abs_product(dy, w2.T)
+    if act == "none":
+        return ndh
+    nz = abs_product(x, w1) + np.abs(b1s)
+    return ndh * np.abs(activation_grad(z, act)) + np.abs(dh) * nz
+
+
 def mlp_backward_norms(X, W1, W2, dY, b1=None, act="gelu"):
     """Elementwise error normalisers for the MLP gradients, by first-order
     error propagation through the unpartitioned backward pass:

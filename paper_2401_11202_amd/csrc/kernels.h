@@ -114,4 +114,41 @@ struct RmsParams {
 };
 hipError_t launch_rmsnorm(const RmsParams& p, hipStream_t s);
 
+// out[c][r] = in[r][c] for a bf16 [rows, cols] matrix (rows, cols multiples
+// of 8; 64 x 64 tiles through LDS).
+struct TransposeParams {
+  const uint16_t* in;
+  uint16_t* out;
+  int64_t ldi, ldo;
+  int rows, cols;
+};
+hipError_t launch_transpose_bf16(const TransposeParams& p, hipStream_t s);
+
+// Backward of H = act(Z) for Z, dH [rows, cols] bf16: dZ = dH * act'(Z)
+// (row-major) and the transposes H^T, dZ^T [cols, rows] (for the weight
+// gradients' contractions over rows).  act 0 = identity, 1 = GELU-erf.
+struct ActBwdParams {
+  const uint16_t* Z;
+  const uint16_t* dH;
+  uint16_t* dZ;
+  uint16_t* Ht;
+  uint16_t* dZt;
+  int64_t ld, ldt;
+  int rows, cols;
+  int act;
+};
+hipError_t launch_act_backward(const ActBwdParams& p, hipStream_t s);
+
+// out[c] = sum over rows of in[r][c] (bf16 in, fp32 out), rows summed in
+// blocks of `chunk` into partial[ceil(rows / chunk)][cols], then the blocks in
+// order: deterministic.
+struct ColSumParams {
+  const uint16_t* in;
+  float* partial;
+  float* out;
+  int64_t ld;
+  int rows, cols, chunk;
+};
+hipError_t launch_colsum(const ColSumParams& p, hipStream_t s);
+
 }  // namespace partir

@@ -59,7 +59,7 @@ bool valid_dtype(int dt) { return dt == PARTIR_F32 || dt == PARTIR_BF16; }
 // ---------------------------------------------------------------------------
 // Plans
 // ---------------------------------------------------------------------------
-enum LaunchKind { L_GEMM_BF16, L_GEMM_F32, L_REDUCE, L_ATTN, L_ATTN_COMBINE, L_RMS };
+enum LaunchKind { L_GEMM_BF16, L_GEMM_F32, L_REDUCE, L_ATTN, L_ATTN_COMBINE, L_RMS, L_TRANSPOSE, L_ACT_BWD, L_COLSUM };
 
 struct Launch {
   LaunchKind kind;
@@ -70,6 +70,9 @@ struct Launch {
   ReduceParams reduce{};
   AttnParams attn{};
   RmsParams rms{};
+  TransposeParams tr{};
+  ActBwdParams act{};
+  ColSumParams cs{};
 };
 
 struct Plan {
@@ -238,6 +241,9 @@ hipError_t run_one(const Launch& L, hipStream_t s) {
     case L_ATTN: return launch_attention(L.attn, s);
     case L_ATTN_COMBINE: return launch_attention_combine(L.attn, s);
     case L_RMS: return launch_rmsnorm(L.rms, s);
+    case L_TRANSPOSE: return launch_transpose_bf16(L.tr, s);
+    case L_ACT_BWD: return launch_act_backward(L.act, s);
+    case L_COLSUM: return launch_colsum(L.cs, s);
   }
   return hipErrorInvalidValue;
 }
@@ -728,6 +734,160 @@ void plan_attn_core(const AttnCoreArgs& a, void* ws, Plan& plan) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// partir_mlp_block_backward
+// ---------------------------------------------------------------------------
+struct MlpBwdArgs {
+  const void *X = nullptr, *W1t = nullptr, *b1 = nullptr, *W2t = nullptr, *dY = nullptr;
+  void *dX = nullptr, *dW1t = nullptr, *db1 = nullptr, *dW2t = nullptr, *db2 = nullptr;
+  int64_t T, D, F;
+  int act, Rb, Rm;
+};
+
+int validate_mlp_bwd(const MlpBwdArgs& a, bool with_ptrs) {
+  if (a.T < 0 || a.D < 0 || a.F < 0) return fail(PARTIR_E_SHAPE, "T, D, F must be >= 0");
+  if (a.T > (1 << 30) || a.D > (1 << 20) || a.F > (1 << 22) || a.T * std::max(a.D, a.F) > ((int64_t)1 << 37))
+    return fail(PARTIR_E_SHAPE, "dims too large");
+  if (a.Rb < 1 || a.Rm < 1) return fail(PARTIR_E_UNSUPPORTED, "R_batch and R_model must be >= 1");
+  if (a.act != PARTIR_ACT_NONE && a.act != PARTIR_ACT_GELU_ERF) return fail(PARTIR_E_UNSUPPORTED, "act %d", a.act);
+  if (a.T % a.Rb) return fail(PARTIR_E_DIVISIBILITY, "R_batch=%d does not divide T=%lld", a.Rb, (long long)a.T);
+  if (a.F % a.Rm) return fail(PARTIR_E_DIVISIBILITY, "R_model=%d does not divide F=%lld", a.Rm, (long long)a.F);
+  if (a.D % 8 || (a.F / a.Rm) % 8 || (a.T / a.Rb) % 8)
+    return fail(PARTIR_E_LAYOUT, "D, F/R_model and T/R_batch must be multiples of 8 (16-byte runs; the weight "
+                "gradients contract over tokens)");
+  const bool live = a.T * a.D * a.F > 0;
+  if (with_ptrs && live && (!a.X || !a.W1t || !a.W2t || !a.dY))
+    return fail(PARTIR_E_NULL, "X, W1t, W2t and dY must be non-NULL");
+  if (with_ptrs && ((a.T * a.D > 0 && !a.dX) || (a.F * a.D > 0 && (!a.dW1t || !a.dW2t))))
+    return fail(PARTIR_E_NULL, "dX, dW1t and dW2t must be non-NULL when they hold elements");
+  if (with_ptrs && a.db2 && a.T * a.D > 0 && !a.dY) return fail(PARTIR_E_NULL, "db2 needs dY");
+  if (with_ptrs && (!aligned16(a.X) || !aligned16(a.W1t) || !aligned16(a.W2t) || !aligned16(a.dY) ||
+                    !aligned16(a.dX) || !aligned16(a.dW1t) || !aligned16(a.dW2t) || !aligned16(a.b1) ||
+                    !aligned16(a.db1) || !aligned16(a.db2)))
+    return fail(PARTIR_E_LAYOUT, "tensors must be 16-byte aligned");
+  return PARTIR_OK;
+}
+
+void plan_transpose(const void* in, void* out, int64_t rows, int64_t cols, const char* name, Plan& plan) {
+  Launch L;
+  L.kind = L_TRANSPOSE;
+  L.name = name;
+  L.tr.in = (const uint16_t*)in; L.tr.out = (uint16_t*)out;
+  L.tr.ldi = cols; L.tr.ldo = rows; L.tr.rows = (int)rows; L.tr.cols = (int)cols;
+  char buf[160];
+  snprintf(buf, sizeof buf, "transpose: [%lld,%lld] -> [%lld,%lld] bf16", (long long)rows, (long long)cols,
+           (long long)cols, (long long)rows);
+  L.text = buf;
+  plan.launches.push_back(L);
+}
+
+void plan_colsum(const void* in, void* partial, void* out, int64_t rows, int64_t cols, int chunk, const char* name,
+                 Plan& plan) {
+  Launch L;
+  L.kind = L_COLSUM;
+  L.name = name;
+  L.cs.in = (const uint16_t*)in; L.cs.partial = (float*)partial; L.cs.out = (float*)out;
+  L.cs.ld = cols; L.cs.rows = (int)rows; L.cs.cols = (int)cols; L.cs.chunk = chunk;
+  char buf[160];
+  snprintf(buf, sizeof buf, "colsum: sum over %lld rows of [%lld,%lld], blocks of %d in order (the batch #sum of "
+           "a bias gradient)", (long long)rows, (long long)rows, (long long)cols, chunk);
+  L.text = buf;
+  plan.launches.push_back(L);
+}
+
+// Gradients of the Megatron MLP block (same nest as partir_mlp_block):
+//   Z = X W1 + b1, H = act(Z), Y = H W2 + b2; given dY:
+//   dH = dY W2^T     loop b [#tile<0>] loop m [#tile<1>]
+//   dZ = dH * act'(Z)
+//   dW2 = H^T dY     loop m [#tile<0>] loop b [#sum]   (the batch-parallel gradient reduction)
+//   dW1 = X^T dZ     loop m [#tile<1>] loop b [#sum]
+//   dX = dZ W1^T     loop b [#tile<0>] loop m [#sum]   (the model-parallel reduction)
+//   db1 = sum_t dZ, db2 = sum_t dY
+// Weight gradients are written in the weights' stored (transposed) layout.
+void plan_mlp_bwd(const MlpBwdArgs& a, void* ws, Plan& plan) {
+  const int64_t T = a.T, D = a.D, F = a.F;
+  plan.n_shards = a.Rb * a.Rm;
+  plan.n_tile_loops = 2;
+  plan.flops = 10.0 * T * D * F;          // Z recomputed (2TDF) + dH, dW2, dW1, dX (8TDF)
+  if (T == 0 && D == 0 && F == 0) return;
+  const bool live = T * D * F > 0;
+  // without a contraction only the bias-gradient column sums use the workspace
+  const size_t tf = live ? align_up((size_t)T * F * 2) : 0, td = live ? align_up((size_t)T * D * 2) : 0,
+               df = live ? align_up((size_t)D * F * 2) : 0;
+  const int chunk = 64;
+  const size_t cs_bytes = (a.db1 || a.db2) ? align_up((size_t)((T + chunk - 1) / chunk) * std::max(D, F) * 4) : 0;
+  char* base = (char*)ws;
+  size_t off = 0;
+  auto take = [&](size_t n) { char* p = base ? base + off : nullptr; off += n; return (void*)p; };
+  void* Z = take(tf);
+  void* dH = take(tf);
+  void* dZ = take(tf);
+  void* Ht = take(tf);
+  void* dZt = take(tf);
+  void* Xt = take(td);
+  void* dYt = take(td);
+  void* W1 = take(df);
+  void* W2 = take(df);
+  void* csp = take(cs_bytes);
+  void* part = base ? base + off : nullptr;
+  GemmSpec gz, gh, g2, g1, gx;
+  if (live) {
+    plan_transpose(a.X, Xt, T, D, "bwd.transpose", plan);
+    plan_transpose(a.dY, dYt, T, D, "bwd.transpose", plan);
+    plan_transpose(a.W1t, W1, F, D, "bwd.transpose", plan);
+    plan_transpose(a.W2t, W2, D, F, "bwd.transpose", plan);
+    gz.A = a.X; gz.B[0] = a.W1t; gz.C[0] = Z; gz.bias[0] = (const float*)a.b1;
+    gz.lda = D; gz.ldb = D; gz.ldc = F; gz.M = T; gz.N = F; gz.K = D;
+    gz.c_dtype = PARTIR_BF16; gz.rm = a.Rb; gz.rn = a.Rm;
+    gz.name = "mlp.bwd.z"; gz.label = "bwd.z  Z = slice 0 X[b] . slice 1 W1[m] (recomputed)";
+    plan_gemm(gz, nullptr, plan);
+    gh.A = a.dY; gh.B[0] = W2; gh.C[0] = dH;
+    gh.lda = D; gh.ldb = D; gh.ldc = F; gh.M = T; gh.N = F; gh.K = D;
+    gh.c_dtype = PARTIR_BF16; gh.rm = a.Rb; gh.rn = a.Rm;
+    gh.name = "mlp.bwd.dh"; gh.label = "bwd.dh dH = slice 0 dY[b] . (slice 0 W2[m])^T";
+    plan_gemm(gh, nullptr, plan);
+    Launch E;
+    E.kind = L_ACT_BWD;
+    E.name = "mlp.bwd.act";
+    E.act.Z = (const uint16_t*)Z; E.act.dH = (const uint16_t*)dH; E.act.dZ = (uint16_t*)dZ;
+    E.act.Ht = (uint16_t*)Ht; E.act.dZt = (uint16_t*)dZt; E.act.ld = F; E.act.ldt = T;
+    E.act.rows = (int)T; E.act.cols = (int)F; E.act.act = a.act;
+    E.text = a.act ? "act_backward: dZ = dH * gelu'(Z); H^T, dZ^T" : "act_backward: dZ = dH; H^T, dZ^T";
+    plan.launches.push_back(E);
+    g2.A = dYt; g2.B[0] = Ht; g2.C[0] = a.dW2t;
+    g2.lda = T; g2.ldb = T; g2.ldc = F; g2.M = D; g2.N = F; g2.K = T;
+    g2.ab_dtype = PARTIR_BF16; g2.c_dtype = PARTIR_F32; g2.rn = a.Rm; g2.rk = a.Rb;
+    g2.name = "mlp.bwd.dw2"; g2.label = "bwd.dw2 dW2^T = sum_b (slice 0 dY[b])^T . H[b][:, m]";
+    plan_gemm(g2, part, plan);
+    g1.A = dZt; g1.B[0] = Xt; g1.C[0] = a.dW1t;
+    g1.lda = T; g1.ldb = T; g1.ldc = D; g1.M = F; g1.N = D; g1.K = T;
+    g1.c_dtype = PARTIR_F32; g1.rm = a.Rm; g1.rk = a.Rb;
+    g1.name = "mlp.bwd.dw1"; g1.label = "bwd.dw1 dW1^T = sum_b dZ[b][:, m]^T . slice 0 X[b]";
+    plan_gemm(g1, part, plan);
+    gx.A = dZ; gx.B[0] = W1; gx.C[0] = a.dX;
+    gx.lda = F; gx.ldb = F; gx.ldc = D; gx.M = T; gx.N = D; gx.K = F;
+    gx.c_dtype = PARTIR_F32; gx.rm = a.Rb; gx.rk = a.Rm;
+    gx.name = "mlp.bwd.dx"; gx.label = "bwd.dx dX = sum_m dZ[b][:, m] . (slice 1 W1[m])^T";
+    plan_gemm(gx, part, plan);
+    plan.n_sum_loops = 3;
+    if (a.db1) plan_colsum(dZ, csp, a.db1, T, F, chunk, "mlp.bwd.db", plan);
+    if (a.db2) plan_colsum(a.dY, csp, a.db2, T, D, chunk, "mlp.bwd.db", plan);
+  } else {
+    // an empty dim: every gradient that still has elements is an empty sum
+    // (zeros), except db2 = sum_t dY when only F is 0
+    if (T * D > 0) plan_empty_sum(a.dX, T, D, D, false, nullptr, nullptr, 0, false, "mlp.bwd.dx", plan);
+    if (F * D > 0) {
+      plan_empty_sum(a.dW1t, F, D, D, false, nullptr, nullptr, 0, false, "mlp.bwd.dw1", plan);
+      plan_empty_sum(a.dW2t, D, F, F, false, nullptr, nullptr, 0, false, "mlp.bwd.dw2", plan);
+    }
+    if (a.db1 && F > 0) plan_empty_sum(a.db1, 1, F, F, false, nullptr, nullptr, 0, false, "mlp.bwd.db", plan);
+    if (a.db2 && D > 0) plan_colsum(a.dY, csp, a.db2, T, D, chunk, "mlp.bwd.db", plan);
+  }
+  size_t gws = 0;
+  if (live) gws = std::max({gemm_ws_bytes(g2), gemm_ws_bytes(g1), gemm_ws_bytes(gx)});
+  plan.ws_bytes = off + gws;
+}
+
 void fill_info(const Plan& plan, partir_plan_info* info) {
   if (!info) return;
   info->n_virtual_shards = plan.n_shards;
@@ -886,6 +1046,51 @@ int partir_attn_block(const void* X, const void* Wq_t, const void* Wk_t, const v
   Plan plan;
   plan_attn(a, ws, plan);
   keep_plan_text(plan, "attn_block");
+  return execute(plan, stream);
+}
+
+// ---- MLP block backward -----------------------------------------------------------
+size_t partir_mlp_block_backward_workspace(int64_t T, int64_t D, int64_t F, int act, int with_bias_grads,
+                                           int R_batch, int R_model) {
+  MlpBwdArgs a;
+  a.T = T; a.D = D; a.F = F; a.act = act; a.Rb = R_batch; a.Rm = R_model;
+  static char dummy[16] __attribute__((aligned(16)));
+  if (with_bias_grads) { a.db1 = dummy; a.db2 = dummy; }
+  if (validate_mlp_bwd(a, false) != PARTIR_OK) return (size_t)-1;
+  Plan plan;
+  plan_mlp_bwd(a, nullptr, plan);
+  return plan.ws_bytes;
+}
+
+int partir_plan_mlp_block_backward(int64_t T, int64_t D, int64_t F, int act, int R_batch, int R_model,
+                                   partir_plan_info* info) {
+  MlpBwdArgs a;
+  a.T = T; a.D = D; a.F = F; a.act = act; a.Rb = R_batch; a.Rm = R_model;
+  int st = validate_mlp_bwd(a, false);
+  if (st) return st;
+  Plan plan;
+  plan_mlp_bwd(a, nullptr, plan);
+  keep_plan_text(plan, "mlp_block_backward");
+  fill_info(plan, info);
+  return PARTIR_OK;
+}
+
+int partir_mlp_block_backward(const void* X, const void* W1t, const void* b1, const void* W2t, const void* dY,
+                              void* dX, void* dW1t, void* db1, void* dW2t, void* db2, int64_t T, int64_t D,
+                              int64_t F, int act, int R_batch, int R_model, void* ws, size_t ws_bytes,
+                              void* stream) {
+  MlpBwdArgs a;
+  a.X = X; a.W1t = W1t; a.b1 = b1; a.W2t = W2t; a.dY = dY;
+  a.dX = dX; a.dW1t = dW1t; a.db1 = db1; a.dW2t = dW2t; a.db2 = db2;
+  a.T = T; a.D = D; a.F = F; a.act = act; a.Rb = R_batch; a.Rm = R_model;
+  int st = validate_mlp_bwd(a, true);
+  if (st) return st;
+  Plan probe;
+  plan_mlp_bwd(a, nullptr, probe);
+  if ((st = check_ws(probe, ws, ws_bytes))) return st;
+  Plan plan;
+  plan_mlp_bwd(a, ws, plan);
+  keep_plan_text(plan, "mlp_block_backward");
   return execute(plan, stream);
 }
 

@@ -31,7 +31,8 @@ EXPORTS = ("partir_loop_matmul", "partir_loop_matmul_workspace", "partir_mlp_blo
            "partir_plan_mlp_block", "partir_plan_attn_block", "partir_plan_decoder_layer",
            "partir_last_plan_text", "partir_trace_enable", "partir_trace_read", "partir_trace_reset",
            "partir_status_string", "partir_last_error", "partir_version", "partir_propagate",
-           "partir_attention", "partir_attention_workspace", "partir_plan_attention")
+           "partir_attention", "partir_attention_workspace", "partir_plan_attention",
+           "partir_mlp_block_backward", "partir_mlp_block_backward_workspace", "partir_plan_mlp_block_backward")
 
 
 class PartirError(RuntimeError):
@@ -89,6 +90,9 @@ def lib():
         "partir_attention": (I32, [P, P, P, P, I64, I64, I64, I64, I32, F, I32, P, SZ, P]),
         "partir_attention_workspace": (SZ, [I64, I64, I64, I64, I32]),
         "partir_plan_attention": (I32, [I64, I64, I64, I64, I32, I32, ctypes.POINTER(PlanInfo)]),
+        "partir_mlp_block_backward": (I32, [P, P, P, P, P, P, P, P, P, P, I64, I64, I64, I32, I32, I32, P, SZ, P]),
+        "partir_mlp_block_backward_workspace": (SZ, [I64, I64, I64, I32, I32, I32, I32]),
+        "partir_plan_mlp_block_backward": (I32, [I64, I64, I64, I32, I32, I32, ctypes.POINTER(PlanInfo)]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(L, name)
@@ -201,6 +205,34 @@ def mlp_block(X, W1t, W2t, *, b1=None, b2=None, R_batch: int = 1, R_model: int =
                                   _dt(X), od, ACT_GELU if act == "gelu" else ACT_NONE, R_batch, R_model,
                                   _ptr(ws), wsb, _stream(stream)))
     return out
+
+
+def mlp_block_backward(X, W1t, W2t, dY, *, b1=None, R_batch: int = 1, R_model: int = 1, act: str = "gelu",
+                       bias_grads: bool = False, out=None, workspace=None, stream=None):
+    """Gradients of mlp_block w.r.t. X, W1, W2 (and b1, b2 with bias_grads).
+    Returns dX [T, D], dW1t [F, D], dW2t [D, F] (fp32; weight gradients in the
+    weights' stored layout) and, with bias_grads, db1 [F] and db2 [D].
+    ``out``: a tuple of those tensors to write into."""
+    import torch
+    T, D = X.shape
+    F = W1t.shape[0]
+    a = ACT_GELU if act == "gelu" else ACT_NONE
+    f32 = dict(dtype=torch.float32, device=X.device)
+    if out is None:
+        out = (torch.empty((T, D), **f32), torch.empty((F, D), **f32), torch.empty((D, F), **f32)) + \
+            ((torch.empty((F,), **f32), torch.empty((D,), **f32)) if bias_grads else ())
+    dX, dW1t, dW2t = out[:3]
+    db1, db2 = out[3:5] if bias_grads else (None, None)
+    nbytes = lib().partir_mlp_block_backward_workspace(T, D, F, a, int(bias_grads), R_batch, R_model)
+    ws, wsb = _workspace(nbytes, X.device, workspace)
+    _check(lib().partir_mlp_block_backward(_ptr(X), _ptr(W1t), _ptr(b1), _ptr(W2t), _ptr(dY), _ptr(dX), _ptr(dW1t),
+                                           _ptr(db1), _ptr(dW2t), _ptr(db2), T, D, F, a, R_batch, R_model,
+                                           _ptr(ws), wsb, _stream(stream)))
+    return (dX, dW1t, dW2t, db1, db2) if bias_grads else (dX, dW1t, dW2t)
+
+
+def plan_mlp_block_backward(T, D, F, act=ACT_GELU, R_batch=1, R_model=1):
+    return _plan(lib().partir_plan_mlp_block_backward, T, D, F, act, R_batch, R_model)
 
 
 def attn_block_workspace(B, S, D, n_heads, d_head=128, R_batch=1, R_model=1) -> int:

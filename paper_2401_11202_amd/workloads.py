@@ -24,7 +24,7 @@ from . import inputs as I
 @dataclass(frozen=True)
 class Workload:
     name: str
-    kind: str                 # matmul | mlp | attn | decoder | attn_core
+    kind: str                 # matmul | mlp | attn | decoder | attn_core | mlp_train
     wid: int                  # seed id
     dims: Dict[str, int] = field(default_factory=dict)
     dtype: str = "bf16"
@@ -35,6 +35,10 @@ class Workload:
 
 def _mlp(name, wid, T, D, F, Rb, Rm):
     return Workload(name, "mlp", wid, dict(T=T, D=D, F=F, R_batch=Rb, R_model=Rm))
+
+
+def _mlp_train(name, wid, T, D, F, Rb, Rm):
+    return Workload(name, "mlp_train", wid, dict(T=T, D=D, F=F, R_batch=Rb, R_model=Rm))
 
 
 def _attn(name, wid, B, S, D, H, dh, Rb, Rm):
@@ -63,10 +67,16 @@ WORKLOADS = {
     # the key axis is also a loop, here of R_kv = 4 shards
     "attn_core_long": Workload("attn_core_long", "attn_core", 6, dict(B=1, S=8192, H=2, dh=128, R_kv=4)),
     "attn_core_long_R1": Workload("attn_core_long_R1", "attn_core", 6, dict(B=1, S=8192, H=2, dh=128, R_kv=1)),
+    # training step of the Megatron MLP (forward, then the backward nests of
+    # the same partition): the model #sum of dX and the batch #sum of the
+    # weight gradients
+    "mlp_megatron_train": _mlp_train("mlp_megatron_train", 7, 8192, 4096, 16384, 1, 8),
+    "mlp_batch_x_megatron_train": _mlp_train("mlp_batch_x_megatron_train", 8, 8192, 4096, 16384, 2, 4),
     # small twins: same structure and partition sizes, scaled down
     "mlp_megatron_small": _mlp("mlp_megatron_small", 12, 512, 256, 1024, 1, 8),
     "attn_block_small": _attn("attn_block_small", 13, 2, 256, 1024, 8, 128, 1, 8),
     "mlp_batch_x_megatron_small": _mlp("mlp_batch_x_megatron_small", 14, 1024, 512, 2048, 4, 8),
+    "mlp_train_small": _mlp_train("mlp_train_small", 16, 512, 256, 1024, 2, 4),
     "decoder_2layer_small": _dec("decoder_2layer_small", 15, 2, 256, 1024, 8, 128, 1728, 2, 2, 4),
 }
 
@@ -87,6 +97,14 @@ def mlp_inputs(w: Workload):
     W1 = I.gaussian(w.wid, 1, (D, F), D ** -0.5)
     W2 = I.gaussian(w.wid, 2, (F, D), F ** -0.5)
     return dict(X=X, W1=W1, W2=W2)
+
+
+def mlp_train_inputs(w: Workload):
+    """The MLP's inputs plus the output cotangent dY ~ N(0, 1) and b1."""
+    x = mlp_inputs(w)
+    x["dY"] = I.gaussian(w.wid, 3, (w["T"], w["D"]), 1.0)
+    x["b1"] = I.gaussian(w.wid, 4, (w["F"],), 0.5, "f32")
+    return x
 
 
 def attn_inputs(w: Workload):
@@ -118,7 +136,7 @@ def attn_core_inputs(w: Workload):
 
 def make_inputs(w: Workload):
     return {"matmul": matmul_inputs, "mlp": mlp_inputs, "attn": attn_inputs,
-            "decoder": decoder_inputs, "attn_core": attn_core_inputs}[w.kind](w)
+            "decoder": decoder_inputs, "attn_core": attn_core_inputs, "mlp_train": mlp_train_inputs}[w.kind](w)
 
 
 # ---------------------------------------------------------------------------
@@ -145,4 +163,7 @@ def flops(w: Workload) -> float:
         return per * w["L"]
     if w.kind == "attn_core":
         return attn_core_flops(w["B"], w["S"], w["H"], w["dh"])
+    if w.kind == "mlp_train":
+        # forward 4TDF; backward dH, dW2, dW1, dX 8TDF (recomputing Z is not counted)
+        return 12.0 * w["T"] * w["D"] * w["F"]
     raise ValueError(w.kind)

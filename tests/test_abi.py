@@ -303,3 +303,61 @@ def test_attention_core_validation(kwargs, status):
     st = P.lib().partir_attention(a["Q"], DUMMY, DUMMY, DUMMY, a["B"], a["S"], a["H"], a["dh"], 1, 0.0, a["R"],
                                   DUMMY, a["ws_bytes"], None)
     assert P.STATUS[st] == status, P.lib().partir_last_error().decode()
+
+
+# ---------------------------------------------------------------------------
+# MLP backward: the gradient reductions of batch (dW) and model (dX) loops
+# ---------------------------------------------------------------------------
+def mlp_bwd(T=512, D=256, F=1024, act=P.ACT_GELU, Rb=2, Rm=4, X=DUMMY, dX=DUMMY, dW=DUMMY, db=None,
+            ws=DUMMY, ws_bytes=1 << 30):
+    return P.lib().partir_mlp_block_backward(X, DUMMY, None, DUMMY, DUMMY, dX, dW, db, dW, db,
+                                             T, D, F, act, Rb, Rm, ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kwargs,status", [
+    (dict(X=NULL), "PARTIR_E_NULL"),
+    (dict(dW=NULL), "PARTIR_E_NULL"),
+    (dict(T=0, dX=NULL, dW=NULL), "PARTIR_E_NULL"),    # the weight gradients still hold elements
+    (dict(T=-1), "PARTIR_E_SHAPE"),
+    (dict(T=1 << 28, F=1 << 12, D=1 << 10), "PARTIR_E_SHAPE"),
+    (dict(Rm=0), "PARTIR_E_UNSUPPORTED"),
+    (dict(act=7), "PARTIR_E_UNSUPPORTED"),
+    (dict(Rm=3), "PARTIR_E_DIVISIBILITY"),
+    (dict(Rb=3), "PARTIR_E_DIVISIBILITY"),
+    (dict(D=252), "PARTIR_E_LAYOUT"),
+    (dict(T=520, Rb=5), "PARTIR_E_HIP"),               # 104 tokens per shard: whole 16-byte runs
+    (dict(T=500, Rb=5), "PARTIR_E_LAYOUT"),            # 100 tokens per shard are not
+    (dict(F=1056, Rm=4), "PARTIR_E_HIP"),              # F/R = 264
+    (dict(F=1040, Rm=4), "PARTIR_E_LAYOUT"),           # F/R = 260
+    (dict(dX=DUMMY_ODD), "PARTIR_E_LAYOUT"),
+    (dict(ws_bytes=100), "PARTIR_E_WORKSPACE"),
+    (dict(), "PARTIR_E_HIP"),
+    (dict(T=0, dX=NULL), "PARTIR_E_HIP"),              # no tokens: dX holds nothing
+    (dict(F=0, dW=NULL), "PARTIR_E_HIP"),              # no hidden units: no weight gradients
+])
+def test_mlp_backward_validation(kwargs, status):
+    assert P.STATUS[mlp_bwd(**kwargs)] == status, P.lib().partir_last_error().decode()
+
+
+def test_mlp_backward_plans():
+    T, D, F = 8192, 4096, 16384
+    p = P.plan_mlp_block_backward(T, D, F, R_batch=2, R_model=8)
+    t = p["text"]
+    assert p["n_virtual_shards"] == 16 and p["n_tile_loops"] == 2 and p["n_sum_loops"] == 3
+    assert p["flops"] == 10.0 * T * D * F
+    assert t.count("transpose") == 4 and "act_backward" in t
+    # the batch #sum of the weight gradients runs over K = tokens, 2 shards
+    assert "dW2^T = sum_b" in t and "#sum K x2 (4096/shard)" in t
+    # the model #sum of dX runs over K = F, 8 shards
+    assert "dX = sum_m" in t and "#sum K x8 (2048/shard)" in t
+    assert P.lib().partir_mlp_block_backward_workspace(T, D, F, P.ACT_GELU, 0, 2, 8) == p["workspace_bytes"]
+    with_b = P.lib().partir_mlp_block_backward_workspace(T, D, F, P.ACT_GELU, 1, 2, 8)
+    assert with_b == p["workspace_bytes"] + T // 64 * F * 4
+
+
+def test_mlp_backward_empty_plans():
+    e = P.plan_mlp_block_backward(0, 256, 1024, R_batch=2, R_model=4)
+    assert e["n_launches"] == 2 and e["workspace_bytes"] == 0 and "empty_sum" in e["text"]
+    f = P.plan_mlp_block_backward(512, 256, 0, R_batch=2, R_model=4)
+    assert f["n_launches"] == 1 and f["workspace_bytes"] == 0          # dX = the empty #sum over m
+    assert P.plan_mlp_block_backward(0, 0, 0)["n_launches"] == 0

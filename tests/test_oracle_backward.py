@@ -173,3 +173,20 @@ def test_mlp_backward_rejects_indivisible():
         O.mlp_block_backward(np.zeros((6, 2)), np.zeros((2, 8)), np.zeros((8, 2)), np.zeros((6, 2)), R_batch=4)
     with pytest.raises(ValueError):
         O.mlp_block_backward(np.zeros((8, 2)), np.zeros((2, 6)), np.zeros((6, 2)), np.zeros((8, 2)), R_model=4)
+
+
+@pytest.mark.parametrize("act", ["gelu", "none"])
+def test_mlp_backward_sampled_matches_full(act):
+    """Entries evaluated one by one by their owning shards equal the full
+    evaluation, normalisers included."""
+    X, W1, W2, dY, b1 = problem(8, T=32, D=8, F=64)
+    g, n = O.mlp_block_backward(X, W1, W2, dY, b1, act, 4, 8, return_norm=True)
+    rows, units = [0, 7, 8, 31], [0, 7, 8, 63, 40]
+    s, sn = O.mlp_block_backward_sampled(X, W1, W2, dY, b1, act, 4, 8, rows, units)
+    pick = {"dX": (g["dX"][rows], n["dX"][rows]), "dW1": (g["dW1"][:, units], n["dW1"][:, units]),
+            "dW2": (g["dW2"][units], n["dW2"][units]), "db1": (g["db1"][units], n["db1"][units]),
+            "db2": (g["db2"], n["db2"])}
+    for k, (val, nv) in pick.items():
+        assert s[k].shape == val.shape
+        assert np.max(np.abs(s[k] - val) / nv) < 1e-13, k
+        assert np.max(np.abs(sn[k] - nv) / nv) < 1e-13, k
