@@ -82,6 +82,7 @@ def setup(w, P, I):
         X, W1t, W2t, dY, b1 = x["X"].to_device(), dev_t(x["W1"]), dev_t(x["W2"]), x["dY"].to_device(), \
             x["b1"].to_device()
         Y = torch.empty((T, D), dtype=torch.float32, device="cuda")
+        Z = torch.empty((T, F), dtype=torch.bfloat16, device="cuda")
         wsf = torch.empty(P.mlp_block_workspace(T, D, F, P.F32, Rb, Rm), dtype=torch.uint8, device="cuda")
         wsb = torch.empty(P.lib().partir_mlp_block_backward_workspace(T, D, F, P.ACT_GELU, 1, Rb, Rm),
                           dtype=torch.uint8, device="cuda")
@@ -93,12 +94,12 @@ def setup(w, P, I):
         def step():
             # forward, then every gradient of the same nest (a training step
             # without the optimizer update, which is elementwise)
-            P.mlp_block(X, W1t, W2t, b1=b1, R_batch=Rb, R_model=Rm, out=Y, workspace=wsf)
-            P.mlp_block_backward(X, W1t, W2t, dY, b1=b1, R_batch=Rb, R_model=Rm, bias_grads=True, out=grads,
+            P.mlp_block_train(X, W1t, W2t, b1=b1, R_batch=Rb, R_model=Rm, out=Y, Z=Z, workspace=wsf)
+            P.mlp_block_backward(X, W1t, W2t, dY, b1=b1, Z=Z, R_batch=Rb, R_model=Rm, bias_grads=True, out=grads,
                                  workspace=wsb)
         f = 2.0 * T * D * F
-        roles = {"mlp.up": f, "mlp.down": f, "mlp.bwd.z": f, "mlp.bwd.dh": f, "mlp.bwd.dw2": f,
-                 "mlp.bwd.dw1": f, "mlp.bwd.dx": f}
+        roles = {"mlp.up": f, "mlp.down": f, "mlp.bwd.dh": f, "mlp.bwd.dw2": f, "mlp.bwd.dw1": f,
+                 "mlp.bwd.dx": f}
         return x, step, roles, "mfma_bf16"
     if w.kind == "attn":
         B, S, D, H = w["B"], w["S"], w["D"], w["H"]

@@ -165,6 +165,18 @@ int partir_mlp_block(const void* X, const void* W1t, const void* b1,
                      int R_batch, int R_model,
                      void* ws, size_t ws_bytes, void* stream);
 
+/* The forward of a training step: partir_mlp_block, and also the
+ * pre-activation Z = X W1 + b1 [T, F] bf16 (row-major, caller-owned, written
+ * by the same up-projection tiles) that partir_mlp_block_backward reads
+ * instead of recomputing it.  Same workspace as partir_mlp_block.  Z must be
+ * non-NULL when T, D and F are all non-zero; errors as partir_mlp_block. */
+int partir_mlp_block_train(const void* X, const void* W1t, const void* b1,
+                           const void* W2t, const void* b2, void* Y, void* Z,
+                           int64_t T, int64_t D, int64_t F,
+                           int in_dtype, int out_dtype, int act,
+                           int R_batch, int R_model,
+                           void* ws, size_t ws_bytes, void* stream);
+
 size_t partir_mlp_block_workspace(int64_t T, int64_t D, int64_t F, int out_dtype,
                                   int R_batch, int R_model);
 
@@ -185,15 +197,18 @@ size_t partir_mlp_block_workspace(int64_t T, int64_t D, int64_t F, int out_dtype
  * X, W1t, W2t, b1 as in partir_mlp_block; dY: [T, D] bf16.  Outputs fp32:
  * dX [T, D]; dW1t = dW1^T [F, D] and dW2t = dW2^T [D, F] (the weights'
  * stored layout); db1 [F], db2 [D] (either may be NULL: not computed).
- * Intermediates Z, dH, dZ are bf16 in the workspace, which also holds the
+ * Z: the pre-activation X W1 + b1 [T, F] bf16 kept by partir_mlp_block_train
+ * (read only), or NULL: then it is recomputed into the workspace.
+ * Intermediates dH, dZ are bf16 in the workspace, which also holds the
  * transposes the token-contracting products read (X^T, dY^T, H^T, dZ^T,
- * W1, W2).  Constraints: D, F/R_model and T/R_batch multiples of 8.  A size
- * of 0 gives empty sums (zeros) for every non-empty gradient.
+ * W1, W2); the workspace query assumes Z is recomputed (an upper bound
+ * otherwise).  Constraints: D, F/R_model and T/R_batch multiples of 8.  A
+ * size of 0 gives empty sums (zeros) for every non-empty gradient.
  * Errors: E_NULL, E_SHAPE, E_DIVISIBILITY, E_LAYOUT, E_WORKSPACE,
  * E_UNSUPPORTED (R < 1, unknown act), E_HIP.
  */
 int partir_mlp_block_backward(const void* X, const void* W1t, const void* b1,
-                              const void* W2t, const void* dY,
+                              const void* W2t, const void* dY, const void* Z,
                               void* dX, void* dW1t, void* db1, void* dW2t, void* db2,
                               int64_t T, int64_t D, int64_t F, int act,
                               int R_batch, int R_model,

@@ -80,6 +80,20 @@ __global__ __launch_bounds__(256) void act_backward_kernel(ActBwdParams p) {
     }
   }
   __syncthreads();
+  if (p.colpart) {
+    // column sums of the stored dZ over this tile's rows: four quarters of 16
+    // rows, then the quarters in order (a fixed order: deterministic)
+    __shared__ float qs[4][TT];
+    const int c = tid & (TT - 1), q = tid >> 6;
+    const int nr = min(TT, p.rows - r0);
+    float s = 0.0f;
+    if (c0 + c < p.cols)
+      for (int r = q * 16; r < min(nr, q * 16 + 16); ++r) s += bf2f(tdz[r][c]);
+    qs[q][c] = s;
+    __syncthreads();
+    if (q == 0 && c0 + c < p.cols)
+      p.colpart[(int64_t)(r0 / TT) * p.cols + c0 + c] = ((qs[0][c] + qs[1][c]) + qs[2][c]) + qs[3][c];
+  }
 #pragma unroll
   for (int k = 0; k < 2; ++k) {
     const int id = tid + 256 * k;
@@ -100,24 +114,48 @@ __global__ __launch_bounds__(256) void act_backward_kernel(ActBwdParams p) {
   }
 }
 
-// stage 1: partial[b][c] = sum_{r in block b} in[r][c], rows ascending
+// stage 1: partial[b][c] = sum_{r in block b} in[r][c] over blocks of 64
+// rows, as four quarters of 16 rows added in order; a thread owns 8 columns
+// (one 16-byte load per row)
 __global__ __launch_bounds__(256) void colsum_partial_kernel(ColSumParams p) {
-  const int c = blockIdx.y * 256 + threadIdx.x;
+  const int c = (blockIdx.y * 256 + threadIdx.x) * 8;
   const int b = blockIdx.x;
   if (c >= p.cols) return;
-  const int r1 = min(p.rows, (b + 1) * p.chunk);
-  float s = 0.0f;
-  for (int r = b * p.chunk; r < r1; ++r) s += bf2f(p.in[(int64_t)r * p.ld + c]);
-  p.partial[(int64_t)b * p.cols + c] = s;
+  const int r0 = b * kColSumChunk, r1 = min(p.rows, r0 + kColSumChunk);
+  float tot[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  for (int q = r0; q < r1; q += 16) {
+    float s[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    const int qe = min(r1, q + 16);
+#pragma unroll 16
+    for (int r = q; r < qe; ++r) {
+      const i32x4 v = *(const i32x4*)(p.in + (int64_t)r * p.ld + c);
+      const uint16_t* e = (const uint16_t*)&v;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) s[j] += bf2f(e[j]);
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) tot[j] += s[j];
+  }
+  float* dst = p.partial + (int64_t)b * p.cols + c;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) dst[j] = tot[j];
 }
 
 // stage 2: out[c] = sum_b partial[b][c], blocks ascending
 __global__ __launch_bounds__(256) void colsum_final_kernel(ColSumParams p) {
   const int c = blockIdx.x * 256 + threadIdx.x;
   if (c >= p.cols) return;
-  const int nb = (p.rows + p.chunk - 1) / p.chunk;
+  const int nb = (p.rows + kColSumChunk - 1) / kColSumChunk;
   float s = 0.0f;
-  for (int b = 0; b < nb; ++b) s += p.partial[(int64_t)b * p.cols + c];
+  int b = 0;
+  for (; b + 8 <= nb; b += 8) {   // eight loads in flight, added in block order
+    float v[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[j] = p.partial[(int64_t)(b + j) * p.cols + c];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) s += v[j];
+  }
+  for (; b < nb; ++b) s += p.partial[(int64_t)b * p.cols + c];
   p.out[c] = s;
 }
 
@@ -144,11 +182,13 @@ hipError_t launch_act_backward(const ActBwdParams& p, hipStream_t s) {
 
 hipError_t launch_colsum(const ColSumParams& p, hipStream_t s) {
   if (p.cols == 0) return hipSuccess;
-  const int nb = (p.rows + p.chunk - 1) / p.chunk;
-  const unsigned gx = (unsigned)((p.cols + 255) / 256);
-  if (gx > 65535) return hipErrorInvalidValue;
-  if (nb > 0) hipLaunchKernelGGL(colsum_partial_kernel, dim3((unsigned)nb, gx), dim3(256), 0, s, p);
-  hipLaunchKernelGGL(colsum_final_kernel, dim3(gx), dim3(256), 0, s, p);
+  if (p.cols % 8) return hipErrorInvalidValue;
+  const int nb = (p.rows + kColSumChunk - 1) / kColSumChunk;
+  const unsigned g8 = (unsigned)((p.cols / 8 + 255) / 256);
+  if (g8 > 65535) return hipErrorInvalidValue;
+  if (nb > 0 && !p.partial_ready)
+    hipLaunchKernelGGL(colsum_partial_kernel, dim3((unsigned)nb, g8), dim3(256), 0, s, p);
+  hipLaunchKernelGGL(colsum_final_kernel, dim3((unsigned)((p.cols + 255) / 256)), dim3(256), 0, s, p);
   return hipGetLastError();
 }
 

@@ -219,40 +219,52 @@ void gemm_bf16_kernel(GemmParams p) {
   const float* bias = pick3(grp, p.bias[0], p.bias[1], p.bias[2]);
   void* Cg = pick3(grp, p.C[0], p.C[1], p.C[2]);
   __syncthreads();   // every wave is done with the K stages
-  if (EPI == EPI_BF16) {
+  if (EPI == EPI_BF16 || EPI == EPI_BF16_SAVE) {
     uint16_t* cs = (uint16_t*)smem;
+    auto stage = [&](bool apply_act) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int ml = wm * 128 + i * 32 + (lane & 31);
+      for (int i = 0; i < 4; ++i) {
+        const int ml = wm * 128 + i * 32 + (lane & 31);
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
+        for (int j = 0; j < 2; ++j)
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int nl = wn * 64 + j * 32 + 8 * g + 4 * h;
-          f32x4 v = {acc[i][j][4 * g + 0], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]};
-          if (bias) {
-            if (nl < cols) v += *(const f32x4*)(bias + col0 + nl);
+          for (int g = 0; g < 4; ++g) {
+            const int nl = wn * 64 + j * 32 + 8 * g + 4 * h;
+            f32x4 v = {acc[i][j][4 * g + 0], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]};
+            if (bias) {
+              if (nl < cols) v += *(const f32x4*)(bias + col0 + nl);
+            }
+            if (ACT && apply_act) {
+#pragma unroll
+              for (int e = 0; e < 4; ++e) v[e] = gelu_erf(v[e]);
+            }
+            const bf16x4 o = {(__bf16)v[0], (__bf16)v[1], (__bf16)v[2], (__bf16)v[3]};
+            *(bf16x4*)(cs + ml * CPB + nl) = o;
           }
-          if (ACT) {
-#pragma unroll
-            for (int e = 0; e < 4; ++e) v[e] = gelu_erf(v[e]);
-          }
-          const bf16x4 o = {(__bf16)v[0], (__bf16)v[1], (__bf16)v[2], (__bf16)v[3]};
-          *(bf16x4*)(cs + ml * CPB + nl) = o;
-        }
-    }
-    __syncthreads();
+      }
+    };
     // 16 rows per pass: thread t writes 8 columns (16 B) of row t / 32
-    const int cr = tid >> 5, cc = (tid & 31) * 8;
+    auto write = [&](uint16_t* out) {
+      const int cr = tid >> 5, cc = (tid & 31) * 8;
 #pragma unroll 4
-    for (int r0 = 0; r0 < BM; r0 += NT / 32) {
-      const int r = r0 + cr;
-      if (r >= rows || cc >= cols) continue;
-      const i32x4 v = *(const i32x4*)(cs + r * CPB + cc);
-      uint16_t* dst = (uint16_t*)Cg + (row0 + r) * p.ldc + col0 + cc;
-      if (cc + 8 <= cols) *(i32x4*)dst = v;
-      else *(int2*)dst = make_int2(v[0], v[1]);   // a 4-column tail (cols % 8 == 4)
+      for (int r0 = 0; r0 < BM; r0 += NT / 32) {
+        const int r = r0 + cr;
+        if (r >= rows || cc >= cols) continue;
+        const i32x4 v = *(const i32x4*)(cs + r * CPB + cc);
+        uint16_t* dst = out + (row0 + r) * p.ldc + col0 + cc;
+        if (cc + 8 <= cols) *(i32x4*)dst = v;
+        else *(int2*)dst = make_int2(v[0], v[1]);   // a 4-column tail (cols % 8 == 4)
+      }
+    };
+    if (EPI == EPI_BF16_SAVE) {   // the pre-activation first, for the backward pass
+      stage(false);
+      __syncthreads();
+      write((uint16_t*)p.aux);
+      __syncthreads();
     }
+    stage(true);
+    __syncthreads();
+    write((uint16_t*)Cg);
   } else {
     // fp32 results (plain, residual or split partial): two halves of 128 rows
     float* cs = (float*)smem;
@@ -325,6 +337,8 @@ hipError_t launch_gemm_bf16(const GemmParams& p, hipStream_t s) {
     case EPI_PARTIAL * 2 + 0: return launch<EPI_PARTIAL, 0>(p, s);
     case EPI_RESID_F32 * 2 + 0: return launch<EPI_RESID_F32, 0>(p, s);
     case EPI_RESID_F32 * 2 + 1: return launch<EPI_RESID_F32, 1>(p, s);
+    case EPI_BF16_SAVE * 2 + 0: return launch<EPI_BF16_SAVE, 0>(p, s);
+    case EPI_BF16_SAVE * 2 + 1: return launch<EPI_BF16_SAVE, 1>(p, s);
     default: return hipErrorInvalidValue;
   }
 }

@@ -11,7 +11,8 @@ enum GemmEpi : int {
   EPI_BF16 = 0,      // C (bf16) = act(acc + bias)
   EPI_F32 = 1,       // C (f32)  = act(acc + bias)
   EPI_PARTIAL = 2,   // partial[split] (f32) = acc        (split-K #sum)
-  EPI_RESID_F32 = 3  // C (f32)  = resid + act(acc + bias) (resid may alias C)
+  EPI_RESID_F32 = 3, // C (f32)  = resid + act(acc + bias) (resid may alias C)
+  EPI_BF16_SAVE = 4  // C (bf16) = act(acc + bias) and aux (bf16) = acc + bias
 };
 
 // C = A . B^T over a grid of virtual shards.
@@ -28,6 +29,7 @@ struct GemmParams {
   const float* bias[3];
   const float* resid;
   float* partial;
+  void* aux;       // EPI_BF16_SAVE: pre-activation output (group 0, leading dim ldc)
   int64_t lda, ldb, ldc, ldr, part_ld, part_stride;
   int M, N, K, ngroups;
   int rm, ms, tpm;
@@ -127,12 +129,15 @@ hipError_t launch_transpose_bf16(const TransposeParams& p, hipStream_t s);
 // Backward of H = act(Z) for Z, dH [rows, cols] bf16: dZ = dH * act'(Z)
 // (row-major) and the transposes H^T, dZ^T [cols, rows] (for the weight
 // gradients' contractions over rows).  act 0 = identity, 1 = GELU-erf.
+// With colpart set, also the column sums of dZ (as stored, bf16) over each
+// block of 64 rows: colpart[row block][col], the first stage of launch_colsum.
 struct ActBwdParams {
   const uint16_t* Z;
   const uint16_t* dH;
   uint16_t* dZ;
   uint16_t* Ht;
   uint16_t* dZt;
+  float* colpart;
   int64_t ld, ldt;
   int rows, cols;
   int act;
@@ -140,14 +145,17 @@ struct ActBwdParams {
 hipError_t launch_act_backward(const ActBwdParams& p, hipStream_t s);
 
 // out[c] = sum over rows of in[r][c] (bf16 in, fp32 out), rows summed in
-// blocks of `chunk` into partial[ceil(rows / chunk)][cols], then the blocks in
-// order: deterministic.
+// blocks of 64 into partial[ceil(rows / 64)][cols], then the blocks in order:
+// deterministic.  cols a multiple of 8.  partial_ready: the first stage was
+// done by the producer of `in` (act_backward's colpart); only the second runs.
+constexpr int kColSumChunk = 64;
 struct ColSumParams {
   const uint16_t* in;
   float* partial;
   float* out;
   int64_t ld;
-  int rows, cols, chunk;
+  int rows, cols;
+  int partial_ready;
 };
 hipError_t launch_colsum(const ColSumParams& p, hipStream_t s);
 

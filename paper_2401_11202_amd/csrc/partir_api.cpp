@@ -116,6 +116,7 @@ struct GemmSpec {
   int act = 0;
   bool resid_add = false;
   int sum_impl = PARTIR_SUM_AUTO;
+  void* aux = nullptr;          // bf16 pre-activation output (kept for a backward pass)
   const char* name = "gemm";    // role, used as the trace name
   const char* label = "gemm";   // loop nest, for the plan text
 };
@@ -171,6 +172,7 @@ void plan_gemm(const GemmSpec& g, void* ws, Plan& plan) {
     }
     p.resid = g.resid;
     p.partial = (float*)ws;
+    p.aux = g.aux;
     p.lda = g.lda; p.ldb = g.ldb; p.ldc = g.ldc; p.ldr = g.ldr;
     p.part_ld = g.N; p.part_stride = g.M * g.N;
     p.M = (int)g.M; p.N = (int)g.N; p.K = (int)g.K; p.ngroups = g.ngroups;
@@ -182,7 +184,9 @@ void plan_gemm(const GemmSpec& g, void* ws, Plan& plan) {
     p.nsplit = split ? g.rk : 1;
     p.group_m = group_m_for(p.tiles_n);
     p.act = split ? 0 : g.act;
-    p.epi = split ? EPI_PARTIAL : epi_store;
+    // a kept pre-activation needs the whole K sum in the tile (never split:
+    // only the up-projection, which has no #sum, asks for it)
+    p.epi = split ? EPI_PARTIAL : (g.aux ? EPI_BF16_SAVE : epi_store);
     L.kind = L_GEMM_BF16;
     L.name = g.name;
     L.text = describe_gemm(g, (int64_t)p.tiles_m * p.tiles_n * p.nsplit, split);
@@ -413,6 +417,7 @@ struct MlpArgs {
   void* Y = nullptr;
   int64_t T, D, F;
   int in, out, act, Rb, Rm;
+  void* Z = nullptr;   // partir_mlp_block_train: the kept pre-activation [T, F] bf16
 };
 
 int validate_mlp(const MlpArgs& a, bool with_ptrs) {
@@ -430,7 +435,7 @@ int validate_mlp(const MlpArgs& a, bool with_ptrs) {
   if (a.F % a.Rm) return fail(PARTIR_E_DIVISIBILITY, "R_model=%d does not divide F=%lld", a.Rm, (long long)a.F);
   if (a.D % 8 || (a.F / a.Rm) % 8) return fail(PARTIR_E_LAYOUT, "D and F/R_model must be multiples of 8");
   if (with_ptrs && (!aligned16(a.X) || !aligned16(a.W1t) || !aligned16(a.W2t) || !aligned16(a.Y) ||
-                    !aligned16(a.b1) || !aligned16(a.b2)))
+                    !aligned16(a.b1) || !aligned16(a.b2) || !aligned16(a.Z)))
     return fail(PARTIR_E_LAYOUT, "tensors must be 16-byte aligned");
   return PARTIR_OK;
 }
@@ -443,7 +448,7 @@ void plan_mlp(const MlpArgs& a, void* ws, Plan& plan) {
   g1.A = a.X; g1.B[0] = a.W1t; g1.C[0] = H; g1.bias[0] = (const float*)a.b1;
   g1.lda = a.D; g1.ldb = a.D; g1.ldc = a.F;
   g1.M = a.T; g1.N = a.F; g1.K = a.D;
-  g1.c_dtype = PARTIR_BF16; g1.rm = a.Rb; g1.rn = a.Rm; g1.act = a.act;
+  g1.c_dtype = PARTIR_BF16; g1.rm = a.Rb; g1.rn = a.Rm; g1.act = a.act; g1.aux = a.Z;
   g1.name = "mlp.up";
   g1.label = "mlp.up   H = act(slice 0 X[b] . slice 1 W1[m])";
   GemmSpec g2;
@@ -739,6 +744,7 @@ void plan_attn_core(const AttnCoreArgs& a, void* ws, Plan& plan) {
 // ---------------------------------------------------------------------------
 struct MlpBwdArgs {
   const void *X = nullptr, *W1t = nullptr, *b1 = nullptr, *W2t = nullptr, *dY = nullptr;
+  const void* Z = nullptr;   // kept pre-activation; NULL: recomputed
   void *dX = nullptr, *dW1t = nullptr, *db1 = nullptr, *dW2t = nullptr, *db2 = nullptr;
   int64_t T, D, F;
   int act, Rb, Rm;
@@ -763,7 +769,7 @@ int validate_mlp_bwd(const MlpBwdArgs& a, bool with_ptrs) {
   if (with_ptrs && a.db2 && a.T * a.D > 0 && !a.dY) return fail(PARTIR_E_NULL, "db2 needs dY");
   if (with_ptrs && (!aligned16(a.X) || !aligned16(a.W1t) || !aligned16(a.W2t) || !aligned16(a.dY) ||
                     !aligned16(a.dX) || !aligned16(a.dW1t) || !aligned16(a.dW2t) || !aligned16(a.b1) ||
-                    !aligned16(a.db1) || !aligned16(a.db2)))
+                    !aligned16(a.db1) || !aligned16(a.db2) || !aligned16(a.Z)))
     return fail(PARTIR_E_LAYOUT, "tensors must be 16-byte aligned");
   return PARTIR_OK;
 }
@@ -781,16 +787,17 @@ void plan_transpose(const void* in, void* out, int64_t rows, int64_t cols, const
   plan.launches.push_back(L);
 }
 
-void plan_colsum(const void* in, void* partial, void* out, int64_t rows, int64_t cols, int chunk, const char* name,
-                 Plan& plan) {
+void plan_colsum(const void* in, void* partial, void* out, int64_t rows, int64_t cols, bool partial_ready,
+                 const char* name, Plan& plan) {
   Launch L;
   L.kind = L_COLSUM;
   L.name = name;
   L.cs.in = (const uint16_t*)in; L.cs.partial = (float*)partial; L.cs.out = (float*)out;
-  L.cs.ld = cols; L.cs.rows = (int)rows; L.cs.cols = (int)cols; L.cs.chunk = chunk;
-  char buf[160];
+  L.cs.ld = cols; L.cs.rows = (int)rows; L.cs.cols = (int)cols; L.cs.partial_ready = partial_ready;
+  char buf[200];
   snprintf(buf, sizeof buf, "colsum: sum over %lld rows of [%lld,%lld], blocks of %d in order (the batch #sum of "
-           "a bias gradient)", (long long)rows, (long long)rows, (long long)cols, chunk);
+           "a bias gradient)%s", (long long)rows, (long long)rows, (long long)cols, kColSumChunk,
+           partial_ready ? "; block sums from act_backward" : "");
   L.text = buf;
   plan.launches.push_back(L);
 }
@@ -814,12 +821,12 @@ void plan_mlp_bwd(const MlpBwdArgs& a, void* ws, Plan& plan) {
   // without a contraction only the bias-gradient column sums use the workspace
   const size_t tf = live ? align_up((size_t)T * F * 2) : 0, td = live ? align_up((size_t)T * D * 2) : 0,
                df = live ? align_up((size_t)D * F * 2) : 0;
-  const int chunk = 64;
-  const size_t cs_bytes = (a.db1 || a.db2) ? align_up((size_t)((T + chunk - 1) / chunk) * std::max(D, F) * 4) : 0;
+  const size_t cs_bytes =
+      (a.db1 || a.db2) ? align_up((size_t)((T + kColSumChunk - 1) / kColSumChunk) * std::max(D, F) * 4) : 0;
   char* base = (char*)ws;
   size_t off = 0;
   auto take = [&](size_t n) { char* p = base ? base + off : nullptr; off += n; return (void*)p; };
-  void* Z = take(tf);
+  void* Z = a.Z ? (void*)a.Z : take(tf);
   void* dH = take(tf);
   void* dZ = take(tf);
   void* Ht = take(tf);
@@ -836,11 +843,13 @@ void plan_mlp_bwd(const MlpBwdArgs& a, void* ws, Plan& plan) {
     plan_transpose(a.dY, dYt, T, D, "bwd.transpose", plan);
     plan_transpose(a.W1t, W1, F, D, "bwd.transpose", plan);
     plan_transpose(a.W2t, W2, D, F, "bwd.transpose", plan);
-    gz.A = a.X; gz.B[0] = a.W1t; gz.C[0] = Z; gz.bias[0] = (const float*)a.b1;
-    gz.lda = D; gz.ldb = D; gz.ldc = F; gz.M = T; gz.N = F; gz.K = D;
-    gz.c_dtype = PARTIR_BF16; gz.rm = a.Rb; gz.rn = a.Rm;
-    gz.name = "mlp.bwd.z"; gz.label = "bwd.z  Z = slice 0 X[b] . slice 1 W1[m] (recomputed)";
-    plan_gemm(gz, nullptr, plan);
+    if (!a.Z) {
+      gz.A = a.X; gz.B[0] = a.W1t; gz.C[0] = Z; gz.bias[0] = (const float*)a.b1;
+      gz.lda = D; gz.ldb = D; gz.ldc = F; gz.M = T; gz.N = F; gz.K = D;
+      gz.c_dtype = PARTIR_BF16; gz.rm = a.Rb; gz.rn = a.Rm;
+      gz.name = "mlp.bwd.z"; gz.label = "bwd.z  Z = slice 0 X[b] . slice 1 W1[m] (recomputed)";
+      plan_gemm(gz, nullptr, plan);
+    }
     gh.A = a.dY; gh.B[0] = W2; gh.C[0] = dH;
     gh.lda = D; gh.ldb = D; gh.ldc = F; gh.M = T; gh.N = F; gh.K = D;
     gh.c_dtype = PARTIR_BF16; gh.rm = a.Rb; gh.rn = a.Rm;
@@ -851,6 +860,7 @@ void plan_mlp_bwd(const MlpBwdArgs& a, void* ws, Plan& plan) {
     E.name = "mlp.bwd.act";
     E.act.Z = (const uint16_t*)Z; E.act.dH = (const uint16_t*)dH; E.act.dZ = (uint16_t*)dZ;
     E.act.Ht = (uint16_t*)Ht; E.act.dZt = (uint16_t*)dZt; E.act.ld = F; E.act.ldt = T;
+    E.act.colpart = a.db1 ? (float*)csp : nullptr;   // db1's block sums, fused
     E.act.rows = (int)T; E.act.cols = (int)F; E.act.act = a.act;
     E.text = a.act ? "act_backward: dZ = dH * gelu'(Z); H^T, dZ^T" : "act_backward: dZ = dH; H^T, dZ^T";
     plan.launches.push_back(E);
@@ -870,8 +880,9 @@ void plan_mlp_bwd(const MlpBwdArgs& a, void* ws, Plan& plan) {
     gx.name = "mlp.bwd.dx"; gx.label = "bwd.dx dX = sum_m dZ[b][:, m] . (slice 1 W1[m])^T";
     plan_gemm(gx, part, plan);
     plan.n_sum_loops = 3;
-    if (a.db1) plan_colsum(dZ, csp, a.db1, T, F, chunk, "mlp.bwd.db", plan);
-    if (a.db2) plan_colsum(a.dY, csp, a.db2, T, D, chunk, "mlp.bwd.db", plan);
+    // db1 from act_backward's block sums (before anything reuses csp), then db2
+    if (a.db1) plan_colsum(dZ, csp, a.db1, T, F, true, "mlp.bwd.db", plan);
+    if (a.db2) plan_colsum(a.dY, csp, a.db2, T, D, false, "mlp.bwd.db", plan);
   } else {
     // an empty dim: every gradient that still has elements is an empty sum
     // (zeros), except db2 = sum_t dY when only F is 0
@@ -881,7 +892,7 @@ void plan_mlp_bwd(const MlpBwdArgs& a, void* ws, Plan& plan) {
       plan_empty_sum(a.dW2t, D, F, F, false, nullptr, nullptr, 0, false, "mlp.bwd.dw2", plan);
     }
     if (a.db1 && F > 0) plan_empty_sum(a.db1, 1, F, F, false, nullptr, nullptr, 0, false, "mlp.bwd.db", plan);
-    if (a.db2 && D > 0) plan_colsum(a.dY, csp, a.db2, T, D, chunk, "mlp.bwd.db", plan);
+    if (a.db2 && D > 0) plan_colsum(a.dY, csp, a.db2, T, D, false, "mlp.bwd.db", plan);
   }
   size_t gws = 0;
   if (live) gws = std::max({gemm_ws_bytes(g2), gemm_ws_bytes(g1), gemm_ws_bytes(gx)});
@@ -1009,6 +1020,22 @@ int partir_mlp_block(const void* X, const void* W1t, const void* b1, const void*
   return execute(plan, stream);
 }
 
+int partir_mlp_block_train(const void* X, const void* W1t, const void* b1, const void* W2t, const void* b2,
+                           void* Y, void* Z, int64_t T, int64_t D, int64_t F, int in_dtype, int out_dtype,
+                           int act, int R_batch, int R_model, void* ws, size_t ws_bytes, void* stream) {
+  MlpArgs a{X, W1t, b1, W2t, b2, Y, T, D, F, in_dtype, out_dtype, act, R_batch, R_model, Z};
+  if (T * D * F > 0 && !Z) return fail(PARTIR_E_NULL, "Z must be non-NULL (unless empty)");
+  int st = validate_mlp(a, true);
+  if (st) return st;
+  Plan probe;
+  plan_mlp(a, nullptr, probe);
+  if ((st = check_ws(probe, ws, ws_bytes))) return st;
+  Plan plan;
+  plan_mlp(a, ws, plan);
+  keep_plan_text(plan, "mlp_block_train");
+  return execute(plan, stream);
+}
+
 // ---- attn_block ------------------------------------------------------------------
 size_t partir_attn_block_workspace(int64_t B, int64_t S, int64_t D, int64_t n_heads, int64_t d_head,
                                    int R_batch, int R_model) {
@@ -1076,11 +1103,11 @@ int partir_plan_mlp_block_backward(int64_t T, int64_t D, int64_t F, int act, int
 }
 
 int partir_mlp_block_backward(const void* X, const void* W1t, const void* b1, const void* W2t, const void* dY,
-                              void* dX, void* dW1t, void* db1, void* dW2t, void* db2, int64_t T, int64_t D,
-                              int64_t F, int act, int R_batch, int R_model, void* ws, size_t ws_bytes,
+                              const void* Z, void* dX, void* dW1t, void* db1, void* dW2t, void* db2, int64_t T,
+                              int64_t D, int64_t F, int act, int R_batch, int R_model, void* ws, size_t ws_bytes,
                               void* stream) {
   MlpBwdArgs a;
-  a.X = X; a.W1t = W1t; a.b1 = b1; a.W2t = W2t; a.dY = dY;
+  a.X = X; a.W1t = W1t; a.b1 = b1; a.W2t = W2t; a.dY = dY; a.Z = Z;
   a.dX = dX; a.dW1t = dW1t; a.db1 = db1; a.dW2t = dW2t; a.db2 = db2;
   a.T = T; a.D = D; a.F = F; a.act = act; a.Rb = R_batch; a.Rm = R_model;
   int st = validate_mlp_bwd(a, true);

@@ -32,7 +32,8 @@ EXPORTS = ("partir_loop_matmul", "partir_loop_matmul_workspace", "partir_mlp_blo
            "partir_last_plan_text", "partir_trace_enable", "partir_trace_read", "partir_trace_reset",
            "partir_status_string", "partir_last_error", "partir_version", "partir_propagate",
            "partir_attention", "partir_attention_workspace", "partir_plan_attention",
-           "partir_mlp_block_backward", "partir_mlp_block_backward_workspace", "partir_plan_mlp_block_backward")
+           "partir_mlp_block_backward", "partir_mlp_block_backward_workspace", "partir_plan_mlp_block_backward",
+           "partir_mlp_block_train")
 
 
 class PartirError(RuntimeError):
@@ -90,7 +91,8 @@ def lib():
         "partir_attention": (I32, [P, P, P, P, I64, I64, I64, I64, I32, F, I32, P, SZ, P]),
         "partir_attention_workspace": (SZ, [I64, I64, I64, I64, I32]),
         "partir_plan_attention": (I32, [I64, I64, I64, I64, I32, I32, ctypes.POINTER(PlanInfo)]),
-        "partir_mlp_block_backward": (I32, [P, P, P, P, P, P, P, P, P, P, I64, I64, I64, I32, I32, I32, P, SZ, P]),
+        "partir_mlp_block_backward": (I32, [P, P, P, P, P, P, P, P, P, P, P, I64, I64, I64, I32, I32, I32, P, SZ, P]),
+        "partir_mlp_block_train": (I32, [P, P, P, P, P, P, P, I64, I64, I64, I32, I32, I32, I32, I32, P, SZ, P]),
         "partir_mlp_block_backward_workspace": (SZ, [I64, I64, I64, I32, I32, I32, I32]),
         "partir_plan_mlp_block_backward": (I32, [I64, I64, I64, I32, I32, I32, ctypes.POINTER(PlanInfo)]),
     }
@@ -207,12 +209,32 @@ def mlp_block(X, W1t, W2t, *, b1=None, b2=None, R_batch: int = 1, R_model: int =
     return out
 
 
-def mlp_block_backward(X, W1t, W2t, dY, *, b1=None, R_batch: int = 1, R_model: int = 1, act: str = "gelu",
-                       bias_grads: bool = False, out=None, workspace=None, stream=None):
+def mlp_block_train(X, W1t, W2t, *, b1=None, b2=None, R_batch: int = 1, R_model: int = 1, act: str = "gelu",
+                    out_dtype=None, out=None, Z=None, workspace=None, stream=None):
+    """mlp_block that also keeps the pre-activation Z = X W1 + b1 [T, F] bf16
+    for mlp_block_backward.  Returns (Y, Z)."""
+    import torch
+    T, D = X.shape
+    F = W1t.shape[0]
+    od = F32 if out_dtype in (None, torch.float32) else BF16
+    if out is None:
+        out = torch.empty((T, D), dtype=_tdt(od), device=X.device)
+    if Z is None:
+        Z = torch.empty((T, F), dtype=torch.bfloat16, device=X.device)
+    ws, wsb = _workspace(mlp_block_workspace(T, D, F, od, R_batch, R_model), X.device, workspace)
+    _check(lib().partir_mlp_block_train(_ptr(X), _ptr(W1t), _ptr(b1), _ptr(W2t), _ptr(b2), _ptr(out), _ptr(Z),
+                                        T, D, F, _dt(X), od, ACT_GELU if act == "gelu" else ACT_NONE, R_batch,
+                                        R_model, _ptr(ws), wsb, _stream(stream)))
+    return out, Z
+
+
+def mlp_block_backward(X, W1t, W2t, dY, *, b1=None, Z=None, R_batch: int = 1, R_model: int = 1,
+                       act: str = "gelu", bias_grads: bool = False, out=None, workspace=None, stream=None):
     """Gradients of mlp_block w.r.t. X, W1, W2 (and b1, b2 with bias_grads).
     Returns dX [T, D], dW1t [F, D], dW2t [D, F] (fp32; weight gradients in the
     weights' stored layout) and, with bias_grads, db1 [F] and db2 [D].
-    ``out``: a tuple of those tensors to write into."""
+    ``Z``: the pre-activation kept by mlp_block_train (else recomputed);
+    ``out``: a tuple of the result tensors to write into."""
     import torch
     T, D = X.shape
     F = W1t.shape[0]
@@ -225,9 +247,9 @@ def mlp_block_backward(X, W1t, W2t, dY, *, b1=None, R_batch: int = 1, R_model: i
     db1, db2 = out[3:5] if bias_grads else (None, None)
     nbytes = lib().partir_mlp_block_backward_workspace(T, D, F, a, int(bias_grads), R_batch, R_model)
     ws, wsb = _workspace(nbytes, X.device, workspace)
-    _check(lib().partir_mlp_block_backward(_ptr(X), _ptr(W1t), _ptr(b1), _ptr(W2t), _ptr(dY), _ptr(dX), _ptr(dW1t),
-                                           _ptr(db1), _ptr(dW2t), _ptr(db2), T, D, F, a, R_batch, R_model,
-                                           _ptr(ws), wsb, _stream(stream)))
+    _check(lib().partir_mlp_block_backward(_ptr(X), _ptr(W1t), _ptr(b1), _ptr(W2t), _ptr(dY), _ptr(Z), _ptr(dX),
+                                           _ptr(dW1t), _ptr(db1), _ptr(dW2t), _ptr(db2), T, D, F, a, R_batch,
+                                           R_model, _ptr(ws), wsb, _stream(stream)))
     return (dX, dW1t, dW2t, db1, db2) if bias_grads else (dX, dW1t, dW2t)
 
 

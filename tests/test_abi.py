@@ -310,7 +310,7 @@ def test_attention_core_validation(kwargs, status):
 # ---------------------------------------------------------------------------
 def mlp_bwd(T=512, D=256, F=1024, act=P.ACT_GELU, Rb=2, Rm=4, X=DUMMY, dX=DUMMY, dW=DUMMY, db=None,
             ws=DUMMY, ws_bytes=1 << 30):
-    return P.lib().partir_mlp_block_backward(X, DUMMY, None, DUMMY, DUMMY, dX, dW, db, dW, db,
+    return P.lib().partir_mlp_block_backward(X, DUMMY, None, DUMMY, DUMMY, None, dX, dW, db, dW, db,
                                              T, D, F, act, Rb, Rm, ws, ws_bytes, None)
 
 
@@ -361,3 +361,15 @@ def test_mlp_backward_empty_plans():
     f = P.plan_mlp_block_backward(512, 256, 0, R_batch=2, R_model=4)
     assert f["n_launches"] == 1 and f["workspace_bytes"] == 0          # dX = the empty #sum over m
     assert P.plan_mlp_block_backward(0, 0, 0)["n_launches"] == 0
+
+
+def test_training_forward_validation(monkeypatch):
+    monkeypatch.setenv("PARTIR_FAIL_LAUNCH", "1")
+    L = P.lib()
+    args = lambda Z, T=512: (DUMMY, DUMMY, None, DUMMY, None, DUMMY, Z, T, 256, 1024, P.BF16, P.F32, P.ACT_GELU,
+                             1, 8, DUMMY, 1 << 30, None)
+    assert P.STATUS[L.partir_mlp_block_train(*args(None))] == "PARTIR_E_NULL"
+    assert P.STATUS[L.partir_mlp_block_train(*args(DUMMY_ODD))] == "PARTIR_E_LAYOUT"
+    assert P.STATUS[L.partir_mlp_block_train(*args(DUMMY))] == "PARTIR_E_HIP"
+    assert L.partir_last_plan_text().decode().startswith("mlp_block_train:")
+    assert P.STATUS[L.partir_mlp_block_train(*args(None, T=0))] == "PARTIR_E_HIP"   # nothing to keep

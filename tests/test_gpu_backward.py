@@ -26,9 +26,14 @@ def dev_t(t: I.HostTensor):
     return I.transposed(t).to_device()
 
 
-def run(x, Rb, Rm, act="gelu", b1=True, bias_grads=True):
-    g = P.mlp_block_backward(x["X"].to_device(), dev_t(x["W1"]), dev_t(x["W2"]), x["dY"].to_device(),
-                             b1=x["b1"].to_device() if b1 else None, R_batch=Rb, R_model=Rm, act=act,
+def run(x, Rb, Rm, act="gelu", b1=True, bias_grads=True, keep_z=False):
+    """The backward pass; with keep_z, after the training forward that keeps Z."""
+    X, W1t, W2t = x["X"].to_device(), dev_t(x["W1"]), dev_t(x["W2"])
+    b1 = x["b1"].to_device() if b1 else None
+    Z = None
+    if keep_z:
+        _, Z = P.mlp_block_train(X, W1t, W2t, b1=b1, R_batch=Rb, R_model=Rm, act=act)
+    g = P.mlp_block_backward(X, W1t, W2t, x["dY"].to_device(), b1=b1, Z=Z, R_batch=Rb, R_model=Rm, act=act,
                              bias_grads=bias_grads)
     torch.cuda.synchronize()
     out = {"dX": host(g[0]), "dW1": host(g[1]).T, "dW2": host(g[2]).T}
@@ -96,13 +101,13 @@ def test_backward_partitions_agree_and_are_deterministic():
     check(a, one, norm)
 
 
-@pytest.mark.parametrize("name", ["mlp_megatron_train", "mlp_batch_x_megatron_train"])
-def test_backward_full_size_sampled(name):
+@pytest.mark.parametrize("name,keep_z", [("mlp_megatron_train", True), ("mlp_batch_x_megatron_train", False)])
+def test_backward_full_size_sampled(name, keep_z):
     w = W.WORKLOADS[name]
     x = W.make_inputs(w)
     T, F, Rb, Rm = w["T"], w["F"], w["R_batch"], w["R_model"]
-    say(f"{name}: T={T} D={w['D']} F={F} R_batch={Rb} R_model={Rm}")
-    got = run(x, Rb, Rm)
+    say(f"{name}: T={T} D={w['D']} F={F} R_batch={Rb} R_model={Rm} Z kept by the forward: {keep_z}")
+    got = run(x, Rb, Rm, keep_z=keep_z)
     rng = np.random.default_rng(w.wid)
     Tb, Fm = T // Rb, F // Rm
     rows = sorted({0, T - 1, Tb - 1, Tb % T} | set(rng.choice(T, 8, replace=False).tolist()))
@@ -113,6 +118,29 @@ def test_backward_full_size_sampled(name):
     picked = {"dX": got["dX"][rows], "dW1": got["dW1"][:, units], "dW2": got["dW2"][units],
               "db1": got["db1"][units], "db2": got["db2"]}
     check(picked, ref, norm)
+
+
+@pytest.mark.parametrize("act", ["gelu", "none"])
+def test_training_forward_keeps_z(act):
+    """The training forward's Y is the plain forward's bit for bit, its Z is
+    X W1 + b1 (oracle, bf16 rounding), and the backward from the kept Z equals
+    the backward that recomputes Z bit for bit (the same GEMM tiles)."""
+    w = W.WORKLOADS["mlp_train_small"]
+    x = W.make_inputs(w)
+    Rb, Rm = w["R_batch"], w["R_model"]
+    X, W1t, W2t, b1 = x["X"].to_device(), dev_t(x["W1"]), dev_t(x["W2"]), x["b1"].to_device()
+    Y, Z = P.mlp_block_train(X, W1t, W2t, b1=b1, R_batch=Rb, R_model=Rm, act=act)
+    Y0 = P.mlp_block(X, W1t, W2t, b1=b1, R_batch=Rb, R_model=Rm, act=act)
+    torch.cuda.synchronize()
+    assert torch.equal(Y, Y0)
+    zref = O.loop_tile(Rm, 1, lambda m: O.matmul(x["X"].f64(), O.slice_(x["W1"].f64(), 1, m, Rm))
+                       + O.slice_(x["b1"].f64(), 0, m, Rm))
+    znorm = O.abs_product(x["X"].f64(), x["W1"].f64()) + np.abs(x["b1"].f64())
+    assert O.normalised_error(host(Z), zref, znorm) <= TOL_BF16
+    kept = run(x, Rb, Rm, act, keep_z=True)
+    recomputed = run(x, Rb, Rm, act)
+    for k in KEYS:
+        assert np.array_equal(kept[k], recomputed[k]), k
 
 
 def test_backward_empty_sizes():
