@@ -663,6 +663,123 @@ def decoder_ref(x, layers, B, S, n_heads, d_head, eps=1e-6):
 
 
 # ---------------------------------------------------------------------------
+# PartIR:SPMD collectives on device-local arrays (Sec. 6)
+# ---------------------------------------------------------------------------
+# A mesh is a list [(axis name, size), ...]; device-local values are dicts
+# {device coordinates (tuple, one entry per axis in mesh order): array}.
+def mesh_devices(mesh):
+    devs = [()]
+    for _, n in mesh:
+        devs = [d + (r,) for d in devs for r in range(n)]
+    return devs
+
+
+def _axis(mesh, axis):
+    names = [a for a, _ in mesh]
+    k = names.index(axis)
+    return k, mesh[k][1]
+
+
+def _peers(dev, k, n):
+    return [dev[:k] + (r,) + dev[k + 1:] for r in range(n)]
+
+
+def replicated(x, mesh):
+    return {d: np.asarray(x, np.float64) for d in mesh_devices(mesh)}
+
+
+def all_slice(local, mesh, dim, axis):
+    """Each device keeps the chunk of its array along `dim` given by its own
+    coordinate on `axis` (equal contiguous chunks, no padding)."""
+    k, n = _axis(mesh, axis)
+    return {d: slice_(x, dim, d[k], n) for d, x in local.items()}
+
+
+def all_gather(local, mesh, dim, axis):
+    """Each device gets the concatenation along `dim` of the arrays of the
+    devices that differ from it only on `axis`, in axis order (the dual of
+    all_slice: the dim grows by the axis size)."""
+    k, n = _axis(mesh, axis)
+    return {d: np.concatenate([np.asarray(local[p], np.float64) for p in _peers(d, k, n)], axis=dim)
+            for d in local}
+
+
+def all_reduce(local, mesh, axis):
+    """Each device gets the sum, in axis order, of the arrays of the devices
+    that differ from it only on `axis` (the result is replicated on it)."""
+    k, n = _axis(mesh, axis)
+    out = {}
+    for d in local:
+        acc = np.array(local[_peers(d, k, n)[0]], dtype=np.float64, copy=True)
+        for p in _peers(d, k, n)[1:]:
+            acc = acc + local[p]
+        out[d] = acc
+    return out
+
+
+def reduce_scatter(local, mesh, dim, axis):
+    """The device with coordinate r on `axis` gets the sum over its axis
+    group of every member's r-th chunk along `dim` (the chunks are summed,
+    not the whole arrays: the collective's own definition)."""
+    k, n = _axis(mesh, axis)
+    out = {}
+    for d in local:
+        parts = [slice_(local[p], dim, d[k], n) for p in _peers(d, k, n)]
+        acc = np.array(parts[0], dtype=np.float64, copy=True)
+        for q in parts[1:]:
+            acc = acc + q
+        out[d] = acc
+    return out
+
+
+def mlp_block_z3(X_loc, W1_loc, W2_loc, b1=None, b2=None, act="gelu", R_batch=1, R_model=1,
+                 sequence_sharded=True):
+    """The lowered SPMD program of the MLP under BP + MP + Z3 on the mesh
+    {B: R_batch, M: R_model} (Sec. 3, the data-parallel fully sharded chain):
+    per device (b, m), with W1_loc = W1[dim 0 block b, dim 1 block m] and
+    W2_loc = W2[dim 0 block m, dim 1 block b]:
+
+      w1 = all_gather<B>(W1_loc, dim 0);  w2 = all_gather<B>(W2_loc, dim 1)
+      x  = all_gather<M>(X_loc, dim 0)    if the activations are sharded on M
+           X_loc                          otherwise (the batch block b)
+      h  = act(x w1 + slice 0 b1[m]);  p = h w2
+      y  = reduce_scatter<M>(p, dim 0) + b2   if sharded on M (the all_reduce
+           all_reduce<M>(p) + b2              fused with the all_slice)
+    Returns {device: y}.
+    """
+    mesh = [("B", R_batch), ("M", R_model)]
+    x = all_gather(X_loc, mesh, 0, "M") if sequence_sharded else {d: np.asarray(v, np.float64)
+                                                                    for d, v in X_loc.items()}
+    w1 = all_gather(W1_loc, mesh, 0, "B")
+    w2 = all_gather(W2_loc, mesh, 1, "B")
+    b1_loc = None if b1 is None else all_slice(replicated(b1, mesh), mesh, 0, "M")
+    p = {}
+    for d in mesh_devices(mesh):
+        z = matmul(x[d], w1[d])
+        if b1_loc is not None:
+            z = z + b1_loc[d]
+        p[d] = matmul(activation(z, act), w2[d])
+    y = reduce_scatter(p, mesh, 0, "M") if sequence_sharded else all_reduce(p, mesh, "M")
+    if b2 is not None:
+        y = {d: v + np.asarray(b2, np.float64) for d, v in y.items()}
+    return y
+
+
+def z3_local_operands(X, W1, W2, R_batch, R_model, sequence_sharded=True):
+    """Value tiling of the whole operands into the device-local arrays the
+    lowering takes as arguments (Sec. 6: arguments used by all_slice become
+    device-local): X by tokens over B (and M), W1 dim 0 over B and dim 1 over
+    M, W2 dim 0 over M and dim 1 over B."""
+    mesh = [("B", R_batch), ("M", R_model)]
+    x = all_slice(replicated(X, mesh), mesh, 0, "B")
+    if sequence_sharded:
+        x = all_slice(x, mesh, 0, "M")
+    w1 = all_slice(all_slice(replicated(W1, mesh), mesh, 0, "B"), mesh, 1, "M")
+    w2 = all_slice(all_slice(replicated(W2, mesh), mesh, 0, "M"), mesh, 1, "B")
+    return x, w1, w2
+
+
+# ---------------------------------------------------------------------------
 # Parity measure (the elementwise forward-error form)
 # ---------------------------------------------------------------------------
 def normalised_error(got, ref, norm):

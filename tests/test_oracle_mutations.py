@@ -13,6 +13,7 @@ import pytest
 from oracle import partir_oracle as O
 from tests import test_oracle_backward as BW
 from tests import test_oracle_core as C
+from tests import test_oracle_spmd as SP
 from tests import test_oracle_ops as P
 from tests import test_oracle_programs as G
 
@@ -102,6 +103,23 @@ def _gelu_grad_minus(x, act):
     return 0.5 * (1 + erf(x / math.sqrt(2))) - x * np.exp(-0.5 * x * x) / math.sqrt(2 * math.pi)
 
 
+def _gather_reversed(local, mesh, dim, axis):
+    k = [a for a, _ in mesh].index(axis)
+    n = mesh[k][1]
+    return {d: np.concatenate([local[d[:k] + (r,) + d[k + 1:]] for r in reversed(range(n))], axis=dim)
+            for d in local}
+
+
+def _scatter_wrong_chunk(local, mesh, dim, axis):
+    k = [a for a, _ in mesh].index(axis)
+    n = mesh[k][1]
+    out = {}
+    for d in local:
+        peers = [d[:k] + (r,) + d[k + 1:] for r in range(n)]
+        out[d] = sum(_real["slice_"](local[p], dim, (d[k] + 1) % n, n) for p in peers)
+    return out
+
+
 def _attend_k_from_q(xb, Wq_m, Wk_m, Wv_m, *rest):
     return _real["_attend_shard"](xb, Wq_m, Wq_m, Wv_m, *rest)
 
@@ -124,6 +142,10 @@ def _run(pins, golden):
                 pin(2, 4)
             elif pin.__name__ == "test_mlp_backward_matches_torch_autograd":
                 pin("gelu", 2, 4)
+            elif pin.__name__ == "test_z3_mlp_integer_exact_equals_unpartitioned":
+                pin(4, 2, True)
+            elif pin.__name__ == "test_reduce_scatter_is_all_reduce_fused_with_all_slice":
+                pin(0, "M")
             else:
                 pin(**kwargs)
         except (AssertionError, ValueError, FloatingPointError):
@@ -157,6 +179,12 @@ CASES = {
     "gelu derivative subtracts x phi(x)": ("activation_grad", _gelu_grad_minus,
                                            [BW.test_gelu_grad_matches_central_differences_and_torch,
                                             BW.test_mlp_backward_central_differences_of_the_forward]),
+    "all_gather concatenates in reverse": ("all_gather", _gather_reversed,
+                                           [SP.test_all_gather_concatenates_in_axis_order,
+                                            SP.test_z3_mlp_integer_exact_equals_unpartitioned]),
+    "reduce_scatter hands out the wrong chunk": ("reduce_scatter", _scatter_wrong_chunk,
+                                                 [SP.test_reduce_scatter_is_all_reduce_fused_with_all_slice,
+                                                  SP.test_z3_mlp_integer_exact_equals_unpartitioned]),
     "keys projected with Wq": ("_attend_shard", _attend_k_from_q, [G.test_attn_block_brute_force]),
 }
 
