@@ -77,6 +77,17 @@ def setup(w, P, I):
         step = lambda: P.mlp_block(X, W1t, W2t, R_batch=w["R_batch"], R_model=w["R_model"], out=Y, workspace=ws)
         roles = {"mlp.up": 2.0 * T * D * F, "mlp.down": 2.0 * T * D * F}
         return x, step, roles, "mfma_bf16"
+    if w.kind == "mlp_z3":
+        T, D, F, Rb, Rm = w["T"], w["D"], w["F"], w["R_batch"], w["R_model"]
+        xs, w1s, w2s = P.z3_device_arrays(x["X"].to_device(), dev_t(x["W1"]), dev_t(x["W2"]), Rb, Rm)
+        b1, b2 = x["b1"].to_device(), x["b2"].to_device()
+        ys = [torch.empty((T // (Rb * Rm), D), dtype=torch.float32, device="cuda") for _ in range(Rb * Rm)]
+        ws = torch.empty(P.lib().partir_mlp_block_sharded_workspace(T, D, F, Rb, Rm), dtype=torch.uint8,
+                         device="cuda")
+        step = lambda: P.mlp_block_sharded(xs, w1s, w2s, R_batch=Rb, R_model=Rm, b1=b1, b2=b2, out_parts=ys,
+                                           workspace=ws)
+        roles = {"mlp.up": 2.0 * T * D * F, "mlp.down": 2.0 * T * D * F}
+        return x, step, roles, "mfma_bf16"
     if w.kind == "mlp_train":
         T, D, F, Rb, Rm = w["T"], w["D"], w["F"], w["R_batch"], w["R_model"]
         X, W1t, W2t, dY, b1 = x["X"].to_device(), dev_t(x["W1"]), dev_t(x["W2"]), x["dY"].to_device(), \
@@ -168,7 +179,7 @@ def cpu_baseline(w, x, target_s):
         dt = time.perf_counter() - t0
         return dict(value=reps * 2.0 * w["M"] * w["N"] * w["K"] / dt / 1e12, unit="TFLOP/s", cores=cores,
                     kind="oracle", sample=f"full output, {reps} evaluations, {dt:.2f} s")
-    if w.kind == "mlp":
+    if w.kind in ("mlp", "mlp_z3"):
         X, W1, W2 = x["X"].f64(), x["W1"].f64(), x["W2"].f64()
         per_row = 4.0 * w["D"] * w["F"]
         rng = np.random.default_rng(0)

@@ -165,6 +165,34 @@ int partir_mlp_block(const void* X, const void* W1t, const void* b1,
                      int R_batch, int R_model,
                      void* ws, size_t ws_bytes, void* stream);
 
+/* The MLP block on device-local arrays: the lowered program of the schedule
+ * BP + MP + Z3 (Sec. 3: batch tiling, Megatron, parameters sharded over the
+ * batch axis) with the input and output activations also sharded over the
+ * model axis (the remark after Sec. 3's FSDP chain), run for every device of
+ * the mesh {B: R_batch, M: R_model} on this GPU.  Device (b, m) is part index
+ * p = b * R_model + m; each part is its own array (any address):
+ *   X_parts[p]   [T/(R_batch R_model), D] bf16: token rows p of X
+ *   W1t_parts[p] [F/R_model, D/R_batch] bf16: W1t rows block m, cols block b
+ *   W2t_parts[p] [D/R_batch, F/R_model] bf16: W2t rows block b, cols block m
+ *   Y_parts[p]   [T/(R_batch R_model), D] out_dtype: token rows p of Y
+ *   b1 [F], b2 [D] fp32 replicated, either may be NULL.
+ * The collectives of the lowering (Sec. 6) are fused away: all_gather of X
+ * over M and of W1, W2 over B become the GEMMs reading each part in place,
+ * and the all_reduce over M with the all_slice after it (a reduce_scatter)
+ * becomes the down-projection's in-accumulator #sum over m whose output rows
+ * are stored by their owner.  Y equals partir_mlp_block on the concatenated
+ * operands.  Arrays are host arrays of R_batch * R_model device pointers
+ * (<= 64 devices).  Constraints: T/(R_batch R_model), D/R_batch and F/R_model
+ * multiples of 64; 16-byte aligned parts.  Workspace: H [T, F] bf16.
+ * Errors: E_NULL, E_SHAPE, E_DIVISIBILITY, E_LAYOUT, E_DTYPE, E_WORKSPACE,
+ * E_UNSUPPORTED, E_HIP. */
+int partir_mlp_block_sharded(const void* const* X_parts, const void* const* W1t_parts,
+                             const void* b1, const void* const* W2t_parts, const void* b2,
+                             void* const* Y_parts, int64_t T, int64_t D, int64_t F,
+                             int out_dtype, int act, int R_batch, int R_model,
+                             void* ws, size_t ws_bytes, void* stream);
+size_t partir_mlp_block_sharded_workspace(int64_t T, int64_t D, int64_t F, int R_batch, int R_model);
+
 /* The forward of a training step: partir_mlp_block, and also the
  * pre-activation Z = X W1 + b1 [T, F] bf16 (row-major, caller-owned, written
  * by the same up-projection tiles) that partir_mlp_block_backward reads
@@ -334,6 +362,8 @@ int partir_plan_attention(int64_t B, int64_t S, int64_t n_heads, int64_t d_head,
                           partir_plan_info* info);
 int partir_plan_mlp_block_backward(int64_t T, int64_t D, int64_t F, int act, int R_batch, int R_model,
                                    partir_plan_info* info);
+int partir_plan_mlp_block_sharded(int64_t T, int64_t D, int64_t F, int act, int R_batch, int R_model,
+                                  partir_plan_info* info);
 int partir_plan_decoder_layer(int64_t B, int64_t S, int64_t D, int64_t n_heads,
                               int64_t d_head, int64_t F, int R_batch, int R_model,
                               partir_plan_info* info);

@@ -62,9 +62,10 @@ __device__ __forceinline__ int swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
 // s_waitcnt with only the vector-memory counter constrained (gfx9 encoding)
 #define WAIT_VMCNT(n) __builtin_amdgcn_s_waitcnt((((n) & 15) | (((n) >> 4) << 14)) | (0x7 << 4) | (0xF << 8))
 
-template <int EPI, int ACT>
-__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2)))
-void gemm_bf16_kernel(GemmParams p) {
+// PARTS: operands in device-local arrays (`t`, a kernel argument); else the
+// plain pointers of `p` and t is unused.
+template <int EPI, int ACT, int PARTS>
+__device__ __forceinline__ void gemm_body(const GemmParams& p, const GemmParts* tb) {
   constexpr int OPB = BM * BK * 2, STAGE = 2 * OPB, KK = BK / 16, RB = 1024 / (BK * 2) /* rows per 1 KiB */;
   constexpr int CPR = BK / 8;   // 16-byte chunks per row
   __shared__ __attribute__((aligned(1024))) char smem[(NS * STAGE > C_LDS) ? NS * STAGE : C_LDS];
@@ -82,12 +83,12 @@ void gemm_bf16_kernel(GemmParams p) {
   // of the tile order so neighbouring tiles share that XCD's L2.
   if ((nwg & 7) == 0) bid = (bid & 7) * (nwg >> 3) + (bid >> 3);
   const int split = bid / ntiles;
-  const int t = bid - split * ntiles;
+  const int tix = bid - split * ntiles;
   const int per_group = p.group_m * p.tiles_n;
-  const int gidx = t / per_group;
+  const int gidx = tix / per_group;
   const int first_m = gidx * p.group_m;
   const int gm = min(p.tiles_m - first_m, p.group_m);
-  const int rr = t - gidx * per_group;
+  const int rr = tix - gidx * per_group;
   const int tm = first_m + rr % gm;
   const int tn = rr / gm;
 
@@ -112,13 +113,36 @@ void gemm_bf16_kernel(GemmParams p) {
   const uint16_t* Btile = Bg + (int64_t)col0 * p.ldb;
   constexpr int NJ = BM / (8 * RB);   // wave loads per operand per k tile
   constexpr int BLK = 8 * RB;          // rows covered by one load of all 8 waves
+  static_assert(BLK == 64, "part tables assume 64-row load blocks");
+  const GemmParts* const t = tb;
   __amdgpu_buffer_rsrc_t ra[NJ], rb[NJ];
+  // start of the B row block j in K part kp (parts: the owning array; a block
+  // with no valid rows takes any part's address, its descriptor reads nothing)
+  auto b_block = [&](int j, int kp) -> const uint16_t* {
+    if (PARTS && t->b_nrows) {
+      if (cols - BLK * j <= 0) return t->b[kp];
+      const int n = col0 + BLK * j;
+      const int nb = n / t->b_nrows;
+      return t->b[nb * t->b_nk + kp] + (int64_t)(n - nb * t->b_nrows) * p.ldb;
+    }
+    return Btile + (int64_t)BLK * j * p.ldb;
+  };
 #pragma unroll
   for (int j = 0; j < NJ; ++j) {
     const int va = min(max(rows - BLK * j, 0), BLK), vb = min(max(cols - BLK * j, 0), BLK);
-    ra[j] = make_rsrc(At + (int64_t)BLK * j * p.lda, (uint32_t)(va * p.lda * 2));
-    rb[j] = make_rsrc(Btile + (int64_t)BLK * j * p.ldb, (uint32_t)(vb * p.ldb * 2));
+    const uint16_t* a_blk = At + (int64_t)BLK * j * p.lda;
+    if (PARTS && t->a_rows) {
+      const int r = row0 + BLK * min(j, (rows - 1) / BLK);   // blocks past the rows: size 0 below
+      const int ab = r / t->a_rows;
+      a_blk = t->a[ab] + (int64_t)(r - ab * t->a_rows) * p.lda;
+    }
+    ra[j] = make_rsrc(a_blk, (uint32_t)(va * p.lda * 2));
+    rb[j] = make_rsrc(b_block(j, 0), (uint32_t)(vb * p.ldb * 2));
   }
+  // K part the B descriptors point into and where it ends (loads are issued
+  // in increasing K, so the part only ever advances)
+  int b_kpart = 0;
+  int b_kend = (PARTS && t->b_nrows) ? t->b_kcols : 0;
   const int lrow = RB * wave + lane / CPR;
   const int lchunk = (lane % CPR) ^ swz(lrow);
   const uint32_t a_voff = (uint32_t)(lrow * p.lda * 2 + lchunk * 16);
@@ -128,12 +152,26 @@ void gemm_bf16_kernel(GemmParams p) {
   auto gload = [&](int kt, int stage) {
     const int kb = k_begin + kt * BK;
     const uint32_t kmask = (kb + lchunk * 8 < k_end) ? 0u : OOB;   // ragged K tail / past the end
-    const uint32_t so = (uint32_t)kb * 2;
+    const uint32_t so = (uint32_t)kb * 2;   // A (and unparted B): K offset in bytes
+    uint32_t so_b = so;
+    if (PARTS && t->b_nrows) {
+      // the all_gather of B along K: K tiles never straddle a part
+      if (kb >= b_kend && b_kpart + 1 < t->b_nk) {
+        const int kp = ++b_kpart;
+        b_kend += t->b_kcols;
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+          const int vb = min(max(cols - BLK * j, 0), BLK);
+          rb[j] = make_rsrc(b_block(j, kp), (uint32_t)(vb * p.ldb * 2));
+        }
+      }
+      so_b = (uint32_t)(kb - (b_kend - t->b_kcols)) * 2;
+    }
     char* base = smem + stage * STAGE + lds_w;
 #pragma unroll
     for (int j = 0; j < NJ; ++j) {
       __builtin_amdgcn_raw_ptr_buffer_load_lds(ra[j], (lds_void*)(base + j * 8192), 16, a_voff | kmask, so, 0, 0);
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rb[j], (lds_void*)(base + OPB + j * 8192), 16, b_voff | kmask, so, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rb[j], (lds_void*)(base + OPB + j * 8192), 16, b_voff | kmask, so_b, 0, 0);
     }
   };
 
@@ -244,14 +282,21 @@ void gemm_bf16_kernel(GemmParams p) {
       }
     };
     // 16 rows per pass: thread t writes 8 columns (16 B) of row t / 32
-    auto write = [&](uint16_t* out) {
+    auto write = [&](uint16_t* out, bool parted) {
       const int cr = tid >> 5, cc = (tid & 31) * 8;
 #pragma unroll 4
       for (int r0 = 0; r0 < BM; r0 += NT / 32) {
         const int r = r0 + cr;
         if (r >= rows || cc >= cols) continue;
         const i32x4 v = *(const i32x4*)(cs + r * CPB + cc);
-        uint16_t* dst = out + (row0 + r) * p.ldc + col0 + cc;
+        int64_t grow = row0 + r;
+        uint16_t* ob = out;
+        if (PARTS && parted) {   // the 16 rows of a pass share one part (c_rows % 16 == 0)
+          const int cb = (row0 + r0) / t->c_rows;
+          ob = (uint16_t*)t->c[cb];
+          grow -= (int64_t)cb * t->c_rows;
+        }
+        uint16_t* dst = ob + grow * p.ldc + col0 + cc;
         if (cc + 8 <= cols) *(i32x4*)dst = v;
         else *(int2*)dst = make_int2(v[0], v[1]);   // a 4-column tail (cols % 8 == 4)
       }
@@ -259,12 +304,12 @@ void gemm_bf16_kernel(GemmParams p) {
     if (EPI == EPI_BF16_SAVE) {   // the pre-activation first, for the backward pass
       stage(false);
       __syncthreads();
-      write((uint16_t*)p.aux);
+      write((uint16_t*)p.aux, false);
       __syncthreads();
     }
     stage(true);
     __syncthreads();
-    write((uint16_t*)Cg);
+    write((uint16_t*)Cg, PARTS && t->c_rows);
   } else {
     // fp32 results (plain, residual or split partial): two halves of 128 rows
     float* cs = (float*)smem;
@@ -305,7 +350,12 @@ void gemm_bf16_kernel(GemmParams p) {
         if (EPI == EPI_PARTIAL) {
           *(f32x4*)(p.partial + split * p.part_stride + m * p.part_ld + n) = v;
         } else if (EPI == EPI_F32) {
-          *(f32x4*)((float*)Cg + m * p.ldc + n) = v;
+          if (PARTS && t->c_rows) {   // the 8 rows of a pass share one part
+            const int cb = (row0 + q * (BM / 2) + r0) / t->c_rows;
+            *(f32x4*)((float*)t->c[cb] + (m - (int64_t)cb * t->c_rows) * p.ldc + n) = v;
+          } else {
+            *(f32x4*)((float*)Cg + m * p.ldc + n) = v;
+          }
         } else {  // EPI_RESID_F32
           const f32x4 rv = *(const f32x4*)(p.resid + m * p.ldr + n);
           *(f32x4*)((float*)Cg + m * p.ldc + n) = rv + v;
@@ -317,9 +367,24 @@ void gemm_bf16_kernel(GemmParams p) {
 }
 
 template <int EPI, int ACT>
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void gemm_bf16_kernel(GemmParams p) { gemm_body<EPI, ACT, 0>(p, nullptr); }
+
+template <int EPI, int ACT>
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void gemm_bf16_parts_kernel(GemmParams p, GemmParts t) { gemm_body<EPI, ACT, 1>(p, &t); }
+
+template <int EPI, int ACT>
 hipError_t launch(const GemmParams& p, hipStream_t s) {
   const int64_t nwg = (int64_t)p.tiles_m * p.tiles_n * p.nsplit;
   hipLaunchKernelGGL((gemm_bf16_kernel<EPI, ACT>), dim3((unsigned)nwg), dim3(NT), 0, s, p);
+  return hipGetLastError();
+}
+
+template <int EPI, int ACT>
+hipError_t launch_parts(const GemmParams& p, const GemmParts& t, hipStream_t s) {
+  const int64_t nwg = (int64_t)p.tiles_m * p.tiles_n * p.nsplit;
+  hipLaunchKernelGGL((gemm_bf16_parts_kernel<EPI, ACT>), dim3((unsigned)nwg), dim3(NT), 0, s, p, t);
   return hipGetLastError();
 }
 
@@ -339,6 +404,19 @@ hipError_t launch_gemm_bf16(const GemmParams& p, hipStream_t s) {
     case EPI_RESID_F32 * 2 + 1: return launch<EPI_RESID_F32, 1>(p, s);
     case EPI_BF16_SAVE * 2 + 0: return launch<EPI_BF16_SAVE, 0>(p, s);
     case EPI_BF16_SAVE * 2 + 1: return launch<EPI_BF16_SAVE, 1>(p, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_gemm_bf16_parts(const GemmParams& p, const GemmParts& t, hipStream_t s) {
+  // device-local arrays: whole-K accumulation only (a split partial has no owner)
+  if (p.nsplit != 1 || (t.a_rows && t.a_rows % 64) || (t.c_rows && t.c_rows % 16) ||
+      (t.b_nrows && (t.b_nrows % 64 || t.b_kcols % 64 || t.b_nk < 1)))
+    return hipErrorInvalidValue;
+  switch (p.epi * 2 + (p.act ? 1 : 0)) {
+    case EPI_BF16 * 2 + 0: return launch_parts<EPI_BF16, 0>(p, t, s);
+    case EPI_BF16 * 2 + 1: return launch_parts<EPI_BF16, 1>(p, t, s);
+    case EPI_F32 * 2 + 0: return launch_parts<EPI_F32, 0>(p, t, s);
     default: return hipErrorInvalidValue;
   }
 }

@@ -43,6 +43,26 @@ struct GemmParams {
 };
 
 hipError_t launch_gemm_bf16(const GemmParams& p, hipStream_t s);
+
+// Operands held as separate device-local arrays (the lowered program's
+// per-device arrays, Sec. 6): the GEMM reads and writes them in place, so an
+// all_gather becomes addressing in the operand fetch and a reduce_scatter
+// the owner's store.  A table with rows/cols 0 is unused (plain pointer).
+//   a: A row blocks of a_rows rows (a_rows % 64 == 0), leading dim lda.
+//   b: B^T blocks, b[nb * b_nk + kb] = rows [nb b_nrows, +b_nrows) and
+//      K columns [kb b_kcols, +b_kcols) (b_nrows % 64 == 0, b_kcols % 64 ==
+//      0), each row-major with leading dim ldb.
+//   c: C row blocks of c_rows rows (c_rows % 16 == 0), leading dim ldc.
+constexpr int kMaxParts = 64;
+struct GemmParts {
+  const uint16_t* a[kMaxParts];
+  const uint16_t* b[kMaxParts];
+  void* c[kMaxParts];
+  int a_rows;
+  int b_nrows, b_kcols, b_nk;
+  int c_rows;
+};
+hipError_t launch_gemm_bf16_parts(const GemmParams& p, const GemmParts& t, hipStream_t s);
 int gemm_bf16_tile_m();
 int gemm_bf16_tile_n();
 

@@ -21,6 +21,7 @@
 #include <cstring>
 #include <algorithm>
 #include <map>
+#include <memory>
 #include <mutex>
 #include <string>
 #include <vector>
@@ -59,7 +60,8 @@ bool valid_dtype(int dt) { return dt == PARTIR_F32 || dt == PARTIR_BF16; }
 // ---------------------------------------------------------------------------
 // Plans
 // ---------------------------------------------------------------------------
-enum LaunchKind { L_GEMM_BF16, L_GEMM_F32, L_REDUCE, L_ATTN, L_ATTN_COMBINE, L_RMS, L_TRANSPOSE, L_ACT_BWD, L_COLSUM };
+enum LaunchKind { L_GEMM_BF16, L_GEMM_F32, L_REDUCE, L_ATTN, L_ATTN_COMBINE, L_RMS, L_TRANSPOSE, L_ACT_BWD, L_COLSUM,
+                  L_GEMM_BF16_PARTS };
 
 struct Launch {
   LaunchKind kind;
@@ -73,6 +75,7 @@ struct Launch {
   TransposeParams tr{};
   ActBwdParams act{};
   ColSumParams cs{};
+  std::shared_ptr<GemmParts> parts;   // L_GEMM_BF16_PARTS: the device-local arrays
 };
 
 struct Plan {
@@ -248,6 +251,7 @@ hipError_t run_one(const Launch& L, hipStream_t s) {
     case L_TRANSPOSE: return launch_transpose_bf16(L.tr, s);
     case L_ACT_BWD: return launch_act_backward(L.act, s);
     case L_COLSUM: return launch_colsum(L.cs, s);
+    case L_GEMM_BF16_PARTS: return launch_gemm_bf16_parts(L.gemm, *L.parts, s);
   }
   return hipErrorInvalidValue;
 }
@@ -1033,6 +1037,156 @@ int partir_mlp_block_train(const void* X, const void* W1t, const void* b1, const
   Plan plan;
   plan_mlp(a, ws, plan);
   keep_plan_text(plan, "mlp_block_train");
+  return execute(plan, stream);
+}
+
+// ---- MLP block on device-local arrays (BP + MP + Z3, activations sharded on M) ------
+// Device (b, m) of the mesh {B: R_batch, M: R_model} is part index b * R_model + m.
+namespace {
+struct MlpShardedArgs {
+  const void* const* X = nullptr;     // [T/(RB RM), D] per device
+  const void* const* W1t = nullptr;   // W1t[F/RM rows m, D/RB cols b] per device
+  const void* b1 = nullptr;
+  const void* const* W2t = nullptr;   // W2t[D/RB rows b, F/RM cols m] per device
+  const void* b2 = nullptr;
+  void* const* Y = nullptr;           // [T/(RB RM), D] per device
+  int64_t T = 0, D = 0, F = 0;
+  int out = PARTIR_F32, act = PARTIR_ACT_GELU_ERF, Rb = 1, Rm = 1;
+};
+
+int validate_mlp_sharded(const MlpShardedArgs& a, bool with_ptrs) {
+  if (a.T < 0 || a.D < 0 || a.F < 0) return fail(PARTIR_E_SHAPE, "T, D, F must be >= 0");
+  if (a.T > (1 << 30) || a.D > (1 << 20) || a.F > (1 << 22)) return fail(PARTIR_E_SHAPE, "dims too large");
+  if (a.Rb < 1 || a.Rm < 1) return fail(PARTIR_E_UNSUPPORTED, "R_batch and R_model must be >= 1");
+  const int nd = a.Rb * a.Rm;
+  if (nd > kMaxParts) return fail(PARTIR_E_UNSUPPORTED, "at most %d devices (R_batch * R_model)", kMaxParts);
+  if (!valid_dtype(a.out)) return fail(PARTIR_E_DTYPE, "out_dtype must be F32 or BF16");
+  if (a.act != PARTIR_ACT_NONE && a.act != PARTIR_ACT_GELU_ERF) return fail(PARTIR_E_UNSUPPORTED, "act %d", a.act);
+  if (a.T % nd) return fail(PARTIR_E_DIVISIBILITY, "R_batch*R_model=%d does not divide T=%lld", nd, (long long)a.T);
+  if (a.D % a.Rb) return fail(PARTIR_E_DIVISIBILITY, "R_batch=%d does not divide D=%lld", a.Rb, (long long)a.D);
+  if (a.F % a.Rm) return fail(PARTIR_E_DIVISIBILITY, "R_model=%d does not divide F=%lld", a.Rm, (long long)a.F);
+  if ((a.T / nd) % 64 || (a.D / a.Rb) % 64 || (a.F / a.Rm) % 64)
+    return fail(PARTIR_E_LAYOUT, "T/(R_batch R_model), D/R_batch and F/R_model must be multiples of 64 (the "
+                "GEMM's 64-row load blocks and 64-wide K tiles never straddle two arrays)");
+  if (!with_ptrs) return PARTIR_OK;
+  const bool live = a.T * a.D * a.F > 0, out_live = a.T * a.D > 0;
+  if ((live && (!a.X || !a.W1t || !a.W2t)) || (out_live && !a.Y))
+    return fail(PARTIR_E_NULL, "the part arrays must be non-NULL");
+  if (!aligned16(a.b1) || !aligned16(a.b2)) return fail(PARTIR_E_LAYOUT, "b1, b2 must be 16-byte aligned");
+  for (int i = 0; i < nd; ++i) {
+    if (live && (!a.X[i] || !a.W1t[i] || !a.W2t[i])) return fail(PARTIR_E_NULL, "part %d is NULL", i);
+    if (out_live && !a.Y[i]) return fail(PARTIR_E_NULL, "output part %d is NULL", i);
+    if ((live && (!aligned16(a.X[i]) || !aligned16(a.W1t[i]) || !aligned16(a.W2t[i]))) ||
+        (out_live && !aligned16(a.Y[i])))
+      return fail(PARTIR_E_LAYOUT, "part %d is not 16-byte aligned", i);
+  }
+  return PARTIR_OK;
+}
+
+// The lowered program of the MLP under BP + MP + Z3 with its activations
+// sharded on M (Sec. 3's FSDP chain and the remark after it; Sec. 6's
+// collectives): per device (b, m)
+//   x  = all_gather<M, dim 0>(X_bm)               -> up GEMM's A rows, read in place
+//   w1 = all_gather<B, dim 0 of W1>(W1_bm)        -> up GEMM's B K-blocks, read in place
+//   h  = act(x w1 + b1_m)                         -> H[b rows, m cols] (workspace)
+//   w2 = all_gather<B, dim 1 of W2>(W2_bm)        -> down GEMM's B row blocks, read in place
+//   y  = reduce_scatter<M, dim 0>(h w2) + b2      -> the down GEMM's fused #sum over m, each
+//                                                    row block stored by its owner into Y_bm
+void plan_mlp_sharded(const MlpShardedArgs& a, void* ws, Plan& plan) {
+  const int nd = a.Rb * a.Rm;
+  const int64_t T = a.T, D = a.D, F = a.F, rows_dev = T / nd;
+  plan.n_shards = nd;
+  plan.n_tile_loops = (a.Rb > 1) + 1;
+  plan.flops = 4.0 * T * D * F;
+  if (T * D == 0) return;
+  if (F == 0) {   // every model shard is empty: each device's slice is b2
+    plan.n_sum_loops = 1;
+    for (int i = 0; i < nd; ++i)
+      plan_empty_sum(a.Y ? a.Y[i] : nullptr, rows_dev, D, D, a.out == PARTIR_BF16, (const float*)a.b2, nullptr,
+                     0, false, "mlp.down", plan);
+    return;
+  }
+  void* H = ws;
+  plan.ws_bytes = align_up((size_t)T * F * 2);
+  auto parted = [&](const GemmSpec& g, GemmParts* t, const char* how) {
+    plan_gemm(g, nullptr, plan);
+    Launch& L = plan.launches.back();
+    L.kind = L_GEMM_BF16_PARTS;
+    L.parts.reset(t);
+    L.text += how;
+  };
+  GemmSpec g1;
+  g1.A = nullptr; g1.B[0] = nullptr; g1.C[0] = H; g1.bias[0] = (const float*)a.b1;
+  g1.lda = D; g1.ldb = D / a.Rb; g1.ldc = F;
+  g1.M = T; g1.N = F; g1.K = D;
+  g1.c_dtype = PARTIR_BF16; g1.rm = a.Rb; g1.rn = a.Rm; g1.act = a.act;
+  g1.name = "mlp.up";
+  g1.label = "mlp.up   H = act(all_gather<M>(X)[b] . all_gather<B>(W1)[:, m])";
+  GemmParts* t1 = new GemmParts{};
+  t1->a_rows = (int)rows_dev;
+  t1->b_nrows = (int)(F / a.Rm); t1->b_kcols = (int)(D / a.Rb); t1->b_nk = a.Rb;
+  for (int b = 0; b < a.Rb; ++b)
+    for (int m = 0; m < a.Rm; ++m) {
+      const int dev = b * a.Rm + m;
+      if (a.X) t1->a[dev] = (const uint16_t*)a.X[dev];
+      if (a.W1t) t1->b[m * a.Rb + b] = (const uint16_t*)a.W1t[dev];   // N block m, K block b
+    }
+  parted(g1, t1, "; X rows and W1 blocks read from each device's array (fused all_gathers)");
+  GemmSpec g2;
+  g2.A = H; g2.B[0] = nullptr; g2.C[0] = nullptr; g2.bias[0] = (const float*)a.b2;
+  g2.lda = F; g2.ldb = F / a.Rm; g2.ldc = D;
+  g2.M = T; g2.N = D; g2.K = F;
+  g2.c_dtype = a.out; g2.rm = a.Rb; g2.rk = a.Rm; g2.sum_impl = PARTIR_SUM_FUSED;
+  g2.name = "mlp.down";
+  g2.label = "mlp.down Y = reduce_scatter<M>(sum_m H[:, m] . all_gather<B>(W2)[m, :])";
+  GemmParts* t2 = new GemmParts{};
+  t2->b_nrows = (int)(D / a.Rb); t2->b_kcols = (int)(F / a.Rm); t2->b_nk = a.Rm;
+  t2->c_rows = (int)rows_dev;
+  for (int i = 0; i < nd; ++i) {
+    if (a.W2t) t2->b[i] = (const uint16_t*)a.W2t[i];   // device (b, m): N block b, K block m
+    if (a.Y) t2->c[i] = a.Y[i];
+  }
+  parted(g2, t2, "; W2 blocks read in place; each row block stored by its owner (fused reduce_scatter)");
+}
+}  // namespace
+
+size_t partir_mlp_block_sharded_workspace(int64_t T, int64_t D, int64_t F, int R_batch, int R_model) {
+  MlpShardedArgs a;
+  a.T = T; a.D = D; a.F = F; a.Rb = R_batch; a.Rm = R_model;
+  if (validate_mlp_sharded(a, false) != PARTIR_OK) return (size_t)-1;
+  Plan plan;
+  plan_mlp_sharded(a, nullptr, plan);
+  return plan.ws_bytes;
+}
+
+int partir_plan_mlp_block_sharded(int64_t T, int64_t D, int64_t F, int act, int R_batch, int R_model,
+                                  partir_plan_info* info) {
+  MlpShardedArgs a;
+  a.T = T; a.D = D; a.F = F; a.act = act; a.Rb = R_batch; a.Rm = R_model;
+  int st = validate_mlp_sharded(a, false);
+  if (st) return st;
+  Plan plan;
+  plan_mlp_sharded(a, nullptr, plan);
+  keep_plan_text(plan, "mlp_block_sharded");
+  fill_info(plan, info);
+  return PARTIR_OK;
+}
+
+int partir_mlp_block_sharded(const void* const* X_parts, const void* const* W1t_parts, const void* b1,
+                             const void* const* W2t_parts, const void* b2, void* const* Y_parts, int64_t T,
+                             int64_t D, int64_t F, int out_dtype, int act, int R_batch, int R_model, void* ws,
+                             size_t ws_bytes, void* stream) {
+  MlpShardedArgs a;
+  a.X = X_parts; a.W1t = W1t_parts; a.b1 = b1; a.W2t = W2t_parts; a.b2 = b2; a.Y = Y_parts;
+  a.T = T; a.D = D; a.F = F; a.out = out_dtype; a.act = act; a.Rb = R_batch; a.Rm = R_model;
+  int st = validate_mlp_sharded(a, true);
+  if (st) return st;
+  Plan probe;
+  plan_mlp_sharded(a, nullptr, probe);
+  if ((st = check_ws(probe, ws, ws_bytes))) return st;
+  Plan plan;
+  plan_mlp_sharded(a, ws, plan);
+  keep_plan_text(plan, "mlp_block_sharded");
   return execute(plan, stream);
 }
 

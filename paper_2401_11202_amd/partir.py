@@ -33,7 +33,8 @@ EXPORTS = ("partir_loop_matmul", "partir_loop_matmul_workspace", "partir_mlp_blo
            "partir_status_string", "partir_last_error", "partir_version", "partir_propagate",
            "partir_attention", "partir_attention_workspace", "partir_plan_attention",
            "partir_mlp_block_backward", "partir_mlp_block_backward_workspace", "partir_plan_mlp_block_backward",
-           "partir_mlp_block_train")
+           "partir_mlp_block_train", "partir_mlp_block_sharded", "partir_mlp_block_sharded_workspace",
+           "partir_plan_mlp_block_sharded")
 
 
 class PartirError(RuntimeError):
@@ -58,6 +59,7 @@ class TraceEntry(ctypes.Structure):
 
 _lib = None
 I64, I32, P, SZ, F = ctypes.c_int64, ctypes.c_int, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_float
+PP = ctypes.POINTER(ctypes.c_void_p)   # a host array of device pointers
 
 
 def lib():
@@ -95,6 +97,9 @@ def lib():
         "partir_mlp_block_train": (I32, [P, P, P, P, P, P, P, I64, I64, I64, I32, I32, I32, I32, I32, P, SZ, P]),
         "partir_mlp_block_backward_workspace": (SZ, [I64, I64, I64, I32, I32, I32, I32]),
         "partir_plan_mlp_block_backward": (I32, [I64, I64, I64, I32, I32, I32, ctypes.POINTER(PlanInfo)]),
+        "partir_mlp_block_sharded": (I32, [PP, PP, P, PP, P, PP, I64, I64, I64, I32, I32, I32, I32, P, SZ, P]),
+        "partir_mlp_block_sharded_workspace": (SZ, [I64, I64, I64, I32, I32]),
+        "partir_plan_mlp_block_sharded": (I32, [I64, I64, I64, I32, I32, I32, ctypes.POINTER(PlanInfo)]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(L, name)
@@ -251,6 +256,58 @@ def mlp_block_backward(X, W1t, W2t, dY, *, b1=None, Z=None, R_batch: int = 1, R_
                                            _ptr(dW1t), _ptr(db1), _ptr(dW2t), _ptr(db2), T, D, F, a, R_batch,
                                            R_model, _ptr(ws), wsb, _stream(stream)))
     return (dX, dW1t, dW2t, db1, db2) if bias_grads else (dX, dW1t, dW2t)
+
+
+def _ptr_array(ts):
+    """Host array of the tensors' device pointers (None for an absent list)."""
+    if ts is None:
+        return None
+    arr = (ctypes.c_void_p * len(ts))()
+    for i, t in enumerate(ts):
+        arr[i] = None if t is None else t.data_ptr()
+    return arr
+
+
+def mlp_block_sharded(X_parts, W1t_parts, W2t_parts, *, R_batch: int, R_model: int, b1=None, b2=None,
+                      act: str = "gelu", out_dtype=None, out_parts=None, workspace=None, stream=None):
+    """The MLP block on device-local arrays (BP + MP + Z3, activations sharded
+    over the model axis).  Part p = b * R_model + m of the mesh {B, M}:
+    X_parts[p] [T/(R_batch R_model), D]; W1t_parts[p] = W1t[F/R_model rows m,
+    D/R_batch cols b]; W2t_parts[p] = W2t[D/R_batch rows b, F/R_model cols m].
+    Returns the list of Y parts (token rows p of Y)."""
+    import torch
+    nd = R_batch * R_model
+    rows, D = X_parts[0].shape
+    T = rows * nd
+    F = W1t_parts[0].shape[0] * R_model
+    od = F32 if out_dtype in (None, torch.float32) else BF16
+    if out_parts is None:
+        out_parts = [torch.empty((rows, D), dtype=_tdt(od), device=X_parts[0].device) for _ in range(nd)]
+    ws, wsb = _workspace(lib().partir_mlp_block_sharded_workspace(T, D, F, R_batch, R_model), X_parts[0].device,
+                         workspace)
+    xs, w1s, w2s, ys = (_ptr_array(v) for v in (X_parts, W1t_parts, W2t_parts, out_parts))
+    _check(lib().partir_mlp_block_sharded(xs, w1s, _ptr(b1), w2s, _ptr(b2), ys, T, D, F, od,
+                                          ACT_GELU if act == "gelu" else ACT_NONE, R_batch, R_model,
+                                          _ptr(ws), wsb, _stream(stream)))
+    return out_parts
+
+
+def z3_device_arrays(X, W1t, W2t, R_batch: int, R_model: int):
+    """Copies whole operands into the device-local arrays mlp_block_sharded
+    takes (each part its own allocation): X by token blocks p = b * R_model +
+    m; W1t block (rows m, cols b); W2t block (rows b, cols m)."""
+    nd = R_batch * R_model
+    T, D = X.shape
+    F = W1t.shape[0]
+    tr, dr, fr = T // nd, D // R_batch, F // R_model
+    xs = [X[p * tr:(p + 1) * tr].clone() for p in range(nd)]
+    w1 = [W1t[m * fr:(m + 1) * fr, b * dr:(b + 1) * dr].contiguous() for b in range(R_batch) for m in range(R_model)]
+    w2 = [W2t[b * dr:(b + 1) * dr, m * fr:(m + 1) * fr].contiguous() for b in range(R_batch) for m in range(R_model)]
+    return xs, w1, w2
+
+
+def plan_mlp_block_sharded(T, D, F, act=ACT_GELU, R_batch=1, R_model=1):
+    return _plan(lib().partir_plan_mlp_block_sharded, T, D, F, act, R_batch, R_model)
 
 
 def plan_mlp_block_backward(T, D, F, act=ACT_GELU, R_batch=1, R_model=1):

@@ -24,7 +24,7 @@ from . import inputs as I
 @dataclass(frozen=True)
 class Workload:
     name: str
-    kind: str                 # matmul | mlp | attn | decoder | attn_core | mlp_train
+    kind: str                 # matmul | mlp | attn | decoder | attn_core | mlp_train | mlp_z3
     wid: int                  # seed id
     dims: Dict[str, int] = field(default_factory=dict)
     dtype: str = "bf16"
@@ -72,10 +72,15 @@ WORKLOADS = {
     # weight gradients
     "mlp_megatron_train": _mlp_train("mlp_megatron_train", 7, 8192, 4096, 16384, 1, 8),
     "mlp_batch_x_megatron_train": _mlp_train("mlp_batch_x_megatron_train", 8, 8192, 4096, 16384, 2, 4),
+    # the MLP on device-local arrays under BP + MP + Z3 with the activations
+    # also sharded over the model axis: mesh {B: 2, M: 4}, 8 devices
+    "mlp_z3_sp": Workload("mlp_z3_sp", "mlp_z3", 9, dict(T=8192, D=4096, F=16384, R_batch=2, R_model=4)),
     # small twins: same structure and partition sizes, scaled down
     "mlp_megatron_small": _mlp("mlp_megatron_small", 12, 512, 256, 1024, 1, 8),
     "attn_block_small": _attn("attn_block_small", 13, 2, 256, 1024, 8, 128, 1, 8),
     "mlp_batch_x_megatron_small": _mlp("mlp_batch_x_megatron_small", 14, 1024, 512, 2048, 4, 8),
+    "mlp_z3_sp_small": Workload("mlp_z3_sp_small", "mlp_z3", 17, dict(T=1024, D=256, F=1024, R_batch=2,
+                                                                      R_model=4)),
     "mlp_train_small": _mlp_train("mlp_train_small", 16, 512, 256, 1024, 2, 4),
     "decoder_2layer_small": _dec("decoder_2layer_small", 15, 2, 256, 1024, 8, 128, 1728, 2, 2, 4),
 }
@@ -104,6 +109,15 @@ def mlp_train_inputs(w: Workload):
     x = mlp_inputs(w)
     x["dY"] = I.gaussian(w.wid, 3, (w["T"], w["D"]), 1.0)
     x["b1"] = I.gaussian(w.wid, 4, (w["F"],), 0.5, "f32")
+    return x
+
+
+def mlp_z3_inputs(w: Workload):
+    """The MLP's whole operands (the device-local arrays are their blocks)
+    plus biases b1 ~ N(0, 1/4), b2 ~ N(0, 1/4)."""
+    x = mlp_inputs(w)
+    x["b1"] = I.gaussian(w.wid, 4, (w["F"],), 0.5, "f32")
+    x["b2"] = I.gaussian(w.wid, 5, (w["D"],), 0.5, "f32")
     return x
 
 
@@ -136,7 +150,8 @@ def attn_core_inputs(w: Workload):
 
 def make_inputs(w: Workload):
     return {"matmul": matmul_inputs, "mlp": mlp_inputs, "attn": attn_inputs,
-            "decoder": decoder_inputs, "attn_core": attn_core_inputs, "mlp_train": mlp_train_inputs}[w.kind](w)
+            "decoder": decoder_inputs, "attn_core": attn_core_inputs, "mlp_train": mlp_train_inputs,
+            "mlp_z3": mlp_z3_inputs}[w.kind](w)
 
 
 # ---------------------------------------------------------------------------
@@ -151,7 +166,7 @@ def attn_core_flops(B, S, H, dh, causal=True):
 def flops(w: Workload) -> float:
     if w.kind == "matmul":
         return 2.0 * w["M"] * w["N"] * w["K"]
-    if w.kind == "mlp":
+    if w.kind in ("mlp", "mlp_z3"):
         return 4.0 * w["T"] * w["D"] * w["F"]
     if w.kind == "attn":
         T = w["B"] * w["S"]

@@ -373,3 +373,43 @@ def test_training_forward_validation(monkeypatch):
     assert P.STATUS[L.partir_mlp_block_train(*args(DUMMY))] == "PARTIR_E_HIP"
     assert L.partir_last_plan_text().decode().startswith("mlp_block_train:")
     assert P.STATUS[L.partir_mlp_block_train(*args(None, T=0))] == "PARTIR_E_HIP"   # nothing to keep
+
+
+# ---------------------------------------------------------------------------
+# MLP on device-local arrays (BP + MP + Z3, activations sharded on M)
+# ---------------------------------------------------------------------------
+def sharded(T=1024, D=256, F=1024, Rb=2, Rm=4, parts=DUMMY, ws_bytes=1 << 30, out=P.F32):
+    arr = (ctypes.c_void_p * (Rb * Rm))(*([parts] * (Rb * Rm)))
+    return P.lib().partir_mlp_block_sharded(arr, arr, None, arr, None, arr, T, D, F, out, P.ACT_GELU, Rb, Rm,
+                                            DUMMY, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kwargs,status", [
+    (dict(parts=NULL), "PARTIR_E_NULL"),
+    (dict(parts=DUMMY_ODD), "PARTIR_E_LAYOUT"),
+    (dict(T=1028), "PARTIR_E_DIVISIBILITY"),
+    (dict(D=255), "PARTIR_E_DIVISIBILITY"),
+    (dict(F=1022), "PARTIR_E_DIVISIBILITY"),
+    (dict(T=512), "PARTIR_E_HIP"),                   # 64 rows per device is fine ...
+    (dict(T=256), "PARTIR_E_LAYOUT"),                # ... 32 is not a whole load block
+    (dict(D=64), "PARTIR_E_LAYOUT"),                 # D/R_batch = 32
+    (dict(Rb=8, Rm=16, T=8192 * 16, D=512, F=1024), "PARTIR_E_UNSUPPORTED"),   # 128 devices
+    (dict(out=7), "PARTIR_E_DTYPE"),
+    (dict(ws_bytes=10), "PARTIR_E_WORKSPACE"),
+    (dict(), "PARTIR_E_HIP"),
+])
+def test_sharded_validation(kwargs, status):
+    assert P.STATUS[sharded(**kwargs)] == status, P.lib().partir_last_error().decode()
+
+
+def test_sharded_plan():
+    p = P.plan_mlp_block_sharded(8192, 4096, 16384, R_batch=2, R_model=4)
+    assert p["n_launches"] == 2 and p["n_sum_loops"] == 1 and p["n_sum_splitk"] == 0
+    assert p["n_virtual_shards"] == 8 and p["workspace_bytes"] == 8192 * 16384 * 2
+    assert "fused all_gathers" in p["text"] and "fused reduce_scatter" in p["text"]
+    assert P.lib().partir_mlp_block_sharded_workspace(8192, 4096, 16384, 2, 4) == p["workspace_bytes"]
+    # a small grid still accumulates the whole #sum in the tile: the owner writes its rows
+    s = P.plan_mlp_block_sharded(1024, 256, 1024, R_batch=2, R_model=4)
+    assert s["n_sum_splitk"] == 0 and s["n_launches"] == 2
+    e = P.plan_mlp_block_sharded(1024, 256, 0, R_batch=2, R_model=4)
+    assert e["n_launches"] == 8 and e["workspace_bytes"] == 0        # b2 into each device's part
