@@ -147,6 +147,42 @@ def causal_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, scale: float,
     return matmul(p, v)
 
 
+def attention_backward(q, k, v, do, scale: float, causal: bool = True, return_norm: bool = False):
+    """Gradients of o = causal_attention(q, k, v) for the cotangent do, one
+    head of one sequence (positions 0..n-1), by the chain rule through
+    s = scale q k^T, p = softmax_rows(s), o = p v:
+
+      dv = p^T do;  dp = do v^T;  ds = p * (dp - rowsum(do * o));
+      dq = scale ds k;  dk = scale ds^T q.
+
+    (rowsum(do * o)_i = sum_j p_ij dp_ij: the softmax Jacobian applied to dp.)
+    With return_norm also first-order error normalisers: for each gradient
+    its last product with ds replaced by p * (|do||v|^T + rowsum|do * o|)
+    (the magnitude of dp - D) and every other operand by its magnitude.
+    Returns (dq, dk, dv) or ((dq, dk, dv), (nq, nk, nv)).
+    """
+    q, k, v, do = (np.asarray(a, np.float64) for a in (q, k, v, do))
+    n = q.shape[0]
+    s = matmul(q, k.T) * scale
+    if causal:
+        pos = np.arange(n)
+        s = np.where(pos[None, :] <= pos[:, None], s, -np.inf)
+    p = np.exp(s - np.max(s, axis=1, keepdims=True))
+    p = p / np.sum(p, axis=1, keepdims=True)
+    o = matmul(p, v)
+    dv = matmul(p.T, do)
+    dp = matmul(do, v.T)
+    d = np.sum(do * o, axis=1, keepdims=True)
+    ds = p * (dp - d)
+    dq = scale * matmul(ds, k)
+    dk = scale * matmul(ds.T, q)
+    if not return_norm:
+        return dq, dk, dv
+    nds = p * (abs_product(do, v.T) + np.sum(np.abs(do * o), axis=1, keepdims=True))
+    return (dq, dk, dv), (scale * matmul(nds, np.abs(k)), scale * matmul(nds.T, np.abs(q)),
+                          matmul(p.T, np.abs(do)))
+
+
 # ---------------------------------------------------------------------------
 # The key axis as a loop: a custom associative #sum (Sec. 5.2.1 footnote)
 # ---------------------------------------------------------------------------

@@ -190,3 +190,72 @@ def test_mlp_backward_sampled_matches_full(act):
         assert s[k].shape == val.shape
         assert np.max(np.abs(s[k] - val) / nv) < 1e-13, k
         assert np.max(np.abs(sn[k] - nv) / nv) < 1e-13, k
+
+
+# ---------------------------------------------------------------------------
+# attention core gradients
+# ---------------------------------------------------------------------------
+def attn_problem(seed, n=12, dh=4):
+    rng = np.random.default_rng(seed)
+    return [rng.standard_normal((n, dh)) for _ in range(4)]
+
+
+@pytest.mark.parametrize("causal", [True, False])
+def test_attention_backward_matches_torch_autograd(causal):
+    q, k, v, do = attn_problem(20)
+    scale = 0.5
+    dq, dk, dv = O.attention_backward(q, k, v, do, scale, causal)
+    ts = [torch.from_numpy(a.copy()).requires_grad_(True) for a in (q, k, v)]
+    s = ts[0] @ ts[1].T * scale
+    if causal:
+        s = s.masked_fill(torch.triu(torch.ones(12, 12, dtype=torch.bool), 1), float("-inf"))
+    (torch.softmax(s, dim=1) @ ts[2]).backward(torch.from_numpy(do))
+    for got, t in zip((dq, dk, dv), ts):
+        assert np.max(np.abs(got - t.grad.numpy())) < 1e-12
+
+
+def test_attention_backward_central_differences():
+    """<causal_attention(q, k, v), do> differentiated entry by entry."""
+    q, k, v, do = attn_problem(21, n=6, dh=3)
+    scale, h = 0.7, 1e-6
+    g = O.attention_backward(q, k, v, do, scale, True)
+    args = [q, k, v]
+    loss = lambda a: float(np.sum(O.causal_attention(a[0], a[1], a[2], scale, True) * do))
+    for which in range(3):
+        for idx in np.ndindex(args[which].shape):
+            up = [a.copy() for a in args]
+            dn = [a.copy() for a in args]
+            up[which][idx] += h
+            dn[which][idx] -= h
+            fd = (loss(up) - loss(dn)) / (2 * h)
+            assert abs(g[which][idx] - fd) < 1e-7 * max(1.0, abs(fd)), (which, idx)
+
+
+def test_attention_backward_closed_forms():
+    q, k, v, do = attn_problem(22)
+    # query 0 sees only key 0 (p = 1): its score gradient vanishes, so dq_0 = 0,
+    # and dv gets do_0 in full from it
+    dq, dk, dv = O.attention_backward(q, k, v, do, 0.3, True)
+    assert np.max(np.abs(dq[0])) < 1e-15
+    # the last key is seen only by the last query: dv_last = p_last,last do_last
+    s = q[-1] @ k.T * 0.3
+    p = np.exp(s - s.max())
+    p /= p.sum()
+    assert np.max(np.abs(dv[-1] - p[-1] * do[-1])) < 1e-14
+    # a constant shift of v's rows changes o by the same constant: dq, dk unchanged
+    dq2, dk2, _ = O.attention_backward(q, k, v + 5.0, do, 0.3, True)
+    assert np.max(np.abs(dq2 - dq)) < 1e-11 and np.max(np.abs(dk2 - dk)) < 1e-11
+    # softmax is shift-invariant along a row, so each row of ds sums to zero:
+    # sum_j dk_j = scale sum_i (sum_j ds_ij) q_i = 0, and with all-equal keys
+    # dq = scale ds k is zero
+    kk = np.tile(k[:1], (12, 1))
+    dq3, _, _ = O.attention_backward(q, kk, v, do, 0.3, False)
+    assert np.max(np.abs(dq3)) < 1e-13
+    assert np.max(np.abs(np.sum(dk, axis=0))) < 1e-12
+
+
+def test_attention_backward_norms_bound():
+    q, k, v, do = attn_problem(23, n=16, dh=8)
+    (dq, dk, dv), (nq, nk, nv) = O.attention_backward(q, k, v, do, 0.35, True, return_norm=True)
+    for g, n in ((dq, nq), (dk, nk), (dv, nv)):
+        assert np.all(np.abs(g) <= n * (1 + 1e-12))

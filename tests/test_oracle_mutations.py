@@ -120,6 +120,19 @@ def _scatter_wrong_chunk(local, mesh, dim, axis):
     return out
 
 
+def _attn_bwd_without_rowsum(q, k, v, do, scale, causal=True, return_norm=False):
+    """The softmax Jacobian applied without its rank-one term: ds = p * dp."""
+    q, k, v, do = (np.asarray(a, np.float64) for a in (q, k, v, do))
+    n = q.shape[0]
+    s = q @ k.T * scale
+    if causal:
+        s = np.where(np.arange(n)[None, :] <= np.arange(n)[:, None], s, -np.inf)
+    p = np.exp(s - s.max(axis=1, keepdims=True))
+    p /= p.sum(axis=1, keepdims=True)
+    ds = p * (do @ v.T)
+    return scale * ds @ k, scale * ds.T @ q, p.T @ do
+
+
 def _attend_k_from_q(xb, Wq_m, Wk_m, Wv_m, *rest):
     return _real["_attend_shard"](xb, Wq_m, Wq_m, Wv_m, *rest)
 
@@ -142,6 +155,8 @@ def _run(pins, golden):
                 pin(2, 4)
             elif pin.__name__ == "test_mlp_backward_matches_torch_autograd":
                 pin("gelu", 2, 4)
+            elif pin.__name__ == "test_attention_backward_matches_torch_autograd":
+                pin(True)
             elif pin.__name__ == "test_z3_mlp_integer_exact_equals_unpartitioned":
                 pin(4, 2, True)
             elif pin.__name__ == "test_reduce_scatter_is_all_reduce_fused_with_all_slice":
@@ -185,6 +200,9 @@ CASES = {
     "reduce_scatter hands out the wrong chunk": ("reduce_scatter", _scatter_wrong_chunk,
                                                  [SP.test_reduce_scatter_is_all_reduce_fused_with_all_slice,
                                                   SP.test_z3_mlp_integer_exact_equals_unpartitioned]),
+    "attention backward drops the rowsum term": ("attention_backward", _attn_bwd_without_rowsum,
+                                                 [BW.test_attention_backward_matches_torch_autograd,
+                                                  BW.test_attention_backward_central_differences]),
     "keys projected with Wq": ("_attend_shard", _attend_k_from_q, [G.test_attn_block_brute_force]),
 }
 
