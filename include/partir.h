@@ -308,6 +308,36 @@ int partir_attention(const void* Q, const void* K, const void* V, void* O,
 
 size_t partir_attention_workspace(int64_t B, int64_t S, int64_t n_heads, int64_t d_head, int R_kv);
 
+/* The forward of a training step: partir_attention, and also the per-row
+ * base-2 log-sum-exp of the scaled scores, lse[t][h] = log2 sum_j
+ * 2^(c s_tj) (c = scale log2 e; equal to the natural log-sum-exp times
+ * log2 e), lse: [B*S, n_heads] fp32, which partir_attention_backward reads
+ * instead of recomputing the softmax denominators.  Same workspace as
+ * partir_attention; lse must be non-NULL when B*S > 0. */
+int partir_attention_train(const void* Q, const void* K, const void* V, void* O, float* lse,
+                           int64_t B, int64_t S, int64_t n_heads, int64_t d_head,
+                           int causal, float scale, int R_kv,
+                           void* ws, size_t ws_bytes, void* stream);
+
+/* Gradients of the attention core (the evaluation trains, Sec. 7).  With
+ * P = softmax of the scaled (masked) scores:
+ *   dV = P^T dO;  dS = P * (dO V^T - rowsum(dO * O));  dQ = scale dS K;
+ *   dK = scale dS^T Q,
+ * per head (the heads #tile carries over: every head's gradients are
+ * independent).  Q, K, V, O, dO, dQ, dK, dV: [B*S, n_heads*d_head] bf16 as in
+ * partir_attention; lse from partir_attention_train.  dQ is accumulated by
+ * one workgroup per query block over the keys, dK and dV by one per key block
+ * over the queries, in a fixed order: deterministic, no atomics.  Workspace:
+ * the rowsums, B*S*n_heads fp32.  Constraints as partir_attention.
+ * Errors: E_NULL, E_SHAPE, E_LAYOUT, E_WORKSPACE, E_HIP. */
+int partir_attention_backward(const void* Q, const void* K, const void* V, const void* O,
+                              const void* dO, const float* lse,
+                              void* dQ, void* dK, void* dV,
+                              int64_t B, int64_t S, int64_t n_heads, int64_t d_head,
+                              int causal, float scale,
+                              void* ws, size_t ws_bytes, void* stream);
+size_t partir_attention_backward_workspace(int64_t B, int64_t S, int64_t n_heads, int64_t d_head);
+
 /* ------------------------------------------------------------------------ */
 /* Pre-norm decoder layer on an fp32 residual stream, in place.               */
 /* ------------------------------------------------------------------------ */
@@ -360,6 +390,8 @@ int partir_plan_attn_block(int64_t B, int64_t S, int64_t D, int64_t n_heads, int
                            int R_batch, int R_model, partir_plan_info* info);
 int partir_plan_attention(int64_t B, int64_t S, int64_t n_heads, int64_t d_head, int causal, int R_kv,
                           partir_plan_info* info);
+int partir_plan_attention_backward(int64_t B, int64_t S, int64_t n_heads, int64_t d_head, int causal,
+                                   partir_plan_info* info);
 int partir_plan_mlp_block_backward(int64_t T, int64_t D, int64_t F, int act, int R_batch, int R_model,
                                    partir_plan_info* info);
 int partir_plan_mlp_block_sharded(int64_t T, int64_t D, int64_t F, int act, int R_batch, int R_model,

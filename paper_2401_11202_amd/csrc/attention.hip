@@ -227,6 +227,7 @@ void attention_kernel(AttnParams p) {
     return;
   }
   // ---- normalise and store O[query][head*128 + d] ------------------------------
+  if (p.lse && h == 0) p.lse[(tok0 + qi) * p.H + head] = m_run + __builtin_amdgcn_logf(l_tot);
   const float inv = 1.0f / l_tot;
   uint16_t* orow = p.O + (tok0 + qi) * p.ldo + head * DH;
 #pragma unroll
@@ -259,6 +260,7 @@ __global__ __launch_bounds__(256) void attention_combine_kernel(AttnParams p) {
     L += w * p.Lpart[s * sstride + th];
     acc += w * *(const f32x4*)(p.Opart + (s * T + t) * (int64_t)(p.H * DH) + head * DH + 4 * c4);
   }
+  if (p.lse && c4 == 0) p.lse[th] = M + __builtin_amdgcn_logf(L);
   const float inv = 1.0f / L;
   const bf16x4 o = {(__bf16)(acc[0] * inv), (__bf16)(acc[1] * inv), (__bf16)(acc[2] * inv), (__bf16)(acc[3] * inv)};
   *(bf16x4*)(p.O + t * p.ldo + head * DH + 4 * c4) = o;

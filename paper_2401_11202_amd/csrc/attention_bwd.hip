@@ -1,0 +1,367 @@
+// Softmax attention backward for gfx950, d_head = 128, bf16 in / bf16 out.
+//
+// Given Q, K, V, the forward output O, its cotangent dO and the per-row
+// log-sum-exp of the scaled scores (base 2: lse2 = log2 sum_j 2^(c s_j),
+// c = scale log2 e), with P = 2^(c S - lse2):
+//     D  = rowsum(dO * O)             dV = P^T dO        dP = dO V^T
+//     dS = P * (dP - D)               dQ = scale dS K    dK = scale dS^T Q
+// Two passes, each a loop over one axis of the score matrix with the other
+// axis held in registers, so every gradient is accumulated by one workgroup
+// in a fixed order (no atomics: deterministic):
+//  * dq pass: workgroup = (sequence, head, 128 queries), 4 waves x 32
+//    queries; keys stream through LDS 64 at a time.  S^T = K Q^T and
+//    dP^T = V dO^T put one query per lane, dQ^T += K^T dS^T (K^T read with
+//    ds_read_b64_tr_b16).  It also writes D for the second pass.
+//  * dkv pass: workgroup = (sequence, head, 128 keys), 4 waves x 32 keys;
+//    queries stream 64 at a time.  S = Q K^T and dP = dO V^T put one key per
+//    lane, dV^T += dO^T P and dK^T += Q^T dS (transposed reads of the dO and
+//    Q tiles).
+// Inside a 16-wide MFMA contraction step the order of the contracted
+// positions is permuted identically on both operands (exact for a sum).
+// All LDS tiles are 64 rows x 256 B with 16-byte chunks XOR-swizzled by row,
+// which serves both the row reads and the transposed reads.
+#include "kernels.h"
+
+namespace partir {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+
+constexpr int DH = 128, NT = 256;
+constexpr int TR = 64;                 // rows of a streamed tile
+constexpr int TP = 256;                // tile row pitch (bytes)
+constexpr int TILE = TR * TP;          // 16 KiB
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint32_t bytes) {
+  const uint64_t a = (uint64_t)p;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)a);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(a >> 32));
+  void* u = (void*)(((uint64_t)hi << 32) | lo);
+  return __builtin_amdgcn_make_buffer_rsrc(u, (short)0, (int)__builtin_amdgcn_readfirstlane(bytes), 0x00020000);
+}
+
+// byte offset of (row, byte column) in a swizzled tile
+__device__ __forceinline__ int toff(int row, int colb) {
+  return row * TP + ((((colb >> 4) ^ (row & 15))) << 4) + (colb & 15);
+}
+
+// Streams two [64 x 128] bf16 tiles (rows `row0..` of X and Y, head columns)
+// through registers into a swizzled LDS stage; 4 + 4 chunks per thread.
+struct TilePair {
+  __amdgpu_buffer_rsrc_t rx, ry;
+  uint32_t ox[4], oy[4];
+  uint32_t stepx, stepy;
+  i32x4 bx[4], by[4];
+  int lr, lc;
+  __device__ void init(const uint16_t* X, int64_t ldx, const uint16_t* Y, int64_t ldy, int S, int tid) {
+    lr = tid >> 4;
+    lc = tid & 15;
+    rx = make_rsrc(X, (uint32_t)((S - 1) * ldx * 2 + DH * 2));
+    ry = make_rsrc(Y, (uint32_t)((S - 1) * ldy * 2 + DH * 2));
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      ox[i] = (uint32_t)((lr + 16 * i) * ldx * 2 + lc * 16);
+      oy[i] = (uint32_t)((lr + 16 * i) * ldy * 2 + lc * 16);
+    }
+    stepx = (uint32_t)(TR * ldx * 2);
+    stepy = (uint32_t)(TR * ldy * 2);
+  }
+  __device__ void load(int blk) {
+    const uint32_t sx = (uint32_t)blk * stepx, sy = (uint32_t)blk * stepy;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      bx[i] = __builtin_bit_cast(i32x4, __builtin_amdgcn_raw_buffer_load_b128(rx, ox[i], sx, 0));
+      by[i] = __builtin_bit_cast(i32x4, __builtin_amdgcn_raw_buffer_load_b128(ry, oy[i], sy, 0));
+    }
+  }
+  __device__ void store(char* tx, char* ty) const {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = lr + 16 * i;
+      *(i32x4*)(tx + toff(r, lc * 16)) = bx[i];
+      *(i32x4*)(ty + toff(r, lc * 16)) = by[i];
+    }
+  }
+};
+
+// A operand of a 32-row MFMA block read row-wise from a tile: rows r0 + (lane
+// & 31), contraction (d) chunk 2 ds + h.
+__device__ __forceinline__ bf16x8 row_frag(const char* tile, int r0, int col, int h, int ds) {
+  return *(const bf16x8*)(tile + toff(r0 + col, (2 * ds + h) * 16));
+}
+
+// A operand X^T[d rows 32 dt.., positions 16 u..] of a tile X [positions x d],
+// the positions permuted as the score registers are (see the forward kernel).
+__device__ __forceinline__ bf16x8 tr_frag(const char* tile, int u, int dt, int v_row, int v_colb) {
+  const int row = 16 * u + v_row, colb = 64 * dt + v_colb;
+  const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(tile + toff(row, colb)));
+  const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(tile + toff(row + 8, colb)));
+  return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+}
+
+__device__ __forceinline__ void zero(f32x16& a) {
+#pragma unroll
+  for (int v = 0; v < 16; ++v) a[v] = 0.0f;
+}
+
+// ---------------------------------------------------------------------------
+// dq pass
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(NT, 1)
+void attention_bwd_dq_kernel(AttnBwdParams p) {
+  __shared__ __attribute__((aligned(1024))) char smem[2 * 2 * TILE];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int h = lane >> 5, col = lane & 31;
+
+  const int nqb = p.S / 128;
+  const int nbh = p.B * p.H;
+  const int qb = nqb - 1 - (int)(blockIdx.x / nbh);   // heaviest query blocks first
+  const int bh = blockIdx.x % nbh;
+  const int b = bh / p.H, head = bh - b * p.H;
+  const int q0 = qb * 128;
+  const int64_t tok0 = (int64_t)b * p.S;
+  const int qi = q0 + 32 * w + col;
+  const int64_t tq = tok0 + qi;
+
+  // Q and dO of this lane's query (B operands), D = rowsum(dO * O)
+  bf16x8 qf[8], gf[8];
+  float dsum = 0.0f;
+  {
+    const uint16_t* qrow = p.Q + tq * p.ldq + head * DH + 8 * h;
+    const uint16_t* grow = p.dO + tq * p.ldg + head * DH + 8 * h;
+    const uint16_t* orow = p.O + tq * p.ldo + head * DH + 8 * h;
+#pragma unroll
+    for (int ds = 0; ds < 8; ++ds) {
+      qf[ds] = *(const bf16x8*)(qrow + 16 * ds);
+      gf[ds] = *(const bf16x8*)(grow + 16 * ds);
+      const bf16x8 of = *(const bf16x8*)(orow + 16 * ds);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) dsum += (float)gf[ds][e] * (float)of[e];
+    }
+  }
+  const float Dq = dsum + __shfl_xor(dsum, 32);
+  const float lse = p.lse[tq * p.H + head];
+  if (h == 0) p.Dstat[tq * p.H + head] = Dq;
+
+  TilePair kv;
+  kv.init(p.K + tok0 * p.ldk + head * DH, p.ldk, p.V + tok0 * p.ldv + head * DH, p.ldv, p.S, tid);
+
+  const int j16 = lane & 15, G = lane >> 4, hh = G >> 1;
+  const int v_row = 4 * hh + (j16 >> 2);
+  const int v_colb = 2 * (16 * (G & 1) + 4 * (j16 & 3));
+
+  f32x16 dq[4];
+#pragma unroll
+  for (int d = 0; d < 4; ++d) zero(dq[d]);
+
+  const int nkb = p.causal ? (q0 + 128) / TR : p.S / TR;
+  const int wave_last_q = q0 + 32 * w + 31;
+  const float c = p.scale_log2;
+  kv.load(0);
+  kv.store(smem, smem + TILE);
+  __syncthreads();
+  for (int kb = 0; kb < nkb; ++kb) {
+    const int cur = kb & 1;
+    if (kb + 1 < nkb) kv.load(kb + 1);
+    const int k0 = kb * TR;
+    if (!p.causal || k0 <= wave_last_q) {
+      const char* ks = smem + cur * 2 * TILE;
+      const char* vs = ks + TILE;
+      bf16x8 dsf[4];
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        f32x16 s, dp;
+        zero(s);
+        zero(dp);
+#pragma unroll
+        for (int ds = 0; ds < 8; ++ds) {
+          s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag(ks, 32 * t, col, h, ds), qf[ds], s, 0, 0, 0);
+          dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag(vs, 32 * t, col, h, ds), gf[ds], dp, 0, 0, 0);
+        }
+        const bool diag = p.causal && k0 + 32 * t + 31 > q0 + 32 * w;   // wave-uniform
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int key = k0 + 32 * t + 8 * (v >> 2) + 4 * h + (v & 3);
+          float pr = __builtin_amdgcn_exp2f(__builtin_fmaf(s[v], c, -lse));
+          if (diag && key > qi) pr = 0.0f;
+          dsf[2 * t + (v >> 3)][v & 7] = (__bf16)(pr * (dp[v] - Dq));
+        }
+      }
+      // dQ^T += K^T dS^T over the 64 keys, 4 steps of 16
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int d = 0; d < 4; ++d)
+          dq[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_frag(ks, u, d, v_row, v_colb), dsf[u], dq[d], 0, 0, 0);
+    }
+    if (kb + 1 < nkb) kv.store(smem + (cur ^ 1) * 2 * TILE, smem + (cur ^ 1) * 2 * TILE + TILE);
+    __syncthreads();
+  }
+
+  // dQ[query][d] = scale * dQ^T: lane holds rows d = 32 dt + 8 (v>>2) + 4 h + (v&3)
+  uint16_t* out = p.dQ + tq * p.lddq + head * DH;
+#pragma unroll
+  for (int d = 0; d < 4; ++d)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const bf16x4 o = {(__bf16)(dq[d][4 * g + 0] * p.scale), (__bf16)(dq[d][4 * g + 1] * p.scale),
+                        (__bf16)(dq[d][4 * g + 2] * p.scale), (__bf16)(dq[d][4 * g + 3] * p.scale)};
+      *(bf16x4*)(out + 32 * d + 8 * g + 4 * h) = o;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// dkv pass
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(NT, 1)
+void attention_bwd_dkv_kernel(AttnBwdParams p) {
+  __shared__ __attribute__((aligned(1024))) char smem[2 * 2 * TILE];
+  __shared__ float stat[2][2][TR];   // [stage][lse2, D][query]
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int h = lane >> 5, col = lane & 31;
+
+  const int nbh = p.B * p.H;
+  const int kblk = (int)(blockIdx.x / nbh);          // earliest key blocks (most queries) first
+  const int bh = blockIdx.x % nbh;
+  const int b = bh / p.H, head = bh - b * p.H;
+  const int k0 = kblk * 128;
+  const int64_t tok0 = (int64_t)b * p.S;
+  const int kj = k0 + 32 * w + col;                  // this lane's key
+  const int64_t tk = tok0 + kj;
+
+  bf16x8 kf[8], vf[8];
+  {
+    const uint16_t* krow = p.K + tk * p.ldk + head * DH + 8 * h;
+    const uint16_t* vrow = p.V + tk * p.ldv + head * DH + 8 * h;
+#pragma unroll
+    for (int ds = 0; ds < 8; ++ds) {
+      kf[ds] = *(const bf16x8*)(krow + 16 * ds);
+      vf[ds] = *(const bf16x8*)(vrow + 16 * ds);
+    }
+  }
+
+  TilePair qg;
+  qg.init(p.Q + tok0 * p.ldq + head * DH, p.ldq, p.dO + tok0 * p.ldg + head * DH, p.ldg, p.S, tid);
+  float st_l = 0.0f, st_d = 0.0f;
+  auto sload = [&](int blk) {
+    if (tid < TR) {
+      const int64_t t = tok0 + (int64_t)blk * TR + tid;
+      st_l = p.lse[t * p.H + head];
+      st_d = p.Dstat[t * p.H + head];
+    }
+  };
+  auto sstore = [&](int buf) {
+    if (tid < TR) {
+      stat[buf][0][tid] = st_l;
+      stat[buf][1][tid] = st_d;
+    }
+  };
+
+  const int j16 = lane & 15, G = lane >> 4, hh = G >> 1;
+  const int v_row = 4 * hh + (j16 >> 2);
+  const int v_colb = 2 * (16 * (G & 1) + 4 * (j16 & 3));
+
+  f32x16 dk[4], dv[4];
+#pragma unroll
+  for (int d = 0; d < 4; ++d) {
+    zero(dk[d]);
+    zero(dv[d]);
+  }
+
+  const int qb_begin = p.causal ? k0 / TR : 0;
+  const int nqb = p.S / TR;
+  const int wave_first_k = k0 + 32 * w;
+  const float c = p.scale_log2;
+  qg.load(qb_begin);
+  sload(qb_begin);
+  qg.store(smem, smem + TILE);
+  sstore(0);
+  __syncthreads();
+  for (int qb = qb_begin; qb < nqb; ++qb) {
+    const int cur = (qb - qb_begin) & 1;
+    if (qb + 1 < nqb) {
+      qg.load(qb + 1);
+      sload(qb + 1);
+    }
+    const int q0 = qb * TR;
+    if (!p.causal || q0 + TR - 1 >= wave_first_k) {
+      const char* qs = smem + cur * 2 * TILE;
+      const char* gs = qs + TILE;
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        if (p.causal && q0 + 32 * t + 31 < wave_first_k) continue;   // wave-uniform: sees none of these keys
+        f32x16 s, dp;
+        zero(s);
+        zero(dp);
+#pragma unroll
+        for (int ds = 0; ds < 8; ++ds) {
+          s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag(qs, 32 * t, col, h, ds), kf[ds], s, 0, 0, 0);
+          dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag(gs, 32 * t, col, h, ds), vf[ds], dp, 0, 0, 0);
+        }
+        // lane: key kj; element v: query q0 + 32 t + 8 (v>>2) + 4 h + (v&3)
+        const bool diag = p.causal && q0 + 32 * t < wave_first_k + 31;   // wave-uniform
+        bf16x8 pf[2], dsf[2];
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int ql = 32 * t + 8 * (v >> 2) + 4 * h + (v & 3);
+          float pr = __builtin_amdgcn_exp2f(__builtin_fmaf(s[v], c, -stat[cur][0][ql]));
+          if (diag && q0 + ql < kj) pr = 0.0f;
+          pf[v >> 3][v & 7] = (__bf16)pr;
+          dsf[v >> 3][v & 7] = (__bf16)(pr * (dp[v] - stat[cur][1][ql]));
+        }
+        // dV^T += dO^T P and dK^T += Q^T dS over these 32 queries (2 steps of 16)
+#pragma unroll
+        for (int uu = 0; uu < 2; ++uu) {
+          const int u = 2 * t + uu;
+#pragma unroll
+          for (int d = 0; d < 4; ++d) {
+            dv[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_frag(gs, u, d, v_row, v_colb), pf[uu], dv[d], 0, 0, 0);
+            dk[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_frag(qs, u, d, v_row, v_colb), dsf[uu], dk[d], 0, 0, 0);
+          }
+        }
+      }
+    }
+    if (qb + 1 < nqb) {
+      qg.store(smem + (cur ^ 1) * 2 * TILE, smem + (cur ^ 1) * 2 * TILE + TILE);
+      sstore(cur ^ 1);
+    }
+    __syncthreads();
+  }
+
+  uint16_t* okr = p.dK + tk * p.lddk + head * DH;
+  uint16_t* ovr = p.dV + tk * p.lddv + head * DH;
+#pragma unroll
+  for (int d = 0; d < 4; ++d)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const bf16x4 ko = {(__bf16)(dk[d][4 * g + 0] * p.scale), (__bf16)(dk[d][4 * g + 1] * p.scale),
+                         (__bf16)(dk[d][4 * g + 2] * p.scale), (__bf16)(dk[d][4 * g + 3] * p.scale)};
+      const bf16x4 vo = {(__bf16)dv[d][4 * g + 0], (__bf16)dv[d][4 * g + 1], (__bf16)dv[d][4 * g + 2],
+                         (__bf16)dv[d][4 * g + 3]};
+      *(bf16x4*)(okr + 32 * d + 8 * g + 4 * h) = ko;
+      *(bf16x4*)(ovr + 32 * d + 8 * g + 4 * h) = vo;
+    }
+}
+
+}  // namespace
+
+hipError_t launch_attention_backward(const AttnBwdParams& p, hipStream_t s) {
+  if (p.B == 0 || p.S == 0 || p.H == 0) return hipSuccess;
+  if (p.S % 128) return hipErrorInvalidValue;
+  const unsigned nwg = (unsigned)(p.S / 128) * p.B * p.H;
+  hipLaunchKernelGGL(attention_bwd_dq_kernel, dim3(nwg), dim3(NT), 0, s, p);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(attention_bwd_dkv_kernel, dim3(nwg), dim3(NT), 0, s, p);
+  return hipGetLastError();
+}
+
+}  // namespace partir

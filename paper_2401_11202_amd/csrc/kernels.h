@@ -119,11 +119,38 @@ struct AttnParams {
   float* Opart = nullptr;   // [nsplit][B*S][H*128] fp32, sum_j 2^(s_j c - m) v_j
   float* Mpart = nullptr;   // [nsplit][B*S][H] running max m (log2 domain, scaled)
   float* Lpart = nullptr;   // [nsplit][B*S][H] sum_j 2^(s_j c - m)
+  // optional: the per-row base-2 log-sum-exp m + log2(l), [B*S][H] fp32,
+  // kept for the backward pass (written by the unsplit kernel or the combine)
+  float* lse = nullptr;
 };
 hipError_t launch_attention(const AttnParams& p, hipStream_t s);
 // O = combine over the shards: M = max m_s, w_s = 2^(m_s - M),
 // O = (sum_s w_s o_s) / (sum_s w_s l_s), s ascending; bf16 into p.O
 hipError_t launch_attention_combine(const AttnParams& p, hipStream_t s);
+
+// Gradients of the attention core (d_head = 128, S a multiple of 128) for
+// the output cotangent dO, from the forward's O and its per-row base-2
+// log-sum-exp lse[token][head] = log2 sum_j 2^(scale log2(e) s_j).  dQ, dK,
+// dV bf16 in the layout of Q, K, V; Dstat [B*S][H] fp32 workspace (the
+// rowsums of dO * O, written by the first pass, read by the second).
+struct AttnBwdParams {
+  const uint16_t* Q;
+  const uint16_t* K;
+  const uint16_t* V;
+  const uint16_t* O;
+  const uint16_t* dO;
+  const float* lse;
+  float* Dstat;
+  uint16_t* dQ;
+  uint16_t* dK;
+  uint16_t* dV;
+  int64_t ldq, ldk, ldv, ldo, ldg, lddq, lddk, lddv;
+  int B, S, H;
+  int causal;
+  float scale;        // softmax scale
+  float scale_log2;   // scale * log2(e)
+};
+hipError_t launch_attention_backward(const AttnBwdParams& p, hipStream_t s);
 
 // y (bf16) = g * x / sqrt(mean(x^2) + eps), one row of D fp32 per wave.
 struct RmsParams {

@@ -61,7 +61,7 @@ bool valid_dtype(int dt) { return dt == PARTIR_F32 || dt == PARTIR_BF16; }
 // Plans
 // ---------------------------------------------------------------------------
 enum LaunchKind { L_GEMM_BF16, L_GEMM_F32, L_REDUCE, L_ATTN, L_ATTN_COMBINE, L_RMS, L_TRANSPOSE, L_ACT_BWD, L_COLSUM,
-                  L_GEMM_BF16_PARTS };
+                  L_GEMM_BF16_PARTS, L_ATTN_BWD };
 
 struct Launch {
   LaunchKind kind;
@@ -76,6 +76,7 @@ struct Launch {
   ActBwdParams act{};
   ColSumParams cs{};
   std::shared_ptr<GemmParts> parts;   // L_GEMM_BF16_PARTS: the device-local arrays
+  AttnBwdParams attn_bwd{};
 };
 
 struct Plan {
@@ -252,6 +253,7 @@ hipError_t run_one(const Launch& L, hipStream_t s) {
     case L_ACT_BWD: return launch_act_backward(L.act, s);
     case L_COLSUM: return launch_colsum(L.cs, s);
     case L_GEMM_BF16_PARTS: return launch_gemm_bf16_parts(L.gemm, *L.parts, s);
+    case L_ATTN_BWD: return launch_attention_backward(L.attn_bwd, s);
   }
   return hipErrorInvalidValue;
 }
@@ -684,6 +686,7 @@ struct AttnCoreArgs {
   int causal;
   float scale;
   int Rkv;
+  float* lse = nullptr;   // partir_attention_train: per-row base-2 log-sum-exp
 };
 
 int validate_attn_core(const AttnCoreArgs& a, bool with_ptrs) {
@@ -728,6 +731,7 @@ void plan_attn_core(const AttnCoreArgs& a, void* ws, Plan& plan) {
   p.Opart = base ? (float*)base : nullptr;
   p.Mpart = base ? (float*)(base + o_bytes) : nullptr;
   p.Lpart = base ? (float*)(base + o_bytes + ml_bytes) : nullptr;
+  p.lse = a.lse;
   char buf[256];
   snprintf(buf, sizeof buf, "attention: loop h [#tile<1>](%lld heads) x loop s [#sum softmax](%d key shards of %d) over "
            "%lld sequences, S=%lld, %s", (long long)a.H, a.Rkv, p.kb_per * 64, (long long)a.B, (long long)a.S,
@@ -741,6 +745,57 @@ void plan_attn_core(const AttnCoreArgs& a, void* ws, Plan& plan) {
     C.text = "attention_combine: O = sum_s 2^(m_s - M) o_s / sum_s 2^(m_s - M) l_s, s ascending";
     plan.launches.push_back(C);
   }
+}
+
+// ---------------------------------------------------------------------------
+// attention core backward
+// ---------------------------------------------------------------------------
+struct AttnBwdArgs {
+  const void *Q = nullptr, *K = nullptr, *V = nullptr, *O = nullptr, *dO = nullptr;
+  const float* lse = nullptr;
+  void *dQ = nullptr, *dK = nullptr, *dV = nullptr;
+  int64_t B = 0, S = 0, H = 0, dh = 0;
+  int causal = 1;
+  float scale = 0.f;
+};
+
+int validate_attn_bwd(const AttnBwdArgs& a, bool with_ptrs) {
+  int st = validate_attn_shapes(a.B, a.S, a.H * a.dh, a.H, a.dh, 1, 1);
+  if (st) return st;
+  if (!with_ptrs || a.B * a.S == 0) return PARTIR_OK;
+  if (!a.Q || !a.K || !a.V || !a.O || !a.dO || !a.lse || !a.dQ || !a.dK || !a.dV)
+    return fail(PARTIR_E_NULL, "Q, K, V, O, dO, lse, dQ, dK and dV must be non-NULL");
+  if (!aligned16(a.Q) || !aligned16(a.K) || !aligned16(a.V) || !aligned16(a.O) || !aligned16(a.dO) ||
+      !aligned16(a.dQ) || !aligned16(a.dK) || !aligned16(a.dV) || ((uintptr_t)a.lse & 3))
+    return fail(PARTIR_E_LAYOUT, "tensors must be 16-byte aligned (lse 4-byte)");
+  return PARTIR_OK;
+}
+
+void plan_attn_bwd(const AttnBwdArgs& a, void* ws, Plan& plan) {
+  const int64_t T = a.B * a.S, D = a.H * a.dh;
+  plan.n_shards = 1;
+  plan.n_tile_loops = 1;   // the heads loop
+  const double pairs = a.causal ? (double)a.S * (a.S + 1) / 2 : (double)a.S * a.S;
+  plan.flops = 2.5 * 4.0 * a.B * a.H * pairs * a.dh;   // dV, dP, dQ, dK and S: 5 products per pair
+  if (T == 0) return;
+  plan.ws_bytes = align_up((size_t)T * a.H * 4);
+  Launch L;
+  L.kind = L_ATTN_BWD;
+  L.name = "attn.bwd";
+  AttnBwdParams& p = L.attn_bwd;
+  p.Q = (const uint16_t*)a.Q; p.K = (const uint16_t*)a.K; p.V = (const uint16_t*)a.V;
+  p.O = (const uint16_t*)a.O; p.dO = (const uint16_t*)a.dO; p.lse = a.lse; p.Dstat = (float*)ws;
+  p.dQ = (uint16_t*)a.dQ; p.dK = (uint16_t*)a.dK; p.dV = (uint16_t*)a.dV;
+  p.ldq = p.ldk = p.ldv = p.ldo = p.ldg = p.lddq = p.lddk = p.lddv = D;
+  p.B = (int)a.B; p.S = (int)a.S; p.H = (int)a.H; p.causal = a.causal;
+  p.scale = a.scale > 0 ? a.scale : 1.0f / std::sqrt((float)a.dh);
+  p.scale_log2 = p.scale * 1.4426950408889634f;
+  char buf[256];
+  snprintf(buf, sizeof buf, "attention_backward: loop h [#tile<1>](%lld heads) over %lld sequences, S=%lld, %s; "
+           "dq pass (keys streamed) then dk/dv pass (queries streamed)", (long long)a.H, (long long)a.B,
+           (long long)a.S, a.causal ? "causal" : "full");
+  L.text = buf;
+  plan.launches.push_back(L);
 }
 
 // ---------------------------------------------------------------------------
@@ -1308,6 +1363,62 @@ int partir_attention(const void* Q, const void* K, const void* V, void* O, int64
   Plan plan;
   plan_attn_core(a, ws, plan);
   keep_plan_text(plan, "attention");
+  return execute(plan, stream);
+}
+
+int partir_attention_train(const void* Q, const void* K, const void* V, void* O, float* lse, int64_t B, int64_t S,
+                           int64_t n_heads, int64_t d_head, int causal, float scale, int R_kv, void* ws,
+                           size_t ws_bytes, void* stream) {
+  AttnCoreArgs a{Q, K, V, O, B, S, n_heads, d_head, causal ? 1 : 0, scale, R_kv, lse};
+  int st = validate_attn_core(a, true);
+  if (st) return st;
+  if (B * S > 0 && !lse) return fail(PARTIR_E_NULL, "lse must be non-NULL");
+  if ((uintptr_t)lse & 3) return fail(PARTIR_E_LAYOUT, "lse must be 4-byte aligned");
+  Plan probe;
+  plan_attn_core(a, nullptr, probe);
+  if ((st = check_ws(probe, ws, ws_bytes))) return st;
+  Plan plan;
+  plan_attn_core(a, ws, plan);
+  keep_plan_text(plan, "attention_train");
+  return execute(plan, stream);
+}
+
+size_t partir_attention_backward_workspace(int64_t B, int64_t S, int64_t n_heads, int64_t d_head) {
+  AttnBwdArgs a;
+  a.B = B; a.S = S; a.H = n_heads; a.dh = d_head;
+  if (validate_attn_bwd(a, false) != PARTIR_OK) return (size_t)-1;
+  Plan plan;
+  plan_attn_bwd(a, nullptr, plan);
+  return plan.ws_bytes;
+}
+
+int partir_plan_attention_backward(int64_t B, int64_t S, int64_t n_heads, int64_t d_head, int causal,
+                                   partir_plan_info* info) {
+  AttnBwdArgs a;
+  a.B = B; a.S = S; a.H = n_heads; a.dh = d_head; a.causal = causal ? 1 : 0;
+  int st = validate_attn_bwd(a, false);
+  if (st) return st;
+  Plan plan;
+  plan_attn_bwd(a, nullptr, plan);
+  keep_plan_text(plan, "attention_backward");
+  fill_info(plan, info);
+  return PARTIR_OK;
+}
+
+int partir_attention_backward(const void* Q, const void* K, const void* V, const void* O, const void* dO,
+                              const float* lse, void* dQ, void* dK, void* dV, int64_t B, int64_t S, int64_t n_heads,
+                              int64_t d_head, int causal, float scale, void* ws, size_t ws_bytes, void* stream) {
+  AttnBwdArgs a;
+  a.Q = Q; a.K = K; a.V = V; a.O = O; a.dO = dO; a.lse = lse; a.dQ = dQ; a.dK = dK; a.dV = dV;
+  a.B = B; a.S = S; a.H = n_heads; a.dh = d_head; a.causal = causal ? 1 : 0; a.scale = scale;
+  int st = validate_attn_bwd(a, true);
+  if (st) return st;
+  Plan probe;
+  plan_attn_bwd(a, nullptr, probe);
+  if ((st = check_ws(probe, ws, ws_bytes))) return st;
+  Plan plan;
+  plan_attn_bwd(a, ws, plan);
+  keep_plan_text(plan, "attention_backward");
   return execute(plan, stream);
 }
 

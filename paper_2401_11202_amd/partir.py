@@ -34,7 +34,8 @@ EXPORTS = ("partir_loop_matmul", "partir_loop_matmul_workspace", "partir_mlp_blo
            "partir_attention", "partir_attention_workspace", "partir_plan_attention",
            "partir_mlp_block_backward", "partir_mlp_block_backward_workspace", "partir_plan_mlp_block_backward",
            "partir_mlp_block_train", "partir_mlp_block_sharded", "partir_mlp_block_sharded_workspace",
-           "partir_plan_mlp_block_sharded")
+           "partir_plan_mlp_block_sharded", "partir_attention_train", "partir_attention_backward",
+           "partir_attention_backward_workspace", "partir_plan_attention_backward")
 
 
 class PartirError(RuntimeError):
@@ -100,6 +101,10 @@ def lib():
         "partir_mlp_block_sharded": (I32, [PP, PP, P, PP, P, PP, I64, I64, I64, I32, I32, I32, I32, P, SZ, P]),
         "partir_mlp_block_sharded_workspace": (SZ, [I64, I64, I64, I32, I32]),
         "partir_plan_mlp_block_sharded": (I32, [I64, I64, I64, I32, I32, I32, ctypes.POINTER(PlanInfo)]),
+        "partir_attention_train": (I32, [P, P, P, P, P, I64, I64, I64, I64, I32, F, I32, P, SZ, P]),
+        "partir_attention_backward": (I32, [P, P, P, P, P, P, P, P, P, I64, I64, I64, I64, I32, F, P, SZ, P]),
+        "partir_attention_backward_workspace": (SZ, [I64, I64, I64, I64]),
+        "partir_plan_attention_backward": (I32, [I64, I64, I64, I64, I32, ctypes.POINTER(PlanInfo)]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(L, name)
@@ -346,6 +351,39 @@ def attention(Q, K, V, *, B: int, S: int, n_heads: int, d_head: int = 128, causa
     _check(lib().partir_attention(_ptr(Q), _ptr(K), _ptr(V), _ptr(out), B, S, n_heads, d_head, int(causal),
                                   float(scale), R_kv, _ptr(ws), wsb, _stream(stream)))
     return out
+
+
+def attention_train(Q, K, V, *, B: int, S: int, n_heads: int, d_head: int = 128, causal: bool = True,
+                    scale: float = 0.0, R_kv: int = 1, out=None, lse=None, workspace=None, stream=None):
+    """attention that also returns the per-row base-2 log-sum-exp [B*S, n_heads]
+    fp32 for attention_backward.  Returns (O, lse)."""
+    import torch
+    if out is None:
+        out = torch.empty_like(Q)
+    if lse is None:
+        lse = torch.empty((B * S, n_heads), dtype=torch.float32, device=Q.device)
+    ws, wsb = _workspace(lib().partir_attention_workspace(B, S, n_heads, d_head, R_kv), Q.device, workspace)
+    _check(lib().partir_attention_train(_ptr(Q), _ptr(K), _ptr(V), _ptr(out), _ptr(lse), B, S, n_heads, d_head,
+                                        int(causal), scale, R_kv, _ptr(ws), wsb, _stream(stream)))
+    return out, lse
+
+
+def attention_backward(Q, K, V, O, dO, lse, *, B: int, S: int, n_heads: int, d_head: int = 128,
+                       causal: bool = True, scale: float = 0.0, out=None, workspace=None, stream=None):
+    """Gradients (dQ, dK, dV) of attention for the output cotangent dO (bf16,
+    the layout of Q, K, V), from the forward's O and lse."""
+    import torch
+    if out is None:
+        out = (torch.empty_like(Q), torch.empty_like(K), torch.empty_like(V))
+    ws, wsb = _workspace(lib().partir_attention_backward_workspace(B, S, n_heads, d_head), Q.device, workspace)
+    _check(lib().partir_attention_backward(_ptr(Q), _ptr(K), _ptr(V), _ptr(O), _ptr(dO), _ptr(lse), _ptr(out[0]),
+                                           _ptr(out[1]), _ptr(out[2]), B, S, n_heads, d_head, int(causal), scale,
+                                           _ptr(ws), wsb, _stream(stream)))
+    return out
+
+
+def plan_attention_backward(B, S, n_heads, d_head=128, causal=True):
+    return _plan(lib().partir_plan_attention_backward, B, S, n_heads, d_head, int(causal))
 
 
 def plan_attention(B, S, n_heads, d_head=128, causal=True, R_kv=1):

@@ -413,3 +413,43 @@ def test_sharded_plan():
     assert s["n_sum_splitk"] == 0 and s["n_launches"] == 2
     e = P.plan_mlp_block_sharded(1024, 256, 0, R_batch=2, R_model=4)
     assert e["n_launches"] == 8 and e["workspace_bytes"] == 0        # b2 into each device's part
+
+
+# ---------------------------------------------------------------------------
+# attention core backward
+# ---------------------------------------------------------------------------
+def attn_bwd(B=2, S=2048, H=8, dh=128, ptr=DUMMY, lse=DUMMY, ws_bytes=1 << 30):
+    return P.lib().partir_attention_backward(ptr, DUMMY, DUMMY, DUMMY, DUMMY, lse, DUMMY, DUMMY, DUMMY,
+                                             B, S, H, dh, 1, 0.0, DUMMY, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kwargs,status", [
+    (dict(ptr=NULL), "PARTIR_E_NULL"),
+    (dict(lse=NULL), "PARTIR_E_NULL"),
+    (dict(ptr=DUMMY_ODD), "PARTIR_E_LAYOUT"),
+    (dict(lse=ctypes.c_void_p(0x10002)), "PARTIR_E_LAYOUT"),
+    (dict(S=200), "PARTIR_E_SHAPE"),
+    (dict(dh=64), "PARTIR_E_SHAPE"),
+    (dict(ws_bytes=0), "PARTIR_E_WORKSPACE"),
+    (dict(), "PARTIR_E_HIP"),
+    (dict(B=0, ptr=NULL, lse=NULL, ws_bytes=0), "PARTIR_E_HIP"),   # no tokens: valid, nothing launched
+])
+def test_attention_backward_validation(kwargs, status):
+    assert P.STATUS[attn_bwd(**kwargs)] == status, P.lib().partir_last_error().decode()
+
+
+def test_attention_backward_plan():
+    p = P.plan_attention_backward(4, 2048, 32, 128, True)
+    assert p["n_launches"] == 1 and p["workspace_bytes"] == 4 * 2048 * 32 * 4
+    assert p["flops"] == 2.5 * 4.0 * 4 * 32 * (2048 * 2049 / 2) * 128
+    assert "dq pass" in p["text"]
+    assert P.lib().partir_attention_backward_workspace(4, 2048, 32, 128) == p["workspace_bytes"]
+
+
+def test_attention_train_validation(monkeypatch):
+    monkeypatch.setenv("PARTIR_FAIL_LAUNCH", "1")
+    L = P.lib()
+    st = L.partir_attention_train(DUMMY, DUMMY, DUMMY, DUMMY, None, 2, 2048, 8, 128, 1, 0.0, 1, DUMMY, 0, None)
+    assert P.STATUS[st] == "PARTIR_E_NULL"
+    st = L.partir_attention_train(DUMMY, DUMMY, DUMMY, DUMMY, DUMMY, 2, 2048, 8, 128, 1, 0.0, 1, DUMMY, 0, None)
+    assert P.STATUS[st] == "PARTIR_E_HIP"

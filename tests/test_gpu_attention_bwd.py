@@ -1,0 +1,104 @@
+"""GPU parity of partir_attention_backward (and the lse of
+partir_attention_train) against the oracle's attention_backward.
+
+Every gradient element is compared on small shapes (causal and full), and at
+the attention-block size (4 x 2048 tokens, 32 heads) on seeded heads that the
+oracle evaluates whole.  Errors are normalised by the oracle's first-order
+bounds (each gradient's last product with |operands|).
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import partir_oracle as O
+from paper_2401_11202_amd import inputs as I
+from paper_2401_11202_amd import partir as P
+from tests.gpu_common import TOL_BF16, host, say
+
+pytestmark = pytest.mark.gpu
+DH = 128
+
+
+def make(seed, B, S, H):
+    D = H * DH
+    return [I.gaussian(seed, i, (B * S, D), 1.0, "bf16") for i in range(4)]   # Q, K, V, dO
+
+
+def run(Q, K, V, G, B, S, H, causal, R_kv=1):
+    q, k, v, g = (t.to_device() for t in (Q, K, V, G))
+    o, lse = P.attention_train(q, k, v, B=B, S=S, n_heads=H, causal=causal, R_kv=R_kv)
+    dq, dk, dv = P.attention_backward(q, k, v, o, g, lse, B=B, S=S, n_heads=H, causal=causal)
+    torch.cuda.synchronize()
+    return host(dq), host(dk), host(dv), lse.double().cpu().numpy()
+
+
+def check_head(got, Q, K, V, G, b, h, S, causal):
+    rows = slice(b * S, (b + 1) * S)
+    cols = slice(h * DH, (h + 1) * DH)
+    ref, nrm = O.attention_backward(Q.f64()[rows, cols], K.f64()[rows, cols], V.f64()[rows, cols],
+                                    G.f64()[rows, cols], DH ** -0.5, causal, return_norm=True)
+    errs = [O.normalised_error(g[rows, cols], r, n) for g, r, n in zip(got[:3], ref, nrm)]
+    # lse: log2 of the softmax denominator of the scaled scores
+    s = Q.f64()[rows, cols] @ K.f64()[rows, cols].T * DH ** -0.5
+    if causal:
+        s = np.where(np.tril(np.ones((S, S), bool)), s, -np.inf)
+    mx = s.max(axis=1)
+    lse = (mx + np.log(np.exp(s - mx[:, None]).sum(axis=1))) * math.log2(math.e)
+    lse_err = float(np.max(np.abs(got[3][rows, h] - lse)))
+    return errs, lse_err
+
+
+@pytest.mark.parametrize("causal", [True, False])
+def test_attention_backward_small_every_element(causal):
+    B, S, H = 2, 256, 2
+    Q, K, V, G = make(130, B, S, H)
+    say(f"attention backward B={B} S={S} H={H} causal={causal}")
+    got = run(Q, K, V, G, B, S, H, causal)
+    for b in range(B):
+        for h in range(H):
+            errs, lse_err = check_head(got, Q, K, V, G, b, h, S, causal)
+            say(f"    (b={b}, h={h}) dQ {errs[0]:.2e} dK {errs[1]:.2e} dV {errs[2]:.2e} lse {lse_err:.2e}")
+            assert max(errs) <= TOL_BF16
+            assert lse_err <= 1e-4
+
+
+def test_attention_backward_from_split_forward_and_deterministic():
+    """The lse of the split-key forward (R_kv = 4, written by the combine)
+    drives the same gradients; two runs agree bit for bit."""
+    B, S, H = 1, 1024, 2
+    Q, K, V, G = make(131, B, S, H)
+    one = run(Q, K, V, G, B, S, H, True, R_kv=1)
+    four = run(Q, K, V, G, B, S, H, True, R_kv=4)
+    again = run(Q, K, V, G, B, S, H, True, R_kv=4)
+    for a, c in zip(four, again):
+        assert np.array_equal(a, c)
+    assert np.max(np.abs(one[3] - four[3])) < 1e-4
+    for h in range(H):
+        errs, _ = check_head(four, Q, K, V, G, 0, h, S, True)
+        assert max(errs) <= TOL_BF16
+
+
+def test_attention_backward_block_size_sampled_heads():
+    B, S, H = 4, 2048, 32
+    Q, K, V, G = make(132, B, S, H)
+    say(f"attention backward B={B} S={S} H={H} causal")
+    got = run(Q, K, V, G, B, S, H, True)
+    rng = np.random.default_rng(132)
+    heads = [(0, 0), (B - 1, H - 1)] + [(int(rng.integers(B)), int(rng.integers(H))) for _ in range(1)]
+    for b, h in heads:
+        errs, lse_err = check_head(got, Q, K, V, G, b, h, S, True)
+        say(f"    (b={b}, h={h}) dQ {errs[0]:.2e} dK {errs[1]:.2e} dV {errs[2]:.2e} lse {lse_err:.2e}")
+        assert max(errs) <= TOL_BF16 and lse_err <= 1e-4
+
+
+def test_attention_backward_validation():
+    Q = torch.zeros((256, 256), dtype=torch.bfloat16, device="cuda")
+    lse = torch.zeros((256, 2), dtype=torch.float32, device="cuda")
+    with pytest.raises(P.PartirError) as e:
+        P.attention_backward(Q, Q, Q, Q, Q, lse, B=1, S=200, n_heads=2)
+    assert e.value.status == P.ERR["PARTIR_E_SHAPE"]
+    # no tokens: nothing to do
+    E = torch.empty((0, 256), dtype=torch.bfloat16, device="cuda")
+    P.attention_backward(E, E, E, E, E, torch.empty((0, 2), device="cuda"), B=0, S=256, n_heads=2)
