@@ -586,6 +586,79 @@ def attn_ref(X, Wq, Wk, Wv, Wo, B, S, n_heads, d_head, causal=True, scale=None):
     return matmul(A, Wo)
 
 
+def attn_block_backward(X, Wq, Wk, Wv, Wo, dY, B, S, n_heads, d_head, causal=True, scale=None,
+                        R_batch=1, R_model=1, return_norm=False):
+    """Gradients of attn_block for the output cotangent dY, as loop nests over
+    the forward's batch (b) and model (m, heads) shards:
+
+      q|k|v[b, m] = slice 0 X[b] @ slice 1 W{q,k,v}[m];  a[b, m] = heads' attention
+      dA[b, m]    = slice 0 dY[b] @ (slice 0 Wo[m])^T          (#tile<0> b, #tile<1> m)
+      dq|dk|dv[b, m] = per (sequence, head) attention_backward(q, k, v, dA)
+      dX  = loop b [#tile<0>] { loop m [#sum] { dq Wq[m]^T + dk Wk[m]^T + dv Wv[m]^T } }
+      dWq = loop m [#tile<1>] { loop b [#sum] { (slice 0 X[b])^T dq[b, m] } }  (k, v alike)
+      dWo = loop m [#tile<0>] { loop b [#sum] { a[b, m]^T slice 0 dY[b] } }
+
+    Weights in their logical [fan_in, fan_out] orientation.  Returns a dict
+    dX, dWq, dWk, dWv, dWo; with return_norm also a dict of normalisers that
+    propagate magnitudes through the same nests (attention_backward's bounds
+    with dA replaced by |dY| |Wo|^T, the attention output by p |v|).
+    """
+    if scale is None:
+        scale = 1.0 / math.sqrt(d_head)
+    T, D = X.shape
+    if T != B * S or n_heads * d_head != Wq.shape[1]:
+        raise ValueError("shape mismatch")
+    if B % R_batch or n_heads % R_model:
+        raise ValueError("indivisible partition")
+    X, Wq, Wk, Wv, Wo, dY = (np.asarray(a, np.float64) for a in (X, Wq, Wk, Wv, Wo, dY))
+    nseq, hps = B // R_batch, n_heads // R_model
+    sh = {}
+    for b in range(R_batch):
+        xb, dyb = slice_(X, 0, b, R_batch), slice_(dY, 0, b, R_batch)
+        for m in range(R_model):
+            w = [slice_(W, 1, m, R_model) for W in (Wq, Wk, Wv)]
+            wo = slice_(Wo, 0, m, R_model)
+            q, k, v = (matmul(xb, wi) for wi in w)
+            da = matmul(dyb, wo.T)
+            nda = abs_product(dyb, wo.T)
+            grads = [np.zeros_like(q) for _ in range(3)]
+            norms = [np.zeros_like(q) for _ in range(3)]
+            a, na = np.zeros_like(q), np.zeros_like(q)
+            for sq in range(nseq):
+                rs = slice(sq * S, (sq + 1) * S)
+                for hh in range(hps):
+                    cs = slice(hh * d_head, (hh + 1) * d_head)
+                    a[rs, cs] = causal_attention(q[rs, cs], k[rs, cs], v[rs, cs], scale, causal)
+                    na[rs, cs] = causal_attention(q[rs, cs], k[rs, cs], np.abs(v[rs, cs]), scale, causal)
+                    g = attention_backward(q[rs, cs], k[rs, cs], v[rs, cs], da[rs, cs], scale, causal)
+                    _, n = attention_backward(q[rs, cs], k[rs, cs], v[rs, cs], nda[rs, cs], scale, causal,
+                                              return_norm=True)
+                    for i in range(3):
+                        grads[i][rs, cs] = g[i]
+                        norms[i][rs, cs] = n[i]
+            sh[b, m] = dict(x=xb, dy=dyb, w=w, a=a, na=na, g=grads, n=norms)
+    out = {
+        "dX": loop_tile(R_batch, 0, lambda b: loop_sum(R_model, lambda m: sum(
+            matmul(sh[b, m]["g"][i], sh[b, m]["w"][i].T) for i in range(3)))),
+        "dWo": loop_tile(R_model, 0, lambda m: loop_sum(R_batch, lambda b: matmul(sh[b, m]["a"].T, sh[b, m]["dy"]))),
+    }
+    for i, key in enumerate(("dWq", "dWk", "dWv")):
+        out[key] = loop_tile(R_model, 1, lambda m, i=i: loop_sum(
+            R_batch, lambda b: matmul(sh[b, m]["x"].T, sh[b, m]["g"][i])))
+    if not return_norm:
+        return out
+    nrm = {
+        "dX": loop_tile(R_batch, 0, lambda b: loop_sum(R_model, lambda m: sum(
+            abs_product(sh[b, m]["n"][i], sh[b, m]["w"][i].T) for i in range(3)))),
+        "dWo": loop_tile(R_model, 0, lambda m: loop_sum(R_batch, lambda b: matmul(sh[b, m]["na"].T,
+                                                                                 np.abs(sh[b, m]["dy"])))),
+    }
+    for i, key in enumerate(("dWq", "dWk", "dWv")):
+        nrm[key] = loop_tile(R_model, 1, lambda m, i=i: loop_sum(
+            R_batch, lambda b: abs_product(sh[b, m]["x"].T, sh[b, m]["n"][i])))
+    return out, nrm
+
+
 # ---------------------------------------------------------------------------
 # Pre-norm decoder layer / stack (residual stream kept unrounded)
 # ---------------------------------------------------------------------------

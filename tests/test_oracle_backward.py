@@ -259,3 +259,75 @@ def test_attention_backward_norms_bound():
     (dq, dk, dv), (nq, nk, nv) = O.attention_backward(q, k, v, do, 0.35, True, return_norm=True)
     for g, n in ((dq, nq), (dk, nk), (dv, nv)):
         assert np.all(np.abs(g) <= n * (1 + 1e-12))
+
+
+# ---------------------------------------------------------------------------
+# attention block gradients
+# ---------------------------------------------------------------------------
+def attn_block_problem(seed, B=2, S=4, H=2, dh=2):
+    rng = np.random.default_rng(seed)
+    D = H * dh
+    X = rng.standard_normal((B * S, D))
+    Ws = [rng.standard_normal((D, D)) / math.sqrt(D) for _ in range(4)]
+    dY = rng.standard_normal((B * S, D))
+    return X, Ws, dY
+
+
+def torch_attn_block_grads(X, Ws, dY, B, S, H, dh, causal):
+    ts = [torch.from_numpy(a.copy()).requires_grad_(True) for a in [X] + Ws]
+    Xt, Wq, Wk, Wv, Wo = ts
+    Q, K, V = Xt @ Wq, Xt @ Wk, Xt @ Wv
+    A = torch.zeros_like(Q)
+    outs = []
+    for s in range(B):
+        row = []
+        for h in range(H):
+            rs, cs = slice(s * S, (s + 1) * S), slice(h * dh, (h + 1) * dh)
+            sc = Q[rs, cs] @ K[rs, cs].T / math.sqrt(dh)
+            if causal:
+                sc = sc.masked_fill(torch.triu(torch.ones(S, S, dtype=torch.bool), 1), float("-inf"))
+            row.append(torch.softmax(sc, dim=1) @ V[rs, cs])
+        outs.append(torch.cat(row, dim=1))
+    A = torch.cat(outs, dim=0)
+    (A @ Wo).backward(torch.from_numpy(dY))
+    return {k: t.grad.numpy() for k, t in zip(("dX", "dWq", "dWk", "dWv", "dWo"), ts)}
+
+
+@pytest.mark.parametrize("Rb,Rm", [(1, 1), (2, 2), (1, 2), (2, 1)])
+@pytest.mark.parametrize("causal", [True, False])
+def test_attn_block_backward_matches_torch_autograd(Rb, Rm, causal):
+    B, S, H, dh = 2, 4, 2, 2
+    X, Ws, dY = attn_block_problem(30 + Rb * 4 + Rm, B, S, H, dh)
+    want = torch_attn_block_grads(X, Ws, dY, B, S, H, dh, causal)
+    got = O.attn_block_backward(X, *Ws, dY, B, S, H, dh, causal, None, Rb, Rm)
+    for k in want:
+        assert got[k].shape == want[k].shape
+        assert np.max(np.abs(got[k] - want[k])) < 1e-12, k
+
+
+def test_attn_block_backward_central_differences():
+    B, S, H, dh = 2, 3, 2, 2
+    X, Ws, dY = attn_block_problem(31, B, S, H, dh)
+    g = O.attn_block_backward(X, *Ws, dY, B, S, H, dh, True, None, 2, 2)
+    args = [X] + Ws
+    names = ("dX", "dWq", "dWk", "dWv", "dWo")
+    loss = lambda a: float(np.sum(O.attn_block(a[0], a[1], a[2], a[3], a[4], B, S, H, dh, True, None, 2, 2) * dY))
+    rng = np.random.default_rng(0)
+    for which, key in enumerate(names):
+        for _ in range(4):
+            idx = tuple(int(rng.integers(n)) for n in args[which].shape)
+            up = [a.copy() for a in args]
+            dn = [a.copy() for a in args]
+            up[which][idx] += 1e-6
+            dn[which][idx] -= 1e-6
+            fd = (loss(up) - loss(dn)) / 2e-6
+            assert abs(g[key][idx] - fd) < 1e-7 * max(1.0, abs(fd)), (key, idx)
+
+
+def test_attn_block_backward_norms_bound():
+    B, S, H, dh = 2, 8, 4, 4
+    X, Ws, dY = attn_block_problem(32, B, S, H, dh)
+    g, n = O.attn_block_backward(X, *Ws, dY, B, S, H, dh, True, None, 2, 2, return_norm=True)
+    for k in g:
+        assert n[k].shape == g[k].shape
+        assert np.all(np.abs(g[k]) <= n[k] * (1 + 1e-12)), k
