@@ -659,6 +659,79 @@ def attn_block_backward(X, Wq, Wk, Wv, Wo, dY, B, S, n_heads, d_head, causal=Tru
     return out, nrm
 
 
+def attn_block_backward_sampled(X, Wq, Wk, Wv, Wo, dY, B, S, n_heads, d_head, causal=True, scale=None,
+                                R_batch=1, R_model=1, seq=0, rows=(), head=0):
+    """The nests of attn_block_backward evaluated only where asked, each entry
+    through the shards that own it: dX at positions ``rows`` of sequence
+    ``seq`` (its batch shard; #sum over every model shard and head), and the
+    weight gradients of one ``head`` (its model shard; #sum over every batch
+    shard): dWq|dWk|dWv[:, head columns] and dWo[head rows, :].  Returns
+    (values, normalisers) as dicts with dX [len(rows), D], dWq/dWk/dWv
+    [D, d_head], dWo [d_head, D]."""
+    if scale is None:
+        scale = 1.0 / math.sqrt(d_head)
+    T, D = X.shape
+    if B % R_batch or n_heads % R_model:
+        raise ValueError("indivisible partition")
+    X, Wq, Wk, Wv, Wo, dY = (np.asarray(a, np.float64) for a in (X, Wq, Wk, Wv, Wo, dY))
+    Tb, hps, nseq = T // R_batch, n_heads // R_model, B // R_batch
+    rows = np.asarray(rows, int)
+
+    def head_grads(xs, dys, m, hh):
+        """One (sequence, head) of model shard m: attention inputs and gradients."""
+        cs = slice(hh * d_head, (hh + 1) * d_head)
+        w = [slice_(W, 1, m, R_model)[:, cs] for W in (Wq, Wk, Wv)]
+        wo = slice_(Wo, 0, m, R_model)[cs]
+        q, k, v = (matmul(xs, wi) for wi in w)
+        da, nda = matmul(dys, wo.T), abs_product(dys, wo.T)
+        g = attention_backward(q, k, v, da, scale, causal)
+        _, n = attention_backward(q, k, v, nda, scale, causal, return_norm=True)
+        a = causal_attention(q, k, v, scale, causal)
+        na = causal_attention(q, k, np.abs(v), scale, causal)
+        return w, g, n, a, na
+
+    # dX rows: batch shard of the sequence, #sum over model shards and their heads
+    b = seq // nseq
+    xb, dyb = slice_(X, 0, b, R_batch), slice_(dY, 0, b, R_batch)
+    sl = slice((seq - b * nseq) * S, (seq - b * nseq + 1) * S)
+    xs, dys = xb[sl], dyb[sl]
+
+    def dx_shard(m):
+        val, nv = np.zeros((len(rows), D)), np.zeros((len(rows), D))
+        for hh in range(hps):
+            w, g, n, _, _ = head_grads(xs, dys, m, hh)
+            for i in range(3):
+                val += matmul(g[i][rows], w[i].T)
+                nv += abs_product(n[i][rows], w[i].T)
+        return val, nv
+
+    parts = [dx_shard(m) for m in range(R_model)]
+    out = {"dX": loop_sum(R_model, lambda m: parts[m][0])}
+    nrm = {"dX": loop_sum(R_model, lambda m: parts[m][1])}
+    # weight gradients of one head: its model shard, #sum over batch shards
+    m, hh = head // hps, head % hps
+
+    def w_shard(bb):
+        xbb, dybb = slice_(X, 0, bb, R_batch), slice_(dY, 0, bb, R_batch)
+        acc = [np.zeros((D, d_head)) for _ in range(3)] + [np.zeros((d_head, D))]
+        nac = [np.zeros((D, d_head)) for _ in range(3)] + [np.zeros((d_head, D))]
+        for sq in range(nseq):
+            rs = slice(sq * S, (sq + 1) * S)
+            _, g, n, a, na = head_grads(xbb[rs], dybb[rs], m, hh)
+            for i in range(3):
+                acc[i] += matmul(xbb[rs].T, g[i])
+                nac[i] += abs_product(xbb[rs].T, n[i])
+            acc[3] += matmul(a.T, dybb[rs])
+            nac[3] += matmul(na.T, np.abs(dybb[rs]))
+        return acc, nac
+
+    wp = [w_shard(bb) for bb in range(R_batch)]
+    for i, key in enumerate(("dWq", "dWk", "dWv", "dWo")):
+        out[key] = loop_sum(R_batch, lambda bb: wp[bb][0][i])
+        nrm[key] = loop_sum(R_batch, lambda bb: wp[bb][1][i])
+    return out, nrm
+
+
 # ---------------------------------------------------------------------------
 # Pre-norm decoder layer / stack (residual stream kept unrounded)
 # ---------------------------------------------------------------------------

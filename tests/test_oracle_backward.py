@@ -331,3 +331,19 @@ def test_attn_block_backward_norms_bound():
     for k in g:
         assert n[k].shape == g[k].shape
         assert np.all(np.abs(g[k]) <= n[k] * (1 + 1e-12)), k
+
+
+def test_attn_block_backward_sampled_matches_full():
+    B, S, H, dh = 4, 8, 4, 2
+    X, Ws, dY = attn_block_problem(33, B, S, H, dh)
+    g, n = O.attn_block_backward(X, *Ws, dY, B, S, H, dh, True, None, 2, 2, return_norm=True)
+    seq, rows, head = 3, [0, 5, 7], 2
+    sg, sn = O.attn_block_backward_sampled(X, *Ws, dY, B, S, H, dh, True, None, 2, 2, seq, rows, head)
+    cs = slice(head * dh, (head + 1) * dh)
+    pick = {"dX": (g["dX"][seq * S + np.array(rows)], n["dX"][seq * S + np.array(rows)]),
+            "dWq": (g["dWq"][:, cs], n["dWq"][:, cs]), "dWk": (g["dWk"][:, cs], n["dWk"][:, cs]),
+            "dWv": (g["dWv"][:, cs], n["dWv"][:, cs]), "dWo": (g["dWo"][cs], n["dWo"][cs])}
+    for k, (val, nv) in pick.items():
+        assert sg[k].shape == val.shape, k
+        assert np.max(np.abs(sg[k] - val) / nv) < 1e-12, k
+        assert np.max(np.abs(sn[k] - nv) / nv) < 1e-12, k
