@@ -77,6 +77,29 @@ def setup(w, P, I):
         step = lambda: P.mlp_block(X, W1t, W2t, R_batch=w["R_batch"], R_model=w["R_model"], out=Y, workspace=ws)
         roles = {"mlp.up": 2.0 * T * D * F, "mlp.down": 2.0 * T * D * F}
         return x, step, roles, "mfma_bf16"
+    if w.kind == "attn_train":
+        B, S, D, H, dh, Rb, Rm = w["B"], w["S"], w["D"], w["H"], w["dh"], w["R_batch"], w["R_model"]
+        T = B * S
+        X, dY = x["X"].to_device(), x["dY"].to_device()
+        Ws = [dev_t(x[k]) for k in ("Wq", "Wk", "Wv", "Wo")]
+        Y = torch.empty((T, D), dtype=torch.float32, device="cuda")
+        saved = torch.empty(P.lib().partir_attn_block_saved_bytes(B, S, D, H), dtype=torch.uint8, device="cuda")
+        wsf = torch.empty(P.attn_block_workspace(B, S, D, H, dh, Rb, Rm), dtype=torch.uint8, device="cuda")
+        wsb = torch.empty(P.lib().partir_attn_block_backward_workspace(B, S, D, H, dh, Rb, Rm), dtype=torch.uint8,
+                          device="cuda")
+        f32 = dict(dtype=torch.float32, device="cuda")
+        grads = (torch.empty((T, D), **f32),) + tuple(torch.empty((D, D), **f32) for _ in range(4))
+
+        def step():
+            P.attn_block_train(X, *Ws, B=B, S=S, n_heads=H, d_head=dh, R_batch=Rb, R_model=Rm, out=Y, saved=saved,
+                               workspace=wsf)
+            P.attn_block_backward(X, *Ws, saved, dY, B=B, S=S, n_heads=H, d_head=dh, R_batch=Rb, R_model=Rm,
+                                  out=grads, workspace=wsb)
+        core = W.attn_core_flops(B, S, H, dh)
+        roles = {"attn.qkv": 6.0 * T * D * D, "attn.out": 2.0 * T * D * D, "attn.core": core,
+                 "attn.bwd.da": 2.0 * T * D * D, "attn.bwd": 2.5 * core, "attn.bwd.dx": 6.0 * T * D * D,
+                 "attn.bwd.dwqkv": 6.0 * T * D * D, "attn.bwd.dwo": 2.0 * T * D * D}
+        return x, step, roles, "mfma_bf16"
     if w.kind == "mlp_z3":
         T, D, F, Rb, Rm = w["T"], w["D"], w["F"], w["R_batch"], w["R_model"]
         xs, w1s, w2s = P.z3_device_arrays(x["X"].to_device(), dev_t(x["W1"]), dev_t(x["W2"]), Rb, Rm)
@@ -164,6 +187,7 @@ def setup(w, P, I):
 def cpu_baseline(w, x, target_s):
     import numpy as np
     from oracle import partir_oracle as O
+    from paper_2401_11202_amd import workloads as W
     try:
         from threadpoolctl import threadpool_info
         cores = max(i.get("num_threads", 1) for i in threadpool_info()) or 1
@@ -232,6 +256,22 @@ def cpu_baseline(w, x, target_s):
         return dict(value=flops / dt / 1e12, unit="TFLOP/s", cores=cores, kind="oracle",
                     sample=f"{nq} output rows at the end of one {S}-token sequence (K/V of the whole "
                            f"sequence), {dt:.1f} s")
+    if w.kind == "attn_train":
+        B, S, D, H, dh = w["B"], w["S"], w["D"], w["H"], w["dh"]
+        args = [x[k].f64() for k in ("X", "Wq", "Wk", "Wv", "Wo", "dY")]
+        rows = list(range(S - 8, S))
+        t0 = time.perf_counter()
+        O.attn_block_backward_sampled(*args, B, S, H, dh, True, None, w["R_batch"], w["R_model"], B - 1, rows, 0)
+        dt = time.perf_counter() - t0
+        # algorithmic work of the sample: dX rows (every head of one sequence:
+        # q, k, v projections, the attention backward, the products with the
+        # weights) and one head's weight gradients over every sequence
+        core_seq = W.attn_core_flops(1, S, H, dh)
+        dx_part = 6.0 * S * D * D + 3.5 * core_seq + 6.0 * len(rows) * D * D
+        w_part = B * (6.0 * S * D * dh + 3.5 * core_seq / H + 8.0 * S * D * dh)
+        return dict(value=(dx_part + w_part) / dt / 1e12, unit="TFLOP/s", cores=cores, kind="oracle",
+                    sample=f"dX at {len(rows)} positions of one {S}-token sequence and one head's weight gradients "
+                           f"over all {B} sequences, through the shards that own them, {dt:.1f} s")
     if w.kind == "attn_core":
         S, H, dh = w["S"], w["H"], w["dh"]
         q, k, v = x["Q"].f64(), x["K"].f64(), x["V"].f64()

@@ -277,6 +277,46 @@ int partir_attn_block(const void* X, const void* Wq_t, const void* Wk_t,
 size_t partir_attn_block_workspace(int64_t B, int64_t S, int64_t D, int64_t n_heads,
                                    int64_t d_head, int R_batch, int R_model);
 
+/* The forward of a training step: partir_attn_block, and also Q, K, V, the
+ * attention output A and the per-row lse kept in the caller's buffer `saved`
+ * (partir_attn_block_saved_bytes bytes: Q | K | V | A, each [B*S, D] bf16 at
+ * 256-byte aligned offsets, then lse [B*S, n_heads] fp32) for
+ * partir_attn_block_backward.  Workspace: that of partir_attn_block minus the
+ * Q, K, V, A it no longer holds (partir_attn_block_workspace is an upper
+ * bound). */
+int partir_attn_block_train(const void* X, const void* Wq_t, const void* Wk_t,
+                            const void* Wv_t, const void* Wo_t, void* Y, void* saved,
+                            int64_t B, int64_t S, int64_t D, int64_t n_heads, int64_t d_head,
+                            int causal, float scale, int in_dtype, int out_dtype,
+                            int R_batch, int R_model,
+                            void* ws, size_t ws_bytes, void* stream);
+size_t partir_attn_block_saved_bytes(int64_t B, int64_t S, int64_t D, int64_t n_heads);
+
+/* Gradients of the attention block for dY [B*S, D] bf16 (the evaluation
+ * trains, Sec. 7), with the forward's batch (R_batch) and heads (R_model)
+ * loops:
+ *   dA = dY Wo^T                   loop b [#tile<0>] { loop m [#tile<1>] }
+ *   dQ, dK, dV = per-head attention gradients (partir_attention_backward)
+ *   dX = dQ Wq^T + dK Wk^T + dV Wv^T   loop b [#tile<0>] { loop m [#sum] }, and
+ *                                      the sum over the three projections
+ *   dW{q,k,v} = X^T d{Q,K,V}       loop m [#tile<1>] { loop b [#sum] }
+ *   dWo = A^T dY                   loop m [#tile<0>] { loop b [#sum] }
+ * Weights and their gradients in the stored layout W^T [out, in] (dW*_t
+ * fp32 [D, D]); dX fp32 [B*S, D]; `saved` from partir_attn_block_train.  The
+ * workspace holds dA, [dQ dK dV], the transposes the token-contracting
+ * products read and the transposed weights.  Constraints as
+ * partir_attn_block.  Errors: E_NULL, E_SHAPE, E_DIVISIBILITY, E_LAYOUT,
+ * E_WORKSPACE, E_UNSUPPORTED, E_HIP. */
+int partir_attn_block_backward(const void* X, const void* Wq_t, const void* Wk_t,
+                               const void* Wv_t, const void* Wo_t, const void* saved,
+                               const void* dY, void* dX, void* dWq_t, void* dWk_t,
+                               void* dWv_t, void* dWo_t,
+                               int64_t B, int64_t S, int64_t D, int64_t n_heads, int64_t d_head,
+                               int causal, float scale, int R_batch, int R_model,
+                               void* ws, size_t ws_bytes, void* stream);
+size_t partir_attn_block_backward_workspace(int64_t B, int64_t S, int64_t D, int64_t n_heads,
+                                            int64_t d_head, int R_batch, int R_model);
+
 /* ------------------------------------------------------------------------ */
 /* Attention core alone, with the key axis as a loop whose reduction is a     */
 /* custom associative #sum (Sec. 5.2.1 footnote: any associative reduction).  */
@@ -392,6 +432,8 @@ int partir_plan_attention(int64_t B, int64_t S, int64_t n_heads, int64_t d_head,
                           partir_plan_info* info);
 int partir_plan_attention_backward(int64_t B, int64_t S, int64_t n_heads, int64_t d_head, int causal,
                                    partir_plan_info* info);
+int partir_plan_attn_block_backward(int64_t B, int64_t S, int64_t D, int64_t n_heads, int64_t d_head,
+                                    int causal, int R_batch, int R_model, partir_plan_info* info);
 int partir_plan_mlp_block_backward(int64_t T, int64_t D, int64_t F, int act, int R_batch, int R_model,
                                    partir_plan_info* info);
 int partir_plan_mlp_block_sharded(int64_t T, int64_t D, int64_t F, int act, int R_batch, int R_model,

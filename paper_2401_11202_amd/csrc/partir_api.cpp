@@ -489,6 +489,7 @@ struct AttnArgs {
   int causal;
   float scale;
   int in, out, Rb, Rm;
+  void* saved = nullptr;   // partir_attn_block_train: Q | K | V | O | lse kept for the backward
 };
 
 int validate_attn_shapes(int64_t B, int64_t S, int64_t D, int64_t H, int64_t dh, int Rb, int Rm) {
@@ -521,7 +522,7 @@ int validate_attn(const AttnArgs& a, bool with_ptrs) {
 // QKV projection + attention core into (Q, K, V, O) inside the workspace.
 void plan_attention_core(const void* Xn, const void* Wq, const void* Wk, const void* Wv, char* qkvo,
                          int64_t B, int64_t S, int64_t D, int64_t H, int64_t dh, int causal, float scale,
-                         int Rb, int Rm, Plan& plan) {
+                         int Rb, int Rm, Plan& plan, float* lse = nullptr) {
   const int64_t T = B * S;
   const size_t one = align_up((size_t)T * D * 2);
   void* Q = qkvo ? qkvo : nullptr;
@@ -546,6 +547,7 @@ void plan_attention_core(const void* Xn, const void* Wq, const void* Wk, const v
   p.B = (int)B; p.S = (int)S; p.H = (int)H; p.causal = causal;
   const float sc = scale > 0 ? scale : 1.0f / std::sqrt((float)dh);
   p.scale_log2 = sc * 1.4426950408889634f;
+  p.lse = lse;
   char buf[256];
   snprintf(buf, sizeof buf, "attention: loop h [#tile<1>](%lld heads/shard) over %lld sequences x %lld heads, "
            "S=%lld, %s, %lld WGs", (long long)(H / Rm), (long long)B, (long long)H, (long long)S,
@@ -564,10 +566,14 @@ void plan_attn(const AttnArgs& a, void* ws, Plan& plan) {
     return;
   }
   char* base = (char*)ws;
-  const size_t core = attn_core_bytes(T, a.D);
-  plan_attention_core(a.X, a.Wq, a.Wk, a.Wv, base, a.B, a.S, a.D, a.H, a.dh, a.causal, a.scale, a.Rb, a.Rm, plan);
+  // training: Q, K, V, O and the lse go to the caller's buffer, not the workspace
+  const size_t core = a.saved ? 0 : attn_core_bytes(T, a.D);
+  char* qkvo = a.saved ? (char*)a.saved : base;
+  float* lse = a.saved ? (float*)((char*)a.saved + attn_core_bytes(T, a.D)) : nullptr;
+  plan_attention_core(a.X, a.Wq, a.Wk, a.Wv, qkvo, a.B, a.S, a.D, a.H, a.dh, a.causal, a.scale, a.Rb, a.Rm, plan,
+                      lse);
   GemmSpec g;
-  g.A = base ? base + 3 * align_up((size_t)T * a.D * 2) : nullptr;
+  g.A = qkvo ? qkvo + 3 * align_up((size_t)T * a.D * 2) : nullptr;
   g.B[0] = a.Wo; g.C[0] = a.Y;
   g.lda = a.D; g.ldb = a.D; g.ldc = a.D;
   g.M = T; g.N = a.D; g.K = a.D;
@@ -799,6 +805,126 @@ void plan_attn_bwd(const AttnBwdArgs& a, void* ws, Plan& plan) {
 }
 
 // ---------------------------------------------------------------------------
+// attention block backward
+// ---------------------------------------------------------------------------
+void plan_transpose(const void* in, void* out, int64_t rows, int64_t cols, const char* name, Plan& plan);
+void plan_transpose_ld(const void* in, int64_t ldi, void* out, int64_t ldo, int64_t rows, int64_t cols,
+                       const char* name, Plan& plan);
+
+struct AttnBlockBwdArgs {
+  const void *X = nullptr, *Wq = nullptr, *Wk = nullptr, *Wv = nullptr, *Wo = nullptr;   // stored W^T [out, in]
+  const void* saved = nullptr;                                                         // from the training forward
+  const void* dY = nullptr;
+  void *dX = nullptr, *dWq = nullptr, *dWk = nullptr, *dWv = nullptr, *dWo = nullptr;
+  int64_t B = 0, S = 0, D = 0, H = 0, dh = 0;
+  int causal = 1;
+  float scale = 0.f;
+  int Rb = 1, Rm = 1;
+};
+
+int validate_attn_block_bwd(const AttnBlockBwdArgs& a, bool with_ptrs) {
+  int st = validate_attn_shapes(a.B, a.S, a.D, a.H, a.dh, a.Rb, a.Rm);
+  if (st) return st;
+  if (!with_ptrs || a.B * a.S == 0) return PARTIR_OK;
+  const void* ps[] = {a.X, a.Wq, a.Wk, a.Wv, a.Wo, a.saved, a.dY, a.dX, a.dWq, a.dWk, a.dWv, a.dWo};
+  for (const void* q : ps) {
+    if (!q) return fail(PARTIR_E_NULL, "every tensor must be non-NULL");
+    if (!aligned16(q)) return fail(PARTIR_E_LAYOUT, "tensors must be 16-byte aligned");
+  }
+  return PARTIR_OK;
+}
+
+// Gradients of the attention block (same nest as partir_attn_block), Wo etc.
+// in their stored layout W^T [out, in]:
+//   dA = dY Wo^T                  loop b [#tile<0>] loop m [#tile<1>] (heads)
+//   dQ|dK|dV = attention backward per head
+//   dX = [dQ dK dV] [Wq Wk Wv]^T  loop b [#tile<0>] loop m [#sum], and the sum over q, k, v
+//   dW{q,k,v}^T = dQKV^T X        loop m [#tile<0>] loop b [#sum]
+//   dWo^T = dY^T A                loop m [#tile<1>] loop b [#sum]
+void plan_attn_block_bwd(const AttnBlockBwdArgs& a, void* ws, Plan& plan) {
+  const int64_t T = a.B * a.S, D = a.D;
+  plan.n_shards = a.Rb * a.Rm;
+  plan.n_tile_loops = (a.Rb > 1) + 1;
+  const double pairs = a.causal ? (double)a.S * (a.S + 1) / 2 : (double)a.S * a.S;
+  plan.flops = 16.0 * T * D * D + 2.5 * 4.0 * a.B * a.H * pairs * a.dh;
+  if (T == 0) return;
+  const size_t dd = align_up((size_t)D * D * 2), td = align_up((size_t)T * D * 2);
+  const size_t one = td;   // saved layout: Q | K | V | O | lse
+  const char* sv = (const char*)a.saved;
+  const void* Q = sv;
+  const void* K = sv ? sv + one : nullptr;
+  const void* V = sv ? sv + 2 * one : nullptr;
+  const void* Ao = sv ? sv + 3 * one : nullptr;
+  const float* lse = sv ? (const float*)(sv + 4 * one) : nullptr;
+  char* base = (char*)ws;
+  size_t off = 0;
+  auto take = [&](size_t n) { char* p = base ? base + off : nullptr; off += n; return (void*)p; };
+  void* WoT = take(dd);
+  void* WqkvT = take(3 * dd);
+  void* dA = take(td);
+  void* dQKV = take(3 * td);
+  void* dQKVt = take(3 * td);
+  void* Xt = take(td);
+  void* dYt = take(td);
+  void* At = take(td);
+  void* Dst = take(align_up((size_t)T * a.H * 4));
+  void* part = base ? base + off : nullptr;
+  plan_transpose(a.Wo, WoT, D, D, "bwd.transpose", plan);
+  GemmSpec ga;
+  ga.A = a.dY; ga.B[0] = WoT; ga.C[0] = dA;
+  ga.lda = D; ga.ldb = D; ga.ldc = D; ga.M = T; ga.N = D; ga.K = D;
+  ga.c_dtype = PARTIR_BF16; ga.rm = a.Rb; ga.rn = a.Rm;
+  ga.name = "attn.bwd.da"; ga.label = "bwd.da dA = slice 0 dY[b] . (slice 0 Wo[m])^T";
+  plan_gemm(ga, nullptr, plan);
+  AttnBwdArgs c;
+  c.Q = Q; c.K = K; c.V = V; c.O = Ao; c.dO = dA; c.lse = lse;
+  c.dQ = dQKV; c.dK = dQKV ? (char*)dQKV + D * 2 : nullptr; c.dV = dQKV ? (char*)dQKV + 2 * D * 2 : nullptr;
+  c.B = a.B; c.S = a.S; c.H = a.H; c.dh = a.dh; c.causal = a.causal; c.scale = a.scale;
+  Plan core;
+  plan_attn_bwd(c, Dst, core);
+  Launch L = core.launches.back();
+  L.attn_bwd.lddq = L.attn_bwd.lddk = L.attn_bwd.lddv = 3 * D;   // [dQ | dK | dV] side by side
+  plan.launches.push_back(L);
+  const void* Wqkv[3] = {a.Wq, a.Wk, a.Wv};
+  for (int i = 0; i < 3; ++i)
+    plan_transpose_ld(Wqkv[i], D, WqkvT ? (char*)WqkvT + i * D * 2 : nullptr, 3 * D, D, D, "bwd.transpose", plan);
+  GemmSpec gx;
+  gx.A = dQKV; gx.B[0] = WqkvT; gx.C[0] = a.dX;
+  gx.lda = 3 * D; gx.ldb = 3 * D; gx.ldc = D; gx.M = T; gx.N = D; gx.K = 3 * D;
+  gx.c_dtype = PARTIR_F32; gx.rm = a.Rb;
+  gx.name = "attn.bwd.dx"; gx.label = "bwd.dx dX = sum over m and q|k|v of dQKV[b][:, m] . W{q,k,v}[:, m]^T";
+  plan_gemm(gx, part, plan);
+  plan_transpose(dQKV, dQKVt, T, 3 * D, "bwd.transpose", plan);
+  plan_transpose(a.X, Xt, T, D, "bwd.transpose", plan);
+  GemmSpec gw;
+  gw.A = dQKVt; gw.B[0] = Xt; gw.C[0] = nullptr;
+  gw.lda = T; gw.ldb = T; gw.ldc = D; gw.M = 3 * D; gw.N = D; gw.K = T;
+  gw.c_dtype = PARTIR_F32; gw.rm = 3 * a.Rm; gw.rk = a.Rb; gw.sum_impl = PARTIR_SUM_FUSED;
+  gw.name = "attn.bwd.dwqkv";
+  gw.label = "bwd.dwqkv dW{q,k,v}^T = sum_b dQKV[b][:, m]^T . slice 0 X[b]";
+  plan_gemm(gw, nullptr, plan);
+  {
+    Launch& W = plan.launches.back();
+    W.kind = L_GEMM_BF16_PARTS;
+    GemmParts* t = new GemmParts{};
+    t->c_rows = (int)D;
+    t->c[0] = a.dWq; t->c[1] = a.dWk; t->c[2] = a.dWv;
+    W.parts.reset(t);
+    W.text += "; rows stored into dWq^T, dWk^T, dWv^T";
+  }
+  plan_transpose(a.dY, dYt, T, D, "bwd.transpose", plan);
+  plan_transpose(Ao, At, T, D, "bwd.transpose", plan);
+  GemmSpec go;
+  go.A = dYt; go.B[0] = At; go.C[0] = a.dWo;
+  go.lda = T; go.ldb = T; go.ldc = D; go.M = D; go.N = D; go.K = T;
+  go.c_dtype = PARTIR_F32; go.rn = a.Rm; go.rk = a.Rb;
+  go.name = "attn.bwd.dwo"; go.label = "bwd.dwo dWo^T = sum_b (slice 0 dY[b])^T . A[b][:, m]";
+  plan_gemm(go, part, plan);
+  plan.n_sum_loops = 4;
+  plan.ws_bytes = off + std::max(gemm_ws_bytes(gx), gemm_ws_bytes(go));
+}
+
+// ---------------------------------------------------------------------------
 // partir_mlp_block_backward
 // ---------------------------------------------------------------------------
 struct MlpBwdArgs {
@@ -844,6 +970,14 @@ void plan_transpose(const void* in, void* out, int64_t rows, int64_t cols, const
            (long long)cols, (long long)rows);
   L.text = buf;
   plan.launches.push_back(L);
+}
+
+// out[c][r] = in[r][c] with explicit leading dims (a column block of a wider output)
+void plan_transpose_ld(const void* in, int64_t ldi, void* out, int64_t ldo, int64_t rows, int64_t cols,
+                       const char* name, Plan& plan) {
+  plan_transpose(in, out, rows, cols, name, plan);
+  plan.launches.back().tr.ldi = ldi;
+  plan.launches.back().tr.ldo = ldo;
 }
 
 void plan_colsum(const void* in, void* partial, void* out, int64_t rows, int64_t cols, bool partial_ready,
@@ -1282,6 +1416,74 @@ int partir_attn_block(const void* X, const void* Wq_t, const void* Wk_t, const v
   Plan plan;
   plan_attn(a, ws, plan);
   keep_plan_text(plan, "attn_block");
+  return execute(plan, stream);
+}
+
+size_t partir_attn_block_saved_bytes(int64_t B, int64_t S, int64_t D, int64_t n_heads) {
+  if (B < 0 || S < 0 || D < 0 || n_heads < 0) return (size_t)-1;
+  return attn_core_bytes(B * S, D) + align_up((size_t)(B * S * n_heads) * 4);
+}
+
+int partir_attn_block_train(const void* X, const void* Wq_t, const void* Wk_t, const void* Wv_t, const void* Wo_t,
+                            void* Y, void* saved, int64_t B, int64_t S, int64_t D, int64_t n_heads, int64_t d_head,
+                            int causal, float scale, int in_dtype, int out_dtype, int R_batch, int R_model,
+                            void* ws, size_t ws_bytes, void* stream) {
+  AttnArgs a{X, Wq_t, Wk_t, Wv_t, Wo_t, Y, B, S, D, n_heads, d_head, causal ? 1 : 0, scale,
+             in_dtype, out_dtype, R_batch, R_model, saved};
+  int st = validate_attn(a, true);
+  if (st) return st;
+  if (B * S > 0 && !saved) return fail(PARTIR_E_NULL, "saved must be non-NULL");
+  if (!aligned16(saved)) return fail(PARTIR_E_LAYOUT, "saved must be 16-byte aligned");
+  Plan probe;
+  plan_attn(a, nullptr, probe);
+  if ((st = check_ws(probe, ws, ws_bytes))) return st;
+  Plan plan;
+  plan_attn(a, ws, plan);
+  keep_plan_text(plan, "attn_block_train");
+  return execute(plan, stream);
+}
+
+size_t partir_attn_block_backward_workspace(int64_t B, int64_t S, int64_t D, int64_t n_heads, int64_t d_head,
+                                            int R_batch, int R_model) {
+  AttnBlockBwdArgs a;
+  a.B = B; a.S = S; a.D = D; a.H = n_heads; a.dh = d_head; a.Rb = R_batch; a.Rm = R_model;
+  if (validate_attn_block_bwd(a, false) != PARTIR_OK) return (size_t)-1;
+  Plan plan;
+  plan_attn_block_bwd(a, nullptr, plan);
+  return plan.ws_bytes;
+}
+
+int partir_plan_attn_block_backward(int64_t B, int64_t S, int64_t D, int64_t n_heads, int64_t d_head, int causal,
+                                    int R_batch, int R_model, partir_plan_info* info) {
+  AttnBlockBwdArgs a;
+  a.B = B; a.S = S; a.D = D; a.H = n_heads; a.dh = d_head; a.causal = causal ? 1 : 0; a.Rb = R_batch; a.Rm = R_model;
+  int st = validate_attn_block_bwd(a, false);
+  if (st) return st;
+  Plan plan;
+  plan_attn_block_bwd(a, nullptr, plan);
+  keep_plan_text(plan, "attn_block_backward");
+  fill_info(plan, info);
+  return PARTIR_OK;
+}
+
+int partir_attn_block_backward(const void* X, const void* Wq_t, const void* Wk_t, const void* Wv_t,
+                               const void* Wo_t, const void* saved, const void* dY, void* dX, void* dWq_t,
+                               void* dWk_t, void* dWv_t, void* dWo_t, int64_t B, int64_t S, int64_t D,
+                               int64_t n_heads, int64_t d_head, int causal, float scale, int R_batch, int R_model,
+                               void* ws, size_t ws_bytes, void* stream) {
+  AttnBlockBwdArgs a;
+  a.X = X; a.Wq = Wq_t; a.Wk = Wk_t; a.Wv = Wv_t; a.Wo = Wo_t; a.saved = saved; a.dY = dY;
+  a.dX = dX; a.dWq = dWq_t; a.dWk = dWk_t; a.dWv = dWv_t; a.dWo = dWo_t;
+  a.B = B; a.S = S; a.D = D; a.H = n_heads; a.dh = d_head; a.causal = causal ? 1 : 0; a.scale = scale;
+  a.Rb = R_batch; a.Rm = R_model;
+  int st = validate_attn_block_bwd(a, true);
+  if (st) return st;
+  Plan probe;
+  plan_attn_block_bwd(a, nullptr, probe);
+  if ((st = check_ws(probe, ws, ws_bytes))) return st;
+  Plan plan;
+  plan_attn_block_bwd(a, ws, plan);
+  keep_plan_text(plan, "attn_block_backward");
   return execute(plan, stream);
 }
 

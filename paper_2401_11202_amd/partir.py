@@ -35,7 +35,9 @@ EXPORTS = ("partir_loop_matmul", "partir_loop_matmul_workspace", "partir_mlp_blo
            "partir_mlp_block_backward", "partir_mlp_block_backward_workspace", "partir_plan_mlp_block_backward",
            "partir_mlp_block_train", "partir_mlp_block_sharded", "partir_mlp_block_sharded_workspace",
            "partir_plan_mlp_block_sharded", "partir_attention_train", "partir_attention_backward",
-           "partir_attention_backward_workspace", "partir_plan_attention_backward")
+           "partir_attention_backward_workspace", "partir_plan_attention_backward", "partir_attn_block_train",
+           "partir_attn_block_saved_bytes", "partir_attn_block_backward", "partir_attn_block_backward_workspace",
+           "partir_plan_attn_block_backward")
 
 
 class PartirError(RuntimeError):
@@ -105,6 +107,14 @@ def lib():
         "partir_attention_backward": (I32, [P, P, P, P, P, P, P, P, P, I64, I64, I64, I64, I32, F, P, SZ, P]),
         "partir_attention_backward_workspace": (SZ, [I64, I64, I64, I64]),
         "partir_plan_attention_backward": (I32, [I64, I64, I64, I64, I32, ctypes.POINTER(PlanInfo)]),
+        "partir_attn_block_train": (I32, [P, P, P, P, P, P, P, I64, I64, I64, I64, I64, I32, F, I32, I32, I32, I32,
+                                          P, SZ, P]),
+        "partir_attn_block_saved_bytes": (SZ, [I64, I64, I64, I64]),
+        "partir_attn_block_backward": (I32, [P, P, P, P, P, P, P, P, P, P, P, P, I64, I64, I64, I64, I64, I32, F,
+                                             I32, I32, P, SZ, P]),
+        "partir_attn_block_backward_workspace": (SZ, [I64, I64, I64, I64, I64, I32, I32]),
+        "partir_plan_attn_block_backward": (I32, [I64, I64, I64, I64, I64, I32, I32, I32,
+                                                  ctypes.POINTER(PlanInfo)]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(L, name)
@@ -380,6 +390,46 @@ def attention_backward(Q, K, V, O, dO, lse, *, B: int, S: int, n_heads: int, d_h
                                            _ptr(out[1]), _ptr(out[2]), B, S, n_heads, d_head, int(causal), scale,
                                            _ptr(ws), wsb, _stream(stream)))
     return out
+
+
+def attn_block_train(X, Wq_t, Wk_t, Wv_t, Wo_t, *, B: int, S: int, n_heads: int, d_head: int = 128,
+                     causal: bool = True, scale: float = 0.0, R_batch: int = 1, R_model: int = 1, out=None,
+                     saved=None, workspace=None, stream=None):
+    """attn_block that also keeps Q, K, V, A and lse in `saved` (a uint8
+    tensor) for attn_block_backward.  Returns (Y, saved)."""
+    import torch
+    T, D = X.shape
+    if out is None:
+        out = torch.empty((T, D), dtype=torch.float32, device=X.device)
+    if saved is None:
+        saved = torch.empty(max(1, lib().partir_attn_block_saved_bytes(B, S, D, n_heads)), dtype=torch.uint8,
+                            device=X.device)
+    ws, wsb = _workspace(attn_block_workspace(B, S, D, n_heads, d_head, R_batch, R_model), X.device, workspace)
+    _check(lib().partir_attn_block_train(_ptr(X), _ptr(Wq_t), _ptr(Wk_t), _ptr(Wv_t), _ptr(Wo_t), _ptr(out),
+                                         _ptr(saved), B, S, D, n_heads, d_head, int(causal), scale, _dt(X),
+                                         _dt(out), R_batch, R_model, _ptr(ws), wsb, _stream(stream)))
+    return out, saved
+
+
+def attn_block_backward(X, Wq_t, Wk_t, Wv_t, Wo_t, saved, dY, *, B: int, S: int, n_heads: int,
+                        d_head: int = 128, causal: bool = True, scale: float = 0.0, R_batch: int = 1,
+                        R_model: int = 1, out=None, workspace=None, stream=None):
+    """Gradients (dX, dWq_t, dWk_t, dWv_t, dWo_t), fp32, weights' stored layout."""
+    import torch
+    T, D = X.shape
+    f32 = dict(dtype=torch.float32, device=X.device)
+    if out is None:
+        out = (torch.empty((T, D), **f32),) + tuple(torch.empty((D, D), **f32) for _ in range(4))
+    ws, wsb = _workspace(lib().partir_attn_block_backward_workspace(B, S, D, n_heads, d_head, R_batch, R_model),
+                         X.device, workspace)
+    _check(lib().partir_attn_block_backward(_ptr(X), _ptr(Wq_t), _ptr(Wk_t), _ptr(Wv_t), _ptr(Wo_t), _ptr(saved),
+                                            _ptr(dY), *(_ptr(o) for o in out), B, S, D, n_heads, d_head,
+                                            int(causal), scale, R_batch, R_model, _ptr(ws), wsb, _stream(stream)))
+    return out
+
+
+def plan_attn_block_backward(B, S, D, n_heads, d_head=128, causal=True, R_batch=1, R_model=1):
+    return _plan(lib().partir_plan_attn_block_backward, B, S, D, n_heads, d_head, int(causal), R_batch, R_model)
 
 
 def plan_attention_backward(B, S, n_heads, d_head=128, causal=True):

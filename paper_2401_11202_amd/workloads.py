@@ -24,7 +24,7 @@ from . import inputs as I
 @dataclass(frozen=True)
 class Workload:
     name: str
-    kind: str                 # matmul | mlp | attn | decoder | attn_core | mlp_train | mlp_z3
+    kind: str                 # matmul | mlp | attn | decoder | attn_core | mlp_train | mlp_z3 | attn_train
     wid: int                  # seed id
     dims: Dict[str, int] = field(default_factory=dict)
     dtype: str = "bf16"
@@ -72,6 +72,10 @@ WORKLOADS = {
     # weight gradients
     "mlp_megatron_train": _mlp_train("mlp_megatron_train", 7, 8192, 4096, 16384, 1, 8),
     "mlp_batch_x_megatron_train": _mlp_train("mlp_batch_x_megatron_train", 8, 8192, 4096, 16384, 2, 4),
+    # training step of the attention block (forward keeping Q, K, V, A, lse,
+    # then every gradient of the same nest)
+    "attn_block_train": Workload("attn_block_train", "attn_train", 10,
+                                 dict(B=4, S=2048, D=4096, H=32, dh=128, R_batch=1, R_model=8)),
     # the MLP on device-local arrays under BP + MP + Z3 with the activations
     # also sharded over the model axis: mesh {B: 2, M: 4}, 8 devices
     "mlp_z3_sp": Workload("mlp_z3_sp", "mlp_z3", 9, dict(T=8192, D=4096, F=16384, R_batch=2, R_model=4)),
@@ -125,7 +129,10 @@ def attn_inputs(w: Workload):
     B, S, D = w["B"], w["S"], w["D"]
     X = I.gaussian(w.wid, 0, (B * S, D), 1.0)
     Ws = {n: I.gaussian(w.wid, 1 + i, (D, D), D ** -0.5) for i, n in enumerate(("Wq", "Wk", "Wv", "Wo"))}
-    return dict(X=X, **Ws)
+    out = dict(X=X, **Ws)
+    if w.kind == "attn_train":   # the output cotangent dY ~ N(0, 1)
+        out["dY"] = I.gaussian(w.wid, 20, (B * S, D), 1.0)
+    return out
 
 
 def decoder_inputs(w: Workload):
@@ -151,7 +158,7 @@ def attn_core_inputs(w: Workload):
 def make_inputs(w: Workload):
     return {"matmul": matmul_inputs, "mlp": mlp_inputs, "attn": attn_inputs,
             "decoder": decoder_inputs, "attn_core": attn_core_inputs, "mlp_train": mlp_train_inputs,
-            "mlp_z3": mlp_z3_inputs}[w.kind](w)
+            "mlp_z3": mlp_z3_inputs, "attn_train": attn_inputs}[w.kind](w)
 
 
 # ---------------------------------------------------------------------------
@@ -181,4 +188,8 @@ def flops(w: Workload) -> float:
     if w.kind == "mlp_train":
         # forward 4TDF; backward dH, dW2, dW1, dX 8TDF (recomputing Z is not counted)
         return 12.0 * w["T"] * w["D"] * w["F"]
+    if w.kind == "attn_train":
+        # forward 8TD^2 + core; backward dA, dX, dW{q,k,v}, dWo 16TD^2 + 2.5 x core
+        T = w["B"] * w["S"]
+        return 24.0 * T * w["D"] * w["D"] + 3.5 * attn_core_flops(w["B"], w["S"], w["H"], w["dh"])
     raise ValueError(w.kind)

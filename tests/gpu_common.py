@@ -14,6 +14,19 @@ from paper_2401_11202_amd import inputs as I
 # accumulation.
 TOL_F32 = 1e-4
 TOL_BF16 = 2e-2
+# Chained products (backward passes) round several bf16 intermediates
+# (2^-9 relative each); the error normalised by the whole gradient's size,
+# ||got - ref||_F / ||ref||_F, must stay at the level of a few such roundings.
+# This catches a wrong factor that the elementwise |A|.|B| normaliser, loose
+# by ~sqrt(K) per contraction, would let through.
+TOL_REL_FRO = 1e-2
+
+
+def rel_fro(got, ref) -> float:
+    got = np.asarray(got, np.float64)
+    ref = np.asarray(ref, np.float64)
+    den = float(np.linalg.norm(ref))
+    return float(np.linalg.norm(got - ref)) / den if den > 0 else float(np.linalg.norm(got))
 
 
 def say(*a):

@@ -15,7 +15,7 @@ import torch
 from oracle import partir_oracle as O
 from paper_2401_11202_amd import inputs as I
 from paper_2401_11202_amd import partir as P
-from tests.gpu_common import TOL_BF16, host, say
+from tests.gpu_common import TOL_BF16, TOL_REL_FRO, host, rel_fro, say
 
 pytestmark = pytest.mark.gpu
 DH = 128
@@ -40,6 +40,9 @@ def check_head(got, Q, K, V, G, b, h, S, causal):
     ref, nrm = O.attention_backward(Q.f64()[rows, cols], K.f64()[rows, cols], V.f64()[rows, cols],
                                     G.f64()[rows, cols], DH ** -0.5, causal, return_norm=True)
     errs = [O.normalised_error(g[rows, cols], r, n) for g, r, n in zip(got[:3], ref, nrm)]
+    fros = [rel_fro(g[rows, cols], r) for g, r in zip(got[:3], ref)]
+    say(f"      relative Frobenius dQ {fros[0]:.2e} dK {fros[1]:.2e} dV {fros[2]:.2e}")
+    assert max(fros) <= TOL_REL_FRO
     # lse: log2 of the softmax denominator of the scaled scores
     s = Q.f64()[rows, cols] @ K.f64()[rows, cols].T * DH ** -0.5
     if causal:
