@@ -961,6 +961,62 @@ def z3_local_operands(X, W1, W2, R_batch, R_model, sequence_sharded=True):
     return x, w1, w2
 
 
+def decoder_layer_z3(x_loc, p_loc, g1, g2, B, S, n_heads, d_head, eps=1e-6, R_batch=1, R_model=1):
+    """The lowered SPMD program of decoder_layer under BP + MP + Z3 with the
+    residual stream sharded over the model axis as well (sequence-parallel
+    norms), per device (b, m) of the mesh {B, M}:
+
+      xn = all_gather<M>(rmsnorm(x_loc, g1), dim 0)        the norm on the local tokens
+      q|k|v = xn @ all_gather<B>(W{q,k,v}_loc, dim 0)       the shard's heads
+      a  = causal attention of those heads over the batch block's sequences
+      x_loc += reduce_scatter<M>(a @ all_gather<B>(Wo_loc, dim 1), dim 0)
+      hn = all_gather<M>(rmsnorm(x_loc, g2), dim 0)
+      x_loc += reduce_scatter<M>(gelu(hn @ all_gather<B>(W1_loc, dim 0))
+                                 @ all_gather<B>(W2_loc, dim 1), dim 0)
+
+    x_loc {device: [T/(R_batch R_model), D]}; p_loc {name: {device: block}}
+    with Wq, Wk, Wv, W1 blocks (dim 0 block b, dim 1 block m) and Wo, W2
+    blocks (dim 0 block m, dim 1 block b).  Returns the new x_loc."""
+    mesh = [("B", R_batch), ("M", R_model)]
+    scale = 1.0 / math.sqrt(d_head)
+    hps, nseq = n_heads // R_model, B // R_batch
+    x = {d: np.asarray(v, np.float64) for d, v in x_loc.items()}
+    gathered = {k: all_gather(p_loc[k], mesh, 0, "B") for k in ("Wq", "Wk", "Wv", "W1")}
+    gathered.update({k: all_gather(p_loc[k], mesh, 1, "B") for k in ("Wo", "W2")})
+    xn = all_gather({d: rmsnorm(v, g1, eps) for d, v in x.items()}, mesh, 0, "M")
+    part = {}
+    for d in mesh_devices(mesh):
+        q, k, v = (matmul(xn[d], gathered[w][d]) for w in ("Wq", "Wk", "Wv"))
+        a = np.zeros_like(q)
+        for sq in range(nseq):
+            rs = slice(sq * S, (sq + 1) * S)
+            for hh in range(hps):
+                cs = slice(hh * d_head, (hh + 1) * d_head)
+                a[rs, cs] = causal_attention(q[rs, cs], k[rs, cs], v[rs, cs], scale, True)
+        part[d] = matmul(a, gathered["Wo"][d])
+    rs_ = reduce_scatter(part, mesh, 0, "M")
+    x = {d: x[d] + rs_[d] for d in x}
+    hn = all_gather({d: rmsnorm(v, g2, eps) for d, v in x.items()}, mesh, 0, "M")
+    part = {d: matmul(gelu_erf(matmul(hn[d], gathered["W1"][d])), gathered["W2"][d]) for d in mesh_devices(mesh)}
+    rs_ = reduce_scatter(part, mesh, 0, "M")
+    return {d: x[d] + rs_[d] for d in x}
+
+
+def z3_local_decoder(x, p, R_batch, R_model):
+    """Value tiling of a decoder layer's whole operands into device-local
+    arrays: x by tokens over B then M; Wq, Wk, Wv, W1 dim 0 over B and dim 1
+    over M; Wo, W2 dim 0 over M and dim 1 over B (Sec. 6: sliced arguments
+    become device-local)."""
+    mesh = [("B", R_batch), ("M", R_model)]
+    x_loc = all_slice(all_slice(replicated(x, mesh), mesh, 0, "B"), mesh, 0, "M")
+    p_loc = {}
+    for k in ("Wq", "Wk", "Wv", "W1"):
+        p_loc[k] = all_slice(all_slice(replicated(p[k], mesh), mesh, 0, "B"), mesh, 1, "M")
+    for k in ("Wo", "W2"):
+        p_loc[k] = all_slice(all_slice(replicated(p[k], mesh), mesh, 0, "M"), mesh, 1, "B")
+    return x_loc, p_loc
+
+
 # ---------------------------------------------------------------------------
 # Parity measure (the elementwise forward-error form)
 # ---------------------------------------------------------------------------

@@ -150,3 +150,40 @@ def test_z3_local_operand_blocks():
     assert np.array_equal(w1[(1, 2)], W1[4:8, 8:12])
     assert np.array_equal(w2[(1, 2)], W2[8:12, 4:8])
     assert np.array_equal(x[(1, 2)], X[20:24])       # token block b * R_model + m = 5 of 6
+
+
+@pytest.mark.parametrize("RB,RM", [(1, 1), (2, 2), (1, 4), (2, 1)])
+def test_decoder_z3_equals_shard_interpreter_and_reference(RB, RM):
+    """Sequence-parallel norms: the norms run on each device's tokens; the
+    layer still equals the unpartitioned decoder and the shard interpreter."""
+    rng = np.random.default_rng(RB * 7 + RM)
+    B, S, H, dh, F = 2, 8, 4, 2, 16
+    D = H * dh
+    x = rng.standard_normal((B * S, D))
+    p = {"g1": 1 + 0.1 * rng.standard_normal(D), "g2": 1 + 0.1 * rng.standard_normal(D)}
+    for k in ("Wq", "Wk", "Wv", "Wo"):
+        p[k] = rng.standard_normal((D, D)) / math.sqrt(D)
+    p["W1"], p["W2"] = rng.standard_normal((D, F)) / math.sqrt(D), rng.standard_normal((F, D)) / math.sqrt(F)
+    x_loc, p_loc = O.z3_local_decoder(x, p, RB, RM)
+    y = O.decoder_layer_z3(x_loc, p_loc, p["g1"], p["g2"], B, S, H, dh, 1e-6, RB, RM)
+    got = gather_rows(y, RB, RM)
+    assert np.max(np.abs(got - O.decoder_ref(x, [p], B, S, H, dh, 1e-6))) < 1e-12
+    assert np.max(np.abs(got - O.decoder_layer(x, p, B, S, H, dh, 1e-6, RB, RM))) < 1e-12
+
+
+def test_decoder_z3_norm_is_local():
+    """Scaling one device's tokens scales nothing else: the norm of a token
+    row depends on that row only (no communication for the norms)."""
+    rng = np.random.default_rng(5)
+    x = rng.standard_normal((8, 4))
+    mesh = [("B", 2), ("M", 2)]
+    loc = O.all_slice(O.all_slice(O.replicated(x, mesh), mesh, 0, "B"), mesh, 0, "M")
+    g = np.ones(4)
+    before = {d: O.rmsnorm(v, g, 1e-6) for d, v in loc.items()}
+    loc[(1, 0)] = loc[(1, 0)] * 3.0
+    after = {d: O.rmsnorm(v, g, 1e-6) for d, v in loc.items()}
+    for d in loc:
+        if d != (1, 0):
+            assert np.array_equal(after[d], before[d])
+    # and the scaled device's rows are normalised to the same values (up to eps)
+    assert np.max(np.abs(after[(1, 0)] - before[(1, 0)])) < 1e-5
