@@ -169,6 +169,30 @@ def setup(w, P, I):
                  "mlp.up": L * 2.0 * T * D * F, "mlp.down": L * 2.0 * T * D * F}
         roles = {k: v / L for k, v in roles.items()}   # per launch
         return x, step, roles, "mfma_bf16"
+    if w.kind == "decoder_z3":
+        B, S, D, H, F, Rb, Rm = w["B"], w["S"], w["D"], w["H"], w["F"], w["R_batch"], w["R_model"]
+        T = B * S
+        x0, _ = P.z3_decoder_arrays(x["x"].to_device(), {}, Rb, Rm)
+        xs = [t.clone() for t in x0]
+        layers = []
+        for p in x["layers"]:
+            _, parts = P.z3_decoder_arrays(x0[0], {k: dev_t(p[k]) for k in ("Wq", "Wk", "Wv", "Wo", "W1", "W2")},
+                                           Rb, Rm)
+            layers.append(dict(g1=p["g1"].to_device(), g2=p["g2"].to_device(), parts=parts))
+        ws = torch.empty(P.lib().partir_decoder_layer_sharded_workspace(B, S, D, H, w["dh"], F, Rb, Rm),
+                         dtype=torch.uint8, device="cuda")
+
+        def step():
+            for a, b0 in zip(xs, x0):   # the stack runs in place on the residual parts
+                a.copy_(b0)
+            for l in layers:
+                P.decoder_layer_sharded(xs, l["g1"], l["g2"], l["parts"], B=B, S=S, n_heads=H, d_head=w["dh"],
+                                        R_batch=Rb, R_model=Rm, workspace=ws)
+        L = w["L"]
+        roles = {"attn.qkv": 2.0 * T * D * D, "attn.out": 2.0 * T * D * D,
+                 "attn.core": W.attn_core_flops(B, S, H, w["dh"]),
+                 "mlp.up": 2.0 * T * D * F, "mlp.down": 2.0 * T * D * F}
+        return x, step, roles, "mfma_bf16"
     if w.kind == "attn_core":
         B, S, H, dh = w["B"], w["S"], w["H"], w["dh"]
         Q, K, V = (x[n].to_device() for n in ("Q", "K", "V"))
@@ -285,7 +309,7 @@ def cpu_baseline(w, x, target_s):
         flops = 4.0 * H * dh * float(np.sum(rows + 1))
         return dict(value=flops / dt / 1e12, unit="TFLOP/s", cores=cores, kind="oracle",
                     sample=f"{nq} query rows x {H} heads at the end of the {S}-token sequence, {dt:.1f} s")
-    if w.kind == "decoder":
+    if w.kind in ("decoder", "decoder_z3"):
         S, D, F = w["S"], w["D"], w["F"]
         layers = [{k: v.f64() for k, v in p.items()} for p in x["layers"]]
         pos = 256

@@ -193,6 +193,37 @@ int partir_mlp_block_sharded(const void* const* X_parts, const void* const* W1t_
                              void* ws, size_t ws_bytes, void* stream);
 size_t partir_mlp_block_sharded_workspace(int64_t T, int64_t D, int64_t F, int R_batch, int R_model);
 
+/* The decoder layer on device-local arrays: BP + MP + Z3 with the residual
+ * stream sharded over the model axis too, so the RMSNorms run on each
+ * device's own tokens (sequence-parallel norms).  Device (b, m) of the mesh
+ * {B: R_batch, M: R_model} is part p = b * R_model + m:
+ *   x_parts[p]   [B*S/(R_batch R_model), D] fp32: token rows p of x, updated
+ *                in place to the layer's output
+ *   Wq|Wk|Wv|W1_parts[p]: W_t[rows block m, cols block b] bf16 (W_t = W^T
+ *                [out, in]; blocks of out/R_model rows and D/R_batch columns)
+ *   Wo|W2_parts[p]: W_t[rows block b, cols block m] (D/R_batch rows, in/R_model
+ *                columns)
+ *   g1, g2 [D] fp32 replicated (g2 may be NULL when F = 0).
+ * Lowered program per device (Sec. 6 collectives, all fused): the norm of the
+ * device's tokens is stored into the gathered activation buffer (all_gather
+ * over M); the projections read the weight parts in place (all_gathers over
+ * B); the attention-out and FFN-down #sums over m stay in the tile and each
+ * row block is added into its owner's residual part (reduce_scatter).  The
+ * result equals partir_decoder_layer on the concatenated x.  Constraints:
+ * those of partir_decoder_layer, T/(R_batch R_model) a multiple of 16,
+ * D/R_batch and F/R_model multiples of 64, at most 64 devices.
+ * Errors: E_NULL, E_SHAPE, E_DIVISIBILITY, E_LAYOUT, E_WORKSPACE,
+ * E_UNSUPPORTED, E_HIP. */
+int partir_decoder_layer_sharded(void* const* x_parts, const void* g1, const void* g2, float eps,
+                                 const void* const* Wq_parts, const void* const* Wk_parts,
+                                 const void* const* Wv_parts, const void* const* Wo_parts,
+                                 const void* const* W1_parts, const void* const* W2_parts,
+                                 int64_t B, int64_t S, int64_t D, int64_t n_heads, int64_t d_head,
+                                 int64_t F, int R_batch, int R_model,
+                                 void* ws, size_t ws_bytes, void* stream);
+size_t partir_decoder_layer_sharded_workspace(int64_t B, int64_t S, int64_t D, int64_t n_heads,
+                                              int64_t d_head, int64_t F, int R_batch, int R_model);
+
 /* The forward of a training step: partir_mlp_block, and also the
  * pre-activation Z = X W1 + b1 [T, F] bf16 (row-major, caller-owned, written
  * by the same up-projection tiles) that partir_mlp_block_backward reads
@@ -438,6 +469,8 @@ int partir_plan_mlp_block_backward(int64_t T, int64_t D, int64_t F, int act, int
                                    partir_plan_info* info);
 int partir_plan_mlp_block_sharded(int64_t T, int64_t D, int64_t F, int act, int R_batch, int R_model,
                                   partir_plan_info* info);
+int partir_plan_decoder_layer_sharded(int64_t B, int64_t S, int64_t D, int64_t n_heads, int64_t d_head,
+                                      int64_t F, int R_batch, int R_model, partir_plan_info* info);
 int partir_plan_decoder_layer(int64_t B, int64_t S, int64_t D, int64_t n_heads,
                               int64_t d_head, int64_t F, int R_batch, int R_model,
                               partir_plan_info* info);

@@ -40,11 +40,17 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(ReduceParams p) {
 }
 
 // One wave per row: fp32 sum of squares over D, then y = bf16(g * x * rstd).
-__global__ __launch_bounds__(256) void rmsnorm_kernel(RmsParams p) {
+// With parts, row r of x lives in the part r / rows_part (device-local arrays).
+template <int PARTS>
+__device__ __forceinline__ void rmsnorm_body(const RmsParams& p, const RmsParts* t) {
   const int lane = threadIdx.x & 63;
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= p.rows) return;
   const float* x = p.x + (int64_t)row * p.ldx;
+  if (PARTS) {
+    const int part = row / t->rows_part;
+    x = t->x[part] + (int64_t)(row - part * t->rows_part) * p.ldx;
+  }
   float ss = 0.0f;
   for (int c = lane * 4; c < p.D; c += 256) {
     const f32x4 v = *(const f32x4*)(x + c);
@@ -63,6 +69,9 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(RmsParams p) {
   }
 }
 
+__global__ __launch_bounds__(256) void rmsnorm_kernel(RmsParams p) { rmsnorm_body<0>(p, nullptr); }
+__global__ __launch_bounds__(256) void rmsnorm_parts_kernel(RmsParams p, RmsParts t) { rmsnorm_body<1>(p, &t); }
+
 }  // namespace
 
 hipError_t launch_splitk_reduce(const ReduceParams& p, hipStream_t s) {
@@ -74,6 +83,12 @@ hipError_t launch_splitk_reduce(const ReduceParams& p, hipStream_t s) {
 
 hipError_t launch_rmsnorm(const RmsParams& p, hipStream_t s) {
   hipLaunchKernelGGL(rmsnorm_kernel, dim3((unsigned)((p.rows + 3) / 4)), dim3(256), 0, s, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_rmsnorm_parts(const RmsParams& p, const RmsParts& t, hipStream_t s) {
+  if (t.rows_part <= 0 || (p.rows + t.rows_part - 1) / t.rows_part > kMaxParts) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(rmsnorm_parts_kernel, dim3((unsigned)((p.rows + 3) / 4)), dim3(256), 0, s, p, t);
   return hipGetLastError();
 }
 

@@ -356,6 +356,10 @@ __device__ __forceinline__ void gemm_body(const GemmParams& p, const GemmParts* 
           } else {
             *(f32x4*)((float*)Cg + m * p.ldc + n) = v;
           }
+        } else if (PARTS && t->c_rows) {   // EPI_RESID_F32 into a part: the residual is the part itself
+          const int cb = (row0 + q * (BM / 2) + r0) / t->c_rows;
+          float* dst = (float*)t->c[cb] + (m - (int64_t)cb * t->c_rows) * p.ldc + n;
+          *(f32x4*)dst = *(const f32x4*)dst + v;
         } else {  // EPI_RESID_F32
           const f32x4 rv = *(const f32x4*)(p.resid + m * p.ldr + n);
           *(f32x4*)((float*)Cg + m * p.ldc + n) = rv + v;
@@ -417,6 +421,7 @@ hipError_t launch_gemm_bf16_parts(const GemmParams& p, const GemmParts& t, hipSt
     case EPI_BF16 * 2 + 0: return launch_parts<EPI_BF16, 0>(p, t, s);
     case EPI_BF16 * 2 + 1: return launch_parts<EPI_BF16, 1>(p, t, s);
     case EPI_F32 * 2 + 0: return launch_parts<EPI_F32, 0>(p, t, s);
+    case EPI_RESID_F32 * 2 + 0: return launch_parts<EPI_RESID_F32, 0>(p, t, s);
     default: return hipErrorInvalidValue;
   }
 }

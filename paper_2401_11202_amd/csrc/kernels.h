@@ -52,7 +52,8 @@ hipError_t launch_gemm_bf16(const GemmParams& p, hipStream_t s);
 //   b: B^T blocks, b[nb * b_nk + kb] = rows [nb b_nrows, +b_nrows) and
 //      K columns [kb b_kcols, +b_kcols) (b_nrows % 64 == 0, b_kcols % 64 ==
 //      0), each row-major with leading dim ldb.
-//   c: C row blocks of c_rows rows (c_rows % 16 == 0), leading dim ldc.
+//   c: C row blocks of c_rows rows (c_rows % 16 == 0), leading dim ldc; with
+//      EPI_RESID_F32 the residual is the part itself (C += result).
 constexpr int kMaxParts = 64;
 struct GemmParts {
   const uint16_t* a[kMaxParts];
@@ -162,6 +163,13 @@ struct RmsParams {
   float eps;
 };
 hipError_t launch_rmsnorm(const RmsParams& p, hipStream_t s);
+// RMSNorm over rows held in device-local arrays: rows [i rows_part, (i+1)
+// rows_part) of x are part x[i] (leading dim ldx); p.x is unused.
+struct RmsParts {
+  const float* x[kMaxParts];
+  int rows_part;
+};
+hipError_t launch_rmsnorm_parts(const RmsParams& p, const RmsParts& t, hipStream_t s);
 
 // out[c][r] = in[r][c] for a bf16 [rows, cols] matrix (rows, cols multiples
 // of 8; 64 x 64 tiles through LDS).

@@ -61,7 +61,7 @@ bool valid_dtype(int dt) { return dt == PARTIR_F32 || dt == PARTIR_BF16; }
 // Plans
 // ---------------------------------------------------------------------------
 enum LaunchKind { L_GEMM_BF16, L_GEMM_F32, L_REDUCE, L_ATTN, L_ATTN_COMBINE, L_RMS, L_TRANSPOSE, L_ACT_BWD, L_COLSUM,
-                  L_GEMM_BF16_PARTS, L_ATTN_BWD };
+                  L_GEMM_BF16_PARTS, L_ATTN_BWD, L_RMS_PARTS };
 
 struct Launch {
   LaunchKind kind;
@@ -76,6 +76,7 @@ struct Launch {
   ActBwdParams act{};
   ColSumParams cs{};
   std::shared_ptr<GemmParts> parts;   // L_GEMM_BF16_PARTS: the device-local arrays
+  std::shared_ptr<RmsParts> rms_parts;   // L_RMS_PARTS
   AttnBwdParams attn_bwd{};
 };
 
@@ -254,6 +255,7 @@ hipError_t run_one(const Launch& L, hipStream_t s) {
     case L_COLSUM: return launch_colsum(L.cs, s);
     case L_GEMM_BF16_PARTS: return launch_gemm_bf16_parts(L.gemm, *L.parts, s);
     case L_ATTN_BWD: return launch_attention_backward(L.attn_bwd, s);
+    case L_RMS_PARTS: return launch_rmsnorm_parts(L.rms, *L.rms_parts, s);
   }
   return hipErrorInvalidValue;
 }
@@ -519,6 +521,9 @@ int validate_attn(const AttnArgs& a, bool with_ptrs) {
   return PARTIR_OK;
 }
 
+void plan_attention_launch(char* qkvo, int64_t B, int64_t S, int64_t D, int64_t H, int64_t dh, int causal,
+                           float scale, int Rm, Plan& plan, float* lse);
+
 // QKV projection + attention core into (Q, K, V, O) inside the workspace.
 void plan_attention_core(const void* Xn, const void* Wq, const void* Wk, const void* Wv, char* qkvo,
                          int64_t B, int64_t S, int64_t D, int64_t H, int64_t dh, int causal, float scale,
@@ -528,7 +533,6 @@ void plan_attention_core(const void* Xn, const void* Wq, const void* Wk, const v
   void* Q = qkvo ? qkvo : nullptr;
   void* K = qkvo ? qkvo + one : nullptr;
   void* V = qkvo ? qkvo + 2 * one : nullptr;
-  void* O = qkvo ? qkvo + 3 * one : nullptr;
   GemmSpec g;
   g.A = Xn; g.B[0] = Wq; g.B[1] = Wk; g.B[2] = Wv; g.C[0] = Q; g.C[1] = K; g.C[2] = V;
   g.ngroups = 3;
@@ -538,6 +542,18 @@ void plan_attention_core(const void* Xn, const void* Wq, const void* Wk, const v
   g.name = "attn.qkv";
   g.label = "attn.qkv Q|K|V = slice 0 X[b] . slice 1 W{q,k,v}[m]";
   plan_gemm(g, nullptr, plan);
+  plan_attention_launch(qkvo, B, S, D, H, dh, causal, scale, Rm, plan, lse);
+}
+
+// The attention core over (Q, K, V) -> O at qkvo (four [T, D] blocks).
+void plan_attention_launch(char* qkvo, int64_t B, int64_t S, int64_t D, int64_t H, int64_t dh, int causal,
+                           float scale, int Rm, Plan& plan, float* lse) {
+  const int64_t T = B * S;
+  const size_t one = align_up((size_t)T * D * 2);
+  void* Q = qkvo ? qkvo : nullptr;
+  void* K = qkvo ? qkvo + one : nullptr;
+  void* V = qkvo ? qkvo + 2 * one : nullptr;
+  void* O = qkvo ? qkvo + 3 * one : nullptr;
   Launch L;
   L.kind = L_ATTN;
   L.name = "attn.core";
@@ -1338,6 +1354,197 @@ void plan_mlp_sharded(const MlpShardedArgs& a, void* ws, Plan& plan) {
   parted(g2, t2, "; W2 blocks read in place; each row block stored by its owner (fused reduce_scatter)");
 }
 }  // namespace
+
+// ---- decoder layer on device-local arrays (BP + MP + Z3, sequence-parallel norms) --
+namespace {
+struct DecShardedArgs {
+  void* const* x = nullptr;                 // [T/(RB RM), D] fp32 per device, updated in place
+  const void *g1 = nullptr, *g2 = nullptr;
+  float eps = 1e-6f;
+  const void* const* W[6] = {nullptr, nullptr, nullptr, nullptr, nullptr, nullptr};   // q, k, v, o, 1, 2
+  int64_t B = 0, S = 0, D = 0, H = 0, dh = 0, F = 0;
+  int Rb = 1, Rm = 1;
+};
+
+int validate_dec_sharded(const DecShardedArgs& a, bool with_ptrs) {
+  int st = validate_attn_shapes(a.B, a.S, a.D, a.H, a.dh, a.Rb, a.Rm);
+  if (st) return st;
+  const int nd = a.Rb * a.Rm;
+  const int64_t T = a.B * a.S;
+  if (nd > kMaxParts) return fail(PARTIR_E_UNSUPPORTED, "at most %d devices (R_batch * R_model)", kMaxParts);
+  if (a.F < 0 || a.F > (1 << 22)) return fail(PARTIR_E_SHAPE, "F out of range");
+  if (!(a.eps >= 0.0f)) return fail(PARTIR_E_SHAPE, "eps must be >= 0");
+  if (a.F % a.Rm) return fail(PARTIR_E_DIVISIBILITY, "R_model=%d does not divide F=%lld", a.Rm, (long long)a.F);
+  if (a.D % a.Rb) return fail(PARTIR_E_DIVISIBILITY, "R_batch=%d does not divide D=%lld", a.Rb, (long long)a.D);
+  if (T % nd) return fail(PARTIR_E_DIVISIBILITY, "R_batch*R_model=%d does not divide T=%lld", nd, (long long)T);
+  if ((T / nd) % 16 || (a.D / a.Rb) % 64 || (a.F / a.Rm) % 64)
+    return fail(PARTIR_E_LAYOUT, "T/(R_batch R_model) must be a multiple of 16 and D/R_batch, F/R_model of 64");
+  if (!with_ptrs || T == 0) return PARTIR_OK;
+  if (!a.x || !a.g1 || (a.F > 0 && !a.g2)) return fail(PARTIR_E_NULL, "x parts, g1 and g2 must be non-NULL");
+  if (!aligned16(a.g1) || !aligned16(a.g2)) return fail(PARTIR_E_LAYOUT, "g1, g2 must be 16-byte aligned");
+  for (int w = 0; w < 6; ++w) {
+    if (w >= 4 && a.F == 0) continue;
+    if (!a.W[w]) return fail(PARTIR_E_NULL, "weight part arrays must be non-NULL");
+  }
+  for (int i = 0; i < nd; ++i) {
+    if (!a.x[i]) return fail(PARTIR_E_NULL, "x part %d is NULL", i);
+    if (!aligned16(a.x[i])) return fail(PARTIR_E_LAYOUT, "x part %d is not 16-byte aligned", i);
+    for (int w = 0; w < 6; ++w) {
+      if (w >= 4 && a.F == 0) continue;
+      if (!a.W[w][i]) return fail(PARTIR_E_NULL, "weight part %d is NULL", i);
+      if (!aligned16(a.W[w][i])) return fail(PARTIR_E_LAYOUT, "weight part %d is not 16-byte aligned", i);
+    }
+  }
+  return PARTIR_OK;
+}
+
+// The decoder layer's lowered program on device-local arrays, per device
+// (b, m): the RMSNorms on the device's own tokens write into the gathered
+// activation buffer (the all_gather over M fused into the norm's store); the
+// projections read the Z3 weight parts in place (all_gathers over B); the
+// out-projection and FFN-down #sums over m are accumulated in the tile and
+// each row block is added into its owner's residual part (reduce_scatter
+// fused with the residual add).
+void plan_dec_sharded(const DecShardedArgs& a, void* ws, Plan& plan) {
+  const int nd = a.Rb * a.Rm;
+  const int64_t T = a.B * a.S, D = a.D, F = a.F, rows_dev = T / nd;
+  plan.n_shards = nd;
+  plan.n_tile_loops = (a.Rb > 1) + 2;
+  plan.flops = 8.0 * T * D * D + 4.0 * a.B * a.H * ((double)a.S * (a.S + 1) / 2) * a.dh + 4.0 * T * D * F;
+  if (T == 0) return;
+  char* base = (char*)ws;
+  const size_t xn_bytes = align_up((size_t)T * D * 2);
+  const size_t core = attn_core_bytes(T, D);
+  const size_t h_bytes = align_up((size_t)T * F * 2);
+  char* xn = base;
+  char* qkvo = base ? base + xn_bytes : nullptr;
+  char* Hf = base ? base + xn_bytes + core : nullptr;
+  plan.ws_bytes = xn_bytes + core + (F > 0 ? h_bytes : 0);
+  auto norms = [&](const void* g) {
+    // one launch over every device's tokens: each row is normalised where it
+    // lives and stored into the gathered buffer
+    plan_rmsnorm(nullptr, (const float*)g, xn, T, D, a.eps, a.Rb, plan);
+    Launch& L = plan.launches.back();
+    L.kind = L_RMS_PARTS;
+    RmsParts* t = new RmsParts{};
+    t->rows_part = (int)rows_dev;
+    for (int i = 0; i < nd; ++i) t->x[i] = a.x ? (const float*)a.x[i] : nullptr;
+    L.rms_parts.reset(t);
+    char buf[200];
+    snprintf(buf, sizeof buf, "rmsnorm: %d devices x %lld tokens x %lld, each device's own tokens (sequence-parallel), "
+             "stored into the gathered buffer (all_gather<M>)", nd, (long long)rows_dev, (long long)D);
+    L.text = buf;
+  };
+  // B part table of a column-parallel weight W^T [out, in]: part (b, m) holds
+  // rows block m, cols block b -> N block m, K block b
+  auto col_parts = [&](const void* const* W, int64_t n_out) {
+    GemmParts* t = new GemmParts{};
+    t->b_nrows = (int)(n_out / a.Rm); t->b_kcols = (int)(D / a.Rb); t->b_nk = a.Rb;
+    for (int b = 0; b < a.Rb; ++b)
+      for (int m = 0; m < a.Rm; ++m) t->b[m * a.Rb + b] = W ? (const uint16_t*)W[b * a.Rm + m] : nullptr;
+    return t;
+  };
+  // row-parallel weight W^T [D, in]: part (b, m) = rows block b, cols block m;
+  // the output rows go into the residual parts
+  auto row_parts = [&](const void* const* W, int64_t k_in) {
+    GemmParts* t = new GemmParts{};
+    t->b_nrows = (int)(D / a.Rb); t->b_kcols = (int)(k_in / a.Rm); t->b_nk = a.Rm;
+    t->c_rows = (int)rows_dev;
+    for (int i = 0; i < nd; ++i) {
+      t->b[i] = W ? (const uint16_t*)W[i] : nullptr;
+      t->c[i] = a.x ? a.x[i] : nullptr;
+    }
+    return t;
+  };
+  auto parted = [&](const GemmSpec& g, GemmParts* t, const char* how) {
+    plan_gemm(g, nullptr, plan);
+    Launch& L = plan.launches.back();
+    L.kind = L_GEMM_BF16_PARTS;
+    L.parts.reset(t);
+    L.text += how;
+  };
+  norms(a.g1);
+  const size_t one = align_up((size_t)T * D * 2);
+  const char* names[3] = {"attn.qkv", "attn.qkv", "attn.qkv"};
+  const char* labels[3] = {"attn.q   Q = xn[b] . all_gather<B>(Wq)[:, m]", "attn.k   K = xn[b] . all_gather<B>(Wk)[:, m]",
+                           "attn.v   V = xn[b] . all_gather<B>(Wv)[:, m]"};
+  for (int i = 0; i < 3; ++i) {
+    GemmSpec g;
+    g.A = xn; g.C[0] = qkvo ? qkvo + i * one : nullptr;
+    g.lda = D; g.ldb = D / a.Rb; g.ldc = D; g.M = T; g.N = D; g.K = D;
+    g.c_dtype = PARTIR_BF16; g.rm = a.Rb; g.rn = a.Rm;
+    g.name = names[i]; g.label = labels[i];
+    parted(g, col_parts(a.W[i], D), "; weight blocks read in place (fused all_gather)");
+  }
+  plan_attention_launch(qkvo, a.B, a.S, D, a.H, a.dh, 1, 0.0f, a.Rm, plan, nullptr);
+  GemmSpec go;
+  go.A = qkvo ? qkvo + 3 * one : nullptr; go.resid_add = true;
+  go.lda = D; go.ldb = D / a.Rm; go.ldc = D; go.M = T; go.N = D; go.K = D;
+  go.c_dtype = PARTIR_F32; go.rm = a.Rb; go.rk = a.Rm; go.sum_impl = PARTIR_SUM_FUSED;
+  go.name = "attn.out"; go.label = "dec.attn_out x_bm += reduce_scatter<M>(sum_m O[:, m] . all_gather<B>(Wo)[m])";
+  parted(go, row_parts(a.W[3], D), "; each row block added into its owner's residual part (fused reduce_scatter)");
+  plan.n_sum_loops = 1;
+  if (F == 0) return;   // an FFN of width 0 adds the empty sum: x is unchanged
+  norms(a.g2);
+  GemmSpec g1;
+  g1.A = xn; g1.C[0] = Hf;
+  g1.lda = D; g1.ldb = D / a.Rb; g1.ldc = F; g1.M = T; g1.N = F; g1.K = D;
+  g1.c_dtype = PARTIR_BF16; g1.rm = a.Rb; g1.rn = a.Rm; g1.act = 1;
+  g1.name = "mlp.up"; g1.label = "dec.ffn_up H = gelu(hn[b] . all_gather<B>(W1)[:, m])";
+  parted(g1, col_parts(a.W[4], F), "; weight blocks read in place (fused all_gather)");
+  GemmSpec g2;
+  g2.A = Hf; g2.resid_add = true;
+  g2.lda = F; g2.ldb = F / a.Rm; g2.ldc = D; g2.M = T; g2.N = D; g2.K = F;
+  g2.c_dtype = PARTIR_F32; g2.rm = a.Rb; g2.rk = a.Rm; g2.sum_impl = PARTIR_SUM_FUSED;
+  g2.name = "mlp.down"; g2.label = "dec.ffn_down x_bm += reduce_scatter<M>(sum_m H[:, m] . all_gather<B>(W2)[m])";
+  parted(g2, row_parts(a.W[5], F), "; each row block added into its owner's residual part (fused reduce_scatter)");
+  plan.n_sum_loops = 2;
+}
+}  // namespace
+
+size_t partir_decoder_layer_sharded_workspace(int64_t B, int64_t S, int64_t D, int64_t n_heads, int64_t d_head,
+                                              int64_t F, int R_batch, int R_model) {
+  DecShardedArgs a;
+  a.B = B; a.S = S; a.D = D; a.H = n_heads; a.dh = d_head; a.F = F; a.Rb = R_batch; a.Rm = R_model;
+  if (validate_dec_sharded(a, false) != PARTIR_OK) return (size_t)-1;
+  Plan plan;
+  plan_dec_sharded(a, nullptr, plan);
+  return plan.ws_bytes;
+}
+
+int partir_plan_decoder_layer_sharded(int64_t B, int64_t S, int64_t D, int64_t n_heads, int64_t d_head, int64_t F,
+                                      int R_batch, int R_model, partir_plan_info* info) {
+  DecShardedArgs a;
+  a.B = B; a.S = S; a.D = D; a.H = n_heads; a.dh = d_head; a.F = F; a.Rb = R_batch; a.Rm = R_model;
+  int st = validate_dec_sharded(a, false);
+  if (st) return st;
+  Plan plan;
+  plan_dec_sharded(a, nullptr, plan);
+  keep_plan_text(plan, "decoder_layer_sharded");
+  fill_info(plan, info);
+  return PARTIR_OK;
+}
+
+int partir_decoder_layer_sharded(void* const* x_parts, const void* g1, const void* g2, float eps,
+                                 const void* const* Wq_parts, const void* const* Wk_parts,
+                                 const void* const* Wv_parts, const void* const* Wo_parts,
+                                 const void* const* W1_parts, const void* const* W2_parts, int64_t B, int64_t S,
+                                 int64_t D, int64_t n_heads, int64_t d_head, int64_t F, int R_batch, int R_model,
+                                 void* ws, size_t ws_bytes, void* stream) {
+  DecShardedArgs a;
+  a.x = x_parts; a.g1 = g1; a.g2 = g2; a.eps = eps;
+  a.W[0] = Wq_parts; a.W[1] = Wk_parts; a.W[2] = Wv_parts; a.W[3] = Wo_parts; a.W[4] = W1_parts; a.W[5] = W2_parts;
+  a.B = B; a.S = S; a.D = D; a.H = n_heads; a.dh = d_head; a.F = F; a.Rb = R_batch; a.Rm = R_model;
+  int st = validate_dec_sharded(a, true);
+  if (st) return st;
+  Plan probe;
+  plan_dec_sharded(a, nullptr, probe);
+  if ((st = check_ws(probe, ws, ws_bytes))) return st;
+  Plan plan;
+  plan_dec_sharded(a, ws, plan);
+  keep_plan_text(plan, "decoder_layer_sharded");
+  return execute(plan, stream);
+}
 
 size_t partir_mlp_block_sharded_workspace(int64_t T, int64_t D, int64_t F, int R_batch, int R_model) {
   MlpShardedArgs a;

@@ -37,7 +37,8 @@ EXPORTS = ("partir_loop_matmul", "partir_loop_matmul_workspace", "partir_mlp_blo
            "partir_plan_mlp_block_sharded", "partir_attention_train", "partir_attention_backward",
            "partir_attention_backward_workspace", "partir_plan_attention_backward", "partir_attn_block_train",
            "partir_attn_block_saved_bytes", "partir_attn_block_backward", "partir_attn_block_backward_workspace",
-           "partir_plan_attn_block_backward")
+           "partir_plan_attn_block_backward", "partir_decoder_layer_sharded",
+           "partir_decoder_layer_sharded_workspace", "partir_plan_decoder_layer_sharded")
 
 
 class PartirError(RuntimeError):
@@ -103,6 +104,11 @@ def lib():
         "partir_mlp_block_sharded": (I32, [PP, PP, P, PP, P, PP, I64, I64, I64, I32, I32, I32, I32, P, SZ, P]),
         "partir_mlp_block_sharded_workspace": (SZ, [I64, I64, I64, I32, I32]),
         "partir_plan_mlp_block_sharded": (I32, [I64, I64, I64, I32, I32, I32, ctypes.POINTER(PlanInfo)]),
+        "partir_decoder_layer_sharded": (I32, [PP, P, P, F, PP, PP, PP, PP, PP, PP, I64, I64, I64, I64, I64, I64, I32,
+                                               I32, P, SZ, P]),
+        "partir_decoder_layer_sharded_workspace": (SZ, [I64, I64, I64, I64, I64, I64, I32, I32]),
+        "partir_plan_decoder_layer_sharded": (I32, [I64, I64, I64, I64, I64, I64, I32, I32,
+                                                    ctypes.POINTER(PlanInfo)]),
         "partir_attention_train": (I32, [P, P, P, P, P, I64, I64, I64, I64, I32, F, I32, P, SZ, P]),
         "partir_attention_backward": (I32, [P, P, P, P, P, P, P, P, P, I64, I64, I64, I64, I32, F, P, SZ, P]),
         "partir_attention_backward_workspace": (SZ, [I64, I64, I64, I64]),
@@ -319,6 +325,46 @@ def z3_device_arrays(X, W1t, W2t, R_batch: int, R_model: int):
     w1 = [W1t[m * fr:(m + 1) * fr, b * dr:(b + 1) * dr].contiguous() for b in range(R_batch) for m in range(R_model)]
     w2 = [W2t[b * dr:(b + 1) * dr, m * fr:(m + 1) * fr].contiguous() for b in range(R_batch) for m in range(R_model)]
     return xs, w1, w2
+
+
+def z3_decoder_arrays(x, W, R_batch: int, R_model: int):
+    """Device-local arrays of a decoder layer (each its own allocation): x
+    (fp32 [T, D]) by token blocks; W = {name: stored W^T} with Wq, Wk, Wv, W1
+    split as (rows block m, cols block b) and Wo, W2 as (rows block b, cols
+    block m), part p = b * R_model + m.  Returns (x_parts, {name: parts})."""
+    nd = R_batch * R_model
+    T = x.shape[0]
+    xs = [x[p * (T // nd):(p + 1) * (T // nd)].clone() for p in range(nd)]
+    parts = {}
+    for k, w in W.items():
+        rows, cols = w.shape
+        col_par = k in ("Wq", "Wk", "Wv", "W1")
+        rr, cc = (rows // R_model, cols // R_batch) if col_par else (rows // R_batch, cols // R_model)
+        out = []
+        for b in range(R_batch):
+            for m in range(R_model):
+                i, j = (m, b) if col_par else (b, m)
+                out.append(w[i * rr:(i + 1) * rr, j * cc:(j + 1) * cc].contiguous())
+        parts[k] = out
+    return xs, parts
+
+
+def decoder_layer_sharded(x_parts, g1, g2, W_parts, *, B: int, S: int, n_heads: int, d_head: int = 128,
+                          R_batch: int = 1, R_model: int = 1, eps: float = 1e-6, workspace=None, stream=None):
+    """One decoder layer on device-local arrays, x_parts updated in place
+    (see z3_decoder_arrays for the layout)."""
+    D = x_parts[0].shape[1]
+    F = W_parts["W1"][0].shape[0] * R_model
+    nbytes = lib().partir_decoder_layer_sharded_workspace(B, S, D, n_heads, d_head, F, R_batch, R_model)
+    ws, wsb = _workspace(nbytes, x_parts[0].device, workspace)
+    ws_ = [_ptr_array(W_parts[k]) for k in ("Wq", "Wk", "Wv", "Wo", "W1", "W2")]
+    _check(lib().partir_decoder_layer_sharded(_ptr_array(x_parts), _ptr(g1), _ptr(g2), eps, *ws_, B, S, D, n_heads,
+                                              d_head, F, R_batch, R_model, _ptr(ws), wsb, _stream(stream)))
+    return x_parts
+
+
+def plan_decoder_layer_sharded(B, S, D, n_heads, d_head=128, F=0, R_batch=1, R_model=1):
+    return _plan(lib().partir_plan_decoder_layer_sharded, B, S, D, n_heads, d_head, F, R_batch, R_model)
 
 
 def plan_mlp_block_sharded(T, D, F, act=ACT_GELU, R_batch=1, R_model=1):

@@ -25,6 +25,7 @@ from . import inputs as I
 class Workload:
     name: str
     kind: str                 # matmul | mlp | attn | decoder | attn_core | mlp_train | mlp_z3 | attn_train
+                              # | decoder_z3
     wid: int                  # seed id
     dims: Dict[str, int] = field(default_factory=dict)
     dtype: str = "bf16"
@@ -79,6 +80,10 @@ WORKLOADS = {
     # the MLP on device-local arrays under BP + MP + Z3 with the activations
     # also sharded over the model axis: mesh {B: 2, M: 4}, 8 devices
     "mlp_z3_sp": Workload("mlp_z3_sp", "mlp_z3", 9, dict(T=8192, D=4096, F=16384, R_batch=2, R_model=4)),
+    # the two-layer decoder on device-local arrays (BP + MP + Z3, the residual
+    # stream and its norms sharded over the model axis too)
+    "decoder_z3_sp": Workload("decoder_z3_sp", "decoder_z3", 5, dict(B=4, S=2048, D=5120, H=40, dh=128, F=13824,
+                                                                     L=2, R_batch=2, R_model=4)),
     # small twins: same structure and partition sizes, scaled down
     "mlp_megatron_small": _mlp("mlp_megatron_small", 12, 512, 256, 1024, 1, 8),
     "attn_block_small": _attn("attn_block_small", 13, 2, 256, 1024, 8, 128, 1, 8),
@@ -158,7 +163,7 @@ def attn_core_inputs(w: Workload):
 def make_inputs(w: Workload):
     return {"matmul": matmul_inputs, "mlp": mlp_inputs, "attn": attn_inputs,
             "decoder": decoder_inputs, "attn_core": attn_core_inputs, "mlp_train": mlp_train_inputs,
-            "mlp_z3": mlp_z3_inputs, "attn_train": attn_inputs}[w.kind](w)
+            "mlp_z3": mlp_z3_inputs, "attn_train": attn_inputs, "decoder_z3": decoder_inputs}[w.kind](w)
 
 
 # ---------------------------------------------------------------------------
@@ -178,7 +183,7 @@ def flops(w: Workload) -> float:
     if w.kind == "attn":
         T = w["B"] * w["S"]
         return 8.0 * T * w["D"] * w["D"] + attn_core_flops(w["B"], w["S"], w["H"], w["dh"])
-    if w.kind == "decoder":
+    if w.kind in ("decoder", "decoder_z3"):
         T = w["B"] * w["S"]
         per = 8.0 * T * w["D"] * w["D"] + attn_core_flops(w["B"], w["S"], w["H"], w["dh"]) \
             + 4.0 * T * w["D"] * w["F"]

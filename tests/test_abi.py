@@ -453,3 +453,38 @@ def test_attention_train_validation(monkeypatch):
     assert P.STATUS[st] == "PARTIR_E_NULL"
     st = L.partir_attention_train(DUMMY, DUMMY, DUMMY, DUMMY, DUMMY, 2, 2048, 8, 128, 1, 0.0, 1, DUMMY, 0, None)
     assert P.STATUS[st] == "PARTIR_E_HIP"
+
+
+# ---------------------------------------------------------------------------
+# decoder layer on device-local arrays (sequence-parallel norms)
+# ---------------------------------------------------------------------------
+def dec_sharded(B=2, S=256, D=1024, H=8, F=2048, Rb=2, Rm=4, part=DUMMY, g=DUMMY, ws_bytes=1 << 34):
+    nd = Rb * Rm
+    arr = (ctypes.c_void_p * nd)(*([part] * nd))
+    return P.lib().partir_decoder_layer_sharded(arr, g, g, 1e-6, arr, arr, arr, arr, arr, arr, B, S, D, H, 128, F,
+                                                Rb, Rm, DUMMY, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kwargs,status", [
+    (dict(part=NULL), "PARTIR_E_NULL"),
+    (dict(g=NULL), "PARTIR_E_NULL"),
+    (dict(part=DUMMY_ODD), "PARTIR_E_LAYOUT"),
+    (dict(F=2050), "PARTIR_E_DIVISIBILITY"),
+    (dict(Rb=4, B=2), "PARTIR_E_DIVISIBILITY"),      # batch shards hold whole sequences
+    (dict(F=1728), "PARTIR_E_LAYOUT"),               # F/R_model = 432 is not a multiple of 64
+    (dict(D=512, H=4, Rb=2, Rm=4, F=2048), "PARTIR_E_HIP"),
+    (dict(S=128, B=1, Rb=1, Rm=8, F=2048, D=1024), "PARTIR_E_HIP"),   # 16 tokens per device
+    (dict(ws_bytes=10), "PARTIR_E_WORKSPACE"),
+    (dict(), "PARTIR_E_HIP"),
+])
+def test_decoder_sharded_validation(kwargs, status):
+    assert P.STATUS[dec_sharded(**kwargs)] == status, P.lib().partir_last_error().decode()
+
+
+def test_decoder_sharded_plan():
+    p = P.plan_decoder_layer_sharded(4, 2048, 5120, 40, 128, 13824, R_batch=2, R_model=4)
+    t = p["text"]
+    assert p["n_sum_loops"] == 2 and p["n_sum_splitk"] == 0 and p["n_virtual_shards"] == 8
+    assert t.count("sequence-parallel") == 2 and t.count("fused reduce_scatter") == 2
+    assert t.count("fused all_gather") == 4
+    assert P.lib().partir_decoder_layer_sharded_workspace(4, 2048, 5120, 40, 128, 13824, 2, 4) == p["workspace_bytes"]
