@@ -25,6 +25,13 @@ COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
           "-Wall", "-Wno-unused-command-line-argument"]
 
 
+# Per-file code generation options.  The attention backward keeps two large
+# accumulator sets live at once; left to its heuristics the compiler parks
+# values in accumulation registers and copies them around every MFMA, so its
+# MFMAs are asked to use ordinary vector registers.
+EXTRA = {"attention_bwd.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=true"]}
+
+
 def hipcc() -> str:
     for cand in (os.environ.get("HIPCC"), shutil.which("hipcc"), "/opt/rocm/bin/hipcc"):
         if cand and os.path.exists(cand):
@@ -34,7 +41,7 @@ def hipcc() -> str:
 
 def _compile(src: str, verbose: bool) -> str:
     obj = os.path.join(OUT_DIR, os.path.basename(src) + ".o")
-    cmd = [hipcc(), *COMMON, "-c", src, "-o", obj]
+    cmd = [hipcc(), *COMMON, *EXTRA.get(os.path.basename(src), []), "-c", src, "-o", obj]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)

@@ -51,41 +51,44 @@ __device__ __forceinline__ int toff(int row, int colb) {
   return row * TP + ((((colb >> 4) ^ (row & 15))) << 4) + (colb & 15);
 }
 
-// Streams two [64 x 128] bf16 tiles (rows `row0..` of X and Y, head columns)
-// through registers into a swizzled LDS stage; 4 + 4 chunks per thread.
-struct TilePair {
+typedef __attribute__((address_space(3))) void lds_void;
+// s_waitcnt with only the vector-memory counter constrained (gfx9 encoding)
+#define WAIT_VMCNT(n) __builtin_amdgcn_s_waitcnt((((n) & 15) | (((n) >> 4) << 14)) | (0x7 << 4) | (0xF << 8))
+
+// Streams two [64 x 128] bf16 tiles (rows of X and Y, head columns) into a
+// swizzled LDS stage with buffer loads that write LDS directly: load j of
+// wave w fills tile rows 16 j + 4 w .. +4 (1 KiB, lane L at byte 16 L), so
+// lane L reads the global chunk that belongs at its LDS position,
+// (L % 16) ^ (row & 15), which does not depend on j (the row step enters as
+// a scalar offset).
+struct TileDma {
   __amdgpu_buffer_rsrc_t rx, ry;
-  uint32_t ox[4], oy[4];
-  uint32_t stepx, stepy;
-  i32x4 bx[4], by[4];
-  int lr, lc;
+  uint32_t vx, vy;           // per-lane byte offsets of load 0
+  uint32_t stepx, stepy;     // bytes per 64-row tile
+  uint32_t jx, jy;           // bytes per 16 rows
+  int w;
   __device__ void init(const uint16_t* X, int64_t ldx, const uint16_t* Y, int64_t ldy, int S, int tid) {
-    lr = tid >> 4;
-    lc = tid & 15;
+    w = tid >> 6;
+    const int lane = tid & 63;
+    const int row = 4 * w + (lane >> 4);
+    const int chunk = (lane & 15) ^ (row & 15);
     rx = make_rsrc(X, (uint32_t)((S - 1) * ldx * 2 + DH * 2));
     ry = make_rsrc(Y, (uint32_t)((S - 1) * ldy * 2 + DH * 2));
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      ox[i] = (uint32_t)((lr + 16 * i) * ldx * 2 + lc * 16);
-      oy[i] = (uint32_t)((lr + 16 * i) * ldy * 2 + lc * 16);
-    }
+    vx = (uint32_t)(row * ldx * 2 + chunk * 16);
+    vy = (uint32_t)(row * ldy * 2 + chunk * 16);
     stepx = (uint32_t)(TR * ldx * 2);
     stepy = (uint32_t)(TR * ldy * 2);
+    jx = (uint32_t)(16 * ldx * 2);
+    jy = (uint32_t)(16 * ldy * 2);
   }
-  __device__ void load(int blk) {
-    const uint32_t sx = (uint32_t)blk * stepx, sy = (uint32_t)blk * stepy;
+  // tile `blk` into the LDS tiles tx, ty (8 loads per wave in flight after)
+  __device__ void load(int blk, char* tx, char* ty) const {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      bx[i] = __builtin_bit_cast(i32x4, __builtin_amdgcn_raw_buffer_load_b128(rx, ox[i], sx, 0));
-      by[i] = __builtin_bit_cast(i32x4, __builtin_amdgcn_raw_buffer_load_b128(ry, oy[i], sy, 0));
-    }
-  }
-  __device__ void store(char* tx, char* ty) const {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int r = lr + 16 * i;
-      *(i32x4*)(tx + toff(r, lc * 16)) = bx[i];
-      *(i32x4*)(ty + toff(r, lc * 16)) = by[i];
+    for (int j = 0; j < 4; ++j) {
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (lds_void*)(tx + j * 4096 + w * 1024), 16, vx,
+                                               (uint32_t)blk * stepx + j * jx, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(ry, (lds_void*)(ty + j * 4096 + w * 1024), 16, vy,
+                                               (uint32_t)blk * stepy + j * jy, 0, 0);
     }
   }
 };
@@ -150,7 +153,7 @@ void attention_bwd_dq_kernel(AttnBwdParams p) {
   const float lse = p.lse[tq * p.H + head];
   if (h == 0) p.Dstat[tq * p.H + head] = Dq;
 
-  TilePair kv;
+  TileDma kv;
   kv.init(p.K + tok0 * p.ldk + head * DH, p.ldk, p.V + tok0 * p.ldv + head * DH, p.ldv, p.S, tid);
 
   const int j16 = lane & 15, G = lane >> 4, hh = G >> 1;
@@ -164,12 +167,13 @@ void attention_bwd_dq_kernel(AttnBwdParams p) {
   const int nkb = p.causal ? (q0 + 128) / TR : p.S / TR;
   const int wave_last_q = q0 + 32 * w + 31;
   const float c = p.scale_log2;
-  kv.load(0);
-  kv.store(smem, smem + TILE);
+  kv.load(0, smem, smem + TILE);
+  WAIT_VMCNT(0);
   __syncthreads();
   for (int kb = 0; kb < nkb; ++kb) {
     const int cur = kb & 1;
-    if (kb + 1 < nkb) kv.load(kb + 1);
+    // the other stage was last read in the previous iteration, before its barrier
+    if (kb + 1 < nkb) kv.load(kb + 1, smem + (cur ^ 1) * 2 * TILE, smem + (cur ^ 1) * 2 * TILE + TILE);
     const int k0 = kb * TR;
     if (!p.causal || k0 <= wave_last_q) {
       const char* ks = smem + cur * 2 * TILE;
@@ -201,7 +205,7 @@ void attention_bwd_dq_kernel(AttnBwdParams p) {
         for (int d = 0; d < 4; ++d)
           dq[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_frag(ks, u, d, v_row, v_colb), dsf[u], dq[d], 0, 0, 0);
     }
-    if (kb + 1 < nkb) kv.store(smem + (cur ^ 1) * 2 * TILE, smem + (cur ^ 1) * 2 * TILE + TILE);
+    WAIT_VMCNT(0);
     __syncthreads();
   }
 
@@ -248,7 +252,7 @@ void attention_bwd_dkv_kernel(AttnBwdParams p) {
     }
   }
 
-  TilePair qg;
+  TileDma qg;
   qg.init(p.Q + tok0 * p.ldq + head * DH, p.ldq, p.dO + tok0 * p.ldg + head * DH, p.ldg, p.S, tid);
   float st_l = 0.0f, st_d = 0.0f;
   auto sload = [&](int blk) {
@@ -280,15 +284,15 @@ void attention_bwd_dkv_kernel(AttnBwdParams p) {
   const int nqb = p.S / TR;
   const int wave_first_k = k0 + 32 * w;
   const float c = p.scale_log2;
-  qg.load(qb_begin);
+  qg.load(qb_begin, smem, smem + TILE);
   sload(qb_begin);
-  qg.store(smem, smem + TILE);
   sstore(0);
+  WAIT_VMCNT(0);
   __syncthreads();
   for (int qb = qb_begin; qb < nqb; ++qb) {
     const int cur = (qb - qb_begin) & 1;
     if (qb + 1 < nqb) {
-      qg.load(qb + 1);
+      qg.load(qb + 1, smem + (cur ^ 1) * 2 * TILE, smem + (cur ^ 1) * 2 * TILE + TILE);
       sload(qb + 1);
     }
     const int q0 = qb * TR;
@@ -329,10 +333,8 @@ void attention_bwd_dkv_kernel(AttnBwdParams p) {
         }
       }
     }
-    if (qb + 1 < nqb) {
-      qg.store(smem + (cur ^ 1) * 2 * TILE, smem + (cur ^ 1) * 2 * TILE + TILE);
-      sstore(cur ^ 1);
-    }
+    if (qb + 1 < nqb) sstore(cur ^ 1);
+    WAIT_VMCNT(0);
     __syncthreads();
   }
 
