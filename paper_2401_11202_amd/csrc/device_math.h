@@ -20,6 +20,18 @@ __device__ __forceinline__ float gelu_erf(float x) {
   return 0.5f * x * (x >= 0.0f ? 2.0f - q : q);
 }
 
+// Phi(x) = (1 + erf(x / sqrt2)) / 2 from the same erfc approximation.
+__device__ __forceinline__ float phi_cdf(float x) {
+  const float z = __builtin_fabsf(x) * 0.70710678118654752f;
+  const float t = __builtin_amdgcn_rcpf(__builtin_fmaf(0.3275911f, z, 1.0f));
+  float q = __builtin_fmaf(t, 1.061405429f, -1.453152027f);
+  q = __builtin_fmaf(t, q, 1.421413741f);
+  q = __builtin_fmaf(t, q, -0.284496736f);
+  q = __builtin_fmaf(t, q, 0.254829592f);
+  q *= t * __builtin_amdgcn_exp2f(-z * z * 1.4426950408889634f);   // erfc(z)
+  return x >= 0.0f ? 1.0f - 0.5f * q : 0.5f * q;
+}
+
 // GELU and its derivative together: gelu'(x) = Phi(x) + x phi(x), with
 // phi(x) = exp(-x^2 / 2) / sqrt(2 pi) sharing the exponential of the erfc
 // approximation above (z = |x| / sqrt2, so exp(-z^2) = exp(-x^2 / 2)).

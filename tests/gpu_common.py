@@ -15,7 +15,7 @@ from paper_2401_11202_amd import inputs as I
 TOL_F32 = 1e-4
 TOL_BF16 = 2e-2
 # Chained products (backward passes) round several bf16 intermediates
-# (2^-9 relative each); the error normalised by the whole gradient's size,
+# (2^-8 relative each); the error normalised by the whole gradient's size,
 # ||got - ref||_F / ||ref||_F, must stay at the level of a few such roundings.
 # This catches a wrong factor that the elementwise |A|.|B| normaliser, loose
 # by ~sqrt(K) per contraction, would let through.

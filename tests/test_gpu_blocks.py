@@ -65,6 +65,30 @@ def test_mlp_small_with_biases():
     assert np.max(np.abs(host(Y) - host(Y0) - b2.f64())) < 1e-5
 
 
+def test_gelu_epilogue_values_across_the_range():
+    """Y = gelu(X I) I with identity weights stores bf16(GELU(x)) for every
+    bf16 value x with 2^-10 <= |x| < 8 (and 0, +-40): within the bf16 unit
+    roundoff (2^-8 relative) of the exact GELU plus the epilogue's documented
+    5.4e-7 |x|."""
+    bits = np.arange(0x3A80, 0x4100, dtype=np.uint32)          # 2^-10 .. just below 8
+    pos = (bits << 16).view(np.float32).astype(np.float64)
+    xs = np.concatenate([pos, -pos, [0.0, 40.0, -40.0]])
+    D = 256
+    rows = -(-len(xs) // D)
+    X = np.zeros(rows * D, np.float32)
+    X[:len(xs)] = xs
+    X = X.reshape(rows, D)
+    Xd = torch.from_numpy(X).to(torch.bfloat16).cuda()
+    assert np.array_equal(Xd.float().cpu().numpy(), X)      # every value exact in bf16
+    eye = torch.eye(D, dtype=torch.bfloat16, device="cuda")
+    Y = P.mlp_block(Xd, eye, eye, R_batch=1, R_model=1, act="gelu", out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    got = host(Y).reshape(-1)[:len(xs)]
+    ref = O.gelu_erf(xs)
+    bound = 2.0 ** -8 * np.abs(ref) + 1e-6 * np.abs(xs) + 1e-30   # bf16 unit roundoff 2^-8
+    assert np.all(np.abs(got - ref) <= bound), float(np.max(np.abs(got - ref) / bound))
+
+
 @pytest.mark.parametrize("Rb,Rm", [(1, 1), (1, 8), (4, 8), (2, 2)])
 def test_mlp_integer_exact(Rb, Rm):
     """act = none with entries in {-1, 0, 1}: H is an integer of magnitude <= D
