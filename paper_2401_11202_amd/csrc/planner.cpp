@@ -418,20 +418,28 @@ class Planner {
       const auto u2 = users(ops[g].out);
       if (u2.size() != 1 || ops[u2[0]].kind != "matmul" || ops[u2[0]].in[0] != ops[g].out) continue;
       const int o2 = u2[0];
-      int rb = 1, rm = 1;
+      int rb = 1, rm = 1, ab = -1, am = -1;
       bool ok = true;
       for (size_t a = 0; a < axes.size() && ok; ++a) {
         const int l1 = loop[o][a], lg = loop[g][a], l2 = loop[o2][a];
         if (l1 == NONE && lg == NONE && l2 == NONE) continue;
-        if (l1 == 0 && lg == 0 && l2 == 0 && rb == 1) rb = axes[a].size;
-        else if (l1 == 1 && lg == 1 && l2 == SUM && rm == 1) rm = axes[a].size;
+        if (l1 == 0 && lg == 0 && l2 == 0 && rb == 1) rb = axes[a].size, ab = (int)a;
+        else if (l1 == 1 && lg == 1 && l2 == SUM && rm == 1) rm = axes[a].size, am = (int)a;
         else ok = false;
       }
       if (!ok) continue;
       used[o] = used[g] = used[o2] = true;
-      out.push_back("call partir_mlp_block " + values[ops[o2].out].name + " R_batch=" + std::to_string(rb) +
-                    " R_model=" + std::to_string(rm) + " ops=" + values[ops[o].out].name + "," +
-                    values[ops[g].out].name + "," + values[ops[o2].out].name);
+      // BP + MP + Z3 with the activations sharded over the model axis: the
+      // weights tiled over the batch axis (w1 dim 0, w2 dim 1) and x tiled
+      // over the model axis on dim 0 are all used whole (all_gathers) -> the
+      // entry point on device-local arrays
+      const int x = ops[o].in[0], w1 = ops[o].in[1], w2 = ops[o2].in[1];
+      const bool z3 = ab >= 0 && am >= 0 && vtile[w1][ab] == 0 && vtile[w2][ab] == 1;
+      const bool sp = am >= 0 && vtile[x][am] == 0;
+      out.push_back(std::string(z3 && sp ? "call partir_mlp_block_sharded " : "call partir_mlp_block ") +
+                    values[ops[o2].out].name + " R_batch=" + std::to_string(rb) + " R_model=" + std::to_string(rm) +
+                    " ops=" + values[ops[o].out].name + "," + values[ops[g].out].name + "," +
+                    values[ops[o2].out].name);
     }
     // a single partitioned matmul: at most one #tile and one #sum loop of one size
     for (size_t o = 0; o < ops.size(); ++o) {

@@ -204,6 +204,19 @@ def test_megatron_mlp_is_emitted_as_one_block_call():
     assert P.propagate(MLP, [("B", {"x": 0})])["calls"] == ["partir_mlp_block y R_batch=4 R_model=1 ops=h,g,y"]
 
 
+def test_fully_sharded_mlp_with_sharded_activations_names_the_device_local_entry_point():
+    """BP, MP, Z3 (Sec. 3: w1 dim 0 and w2 dim 1 on the batch axis) and x
+    tiled on dim 0 over the model axis too: the weights and x are used whole
+    (all_gathers), so the nest runs on device-local arrays."""
+    sched = [("B", {"x": 0}), ("M", {"w1": 1}), ("B", {"w1": 0, "w2": 1}), ("M", {"x": 0})]
+    r = P.propagate(MLP, sched)
+    assert r["loops"]["y"] == [("B", "tile0"), ("M", "sum")]
+    assert ("h", "w1", "B") in r["gathers"] and ("y", "w2", "B") in r["gathers"] and ("h", "x", "M") in r["gathers"]
+    assert r["calls"] == ["partir_mlp_block_sharded y R_batch=4 R_model=8 ops=h,g,y"]
+    # Z3 alone keeps the activations replicated over M: the plain block call
+    assert P.propagate(MLP, sched[:3])["calls"] == ["partir_mlp_block y R_batch=4 R_model=8 ops=h,g,y"]
+
+
 def test_single_matmul_calls():
     prog = "mesh K=4 N=4\narg a 256x512\narg b 512x256\nc = matmul a b\nret c"
     assert P.propagate(prog, [("K", {"b": 0})])["calls"] == ["partir_loop_matmul c tile=none sum=K R=4"]
