@@ -63,6 +63,21 @@ def test_backward_small_full_output(act, Rb, Rm):
     check(got, ref, norm)
 
 
+@pytest.mark.parametrize("Rb,Rm", [(1, 2), (5, 2)])
+def test_backward_ragged_shapes(Rb, Rm):
+    """Tiles and transposes with ragged edges: T = 520, D = 200, F = 336
+    (no dim a multiple of 64; the GEMM tiles are 256 wide)."""
+    T, D, F = 520, 200, 336
+    x = {"X": I.gaussian(115, 0, (T, D), 1.0), "W1": I.gaussian(115, 1, (D, F), D ** -0.5),
+         "W2": I.gaussian(115, 2, (F, D), F ** -0.5), "dY": I.gaussian(115, 3, (T, D), 1.0),
+         "b1": I.gaussian(115, 4, (F,), 0.5, "f32")}
+    say(f"mlp backward ragged T={T} D={D} F={F} R_batch={Rb} R_model={Rm}")
+    got = run(x, Rb, Rm, keep_z=True)
+    ref, norm = O.mlp_block_backward(x["X"].f64(), x["W1"].f64(), x["W2"].f64(), x["dY"].f64(), x["b1"].f64(),
+                                     "gelu", Rb, Rm, return_norm=True)
+    check(got, ref, norm)
+
+
 def test_backward_without_bias():
     w = W.WORKLOADS["mlp_train_small"]
     x = W.make_inputs(w)
