@@ -189,7 +189,7 @@ def setup(w, P, I):
                 P.decoder_layer_sharded(xs, l["g1"], l["g2"], l["parts"], B=B, S=S, n_heads=H, d_head=w["dh"],
                                         R_batch=Rb, R_model=Rm, workspace=ws)
         L = w["L"]
-        roles = {"attn.qkv": 2.0 * T * D * D, "attn.out": 2.0 * T * D * D,
+        roles = {"attn.qkv": 6.0 * T * D * D, "attn.out": 2.0 * T * D * D,
                  "attn.core": W.attn_core_flops(B, S, H, w["dh"]),
                  "mlp.up": 2.0 * T * D * F, "mlp.down": 2.0 * T * D * F}
         return x, step, roles, "mfma_bf16"

@@ -74,7 +74,9 @@ __device__ __forceinline__ int swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
 
 // PARTS: operands in device-local arrays (`t`, a kernel argument); else the
 // plain pointers of `p` and t is unused.
-template <int EPI, int ACT, int PARTS>
+// FIX: the fixup launch of a tail-split GEMM (no K loop: the accumulators are
+// the sum of the stored parts).
+template <int EPI, int ACT, int PARTS, int FIX>
 __device__ __forceinline__ void gemm_body(const GemmParams& p, const GemmParts* tb) {
   constexpr int OPB = BM * BK * 2, STAGE = 2 * OPB, KK = BK / 16, RB = 1024 / (BK * 2) /* rows per 1 KiB */;
   constexpr int CPR = BK / 8;   // 16-byte chunks per row
@@ -91,9 +93,28 @@ __device__ __forceinline__ void gemm_body(const GemmParams& p, const GemmParts* 
   const int ntiles = p.tiles_m * p.tiles_n;
   int bid = blockIdx.x;
   const int nwg = gridDim.x;
-  // Workgroups go round-robin to the 8 XCDs; give each XCD a contiguous run
-  // of the tile order so neighbouring tiles share that XCD's L2.
-  if ((nwg & 7) == 0) bid = (bid & 7) * (nwg >> 3) + (bid >> 3);
+  int tail_unit = -1, tail_part = 0;   // K part of a tail tile
+  if (FIX) {
+    bid = p.tail_base + blockIdx.x;
+  } else if (p.tail_parts > 1) {
+    // XCD x (workgroups go round-robin to the 8 XCDs, in launch order) takes
+    // a contiguous run of the whole tiles, then a contiguous run of the tail
+    // parts, so every XCD gets the same share of both and the parts run last
+    const int nf = p.tail_base, nu = nwg - nf;
+    if (((nf | nu) & 7) == 0) {
+      const int x = bid & 7, i = bid >> 3;
+      bid = (i < (nf >> 3)) ? x * (nf >> 3) + i : nf + x * (nu >> 3) + (i - (nf >> 3));
+    }
+    if (bid >= nf) {
+      tail_unit = bid - nf;
+      tail_part = tail_unit % p.tail_parts;
+      bid = nf + tail_unit / p.tail_parts;
+    }
+  } else if ((nwg & 7) == 0) {
+    // Give each XCD a contiguous run of the tile order so neighbouring tiles
+    // share that XCD's L2.
+    bid = (bid & 7) * (nwg >> 3) + (bid >> 3);
+  }
   const int split = bid / ntiles;
   const int tix = bid - split * ntiles;
   const int per_group = p.group_m * p.tiles_n;
@@ -112,8 +133,12 @@ __device__ __forceinline__ void gemm_body(const GemmParams& p, const GemmParts* 
   const int sn = rem / p.tpn, tni = rem - sn * p.tpn;
   const int col0 = sn * p.ns + tni * BN;
   const int cols = min(BN, p.ns - tni * BN);
-  const int k_begin = (p.nsplit > 1) ? split * p.ks : 0;
-  const int k_end = (p.nsplit > 1) ? k_begin + p.ks : p.K;
+  int k_begin = (p.nsplit > 1) ? split * p.ks : 0;
+  int k_end = (p.nsplit > 1) ? k_begin + p.ks : p.K;
+  if (tail_unit >= 0) {
+    k_begin = tail_part * p.tail_kt * BK;
+    k_end = min(p.K, k_begin + p.tail_kt * BK);
+  }
 
   if (PHI_TAB) {   // Phi table (read after the main loop's barriers)
     float2* tab = (float2*)(smem + MAIN);
@@ -141,10 +166,11 @@ __device__ __forceinline__ void gemm_body(const GemmParams& p, const GemmParts* 
   // with no valid rows takes any part's address, its descriptor reads nothing)
   auto b_block = [&](int j, int kp) -> const uint16_t* {
     if (PARTS && t->b_nrows) {
-      if (cols - BLK * j <= 0) return t->b[kp];
+      const int gb = grp * t->b_gstride;
+      if (cols - BLK * j <= 0) return t->b[gb + kp];
       const int n = col0 + BLK * j;
       const int nb = n / t->b_nrows;
-      return t->b[nb * t->b_nk + kp] + (int64_t)(n - nb * t->b_nrows) * p.ldb;
+      return t->b[gb + nb * t->b_nk + kp] + (int64_t)(n - nb * t->b_nrows) * p.ldb;
     }
     return Btile + (int64_t)BLK * j * p.ldb;
   };
@@ -176,14 +202,17 @@ __device__ __forceinline__ void gemm_body(const GemmParams& p, const GemmParts* 
     const uint32_t so = (uint32_t)kb * 2;   // A (and unparted B): K offset in bytes
     uint32_t so_b = so;
     if (PARTS && t->b_nrows) {
-      // the all_gather of B along K: K tiles never straddle a part
+      // the all_gather of B along K: K tiles never straddle a part (a tail
+      // part may start several parts in)
       if (kb >= b_kend && b_kpart + 1 < t->b_nk) {
-        const int kp = ++b_kpart;
-        b_kend += t->b_kcols;
+        while (kb >= b_kend && b_kpart + 1 < t->b_nk) {
+          ++b_kpart;
+          b_kend += t->b_kcols;
+        }
 #pragma unroll
         for (int j = 0; j < NJ; ++j) {
           const int vb = min(max(cols - BLK * j, 0), BLK);
-          rb[j] = make_rsrc(b_block(j, kp), (uint32_t)(vb * p.ldb * 2));
+          rb[j] = make_rsrc(b_block(j, b_kpart), (uint32_t)(vb * p.ldb * 2));
         }
       }
       so_b = (uint32_t)(kb - (b_kend - t->b_kcols)) * 2;
@@ -238,6 +267,7 @@ __device__ __forceinline__ void gemm_body(const GemmParams& p, const GemmParts* 
   // MFMAs run; then (tile kt+1 landed, every wave done with this stage) the
   // stage is refilled with tile kt+2 and the next tile's first fragments are
   // read during the last step.
+  if constexpr (!FIX) {
 #pragma unroll
   for (int s = 0; s < NS; ++s) gload(s, s);
   WAIT_VMCNT(LPS * (NS - 1));
@@ -268,7 +298,39 @@ __device__ __forceinline__ void gemm_body(const GemmParams& p, const GemmParts* 
   int stage = 0, kt = 0;
   for (; kt + NS < nk; ++kt) stage = tile(kt, stage, true);
   for (; kt < nk; ++kt) stage = tile(kt, stage, false);
+  }
 #undef SGB
+
+  // ---- tail parts ----------------------------------------------------------------
+  // Accumulator register r (= 16 (2 i + j) + 4 g + e) of thread tid is float
+  // 4 (r/4 * NT + tid) + e of a part: float4 stores of consecutive threads.
+  if constexpr (FIX) {
+    const float* src = p.tail_ws + (size_t)blockIdx.x * p.tail_parts * (NT * 128);
+    for (int q = 0; q < p.tail_parts; ++q) {   // ascending K
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            const f32x4 v = *(const f32x4*)(src + (size_t)q * (NT * 128) + (((i * 2 + j) * 4 + g) * NT + tid) * 4);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) acc[i][j][4 * g + e] = q ? acc[i][j][4 * g + e] + v[e] : v[e];
+          }
+    }
+  } else if (tail_unit >= 0) {
+    float* dst = p.tail_ws + (size_t)tail_unit * (NT * 128);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const f32x4 v = {acc[i][j][4 * g + 0], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]};
+          *(f32x4*)(dst + (((i * 2 + j) * 4 + g) * NT + tid) * 4) = v;
+        }
+    return;
+  }
 
   // ---- epilogue ----------------------------------------------------------------
   // Lane holds C[m][n..n+3] for each (i, j, g): 16-byte pieces of 32 rows per
@@ -400,24 +462,94 @@ __device__ __forceinline__ void gemm_body(const GemmParams& p, const GemmParts* 
 
 template <int EPI, int ACT>
 __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2)))
-void gemm_bf16_kernel(GemmParams p) { gemm_body<EPI, ACT, 0>(p, nullptr); }
+void gemm_bf16_kernel(GemmParams p) { gemm_body<EPI, ACT, 0, 0>(p, nullptr); }
 
 template <int EPI, int ACT>
 __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2)))
-void gemm_bf16_parts_kernel(GemmParams p, GemmParts t) { gemm_body<EPI, ACT, 1>(p, &t); }
+void gemm_bf16_parts_kernel(GemmParams p, GemmParts t) { gemm_body<EPI, ACT, 1, 0>(p, &t); }
 
 template <int EPI, int ACT>
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void gemm_bf16_fixup_kernel(GemmParams p) { gemm_body<EPI, ACT, 0, 1>(p, nullptr); }
+
+template <int EPI, int ACT>
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void gemm_bf16_parts_fixup_kernel(GemmParams p, GemmParts t) { gemm_body<EPI, ACT, 1, 1>(p, &t); }
+
+// Workgroups of the main launch: every tile once, or the whole tiles plus
+// tail_parts per tail tile.
+int64_t main_grid(const GemmParams& p) {
+  const int64_t ntiles = (int64_t)p.tiles_m * p.tiles_n;
+  if (p.tail_parts > 1) return p.tail_base + (ntiles - p.tail_base) * p.tail_parts;
+  return ntiles * p.nsplit;
+}
+
+// The tail split's invariants: whole-K accumulation otherwise, every part at
+// least one K tile, a workspace to hold the parts.
+bool tail_ok(const GemmParams& p) {
+  const int64_t ntiles = (int64_t)p.tiles_m * p.tiles_n;
+  const int64_t nk = (p.K + BK - 1) / BK;
+  return p.nsplit == 1 && p.tail_ws && p.tail_base >= 0 && p.tail_base < ntiles && p.tail_kt > 0 &&
+         (int64_t)(p.tail_parts - 1) * p.tail_kt < nk;
+}
+
+template <int EPI, int ACT, int FIX>
 hipError_t launch(const GemmParams& p, hipStream_t s) {
-  const int64_t nwg = (int64_t)p.tiles_m * p.tiles_n * p.nsplit;
-  hipLaunchKernelGGL((gemm_bf16_kernel<EPI, ACT>), dim3((unsigned)nwg), dim3(NT), 0, s, p);
+  if (p.tail_parts > 1 && !tail_ok(p)) return hipErrorInvalidValue;
+  if (FIX) {
+    if (p.tail_parts <= 1) return hipErrorInvalidValue;
+    const int64_t nwg = (int64_t)p.tiles_m * p.tiles_n - p.tail_base;
+    hipLaunchKernelGGL((gemm_bf16_fixup_kernel<EPI, ACT>), dim3((unsigned)nwg), dim3(NT), 0, s, p);
+  } else {
+    hipLaunchKernelGGL((gemm_bf16_kernel<EPI, ACT>), dim3((unsigned)main_grid(p)), dim3(NT), 0, s, p);
+  }
   return hipGetLastError();
 }
 
-template <int EPI, int ACT>
+template <int EPI, int ACT, int FIX>
 hipError_t launch_parts(const GemmParams& p, const GemmParts& t, hipStream_t s) {
-  const int64_t nwg = (int64_t)p.tiles_m * p.tiles_n * p.nsplit;
-  hipLaunchKernelGGL((gemm_bf16_parts_kernel<EPI, ACT>), dim3((unsigned)nwg), dim3(NT), 0, s, p, t);
+  if (p.tail_parts > 1 && !tail_ok(p)) return hipErrorInvalidValue;
+  if (FIX) {
+    if (p.tail_parts <= 1) return hipErrorInvalidValue;
+    const int64_t nwg = (int64_t)p.tiles_m * p.tiles_n - p.tail_base;
+    hipLaunchKernelGGL((gemm_bf16_parts_fixup_kernel<EPI, ACT>), dim3((unsigned)nwg), dim3(NT), 0, s, p, t);
+  } else {
+    hipLaunchKernelGGL((gemm_bf16_parts_kernel<EPI, ACT>), dim3((unsigned)main_grid(p)), dim3(NT), 0, s, p, t);
+  }
   return hipGetLastError();
+}
+
+template <int FIX>
+hipError_t dispatch(const GemmParams& p, hipStream_t s) {
+  switch (p.epi * 2 + (p.act ? 1 : 0)) {
+    case EPI_BF16 * 2 + 0: return launch<EPI_BF16, 0, FIX>(p, s);
+    case EPI_BF16 * 2 + 1: return launch<EPI_BF16, 1, FIX>(p, s);
+    case EPI_F32 * 2 + 0: return launch<EPI_F32, 0, FIX>(p, s);
+    case EPI_F32 * 2 + 1: return launch<EPI_F32, 1, FIX>(p, s);
+    case EPI_PARTIAL * 2 + 0: return FIX ? hipErrorInvalidValue : launch<EPI_PARTIAL, 0, 0>(p, s);
+    case EPI_RESID_F32 * 2 + 0: return launch<EPI_RESID_F32, 0, FIX>(p, s);
+    case EPI_RESID_F32 * 2 + 1: return launch<EPI_RESID_F32, 1, FIX>(p, s);
+    case EPI_BF16_SAVE * 2 + 0: return launch<EPI_BF16_SAVE, 0, FIX>(p, s);
+    case EPI_BF16_SAVE * 2 + 1: return launch<EPI_BF16_SAVE, 1, FIX>(p, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+template <int FIX>
+hipError_t dispatch_parts(const GemmParams& p, const GemmParts& t, hipStream_t s) {
+  // device-local arrays: whole-K accumulation only (a split partial has no owner)
+  if (p.nsplit != 1 || (t.a_rows && t.a_rows % 64) || (t.c_rows && t.c_rows % 16) ||
+      (t.b_nrows && (t.b_nrows % 64 || t.b_kcols % 64 || t.b_nk < 1 || t.b_gstride < 0 ||
+                     (p.ngroups > 1 && t.b_gstride == 0) ||
+                     (int64_t)(p.ngroups - 1) * t.b_gstride + (int64_t)((p.N + t.b_nrows - 1) / t.b_nrows) * t.b_nk > kMaxParts)))
+    return hipErrorInvalidValue;
+  switch (p.epi * 2 + (p.act ? 1 : 0)) {
+    case EPI_BF16 * 2 + 0: return launch_parts<EPI_BF16, 0, FIX>(p, t, s);
+    case EPI_BF16 * 2 + 1: return launch_parts<EPI_BF16, 1, FIX>(p, t, s);
+    case EPI_F32 * 2 + 0: return launch_parts<EPI_F32, 0, FIX>(p, t, s);
+    case EPI_RESID_F32 * 2 + 0: return launch_parts<EPI_RESID_F32, 0, FIX>(p, t, s);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 }  // namespace
@@ -425,33 +557,13 @@ hipError_t launch_parts(const GemmParams& p, const GemmParts& t, hipStream_t s) 
 int gemm_bf16_tile_m() { return BM; }
 int gemm_bf16_tile_n() { return BN; }
 
-hipError_t launch_gemm_bf16(const GemmParams& p, hipStream_t s) {
-  switch (p.epi * 2 + (p.act ? 1 : 0)) {
-    case EPI_BF16 * 2 + 0: return launch<EPI_BF16, 0>(p, s);
-    case EPI_BF16 * 2 + 1: return launch<EPI_BF16, 1>(p, s);
-    case EPI_F32 * 2 + 0: return launch<EPI_F32, 0>(p, s);
-    case EPI_F32 * 2 + 1: return launch<EPI_F32, 1>(p, s);
-    case EPI_PARTIAL * 2 + 0: return launch<EPI_PARTIAL, 0>(p, s);
-    case EPI_RESID_F32 * 2 + 0: return launch<EPI_RESID_F32, 0>(p, s);
-    case EPI_RESID_F32 * 2 + 1: return launch<EPI_RESID_F32, 1>(p, s);
-    case EPI_BF16_SAVE * 2 + 0: return launch<EPI_BF16_SAVE, 0>(p, s);
-    case EPI_BF16_SAVE * 2 + 1: return launch<EPI_BF16_SAVE, 1>(p, s);
-    default: return hipErrorInvalidValue;
-  }
-}
-
+hipError_t launch_gemm_bf16(const GemmParams& p, hipStream_t s) { return dispatch<0>(p, s); }
+hipError_t launch_gemm_bf16_fixup(const GemmParams& p, hipStream_t s) { return dispatch<1>(p, s); }
 hipError_t launch_gemm_bf16_parts(const GemmParams& p, const GemmParts& t, hipStream_t s) {
-  // device-local arrays: whole-K accumulation only (a split partial has no owner)
-  if (p.nsplit != 1 || (t.a_rows && t.a_rows % 64) || (t.c_rows && t.c_rows % 16) ||
-      (t.b_nrows && (t.b_nrows % 64 || t.b_kcols % 64 || t.b_nk < 1)))
-    return hipErrorInvalidValue;
-  switch (p.epi * 2 + (p.act ? 1 : 0)) {
-    case EPI_BF16 * 2 + 0: return launch_parts<EPI_BF16, 0>(p, t, s);
-    case EPI_BF16 * 2 + 1: return launch_parts<EPI_BF16, 1>(p, t, s);
-    case EPI_F32 * 2 + 0: return launch_parts<EPI_F32, 0>(p, t, s);
-    case EPI_RESID_F32 * 2 + 0: return launch_parts<EPI_RESID_F32, 0>(p, t, s);
-    default: return hipErrorInvalidValue;
-  }
+  return dispatch_parts<0>(p, t, s);
+}
+hipError_t launch_gemm_bf16_parts_fixup(const GemmParams& p, const GemmParts& t, hipStream_t s) {
+  return dispatch_parts<1>(p, t, s);
 }
 
 }  // namespace partir

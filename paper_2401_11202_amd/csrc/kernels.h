@@ -40,18 +40,32 @@ struct GemmParams {
   int group_m;     // tile-order grouping for L2 reuse
   int act;         // 0 none, 1 gelu-erf
   int epi;         // GemmEpi
+  // Load balance of the last, partial wave of output tiles (nsplit == 1):
+  // tiles [tail_base, tiles_m * tiles_n) each run as tail_parts workgroups
+  // over consecutive ranges of tail_kt 64-wide K tiles and store their fp32
+  // accumulators to tail_ws ([tile - tail_base][part][128 x 512 floats]); the
+  // fixup launch adds the parts in ascending order and runs the epilogue.
+  // tail_parts <= 1: every tile in one workgroup.
+  float* tail_ws;
+  int tail_base, tail_parts, tail_kt;
 };
 
 hipError_t launch_gemm_bf16(const GemmParams& p, hipStream_t s);
+// The second launch of a GEMM with tail_parts > 1 (after launch_gemm_bf16 on
+// the same stream).
+hipError_t launch_gemm_bf16_fixup(const GemmParams& p, hipStream_t s);
+// Bytes of tail_ws per tail part.
+constexpr size_t kGemmTailPartBytes = 512 * 128 * 4;
 
 // Operands held as separate device-local arrays (the lowered program's
 // per-device arrays, Sec. 6): the GEMM reads and writes them in place, so an
 // all_gather becomes addressing in the operand fetch and a reduce_scatter
 // the owner's store.  A table with rows/cols 0 is unused (plain pointer).
 //   a: A row blocks of a_rows rows (a_rows % 64 == 0), leading dim lda.
-//   b: B^T blocks, b[nb * b_nk + kb] = rows [nb b_nrows, +b_nrows) and
-//      K columns [kb b_kcols, +b_kcols) (b_nrows % 64 == 0, b_kcols % 64 ==
-//      0), each row-major with leading dim ldb.
+//   b: B^T blocks, b[g * b_gstride + nb * b_nk + kb] = group g's rows
+//      [nb b_nrows, +b_nrows) and K columns [kb b_kcols, +b_kcols)
+//      (b_nrows % 64 == 0, b_kcols % 64 == 0), each row-major with leading
+//      dim ldb.
 //   c: C row blocks of c_rows rows (c_rows % 16 == 0), leading dim ldc; with
 //      EPI_RESID_F32 the residual is the part itself (C += result).
 constexpr int kMaxParts = 64;
@@ -60,10 +74,11 @@ struct GemmParts {
   const uint16_t* b[kMaxParts];
   void* c[kMaxParts];
   int a_rows;
-  int b_nrows, b_kcols, b_nk;
+  int b_nrows, b_kcols, b_nk, b_gstride;
   int c_rows;
 };
 hipError_t launch_gemm_bf16_parts(const GemmParams& p, const GemmParts& t, hipStream_t s);
+hipError_t launch_gemm_bf16_parts_fixup(const GemmParams& p, const GemmParts& t, hipStream_t s);
 int gemm_bf16_tile_m();
 int gemm_bf16_tile_n();
 

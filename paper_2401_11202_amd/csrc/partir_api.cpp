@@ -61,7 +61,7 @@ bool valid_dtype(int dt) { return dt == PARTIR_F32 || dt == PARTIR_BF16; }
 // Plans
 // ---------------------------------------------------------------------------
 enum LaunchKind { L_GEMM_BF16, L_GEMM_F32, L_REDUCE, L_ATTN, L_ATTN_COMBINE, L_RMS, L_TRANSPOSE, L_ACT_BWD, L_COLSUM,
-                  L_GEMM_BF16_PARTS, L_ATTN_BWD, L_RMS_PARTS };
+                  L_GEMM_BF16_PARTS, L_ATTN_BWD, L_RMS_PARTS, L_GEMM_BF16_FIXUP, L_GEMM_BF16_PARTS_FIXUP };
 
 struct Launch {
   LaunchKind kind;
@@ -122,6 +122,7 @@ struct GemmSpec {
   bool resid_add = false;
   int sum_impl = PARTIR_SUM_AUTO;
   void* aux = nullptr;          // bf16 pre-activation output (kept for a backward pass)
+  bool tail_ok = false;         // the caller's workspace region holds gemm_ws_bytes (tail split allowed)
   const char* name = "gemm";    // role, used as the trace name
   const char* label = "gemm";   // loop nest, for the plan text
 };
@@ -138,8 +139,28 @@ bool gemm_uses_splitk(const GemmSpec& g) {
   return gemm_tiles(g) < kNumCU;   // too few output tiles: spread the K shards too
 }
 
+// Load balance of the last wave: with ntiles = q * kNumCU + r output tiles
+// (0 < r <= kNumCU / 2), the r tiles of the partial last wave run as `parts`
+// workgroups each over consecutive K ranges, so the last wave holds
+// r * parts <= kNumCU shorter workgroups instead of r whole ones; a fixup
+// launch adds the parts in ascending K order (deterministic) and runs the
+// epilogue.  Returns parts (1: no split) and the first split tile.
+int gemm_tail_parts(const GemmSpec& g, int64_t* tail_base) {
+  *tail_base = 0;
+  if (!g.tail_ok || g.ab_dtype != PARTIR_BF16 || gemm_uses_splitk(g)) return 1;
+  const int64_t ntiles = gemm_tiles(g), r = ntiles % kNumCU, nk = cdiv(g.K, 64);
+  int parts = 1;
+  while (parts < 4 && 2 * parts * r <= kNumCU && nk >= 2 * parts * 8) parts *= 2;   // >= 8 K tiles a part
+  if (r == 0 || parts == 1 || (r * parts) % 8) return 1;   // the XCD schedule wants multiples of 8
+  *tail_base = ntiles - r;
+  return parts;
+}
+
 size_t gemm_ws_bytes(const GemmSpec& g) {
-  return gemm_uses_splitk(g) ? align_up((size_t)g.rk * g.M * g.N * sizeof(float)) : 0;
+  if (gemm_uses_splitk(g)) return align_up((size_t)g.rk * g.M * g.N * sizeof(float));
+  int64_t base;
+  const int parts = gemm_tail_parts(g, &base);
+  return parts > 1 ? align_up((size_t)(gemm_tiles(g) - base) * parts * kGemmTailPartBytes) : 0;
 }
 
 std::string describe_gemm(const GemmSpec& g, int64_t grid, bool split) {
@@ -156,9 +177,10 @@ std::string describe_gemm(const GemmSpec& g, int64_t grid, bool split) {
   return buf;
 }
 
-// Appends the launches of one GEMM to the plan.  `ws` points at this GEMM's
-// partial-buffer region (used only for split-K).
-void plan_gemm(const GemmSpec& g, void* ws, Plan& plan) {
+// Appends the launches of one GEMM to the plan (returns how many).  `ws`
+// points at this GEMM's region of gemm_ws_bytes(g) bytes (split-K partials or
+// the tail parts).
+int plan_gemm(const GemmSpec& g, void* ws, Plan& plan) {
   const bool split = gemm_uses_splitk(g);
   if (g.rk > 1) {
     plan.n_sum_loops += 1;
@@ -192,9 +214,31 @@ void plan_gemm(const GemmSpec& g, void* ws, Plan& plan) {
     // a kept pre-activation needs the whole K sum in the tile (never split:
     // only the up-projection, which has no #sum, asks for it)
     p.epi = split ? EPI_PARTIAL : (g.aux ? EPI_BF16_SAVE : epi_store);
+    int64_t tail_base;
+    p.tail_parts = gemm_tail_parts(g, &tail_base);
+    p.tail_base = (int)tail_base;
+    p.tail_kt = (int)cdiv(cdiv(g.K, 64), p.tail_parts);
+    p.tail_ws = p.tail_parts > 1 ? (float*)ws : nullptr;
     L.kind = L_GEMM_BF16;
     L.name = g.name;
-    L.text = describe_gemm(g, (int64_t)p.tiles_m * p.tiles_n * p.nsplit, split);
+    const int64_t ntiles = (int64_t)p.tiles_m * p.tiles_n;
+    L.text = describe_gemm(g, p.tail_parts > 1 ? tail_base + (ntiles - tail_base) * p.tail_parts : ntiles * p.nsplit,
+                           split);
+    if (p.tail_parts > 1) {
+      char buf[200];
+      snprintf(buf, sizeof buf, "; the last %lld tiles as %d K parts of %d K tiles each",
+               (long long)(ntiles - tail_base), p.tail_parts, p.tail_kt);
+      L.text += buf;
+      plan.launches.push_back(L);
+      Launch Fx = L;
+      Fx.kind = L_GEMM_BF16_FIXUP;
+      Fx.name = std::string(g.name) + ".fixup";
+      snprintf(buf, sizeof buf, "%s.fixup: %lld tiles = sum of their %d K parts in ascending order, then the epilogue",
+               g.name, (long long)(ntiles - tail_base), p.tail_parts);
+      Fx.text = buf;
+      plan.launches.push_back(Fx);
+      return 2;
+    }
   } else {
     const int tile = gemm_f32_tile();
     GemmF32Params& p = L.gemm32;
@@ -236,7 +280,9 @@ void plan_gemm(const GemmSpec& g, void* ws, Plan& plan) {
              g.resid_add ? " + residual" : "");
     R.text = buf;
     plan.launches.push_back(R);
+    return 2;
   }
+  return 1;
 }
 
 // ---------------------------------------------------------------------------
@@ -254,6 +300,8 @@ hipError_t run_one(const Launch& L, hipStream_t s) {
     case L_ACT_BWD: return launch_act_backward(L.act, s);
     case L_COLSUM: return launch_colsum(L.cs, s);
     case L_GEMM_BF16_PARTS: return launch_gemm_bf16_parts(L.gemm, *L.parts, s);
+    case L_GEMM_BF16_FIXUP: return launch_gemm_bf16_fixup(L.gemm, s);
+    case L_GEMM_BF16_PARTS_FIXUP: return launch_gemm_bf16_parts_fixup(L.gemm, *L.parts, s);
     case L_ATTN_BWD: return launch_attention_backward(L.attn_bwd, s);
     case L_RMS_PARTS: return launch_rmsnorm_parts(L.rms, *L.rms_parts, s);
   }
@@ -395,6 +443,7 @@ GemmSpec matmul_spec(const MatmulArgs& a) {
   g.rn = a.tile_axis == PARTIR_AXIS_N ? a.R : 1;
   g.rk = a.sum_axis == PARTIR_AXIS_K ? a.R : 1;
   g.sum_impl = a.sum_impl;
+  g.tail_ok = true;
   g.name = a.ab == PARTIR_BF16 ? "loop_matmul.bf16" : "loop_matmul.f32";
   g.label = "loop_matmul";
   return g;
@@ -524,24 +573,32 @@ int validate_attn(const AttnArgs& a, bool with_ptrs) {
 void plan_attention_launch(char* qkvo, int64_t B, int64_t S, int64_t D, int64_t H, int64_t dh, int causal,
                            float scale, int Rm, Plan& plan, float* lse);
 
-// QKV projection + attention core into (Q, K, V, O) inside the workspace.
-void plan_attention_core(const void* Xn, const void* Wq, const void* Wk, const void* Wv, char* qkvo,
-                         int64_t B, int64_t S, int64_t D, int64_t H, int64_t dh, int causal, float scale,
-                         int Rb, int Rm, Plan& plan, float* lse = nullptr) {
-  const int64_t T = B * S;
+// The QKV projection into (Q, K, V) at qkvo: one launch, three groups.
+GemmSpec qkv_spec(const void* Xn, const void* Wq, const void* Wk, const void* Wv, char* qkvo, int64_t T,
+                  int64_t D, int Rb, int Rm) {
   const size_t one = align_up((size_t)T * D * 2);
-  void* Q = qkvo ? qkvo : nullptr;
-  void* K = qkvo ? qkvo + one : nullptr;
-  void* V = qkvo ? qkvo + 2 * one : nullptr;
   GemmSpec g;
-  g.A = Xn; g.B[0] = Wq; g.B[1] = Wk; g.B[2] = Wv; g.C[0] = Q; g.C[1] = K; g.C[2] = V;
+  g.A = Xn; g.B[0] = Wq; g.B[1] = Wk; g.B[2] = Wv;
+  g.C[0] = qkvo; g.C[1] = qkvo ? qkvo + one : nullptr; g.C[2] = qkvo ? qkvo + 2 * one : nullptr;
   g.ngroups = 3;
   g.lda = D; g.ldb = D; g.ldc = D;
   g.M = T; g.N = D; g.K = D;
   g.c_dtype = PARTIR_BF16; g.rm = Rb; g.rn = Rm;
   g.name = "attn.qkv";
   g.label = "attn.qkv Q|K|V = slice 0 X[b] . slice 1 W{q,k,v}[m]";
-  plan_gemm(g, nullptr, plan);
+  return g;
+}
+
+// QKV projection + attention core into (Q, K, V, O) inside the workspace.
+// With `gemm_ws` (gemm_ws_bytes of the tail-split qkv_spec) the projection
+// may split its last wave.
+void plan_attention_core(const void* Xn, const void* Wq, const void* Wk, const void* Wv, char* qkvo,
+                         int64_t B, int64_t S, int64_t D, int64_t H, int64_t dh, int causal, float scale,
+                         int Rb, int Rm, Plan& plan, float* lse = nullptr, bool tail = false,
+                         char* gemm_ws = nullptr) {
+  GemmSpec g = qkv_spec(Xn, Wq, Wk, Wv, qkvo, B * S, D, Rb, Rm);
+  g.tail_ok = tail;
+  plan_gemm(g, gemm_ws, plan);
   plan_attention_launch(qkvo, B, S, D, H, dh, causal, scale, Rm, plan, lse);
 }
 
@@ -657,20 +714,23 @@ void plan_dec(const DecArgs& a, void* ws, Plan& plan) {
   char* xn = base;
   char* qkvo = base ? base + xn_bytes : nullptr;
   char* Hf = base ? base + xn_bytes + core : nullptr;
-  char* part = base ? base + xn_bytes + core + h_bytes : nullptr;
+  char* part = base ? base + xn_bytes + core + h_bytes : nullptr;   // split-K / tail parts, one GEMM at a time
+  GemmSpec gq = qkv_spec(xn, a.Wq, a.Wk, a.Wv, qkvo, T, a.D, a.Rb, a.Rm);
+  gq.tail_ok = true;
 
   plan_rmsnorm((const float*)a.x, (const float*)a.g1, xn, T, a.D, a.eps, a.Rb, plan);
-  plan_attention_core(xn, a.Wq, a.Wk, a.Wv, qkvo, a.B, a.S, a.D, a.H, a.dh, 1, 0.0f, a.Rb, a.Rm, plan);
+  plan_attention_core(xn, a.Wq, a.Wk, a.Wv, qkvo, a.B, a.S, a.D, a.H, a.dh, 1, 0.0f, a.Rb, a.Rm, plan, nullptr,
+                      true, part);
   GemmSpec go;
   go.A = qkvo ? qkvo + 3 * align_up((size_t)T * a.D * 2) : nullptr;
   go.B[0] = a.Wo; go.C[0] = a.x; go.resid = (const float*)a.x; go.resid_add = true;
   go.lda = a.D; go.ldb = a.D; go.ldc = a.D; go.ldr = a.D;
   go.M = T; go.N = a.D; go.K = a.D;
-  go.c_dtype = PARTIR_F32; go.rm = a.Rb; go.rk = a.Rm;
+  go.c_dtype = PARTIR_F32; go.rm = a.Rb; go.rk = a.Rm; go.tail_ok = true;
   go.name = "attn.out";
   go.label = "dec.attn_out x += sum_m O[:, m heads] . slice 0 Wo[m]";
   plan_gemm(go, part, plan);
-  plan.ws_bytes = xn_bytes + core + gemm_ws_bytes(go);
+  plan.ws_bytes = xn_bytes + core + std::max(gemm_ws_bytes(gq), gemm_ws_bytes(go));
   plan.n_shards = a.Rb * a.Rm;
   plan.n_tile_loops = (a.Rb > 1) + 2;
   plan.flops = 8.0 * T * a.D * a.D + 4.0 * a.B * a.H * ((double)a.S * (a.S + 1) / 2) * a.dh + 4.0 * T * a.D * a.F;
@@ -688,11 +748,12 @@ void plan_dec(const DecArgs& a, void* ws, Plan& plan) {
   g2.A = Hf; g2.B[0] = a.W2; g2.C[0] = a.x; g2.resid = (const float*)a.x; g2.resid_add = true;
   g2.lda = a.F; g2.ldb = a.F; g2.ldc = a.D; g2.ldr = a.D;
   g2.M = T; g2.N = a.D; g2.K = a.F;
-  g2.c_dtype = PARTIR_F32; g2.rm = a.Rb; g2.rk = a.Rm;
+  g2.c_dtype = PARTIR_F32; g2.rm = a.Rb; g2.rk = a.Rm; g2.tail_ok = true;
   g2.name = "mlp.down";
   g2.label = "dec.ffn_down x += sum_m H[:, m] . slice 0 W2[m]";
   plan_gemm(g2, part, plan);
-  plan.ws_bytes = xn_bytes + core + h_bytes + std::max(gemm_ws_bytes(go), gemm_ws_bytes(g2));
+  plan.ws_bytes = xn_bytes + core + h_bytes +
+                  std::max({gemm_ws_bytes(gq), gemm_ws_bytes(go), gemm_ws_bytes(g1), gemm_ws_bytes(g2)});
   plan.n_shards = a.Rb * a.Rm;
   plan.n_tile_loops = (a.Rb > 1) + 2;
   plan.flops = 8.0 * T * a.D * a.D + 4.0 * a.B * a.H * ((double)a.S * (a.S + 1) / 2) * a.dh + 4.0 * T * a.D * a.F;
@@ -1419,7 +1480,34 @@ void plan_dec_sharded(const DecShardedArgs& a, void* ws, Plan& plan) {
   char* xn = base;
   char* qkvo = base ? base + xn_bytes : nullptr;
   char* Hf = base ? base + xn_bytes + core : nullptr;
-  plan.ws_bytes = xn_bytes + core + (F > 0 ? h_bytes : 0);
+  char* gws = base ? base + xn_bytes + core + (F > 0 ? h_bytes : 0) : nullptr;   // tail parts, one GEMM at a time
+  const size_t one = align_up((size_t)T * D * 2);
+  // the four GEMMs: Q|K|V (three groups), attention out, FFN up, FFN down
+  GemmSpec gq;
+  gq.A = xn;
+  for (int i = 0; i < 3; ++i) gq.C[i] = qkvo ? qkvo + i * one : nullptr;
+  gq.ngroups = 3;
+  gq.lda = D; gq.ldb = D / a.Rb; gq.ldc = D; gq.M = T; gq.N = D; gq.K = D;
+  gq.c_dtype = PARTIR_BF16; gq.rm = a.Rb; gq.rn = a.Rm; gq.tail_ok = true;
+  gq.name = "attn.qkv"; gq.label = "attn.qkv Q|K|V = xn[b] . all_gather<B>(W{q,k,v})[:, m]";
+  GemmSpec go;
+  go.A = qkvo ? qkvo + 3 * one : nullptr; go.resid_add = true;
+  go.lda = D; go.ldb = D / a.Rm; go.ldc = D; go.M = T; go.N = D; go.K = D;
+  go.c_dtype = PARTIR_F32; go.rm = a.Rb; go.rk = a.Rm; go.sum_impl = PARTIR_SUM_FUSED; go.tail_ok = true;
+  go.name = "attn.out"; go.label = "dec.attn_out x_bm += reduce_scatter<M>(sum_m O[:, m] . all_gather<B>(Wo)[m])";
+  GemmSpec g1;
+  g1.A = xn; g1.C[0] = Hf;
+  g1.lda = D; g1.ldb = D / a.Rb; g1.ldc = F; g1.M = T; g1.N = F; g1.K = D;
+  g1.c_dtype = PARTIR_BF16; g1.rm = a.Rb; g1.rn = a.Rm; g1.act = 1;
+  g1.name = "mlp.up"; g1.label = "dec.ffn_up H = gelu(hn[b] . all_gather<B>(W1)[:, m])";
+  GemmSpec g2;
+  g2.A = Hf; g2.resid_add = true;
+  g2.lda = F; g2.ldb = F / a.Rm; g2.ldc = D; g2.M = T; g2.N = D; g2.K = F;
+  g2.c_dtype = PARTIR_F32; g2.rm = a.Rb; g2.rk = a.Rm; g2.sum_impl = PARTIR_SUM_FUSED; g2.tail_ok = true;
+  g2.name = "mlp.down"; g2.label = "dec.ffn_down x_bm += reduce_scatter<M>(sum_m H[:, m] . all_gather<B>(W2)[m])";
+  plan.ws_bytes = xn_bytes + core + std::max(gemm_ws_bytes(gq), gemm_ws_bytes(go));
+  if (F > 0) plan.ws_bytes = xn_bytes + core + h_bytes +
+                             std::max({gemm_ws_bytes(gq), gemm_ws_bytes(go), gemm_ws_bytes(g1), gemm_ws_bytes(g2)});
   auto norms = [&](const void* g) {
     // one launch over every device's tokens: each row is normalised where it
     // lives and stored into the gathered buffer
@@ -1435,13 +1523,15 @@ void plan_dec_sharded(const DecShardedArgs& a, void* ws, Plan& plan) {
              "stored into the gathered buffer (all_gather<M>)", nd, (long long)rows_dev, (long long)D);
     L.text = buf;
   };
-  // B part table of a column-parallel weight W^T [out, in]: part (b, m) holds
-  // rows block m, cols block b -> N block m, K block b
-  auto col_parts = [&](const void* const* W, int64_t n_out) {
+  // B part table of column-parallel weights W^T [out, in] (one group per
+  // weight): part (b, m) holds rows block m, cols block b -> N block m, K block b
+  auto col_parts = [&](const void* const* const* W, int ng, int64_t n_out) {
     GemmParts* t = new GemmParts{};
-    t->b_nrows = (int)(n_out / a.Rm); t->b_kcols = (int)(D / a.Rb); t->b_nk = a.Rb;
-    for (int b = 0; b < a.Rb; ++b)
-      for (int m = 0; m < a.Rm; ++m) t->b[m * a.Rb + b] = W ? (const uint16_t*)W[b * a.Rm + m] : nullptr;
+    t->b_nrows = (int)(n_out / a.Rm); t->b_kcols = (int)(D / a.Rb); t->b_nk = a.Rb; t->b_gstride = nd;
+    for (int g = 0; g < ng; ++g)
+      for (int b = 0; b < a.Rb; ++b)
+        for (int m = 0; m < a.Rm; ++m)
+          t->b[g * nd + m * a.Rb + b] = W[g] ? (const uint16_t*)W[g][b * a.Rm + m] : nullptr;
     return t;
   };
   // row-parallel weight W^T [D, in]: part (b, m) = rows block b, cols block m;
@@ -1456,47 +1546,29 @@ void plan_dec_sharded(const DecShardedArgs& a, void* ws, Plan& plan) {
     }
     return t;
   };
+  // one GEMM's launches (main and, with a split last wave, its fixup) on the
+  // device-local arrays of `t`
   auto parted = [&](const GemmSpec& g, GemmParts* t, const char* how) {
-    plan_gemm(g, nullptr, plan);
-    Launch& L = plan.launches.back();
-    L.kind = L_GEMM_BF16_PARTS;
-    L.parts.reset(t);
-    L.text += how;
+    const size_t first = plan.launches.size();
+    plan_gemm(g, gws, plan);
+    std::shared_ptr<GemmParts> sp(t);
+    for (size_t i = first; i < plan.launches.size(); ++i) {
+      Launch& L = plan.launches[i];
+      L.kind = L.kind == L_GEMM_BF16_FIXUP ? L_GEMM_BF16_PARTS_FIXUP : L_GEMM_BF16_PARTS;
+      L.parts = sp;
+      if (i == first) L.text += how;
+    }
   };
   norms(a.g1);
-  const size_t one = align_up((size_t)T * D * 2);
-  const char* names[3] = {"attn.qkv", "attn.qkv", "attn.qkv"};
-  const char* labels[3] = {"attn.q   Q = xn[b] . all_gather<B>(Wq)[:, m]", "attn.k   K = xn[b] . all_gather<B>(Wk)[:, m]",
-                           "attn.v   V = xn[b] . all_gather<B>(Wv)[:, m]"};
-  for (int i = 0; i < 3; ++i) {
-    GemmSpec g;
-    g.A = xn; g.C[0] = qkvo ? qkvo + i * one : nullptr;
-    g.lda = D; g.ldb = D / a.Rb; g.ldc = D; g.M = T; g.N = D; g.K = D;
-    g.c_dtype = PARTIR_BF16; g.rm = a.Rb; g.rn = a.Rm;
-    g.name = names[i]; g.label = labels[i];
-    parted(g, col_parts(a.W[i], D), "; weight blocks read in place (fused all_gather)");
-  }
+  const void* const* wqkv[3] = {a.W[0], a.W[1], a.W[2]};
+  parted(gq, col_parts(wqkv, 3, D), "; weight blocks read in place (fused all_gather)");
   plan_attention_launch(qkvo, a.B, a.S, D, a.H, a.dh, 1, 0.0f, a.Rm, plan, nullptr);
-  GemmSpec go;
-  go.A = qkvo ? qkvo + 3 * one : nullptr; go.resid_add = true;
-  go.lda = D; go.ldb = D / a.Rm; go.ldc = D; go.M = T; go.N = D; go.K = D;
-  go.c_dtype = PARTIR_F32; go.rm = a.Rb; go.rk = a.Rm; go.sum_impl = PARTIR_SUM_FUSED;
-  go.name = "attn.out"; go.label = "dec.attn_out x_bm += reduce_scatter<M>(sum_m O[:, m] . all_gather<B>(Wo)[m])";
   parted(go, row_parts(a.W[3], D), "; each row block added into its owner's residual part (fused reduce_scatter)");
   plan.n_sum_loops = 1;
   if (F == 0) return;   // an FFN of width 0 adds the empty sum: x is unchanged
   norms(a.g2);
-  GemmSpec g1;
-  g1.A = xn; g1.C[0] = Hf;
-  g1.lda = D; g1.ldb = D / a.Rb; g1.ldc = F; g1.M = T; g1.N = F; g1.K = D;
-  g1.c_dtype = PARTIR_BF16; g1.rm = a.Rb; g1.rn = a.Rm; g1.act = 1;
-  g1.name = "mlp.up"; g1.label = "dec.ffn_up H = gelu(hn[b] . all_gather<B>(W1)[:, m])";
-  parted(g1, col_parts(a.W[4], F), "; weight blocks read in place (fused all_gather)");
-  GemmSpec g2;
-  g2.A = Hf; g2.resid_add = true;
-  g2.lda = F; g2.ldb = F / a.Rm; g2.ldc = D; g2.M = T; g2.N = D; g2.K = F;
-  g2.c_dtype = PARTIR_F32; g2.rm = a.Rb; g2.rk = a.Rm; g2.sum_impl = PARTIR_SUM_FUSED;
-  g2.name = "mlp.down"; g2.label = "dec.ffn_down x_bm += reduce_scatter<M>(sum_m H[:, m] . all_gather<B>(W2)[m])";
+  const void* const* w1[1] = {a.W[4]};
+  parted(g1, col_parts(w1, 1, F), "; weight blocks read in place (fused all_gather)");
   parted(g2, row_parts(a.W[5], F), "; each row block added into its owner's residual part (fused reduce_scatter)");
   plan.n_sum_loops = 2;
 }

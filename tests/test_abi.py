@@ -213,8 +213,10 @@ def test_attention_and_decoder_sums():
     a = P.plan_attn_block(4, 2048, 4096, 32, 128, 1, 8)
     assert a["n_sum_loops"] == 1 and a["n_launches"] == 3 and a["n_virtual_shards"] == 8
     d = P.plan_decoder_layer(4, 2048, 5120, 40, 128, 13824, 2, 4)
-    # two #sum loops per layer (attention out-projection and FFN down): Megatron's 2 all_reduces
-    assert d["n_sum_loops"] == 2 and d["n_virtual_shards"] == 8 and d["n_launches"] == 7
+    # two #sum loops per layer (attention out-projection and FFN down): Megatron's 2 all_reduces;
+    # 7 launches plus the fixups of the three GEMMs whose last wave is split (1920 and 640 tiles)
+    assert d["n_sum_loops"] == 2 and d["n_virtual_shards"] == 8 and d["n_launches"] == 10
+    assert d["text"].count(".fixup:") == 3 and d["text"].count("the last 128 tiles as 2 K parts") == 3
 
 
 def test_small_output_uses_split_partials():
@@ -486,5 +488,30 @@ def test_decoder_sharded_plan():
     t = p["text"]
     assert p["n_sum_loops"] == 2 and p["n_sum_splitk"] == 0 and p["n_virtual_shards"] == 8
     assert t.count("sequence-parallel") == 2 and t.count("fused reduce_scatter") == 2
-    assert t.count("fused all_gather") == 4
+    # Q|K|V in one launch (three groups of weight blocks), FFN up
+    assert t.count("fused all_gather") == 2 and t.count(".fixup:") == 3
     assert P.lib().partir_decoder_layer_sharded_workspace(4, 2048, 5120, 40, 128, 13824, 2, 4) == p["workspace_bytes"]
+
+
+@pytest.mark.parametrize("M,N,K,tail,parts", [
+    (8192, 5120, 5120, 128, 2),    # 640 tiles = 2 waves of 256 + 128: the 128 run as 2 K halves
+    (8192, 15360, 5120, 128, 2),   # 1920 tiles
+    (8192, 4096, 4096, 0, 1),      # 512 tiles: whole waves
+    (8192, 13824, 4096, 0, 1),     # 1728 tiles: 192 left over, 2 x 192 would not fit one wave
+    (512, 512, 4096, 4, 4),        # 4 tiles, 64 K tiles: 4 quarters of K each
+    (512, 512, 256, 0, 1),         # 4 K tiles: too short to split
+    (256, 256, 4096, 0, 1),        # 1 tile: 4 parts would not fill the 8 XCDs evenly
+])
+def test_last_wave_tail_split(M, N, K, tail, parts):
+    """The load-balancing split of the last partial wave of output tiles:
+    which tiles, how many K parts, the workspace for their fp32 accumulators
+    and the fixup launch that adds them."""
+    p = P.plan_loop_matmul(M, N, K)
+    t = p["text"]
+    if tail:
+        assert f"the last {tail} tiles as {parts} K parts" in t and ".fixup:" in t
+        assert p["n_launches"] == 2 and p["workspace_bytes"] == tail * parts * 512 * 128 * 4
+    else:
+        assert ".fixup" not in t and p["n_launches"] == 1 and p["workspace_bytes"] == 0
+    assert P.lib().partir_loop_matmul_workspace(M, N, K, P.BF16, P.BF16, P.B_NK, -1, -1, 1, P.SUM_AUTO) == \
+        p["workspace_bytes"]

@@ -199,3 +199,53 @@ def test_degenerate_shard_sizes(dtype):
             say(f"degenerate {dtype} {M}x{N}x{K} tile={tile} sum={summ} R={R} {impl}")
             C = run(A, B, tile, summ, R, bl, out_dtype=torch.float32, sum_impl=impl)
             check(A, B, C, tile, summ, R, tol)
+
+
+# ---------------------------------------------------------------------------
+# The last, partial wave of output tiles split into K parts (load balance):
+# 1000 x 304 outputs are 8 tiles of 256 x 256 (16 with #tile N x4), each run
+# as 4 workgroups over 17 + 17 + 17 + 14 of the 65 K tiles (K = 4112: the
+# last K tile holds 16 columns); a fixup launch adds the parts in order.
+@pytest.mark.parametrize("out", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("tile,summ,R", [(None, None, 1), ("M", None, 4), ("N", None, 4), (None, "K", 2),
+                                         ("M", "K", 2)])
+def test_bf16_last_wave_split_ragged(tile, summ, R, out):
+    M, N, K = 1000, 304, 4112
+    plan = P.plan_loop_matmul(M, N, K, ab=P.BF16, c=P.F32 if out == torch.float32 else P.BF16,
+                              tile=tile, sum=summ, R=R, sum_impl=P.SUM_FUSED)
+    assert "K parts of 17 K tiles" in plan["text"], plan["text"]
+    A = I.gaussian(121, 0, (M, K), 1.0, "bf16")
+    B = I.gaussian(121, 1, (K, N), K ** -0.5, "bf16")
+    say(f"bf16 last-wave split {M}x{N}x{K} tile={tile} sum={summ} R={R} out={out}")
+    C = run(A, B, tile, summ, R, "nk", out_dtype=out, sum_impl="fused")
+    err = check(A, B, C, tile, summ, R, TOL_BF16)
+    assert err <= accum_bound(K) + (2.0 ** -8 if out == torch.bfloat16 else 0.0)
+
+
+def test_last_wave_split_integer_exact_and_deterministic():
+    """Small-integer inputs: every partial and their sum are exact in fp32, so
+    the split tiles equal the oracle bit for bit; repeated calls agree."""
+    M, N, K = 1000, 304, 4112
+    A = I.small_ints(122, 0, (M, K), dtype="bf16")
+    B = I.small_ints(122, 1, (K, N), dtype="bf16")
+    ref = O.matmul(A.f64(), B.f64())
+    c1 = run(A, B, "M", None, 4, "nk", out_dtype=torch.float32)
+    c2 = run(A, B, "M", None, 4, "nk", out_dtype=torch.float32)
+    assert np.array_equal(host(c1), ref) and torch.equal(c1, c2)
+
+
+def test_last_wave_split_full_size_sampled_rows():
+    """8192 x 5120 x 5120 (640 tiles: two whole waves, then 128 tiles as 2 K
+    halves of 40 K tiles): whole output rows, sampled across every tile row,
+    against the oracle's matmul of those rows."""
+    M, N, K = 8192, 5120, 5120
+    assert "the last 128 tiles as 2 K parts of 40 K tiles" in P.plan_loop_matmul(M, N, K)["text"]
+    A = I.gaussian(123, 0, (M, K), 1.0, "bf16")
+    B = I.gaussian(123, 1, (K, N), K ** -0.5, "bf16")
+    say(f"bf16 last-wave split {M}x{N}x{K} (sampled rows)")
+    C = host(run(A, B, None, None, 1, "nk", out_dtype=torch.float32))
+    rows = sorted({0, M - 1} | {256 * t + (37 * t) % 256 for t in range(M // 256)})
+    Ar = A.f64()[rows]
+    err = O.normalised_error(C[rows], O.matmul(Ar, B.f64()), O.abs_product(Ar, B.f64()))
+    say(f"    {len(rows)} rows, max normalised error {err:.3e}")
+    assert err <= accum_bound(K)
