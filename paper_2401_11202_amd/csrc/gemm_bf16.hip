@@ -337,6 +337,10 @@ __device__ __forceinline__ void gemm_body(const GemmParams& p, const GemmParts* 
   // store, which the memory system would see as partial lines.  The tile is
   // therefore staged through LDS and written back row by row, each row as
   // one contiguous run (bf16: 32 lanes x 16 B; fp32: 64 lanes x 16 B).
+  // The output is stored non-temporally (streaming): every workgroup of a
+  // wave stores its tile at the same moment, and the streaming stores drain
+  // that burst faster (measured: 3.5% on bf16, 6-9% on fp32 outputs with a
+  // 4096-long K loop).
   const float* bias = pick3(grp, p.bias[0], p.bias[1], p.bias[2]);
   void* Cg = pick3(grp, p.C[0], p.C[1], p.C[2]);
   __syncthreads();   // every wave is done with the K stages
@@ -387,7 +391,7 @@ __device__ __forceinline__ void gemm_body(const GemmParams& p, const GemmParts* 
           grow -= (int64_t)cb * t->c_rows;
         }
         uint16_t* dst = ob + grow * p.ldc + col0 + cc;
-        if (cc + 8 <= cols) *(i32x4*)dst = v;
+        if (cc + 8 <= cols) __builtin_nontemporal_store(v, (i32x4*)dst);
         else *(int2*)dst = make_int2(v[0], v[1]);   // a 4-column tail (cols % 8 == 4)
       }
     };
@@ -442,17 +446,17 @@ __device__ __forceinline__ void gemm_body(const GemmParams& p, const GemmParts* 
         } else if (EPI == EPI_F32) {
           if (PARTS && t->c_rows) {   // the 8 rows of a pass share one part
             const int cb = (row0 + q * (BM / 2) + r0) / t->c_rows;
-            *(f32x4*)((float*)t->c[cb] + (m - (int64_t)cb * t->c_rows) * p.ldc + n) = v;
+            __builtin_nontemporal_store(v, (f32x4*)((float*)t->c[cb] + (m - (int64_t)cb * t->c_rows) * p.ldc + n));
           } else {
-            *(f32x4*)((float*)Cg + m * p.ldc + n) = v;
+            __builtin_nontemporal_store(v, (f32x4*)((float*)Cg + m * p.ldc + n));
           }
         } else if (PARTS && t->c_rows) {   // EPI_RESID_F32 into a part: the residual is the part itself
           const int cb = (row0 + q * (BM / 2) + r0) / t->c_rows;
           float* dst = (float*)t->c[cb] + (m - (int64_t)cb * t->c_rows) * p.ldc + n;
-          *(f32x4*)dst = *(const f32x4*)dst + v;
+          __builtin_nontemporal_store(*(const f32x4*)dst + v, (f32x4*)dst);
         } else {  // EPI_RESID_F32
           const f32x4 rv = *(const f32x4*)(p.resid + m * p.ldr + n);
-          *(f32x4*)((float*)Cg + m * p.ldc + n) = rv + v;
+          __builtin_nontemporal_store(rv + v, (f32x4*)((float*)Cg + m * p.ldc + n));
         }
       }
       if (q == 0) __syncthreads();   // the second half reuses the buffer
