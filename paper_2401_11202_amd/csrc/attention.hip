@@ -27,7 +27,10 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int DH = 128, BQ = 128, BKV = 64, NT = 256;
 constexpr int KP = 256;                 // K tile row pitch (bytes), chunk-swizzled
-constexpr int VP = 288;                 // V tile row pitch (bytes), padded
+// V tile row pitch (bytes), padded: 320 = 256 + 64 puts consecutive rows 16
+// banks apart, so the 32 lanes of one ds_read_b64_tr_b16 half (4 rows x 2
+// column halves x 4 column quads, 8 B each) cover all 64 banks once
+constexpr int VP = 320;
 constexpr int KT_BYTES = BKV * KP;
 constexpr int VT_BYTES = BKV * VP;
 constexpr int STAGE = KT_BYTES + VT_BYTES;
@@ -126,6 +129,11 @@ void attention_kernel(AttnParams p) {
     gload(kb_begin);
     lstore(0);
   }
+  // Every load so far (the Q fragments included) has landed on every path
+  // into the loop; without this the wait insertion cannot tell on the path
+  // that skips the first block, and waits on the next block's prefetch
+  // before each S^T step.
+  __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
   __syncthreads();
   for (int kb = kb_begin; kb < nkb; ++kb) {
     const int cur = (kb - kb_begin) & 1;
@@ -167,23 +175,29 @@ void attention_kernel(AttnParams p) {
       // the partner lane (lane ^ 32) holds the other keys of this query
       mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
       const float sl2 = p.scale_log2;
-      const float m_new = fmaxf(m_run, mloc * sl2);
-      // rescale O and l only when some lane's max moved (alpha is exactly 1
-      // for the others, so skipping the multiply changes nothing)
-      if (__builtin_amdgcn_ballot_w64(m_new > m_run) != 0) {
-        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      // Lazy rescaling: the subtracted maximum m_run moves only when this
+      // block's maximum exceeds it by more than 8 (log2 units), so every p
+      // stays <= 2^8 (exact range in fp32 and bf16; the softmax does not
+      // depend on the constant subtracted) and O and l are rescaled in few
+      // blocks instead of almost every one.  The first block always sets
+      // m_run (alpha = 0 on the empty accumulators).
+      const float m_blk = mloc * sl2;
+      const bool move = m_blk > m_run + 8.0f;
+      if (__builtin_amdgcn_ballot_w64(move) != 0) {
+        const float m_new = move ? m_blk : m_run;
+        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);   // exactly 1 where m_run stays
         l_run *= alpha;
 #pragma unroll
         for (int d = 0; d < 4; ++d) oacc[d] *= alpha;
+        m_run = m_new;
       }
-      m_run = m_new;
       float lsum = 0.0f;
       bf16x8 pf[4];
 #pragma unroll
       for (int t = 0; t < 2; ++t)
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
-          const float e = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[t][v], sl2, -m_new));
+          const float e = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[t][v], sl2, -m_run));
           lsum += e;
           pf[2 * t + (v >> 3)][v & 7] = (__bf16)e;
         }
