@@ -114,6 +114,8 @@ typedef enum partir_act { PARTIR_ACT_NONE = 0, PARTIR_ACT_GELU_ERF = 1 } partir_
  *
  * A: [M, K] row-major, leading dim lda >= K.   B: per b_layout, leading dim ldb.
  * C: [M, N] row-major, leading dim ldc >= N, overwritten.
+ * Both B layouts are read in place (no transposed copy); a bf16 B given as
+ * [K, N] needs N and N/R (with a tile over N) multiples of 8.
  * ab_dtype: PARTIR_F32 or PARTIR_BF16 (A and B alike); c_dtype: PARTIR_F32,
  * or PARTIR_BF16 when ab_dtype is bf16.  Accumulation is fp32.
  * b_layout: partir_b_layout.  sum_impl: partir_sum_impl (ignored without a

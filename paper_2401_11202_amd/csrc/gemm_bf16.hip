@@ -29,6 +29,8 @@ typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef int i32x4 __attribute__((ext_vector_type(4)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
 constexpr int BM = 256, BN = 256, NT = 512;
 constexpr int BK = 64, NS = 2;
@@ -50,6 +52,19 @@ constexpr int PHI_N = 3072;
 constexpr float PHI_LO = -6.0f, PHI_SCALE = 256.0f;
 constexpr int PHI_BYTES = PHI_N * 8;
 typedef __attribute__((address_space(3))) void lds_void;
+
+// ds_read_b64_tr_b16 through a restrict pointer: the alias scope this gives
+// the read keeps the wait insertion from making it wait on every LDS DMA in
+// flight (the K loop orders its stages by explicit vmcnt waits and barriers).
+__device__ __forceinline__ i16x4 lds_read_tr16(const char* __restrict__ p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)p);
+}
+
+// LDS reads to place after MFMA i of a k step that has nrd of them.
+template <int nrd>
+constexpr int lds_reads_after(int i) {
+  return nrd <= 8 ? (i < nrd ? 1 : 0) : (i < nrd - 8 ? 2 : 1);
+}
 
 // Buffer descriptor of a workgroup-uniform base pointer (kept in SGPRs); any
 // offset at or beyond `bytes` reads as zero.
@@ -75,9 +90,11 @@ __device__ __forceinline__ int swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
 // PARTS: operands in device-local arrays (`t`, a kernel argument); else the
 // plain pointers of `p` and t is unused.
 // FIX: the fixup launch of a tail-split GEMM (no K loop: the accumulators are
-// the sum of the stored parts).
-template <int EPI, int ACT, int PARTS, int FIX>
+// the sum of the stored parts).  AMN / BMN: A stored [K, M] / B stored [K, N]
+// (row-major, the tile's 256 columns contiguous) instead of K-contiguous.
+template <int EPI, int ACT, int PARTS, int FIX, int AMN = 0, int BMN = 0>
 __device__ __forceinline__ void gemm_body(const GemmParams& p, const GemmParts* tb) {
+  static_assert(!(PARTS && (AMN || BMN)), "device-local arrays are K-contiguous");
   constexpr int OPB = BM * BK * 2, STAGE = 2 * OPB, KK = BK / 16, RB = 1024 / (BK * 2) /* rows per 1 KiB */;
   constexpr int CPR = BK / 8;   // 16-byte chunks per row
   constexpr int MAIN = (NS * STAGE > C_LDS) ? NS * STAGE : C_LDS;
@@ -196,8 +213,42 @@ __device__ __forceinline__ void gemm_body(const GemmParams& p, const GemmParts* 
   const uint32_t b_voff = (uint32_t)(lrow * p.ldb * 2 + lchunk * 16);
   const int lds_w = wave * 1024;
   const int nk = (k_end - k_begin + BK - 1) / BK;
+  // MN-major operands: the LDS tile holds 64 k rows of 512 B (the 256 tile
+  // columns).  Load j of wave w fills k rows 16 j + 2 w and +1 (the same
+  // 1 KiB of LDS as in the K-contiguous layout); lane L takes row +L/32 and
+  // LDS chunk L%32 = global chunk (L%32) ^ 4 (row & 3), which makes the
+  // transposed fragment reads below conflict-free.  A descriptor per k tile
+  // bounds the rows at the end of K (rows past it read as zero).
+  const int mn_r = 2 * wave + (lane >> 5);
+  const int mn_chunk = (lane & 31) ^ (4 * (mn_r & 3));
+  const uint32_t a_mvoff = AMN ? (uint32_t)(mn_r * p.lda * 2 + mn_chunk * 16) : 0u;
+  const uint32_t b_mvoff = BMN ? (uint32_t)(mn_r * p.ldb * 2 + mn_chunk * 16) : 0u;
   auto gload = [&](int kt, int stage) {
     const int kb = k_begin + kt * BK;
+    if constexpr (AMN || BMN) {
+      const uint32_t kvalid = (uint32_t)min(max(k_end - kb, 0), BK);
+      char* base = smem + stage * STAGE + lds_w;
+      __amdgpu_buffer_rsrc_t rma, rmb;
+      if (AMN) rma = make_rsrc(p.A + (int64_t)kb * p.lda + row0, kvalid * (uint32_t)p.lda * 2);
+      if (BMN) rmb = make_rsrc(Bg + (int64_t)kb * p.ldb + col0, kvalid * (uint32_t)p.ldb * 2);
+      const uint32_t kmask = (kb + lchunk * 8 < k_end) ? 0u : OOB;
+      const uint32_t so = (uint32_t)kb * 2;
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) {
+        if (AMN)
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(rma, (lds_void*)(base + j * 8192), 16,
+                                                   a_mvoff + (uint32_t)(j * 32 * p.lda), 0, 0, 0);
+        else
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(ra[j], (lds_void*)(base + j * 8192), 16, a_voff | kmask, so, 0, 0);
+        if (BMN)
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(rmb, (lds_void*)(base + OPB + j * 8192), 16,
+                                                   b_mvoff + (uint32_t)(j * 32 * p.ldb), 0, 0, 0);
+        else
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(rb[j], (lds_void*)(base + OPB + j * 8192), 16, b_voff | kmask, so,
+                                                   0, 0);
+      }
+      return;
+    }
     const uint32_t kmask = (kb + lchunk * 8 < k_end) ? 0u : OOB;   // ragged K tail / past the end
     const uint32_t so = (uint32_t)kb * 2;   // A (and unparted B): K offset in bytes
     uint32_t so_b = so;
@@ -239,16 +290,37 @@ __device__ __forceinline__ void gemm_body(const GemmParams& p, const GemmParts* 
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
 
+  // MN-major fragment of 32 columns from bc, k step kk: rows (k) 16 kk + 8 h
+  // + (j16 >> 2), and +4 for the high half, columns bc + 16 (G & 1) + 4 (j16
+  // & 3) .. +3; ds_read_b64_tr_b16 hands lane j16 of each 16-lane group one
+  // column over the group's 4 rows, i.e. lane l holds column bc + l % 32 at
+  // k = 16 kk + 8 h + 0..7, the layout of a K-contiguous fragment.
+  const int j16 = lane & 15;
+  const int mn_row = 8 * h + (j16 >> 2);
+  const int mn_sw = 4 * ((j16 >> 2) & 3);
+  const int mn_col = 16 * ((lane >> 4) & 1) + 4 * (j16 & 3);
+  auto mn_frag = [&](const char* op, int kk, int bc) -> bf16x8 {
+    const int col = bc + mn_col;
+    const char* pl = op + (16 * kk + mn_row) * 512 + (((col >> 3) ^ mn_sw) << 4) + ((col & 4) << 1);
+    const i16x4 lo = lds_read_tr16(pl);
+    const i16x4 hi = lds_read_tr16(pl + 4 * 512);
+    return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+  };
   // fragments of one 16-wide k step: 4 A row blocks and 2 B row blocks
   bf16x8 fa0[4], fb0[2], fa1[4], fb1[2];
   auto ldfrag = [&](int stage, int kk, bf16x8* a, bf16x8* b) {
     const char* st = smem + stage * STAGE;
     const int ko = ((2 * kk + h) ^ fsw) << 4;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) a[i] = *(const bf16x8*)(st + a_rd + i * 32 * BK * 2 + ko);
+    for (int i = 0; i < 4; ++i)
+      a[i] = AMN ? mn_frag(st, kk, wm * 128 + i * 32) : *(const bf16x8*)(st + a_rd + i * 32 * BK * 2 + ko);
 #pragma unroll
-    for (int j = 0; j < 2; ++j) b[j] = *(const bf16x8*)(st + b_rd + j * 32 * BK * 2 + ko);
+    for (int j = 0; j < 2; ++j)
+      b[j] = BMN ? mn_frag(st + OPB, kk, wn * 64 + j * 32) : *(const bf16x8*)(st + b_rd + j * 32 * BK * 2 + ko);
   };
+  // LDS reads per k step (a transposed fragment takes two) and how many go
+  // after each of the step's 8 MFMAs
+  constexpr int NRD = (AMN ? 8 : 4) + (BMN ? 4 : 2);
   // B as the first operand: each lane ends up holding 4 consecutive output
   // columns of one output row.
   auto mma = [&](const bf16x8* a, const bf16x8* b) {
@@ -260,6 +332,15 @@ __device__ __forceinline__ void gemm_body(const GemmParams& p, const GemmParts* 
   };
   // instruction interleaving hints: mask bits MFMA 0x8, VMEM read 0x20, DS read 0x100
 #define SGB(mask, n) __builtin_amdgcn_sched_group_barrier(mask, n, 0)
+  // one k step: each of the 8 MFMAs followed by its share of the LDS reads
+  // and, when refilling, one of the first 6 global loads
+#define SLOT(i, rf)                                                 \
+  SGB(0x8, 1);                                                      \
+  if constexpr (lds_reads_after<NRD>(i) == 2) SGB(0x100, 2);        \
+  else if constexpr (lds_reads_after<NRD>(i) == 1) SGB(0x100, 1);   \
+  if ((rf) && (i) < 6) SGB(0x20, 1);
+#define SLOTS(rf) \
+  SLOT(0, rf) SLOT(1, rf) SLOT(2, rf) SLOT(3, rf) SLOT(4, rf) SLOT(5, rf) SLOT(6, rf) SLOT(7, rf)
 
   constexpr int LPS = 2 * NJ;   // wave loads per k tile
   // prologue: both stages in flight, then wait for tile 0.  In the loop, the
@@ -281,24 +362,22 @@ __device__ __forceinline__ void gemm_body(const GemmParams& p, const GemmParts* 
     for (int kk = 0; kk < KK - 1; ++kk) {
       if (kk & 1) { ldfrag(stage, kk + 1, fa0, fb0); mma(fa1, fb1); }
       else { ldfrag(stage, kk + 1, fa1, fb1); mma(fa0, fb0); }
-#pragma unroll
-      for (int i = 0; i < 6; ++i) { SGB(0x8, 1); SGB(0x100, 1); }
-      SGB(0x8, 2);
+      SLOTS(false);
     }
     WAIT_VMCNT(LPS * (NS - 2));
     __syncthreads();
     if (refill) gload(kt + NS, stage);
     if ((KK - 1) & 1) { ldfrag(next, 0, fa0, fb0); mma(fa1, fb1); }
     else { ldfrag(next, 0, fa1, fb1); mma(fa0, fb0); }
-#pragma unroll
-    for (int i = 0; i < 6; ++i) { SGB(0x8, 1); SGB(0x100, 1); if (refill) SGB(0x20, 1); }
-    SGB(0x8, 2);
+    SLOTS(refill);
     return next;
   };
   int stage = 0, kt = 0;
   for (; kt + NS < nk; ++kt) stage = tile(kt, stage, true);
   for (; kt < nk; ++kt) stage = tile(kt, stage, false);
   }
+#undef SLOTS
+#undef SLOT
 #undef SGB
 
   // ---- tail parts ----------------------------------------------------------------
@@ -476,6 +555,10 @@ template <int EPI, int ACT>
 __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void gemm_bf16_fixup_kernel(GemmParams p) { gemm_body<EPI, ACT, 0, 1>(p, nullptr); }
 
+template <int EPI, int AMN, int BMN>
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void gemm_bf16_mn_kernel(GemmParams p) { gemm_body<EPI, 0, 0, 0, AMN, BMN>(p, nullptr); }
+
 template <int EPI, int ACT>
 __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void gemm_bf16_parts_fixup_kernel(GemmParams p, GemmParts t) { gemm_body<EPI, ACT, 1, 1>(p, &t); }
@@ -523,8 +606,33 @@ hipError_t launch_parts(const GemmParams& p, const GemmParts& t, hipStream_t s) 
   return hipGetLastError();
 }
 
+template <int EPI, int AMN, int BMN>
+hipError_t launch_mn(const GemmParams& p, hipStream_t s) {
+  if (p.tail_parts > 1 && !tail_ok(p)) return hipErrorInvalidValue;
+  hipLaunchKernelGGL((gemm_bf16_mn_kernel<EPI, AMN, BMN>), dim3((unsigned)main_grid(p)), dim3(NT), 0, s, p);
+  return hipGetLastError();
+}
+
+// MN-major operands: no activation (the products that read them are backward
+// passes and plain matmuls); the fixup launch is the common one.
+template <int AMN, int BMN>
+hipError_t dispatch_mn(const GemmParams& p, hipStream_t s) {
+  if (p.act) return hipErrorInvalidValue;
+  switch (p.epi) {
+    case EPI_BF16: return launch_mn<EPI_BF16, AMN, BMN>(p, s);
+    case EPI_F32: return launch_mn<EPI_F32, AMN, BMN>(p, s);
+    case EPI_PARTIAL: return launch_mn<EPI_PARTIAL, AMN, BMN>(p, s);
+    case EPI_RESID_F32: return launch_mn<EPI_RESID_F32, AMN, BMN>(p, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
 template <int FIX>
 hipError_t dispatch(const GemmParams& p, hipStream_t s) {
+  if (!FIX && (p.a_mn || p.b_mn)) {
+    if (p.a_mn && p.b_mn) return dispatch_mn<1, 1>(p, s);
+    return p.a_mn ? dispatch_mn<1, 0>(p, s) : dispatch_mn<0, 1>(p, s);
+  }
   switch (p.epi * 2 + (p.act ? 1 : 0)) {
     case EPI_BF16 * 2 + 0: return launch<EPI_BF16, 0, FIX>(p, s);
     case EPI_BF16 * 2 + 1: return launch<EPI_BF16, 1, FIX>(p, s);
@@ -541,8 +649,9 @@ hipError_t dispatch(const GemmParams& p, hipStream_t s) {
 
 template <int FIX>
 hipError_t dispatch_parts(const GemmParams& p, const GemmParts& t, hipStream_t s) {
-  // device-local arrays: whole-K accumulation only (a split partial has no owner)
-  if (p.nsplit != 1 || (t.a_rows && t.a_rows % 64) || (t.c_rows && t.c_rows % 16) ||
+  // device-local arrays: whole-K accumulation only (a split partial has no
+  // owner), K-contiguous operands
+  if (p.nsplit != 1 || p.a_mn || p.b_mn || (t.a_rows && t.a_rows % 64) || (t.c_rows && t.c_rows % 16) ||
       (t.b_nrows && (t.b_nrows % 64 || t.b_kcols % 64 || t.b_nk < 1 || t.b_gstride < 0 ||
                      (p.ngroups > 1 && t.b_gstride == 0) ||
                      (int64_t)(p.ngroups - 1) * t.b_gstride + (int64_t)((p.N + t.b_nrows - 1) / t.b_nrows) * t.b_nk > kMaxParts)))

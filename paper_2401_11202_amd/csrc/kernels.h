@@ -48,6 +48,10 @@ struct GemmParams {
   // tail_parts <= 1: every tile in one workgroup.
   float* tail_ws;
   int tail_base, tail_parts, tail_kt;
+  // Operand layouts: 0 K-contiguous (A [M, K], B^T [N, K]); 1 MN-major
+  // (A stored [K, M] with leading dim lda, B stored [K, N] with leading dim
+  // ldb).  MN-major operands take no activation.
+  int a_mn, b_mn;
 };
 
 hipError_t launch_gemm_bf16(const GemmParams& p, hipStream_t s);

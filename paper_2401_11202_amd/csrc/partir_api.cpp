@@ -123,6 +123,7 @@ struct GemmSpec {
   int sum_impl = PARTIR_SUM_AUTO;
   void* aux = nullptr;          // bf16 pre-activation output (kept for a backward pass)
   bool tail_ok = false;         // the caller's workspace region holds gemm_ws_bytes (tail split allowed)
+  bool a_mn = false;            // bf16 A stored [K, M] (leading dim lda) instead of [M, K]
   const char* name = "gemm";    // role, used as the trace name
   const char* label = "gemm";   // loop nest, for the plan text
 };
@@ -214,6 +215,8 @@ int plan_gemm(const GemmSpec& g, void* ws, Plan& plan) {
     // a kept pre-activation needs the whole K sum in the tile (never split:
     // only the up-projection, which has no #sum, asks for it)
     p.epi = split ? EPI_PARTIAL : (g.aux ? EPI_BF16_SAVE : epi_store);
+    p.a_mn = g.a_mn;
+    p.b_mn = !g.b_nk;   // B stored [K, N]
     int64_t tail_base;
     p.tail_parts = gemm_tail_parts(g, &tail_base);
     p.tail_base = (int)tail_base;
@@ -388,8 +391,6 @@ int validate_matmul(const MatmulArgs& a, bool with_ptrs) {
   if (!valid_dtype(a.ab) || !valid_dtype(a.c)) return fail(PARTIR_E_DTYPE, "dtype must be F32 or BF16");
   if (a.ab == PARTIR_F32 && a.c != PARTIR_F32) return fail(PARTIR_E_DTYPE, "f32 inputs need an f32 output");
   if (a.b_layout != PARTIR_B_KN && a.b_layout != PARTIR_B_NK) return fail(PARTIR_E_LAYOUT, "b_layout %d", a.b_layout);
-  if (a.ab == PARTIR_BF16 && a.b_layout != PARTIR_B_NK)
-    return fail(PARTIR_E_UNSUPPORTED, "bf16 B must be given transposed (PARTIR_B_NK) in this build");
   if (a.sum_impl < PARTIR_SUM_AUTO || a.sum_impl > PARTIR_SUM_SPLITK)
     return fail(PARTIR_E_UNSUPPORTED, "sum_impl %d", a.sum_impl);
   if (a.tile_axis == PARTIR_AXIS_M && a.M % a.R) return fail(PARTIR_E_DIVISIBILITY, "R=%d does not divide M=%lld", a.R, (long long)a.M);
@@ -409,6 +410,8 @@ int validate_matmul(const MatmulArgs& a, bool with_ptrs) {
   const int rn = a.tile_axis == PARTIR_AXIS_N ? a.R : 1;
   if ((a.K / rk) % vec) return fail(PARTIR_E_LAYOUT, "K/R must be a multiple of %d (16-byte shard views)", vec);
   if ((a.N / rn) % 4) return fail(PARTIR_E_LAYOUT, "N/R must be a multiple of 4 (16-byte shard views)");
+  if (a.ab == PARTIR_BF16 && a.b_layout == PARTIR_B_KN && ((a.N % 8) || ((a.N / rn) % 8)))
+    return fail(PARTIR_E_LAYOUT, "bf16 B as [K, N]: N and N/R must be multiples of 8 (16-byte rows of B)");
   if (with_ptrs && (!aligned16(a.A) || !aligned16(a.B) || !aligned16(a.C)))
     return fail(PARTIR_E_LAYOUT, "A, B and C must be 16-byte aligned");
   return PARTIR_OK;

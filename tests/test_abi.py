@@ -84,7 +84,10 @@ def mm(M=256, N=256, K=512, lda=None, ldb=None, ldc=None, ab=P.F32, c=P.F32, bl=
     (dict(ws_bytes=16), "PARTIR_E_WORKSPACE"),
     (dict(ws=NULL), "PARTIR_E_NULL"),
     (dict(impl=9), "PARTIR_E_UNSUPPORTED"),
-    (dict(ab=P.BF16, bl=P.B_KN), "PARTIR_E_UNSUPPORTED"),
+    # bf16 B as [K, N]: its rows are read in 16-byte chunks
+    (dict(ab=P.BF16, c=P.BF16, bl=P.B_KN, N=260, ldc=264, ldb=264, summ=P.AXIS_NONE, R=1), "PARTIR_E_LAYOUT"),
+    (dict(ab=P.BF16, c=P.BF16, bl=P.B_KN, N=264, tile=P.AXIS_N, summ=P.AXIS_NONE, R=2), "PARTIR_E_LAYOUT"),
+    (dict(ab=P.BF16, c=P.BF16, bl=P.B_KN, N=264, summ=P.AXIS_NONE, R=1, ws=NULL, ws_bytes=0), "PARTIR_E_HIP"),
 ])
 def test_loop_matmul_validation(kwargs, status):
     st = mm(**kwargs)

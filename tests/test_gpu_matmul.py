@@ -249,3 +249,47 @@ def test_last_wave_split_full_size_sampled_rows():
     err = O.normalised_error(C[rows], O.matmul(Ar, B.f64()), O.abs_product(Ar, B.f64()))
     say(f"    {len(rows)} rows, max normalised error {err:.3e}")
     assert err <= accum_bound(K)
+
+
+# ---------------------------------------------------------------------------
+# bf16 B given as a row-major [K, N] array (read in place: MN-major tiles and
+# transposed fragment reads in the GEMM)
+@pytest.mark.parametrize("out", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("tile,summ,R", [(None, None, 1), ("M", None, 4), ("N", None, 4), (None, "K", 4),
+                                         ("M", "K", 4), ("N", "K", 2), (None, "K", 8)])
+def test_bf16_b_kn_modes_ragged(tile, summ, R, out):
+    M, N, K = 600, 544, 448         # several 256-wide tiles with ragged tails
+    A = I.gaussian(124, 0, (M, K), 1.0, "bf16")
+    B = I.gaussian(124, 1, (K, N), K ** -0.5, "bf16")
+    for impl in ("fused", "splitk"):
+        say(f"bf16 B[K,N] {M}x{N}x{K} tile={tile} sum={summ} R={R} out={out} {impl}")
+        C = run(A, B, tile, summ, R, "kn", out_dtype=out, sum_impl=impl)
+        err = check(A, B, C, tile, summ, R, TOL_BF16)
+        assert err <= accum_bound(K) + (2.0 ** -8 if out == torch.bfloat16 else 0.0)
+
+
+def test_bf16_b_kn_integer_exact_and_layouts_agree():
+    """Small integers: B as [K, N] and as B^T [N, K] both give the exact
+    product, bit for bit; also through the last-wave split (K = 4160)."""
+    for M, N, K in [(320, 272, 512), (1000, 320, 4160)]:
+        A = I.small_ints(125, 0, (M, K), dtype="bf16")
+        B = I.small_ints(125, 1, (K, N), dtype="bf16")
+        ref = O.matmul(A.f64(), B.f64())
+        for tile, summ, R in [(None, None, 1), ("M", None, 4), ("N", None, 2), (None, "K", 8)]:
+            say(f"integer bf16 B[K,N] {M}x{N}x{K} tile={tile} sum={summ} R={R}")
+            kn = run(A, B, tile, summ, R, "kn", out_dtype=torch.float32)
+            nk = run(A, B, tile, summ, R, "nk", out_dtype=torch.float32)
+            assert np.array_equal(host(kn), ref) and torch.equal(kn, nk)
+
+
+def test_bf16_b_kn_full_size_sampled_rows():
+    M, N, K = 8192, 4096, 4096
+    A = I.gaussian(126, 0, (M, K), 1.0, "bf16")
+    B = I.gaussian(126, 1, (K, N), K ** -0.5, "bf16")
+    say(f"bf16 B[K,N] {M}x{N}x{K} (sampled rows)")
+    C = host(run(A, B, None, None, 1, "kn", out_dtype=torch.float32))
+    rows = sorted({0, M - 1} | {256 * t + (53 * t) % 256 for t in range(M // 256)})
+    Ar = A.f64()[rows]
+    err = O.normalised_error(C[rows], O.matmul(Ar, B.f64()), O.abs_product(Ar, B.f64()))
+    say(f"    {len(rows)} rows, max normalised error {err:.3e}")
+    assert err <= accum_bound(K)
