@@ -98,7 +98,8 @@ def setup(w, P, I):
         core = W.attn_core_flops(B, S, H, dh)
         roles = {"attn.qkv": 6.0 * T * D * D, "attn.out": 2.0 * T * D * D, "attn.core": core,
                  "attn.bwd.da": 2.0 * T * D * D, "attn.bwd": 2.5 * core, "attn.bwd.dx": 6.0 * T * D * D,
-                 "attn.bwd.dwqkv": 6.0 * T * D * D, "attn.bwd.dwo": 2.0 * T * D * D}
+                 "attn.bwd.dwqkv": 2.0 * T * D * D,   # one launch per weight
+                 "attn.bwd.dwo": 2.0 * T * D * D}
         return x, step, roles, "mfma_bf16"
     if w.kind == "mlp_z3":
         T, D, F, Rb, Rm = w["T"], w["D"], w["F"], w["R_batch"], w["R_model"]

@@ -1,6 +1,5 @@
-// HBM-bound helpers of the MLP backward pass: bf16 transposes (the weight
-// gradients contract over the token dim, which the GEMM wants contiguous),
-// the activation backward fused with the transposes it feeds, and
+// HBM-bound helpers of the MLP backward pass: the activation backward (dZ
+// and H from Z and dH, with the block column sums of dZ for db1 fused) and
 // deterministic column sums for the bias gradients.
 #include "kernels.h"
 #include "device_math.h"
@@ -17,40 +16,8 @@ constexpr int TP = TT + 2;      // LDS row pitch in elements (spreads columns ov
 __device__ __forceinline__ float bf2f(uint16_t u) { return __uint_as_float((uint32_t)u << 16); }
 __device__ __forceinline__ uint16_t f2bf(float f) { return __builtin_bit_cast(uint16_t, (__bf16)f); }
 
-// 256 threads per 64 x 64 tile; thread t moves 16-byte chunks (8 elements).
-__global__ __launch_bounds__(256) void transpose_bf16_kernel(TransposeParams p) {
-  __shared__ uint16_t tile[TT][TP];
-  const int ntc = (p.cols + TT - 1) / TT;      // 1-D grid: tile (row block, col block)
-  const int r0 = (int)(blockIdx.x / ntc) * TT, c0 = (int)(blockIdx.x % ntc) * TT;
-  const int tid = threadIdx.x;
-#pragma unroll
-  for (int k = 0; k < 2; ++k) {
-    const int id = tid + 256 * k;                 // 512 chunks: 64 rows x 8 chunks
-    const int r = id >> 3, c = (id & 7) * 8;
-    if (r0 + r < p.rows && c0 + c < p.cols) {
-      const i32x4 v = *(const i32x4*)(p.in + (int64_t)(r0 + r) * p.ldi + c0 + c);
-      const uint16_t* e = (const uint16_t*)&v;
-#pragma unroll
-      for (int j = 0; j < 8; ++j) tile[r][c + j] = e[j];
-    }
-  }
-  __syncthreads();
-#pragma unroll
-  for (int k = 0; k < 2; ++k) {
-    const int id = tid + 256 * k;                 // output: 64 rows (input cols) x 8 chunks
-    const int oc = id >> 3, orr = (id & 7) * 8;   // output row = input col, 8 input rows
-    if (c0 + oc < p.cols && r0 + orr < p.rows) {
-      i32x4 v;
-      uint16_t* e = (uint16_t*)&v;
-#pragma unroll
-      for (int j = 0; j < 8; ++j) e[j] = tile[orr + j][oc];
-      *(i32x4*)(p.out + (int64_t)(c0 + oc) * p.ldo + r0 + orr) = v;
-    }
-  }
-}
-
+// 256 threads per 64 x 64 tile; thread t handles 16-byte chunks (8 elements).
 __global__ __launch_bounds__(256) void act_backward_kernel(ActBwdParams p) {
-  __shared__ uint16_t th[TT][TP];
   __shared__ uint16_t tdz[TT][TP];
   const int ntc = (p.cols + TT - 1) / TT;      // 1-D grid: tile (row block, col block)
   const int r0 = (int)(blockIdx.x / ntc) * TT, c0 = (int)(blockIdx.x % ntc) * TT;
@@ -65,18 +32,20 @@ __global__ __launch_bounds__(256) void act_backward_kernel(ActBwdParams p) {
       const i32x4 gv = *(const i32x4*)(p.dH + off);
       const uint16_t* z = (const uint16_t*)&zv;
       const uint16_t* g = (const uint16_t*)&gv;
-      i32x4 dzv;
+      i32x4 dzv, hv;
       uint16_t* dz = (uint16_t*)&dzv;
+      uint16_t* hh = (uint16_t*)&hv;
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
         const float x = bf2f(z[j]);
         float y = x, d = 1.0f;
         if (p.act) gelu_erf_and_grad(x, y, d);
         dz[j] = f2bf(bf2f(g[j]) * d);
-        th[r][c + j] = f2bf(y);
+        hh[j] = f2bf(y);
         tdz[r][c + j] = dz[j];
       }
       *(i32x4*)(p.dZ + off) = dzv;
+      *(i32x4*)(p.H + off) = hv;
     }
   }
   __syncthreads();
@@ -93,24 +62,6 @@ __global__ __launch_bounds__(256) void act_backward_kernel(ActBwdParams p) {
     __syncthreads();
     if (q == 0 && c0 + c < p.cols)
       p.colpart[(int64_t)(r0 / TT) * p.cols + c0 + c] = ((qs[0][c] + qs[1][c]) + qs[2][c]) + qs[3][c];
-  }
-#pragma unroll
-  for (int k = 0; k < 2; ++k) {
-    const int id = tid + 256 * k;
-    const int oc = id >> 3, orr = (id & 7) * 8;
-    if (c0 + oc < p.cols && r0 + orr < p.rows) {
-      i32x4 hv, dv;
-      uint16_t* he = (uint16_t*)&hv;
-      uint16_t* de = (uint16_t*)&dv;
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        he[j] = th[orr + j][oc];
-        de[j] = tdz[orr + j][oc];
-      }
-      const int64_t off = (int64_t)(c0 + oc) * p.ldt + r0 + orr;
-      *(i32x4*)(p.Ht + off) = hv;
-      *(i32x4*)(p.dZt + off) = dv;
-    }
   }
 }
 
@@ -164,13 +115,6 @@ __global__ __launch_bounds__(256) void colsum_final_kernel(ColSumParams p) {
 static unsigned tile_grid(int rows, int cols) {
   const int64_t n = (int64_t)((rows + TT - 1) / TT) * ((cols + TT - 1) / TT);
   return n < (int64_t)1 << 31 ? (unsigned)n : 0u;
-}
-
-hipError_t launch_transpose_bf16(const TransposeParams& p, hipStream_t s) {
-  if (p.rows == 0 || p.cols == 0) return hipSuccess;
-  if (p.rows % 8 || p.cols % 8 || !tile_grid(p.rows, p.cols)) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(transpose_bf16_kernel, dim3(tile_grid(p.rows, p.cols)), dim3(256), 0, s, p);
-  return hipGetLastError();
 }
 
 hipError_t launch_act_backward(const ActBwdParams& p, hipStream_t s) {

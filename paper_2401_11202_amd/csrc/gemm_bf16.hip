@@ -230,7 +230,18 @@ __device__ __forceinline__ void gemm_body(const GemmParams& p, const GemmParts* 
       char* base = smem + stage * STAGE + lds_w;
       __amdgpu_buffer_rsrc_t rma, rmb;
       if (AMN) rma = make_rsrc(p.A + (int64_t)kb * p.lda + row0, kvalid * (uint32_t)p.lda * 2);
-      if (BMN) rmb = make_rsrc(Bg + (int64_t)kb * p.ldb + col0, kvalid * (uint32_t)p.ldb * 2);
+      if (BMN) {
+        // B stacked along K from p.B[0..2] (b_kpart_rows rows each; a k tile
+        // never straddles two of them), or one array
+        const uint16_t* bs = Bg;
+        int krow = kb;
+        if (p.b_kpart_rows) {
+          const int part = kb / p.b_kpart_rows;
+          bs = pick3(part, p.B[0], p.B[1], p.B[2]);
+          krow = kb - part * p.b_kpart_rows;
+        }
+        rmb = make_rsrc(bs + (int64_t)krow * p.ldb + col0, kvalid * (uint32_t)p.ldb * 2);
+      }
       const uint32_t kmask = (kb + lchunk * 8 < k_end) ? 0u : OOB;
       const uint32_t so = (uint32_t)kb * 2;
 #pragma unroll
@@ -629,6 +640,10 @@ hipError_t dispatch_mn(const GemmParams& p, hipStream_t s) {
 
 template <int FIX>
 hipError_t dispatch(const GemmParams& p, hipStream_t s) {
+  // B stacked along K: whole 64-row k tiles inside one of the three arrays
+  if (p.b_kpart_rows && (!p.b_mn || p.ngroups != 1 || p.b_kpart_rows % BK || p.K > 3 * p.b_kpart_rows ||
+                         (p.nsplit > 1 && p.ks % BK)))
+    return hipErrorInvalidValue;
   if (!FIX && (p.a_mn || p.b_mn)) {
     if (p.a_mn && p.b_mn) return dispatch_mn<1, 1>(p, s);
     return p.a_mn ? dispatch_mn<1, 0>(p, s) : dispatch_mn<0, 1>(p, s);

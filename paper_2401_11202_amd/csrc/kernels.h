@@ -52,6 +52,9 @@ struct GemmParams {
   // (A stored [K, M] with leading dim lda, B stored [K, N] with leading dim
   // ldb).  MN-major operands take no activation.
   int a_mn, b_mn;
+  // MN-major B only, one group: B is B[0], B[1], B[2] stacked along K,
+  // b_kpart_rows rows each (a multiple of 64); 0: B[group] alone.
+  int b_kpart_rows;
 };
 
 hipError_t launch_gemm_bf16(const GemmParams& p, hipStream_t s);
@@ -190,29 +193,19 @@ struct RmsParts {
 };
 hipError_t launch_rmsnorm_parts(const RmsParams& p, const RmsParts& t, hipStream_t s);
 
-// out[c][r] = in[r][c] for a bf16 [rows, cols] matrix (rows, cols multiples
-// of 8; 64 x 64 tiles through LDS).
-struct TransposeParams {
-  const uint16_t* in;
-  uint16_t* out;
-  int64_t ldi, ldo;
-  int rows, cols;
-};
-hipError_t launch_transpose_bf16(const TransposeParams& p, hipStream_t s);
 
 // Backward of H = act(Z) for Z, dH [rows, cols] bf16: dZ = dH * act'(Z)
-// (row-major) and the transposes H^T, dZ^T [cols, rows] (for the weight
-// gradients' contractions over rows).  act 0 = identity, 1 = GELU-erf.
-// With colpart set, also the column sums of dZ (as stored, bf16) over each
-// block of 64 rows: colpart[row block][col], the first stage of launch_colsum.
+// and H = act(Z), both [rows, cols] bf16 with leading dim ld (the weight
+// gradients read them in place).  act 0 = identity, 1 = GELU-erf.  With
+// colpart set, also the column sums of dZ (as stored, bf16) over each block
+// of 64 rows: colpart[row block][col], the first stage of launch_colsum.
 struct ActBwdParams {
   const uint16_t* Z;
   const uint16_t* dH;
   uint16_t* dZ;
-  uint16_t* Ht;
-  uint16_t* dZt;
+  uint16_t* H;
   float* colpart;
-  int64_t ld, ldt;
+  int64_t ld;
   int rows, cols;
   int act;
 };

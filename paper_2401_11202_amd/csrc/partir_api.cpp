@@ -60,7 +60,7 @@ bool valid_dtype(int dt) { return dt == PARTIR_F32 || dt == PARTIR_BF16; }
 // ---------------------------------------------------------------------------
 // Plans
 // ---------------------------------------------------------------------------
-enum LaunchKind { L_GEMM_BF16, L_GEMM_F32, L_REDUCE, L_ATTN, L_ATTN_COMBINE, L_RMS, L_TRANSPOSE, L_ACT_BWD, L_COLSUM,
+enum LaunchKind { L_GEMM_BF16, L_GEMM_F32, L_REDUCE, L_ATTN, L_ATTN_COMBINE, L_RMS, L_ACT_BWD, L_COLSUM,
                   L_GEMM_BF16_PARTS, L_ATTN_BWD, L_RMS_PARTS, L_GEMM_BF16_FIXUP, L_GEMM_BF16_PARTS_FIXUP };
 
 struct Launch {
@@ -72,7 +72,6 @@ struct Launch {
   ReduceParams reduce{};
   AttnParams attn{};
   RmsParams rms{};
-  TransposeParams tr{};
   ActBwdParams act{};
   ColSumParams cs{};
   std::shared_ptr<GemmParts> parts;   // L_GEMM_BF16_PARTS: the device-local arrays
@@ -124,6 +123,7 @@ struct GemmSpec {
   void* aux = nullptr;          // bf16 pre-activation output (kept for a backward pass)
   bool tail_ok = false;         // the caller's workspace region holds gemm_ws_bytes (tail split allowed)
   bool a_mn = false;            // bf16 A stored [K, M] (leading dim lda) instead of [M, K]
+  int b_kstack = 0;             // B stored [K, N] as B[0], B[1], B[2] stacked along K, this many rows each
   const char* name = "gemm";    // role, used as the trace name
   const char* label = "gemm";   // loop nest, for the plan text
 };
@@ -175,7 +175,13 @@ std::string describe_gemm(const GemmSpec& g, int64_t grid, bool split) {
            g.ngroups > 1 ? " per group" : "", g.rk, (long long)(g.K / g.rk),
            g.rk <= 1 ? "(none)" : (split ? "split-K fp32 partials + ordered reduce" : "fused in accumulator, r ascending"),
            (long long)grid);
-  return buf;
+  std::string t = buf;
+  if (g.ab_dtype == PARTIR_BF16 && (g.a_mn || !g.b_nk)) {
+    t += "; read in place:";
+    if (g.a_mn) t += " A as [K, M]";
+    if (!g.b_nk) t += g.b_kstack ? " B as [K, N] stacked from 3 arrays" : " B as [K, N]";
+  }
+  return t;
 }
 
 // Appends the launches of one GEMM to the plan (returns how many).  `ws`
@@ -217,6 +223,7 @@ int plan_gemm(const GemmSpec& g, void* ws, Plan& plan) {
     p.epi = split ? EPI_PARTIAL : (g.aux ? EPI_BF16_SAVE : epi_store);
     p.a_mn = g.a_mn;
     p.b_mn = !g.b_nk;   // B stored [K, N]
+    p.b_kpart_rows = g.b_kstack;
     int64_t tail_base;
     p.tail_parts = gemm_tail_parts(g, &tail_base);
     p.tail_base = (int)tail_base;
@@ -299,7 +306,6 @@ hipError_t run_one(const Launch& L, hipStream_t s) {
     case L_ATTN: return launch_attention(L.attn, s);
     case L_ATTN_COMBINE: return launch_attention_combine(L.attn, s);
     case L_RMS: return launch_rmsnorm(L.rms, s);
-    case L_TRANSPOSE: return launch_transpose_bf16(L.tr, s);
     case L_ACT_BWD: return launch_act_backward(L.act, s);
     case L_COLSUM: return launch_colsum(L.cs, s);
     case L_GEMM_BF16_PARTS: return launch_gemm_bf16_parts(L.gemm, *L.parts, s);
@@ -887,10 +893,6 @@ void plan_attn_bwd(const AttnBwdArgs& a, void* ws, Plan& plan) {
 // ---------------------------------------------------------------------------
 // attention block backward
 // ---------------------------------------------------------------------------
-void plan_transpose(const void* in, void* out, int64_t rows, int64_t cols, const char* name, Plan& plan);
-void plan_transpose_ld(const void* in, int64_t ldi, void* out, int64_t ldo, int64_t rows, int64_t cols,
-                       const char* name, Plan& plan);
-
 struct AttnBlockBwdArgs {
   const void *X = nullptr, *Wq = nullptr, *Wk = nullptr, *Wv = nullptr, *Wo = nullptr;   // stored W^T [out, in]
   const void* saved = nullptr;                                                         // from the training forward
@@ -939,19 +941,15 @@ void plan_attn_block_bwd(const AttnBlockBwdArgs& a, void* ws, Plan& plan) {
   char* base = (char*)ws;
   size_t off = 0;
   auto take = [&](size_t n) { char* p = base ? base + off : nullptr; off += n; return (void*)p; };
-  void* WoT = take(dd);
-  void* WqkvT = take(3 * dd);
   void* dA = take(td);
   void* dQKV = take(3 * td);
-  void* dQKVt = take(3 * td);
-  void* Xt = take(td);
-  void* dYt = take(td);
-  void* At = take(td);
   void* Dst = take(align_up((size_t)T * a.H * 4));
   void* part = base ? base + off : nullptr;
-  plan_transpose(a.Wo, WoT, D, D, "bwd.transpose", plan);
+  // Every operand is read where it lies: the stored W^T arrays are the
+  // [K, N] right operands of dA and dX, and the activations are the [K, M] /
+  // [K, N] operands of the weight gradients (no transposed copies).
   GemmSpec ga;
-  ga.A = a.dY; ga.B[0] = WoT; ga.C[0] = dA;
+  ga.A = a.dY; ga.B[0] = a.Wo; ga.b_nk = 0; ga.C[0] = dA;
   ga.lda = D; ga.ldb = D; ga.ldc = D; ga.M = T; ga.N = D; ga.K = D;
   ga.c_dtype = PARTIR_BF16; ga.rm = a.Rb; ga.rn = a.Rm;
   ga.name = "attn.bwd.da"; ga.label = "bwd.da dA = slice 0 dY[b] . (slice 0 Wo[m])^T";
@@ -965,38 +963,29 @@ void plan_attn_block_bwd(const AttnBlockBwdArgs& a, void* ws, Plan& plan) {
   Launch L = core.launches.back();
   L.attn_bwd.lddq = L.attn_bwd.lddk = L.attn_bwd.lddv = 3 * D;   // [dQ | dK | dV] side by side
   plan.launches.push_back(L);
-  const void* Wqkv[3] = {a.Wq, a.Wk, a.Wv};
-  for (int i = 0; i < 3; ++i)
-    plan_transpose_ld(Wqkv[i], D, WqkvT ? (char*)WqkvT + i * D * 2 : nullptr, 3 * D, D, D, "bwd.transpose", plan);
   GemmSpec gx;
-  gx.A = dQKV; gx.B[0] = WqkvT; gx.C[0] = a.dX;
-  gx.lda = 3 * D; gx.ldb = 3 * D; gx.ldc = D; gx.M = T; gx.N = D; gx.K = 3 * D;
+  gx.A = dQKV; gx.B[0] = a.Wq; gx.B[1] = a.Wk; gx.B[2] = a.Wv; gx.b_nk = 0; gx.b_kstack = (int)D;
+  gx.C[0] = a.dX;
+  gx.lda = 3 * D; gx.ldb = D; gx.ldc = D; gx.M = T; gx.N = D; gx.K = 3 * D;
   gx.c_dtype = PARTIR_F32; gx.rm = a.Rb;
   gx.name = "attn.bwd.dx"; gx.label = "bwd.dx dX = sum over m and q|k|v of dQKV[b][:, m] . W{q,k,v}[:, m]^T";
   plan_gemm(gx, part, plan);
-  plan_transpose(dQKV, dQKVt, T, 3 * D, "bwd.transpose", plan);
-  plan_transpose(a.X, Xt, T, D, "bwd.transpose", plan);
-  GemmSpec gw;
-  gw.A = dQKVt; gw.B[0] = Xt; gw.C[0] = nullptr;
-  gw.lda = T; gw.ldb = T; gw.ldc = D; gw.M = 3 * D; gw.N = D; gw.K = T;
-  gw.c_dtype = PARTIR_F32; gw.rm = 3 * a.Rm; gw.rk = a.Rb; gw.sum_impl = PARTIR_SUM_FUSED;
-  gw.name = "attn.bwd.dwqkv";
-  gw.label = "bwd.dwqkv dW{q,k,v}^T = sum_b dQKV[b][:, m]^T . slice 0 X[b]";
-  plan_gemm(gw, nullptr, plan);
-  {
-    Launch& W = plan.launches.back();
-    W.kind = L_GEMM_BF16_PARTS;
-    GemmParts* t = new GemmParts{};
-    t->c_rows = (int)D;
-    t->c[0] = a.dWq; t->c[1] = a.dWk; t->c[2] = a.dWv;
-    W.parts.reset(t);
-    W.text += "; rows stored into dWq^T, dWk^T, dWv^T";
+  const char* wnames[3] = {"bwd.dwq dWq^T = sum_b dQ[b][:, m]^T . slice 0 X[b]",
+                           "bwd.dwk dWk^T = sum_b dK[b][:, m]^T . slice 0 X[b]",
+                           "bwd.dwv dWv^T = sum_b dV[b][:, m]^T . slice 0 X[b]"};
+  void* dW[3] = {a.dWq, a.dWk, a.dWv};
+  for (int i = 0; i < 3; ++i) {
+    GemmSpec gw;
+    gw.A = dQKV ? (char*)dQKV + i * D * 2 : nullptr; gw.a_mn = true;
+    gw.B[0] = a.X; gw.b_nk = 0; gw.C[0] = dW[i];
+    gw.lda = 3 * D; gw.ldb = D; gw.ldc = D; gw.M = D; gw.N = D; gw.K = T;
+    gw.c_dtype = PARTIR_F32; gw.rm = a.Rm; gw.rk = a.Rb; gw.sum_impl = PARTIR_SUM_FUSED;
+    gw.name = "attn.bwd.dwqkv"; gw.label = wnames[i];
+    plan_gemm(gw, nullptr, plan);
   }
-  plan_transpose(a.dY, dYt, T, D, "bwd.transpose", plan);
-  plan_transpose(Ao, At, T, D, "bwd.transpose", plan);
   GemmSpec go;
-  go.A = dYt; go.B[0] = At; go.C[0] = a.dWo;
-  go.lda = T; go.ldb = T; go.ldc = D; go.M = D; go.N = D; go.K = T;
+  go.A = a.dY; go.a_mn = true; go.B[0] = Ao; go.b_nk = 0; go.C[0] = a.dWo;
+  go.lda = D; go.ldb = D; go.ldc = D; go.M = D; go.N = D; go.K = T;
   go.c_dtype = PARTIR_F32; go.rn = a.Rm; go.rk = a.Rb;
   go.name = "attn.bwd.dwo"; go.label = "bwd.dwo dWo^T = sum_b (slice 0 dY[b])^T . A[b][:, m]";
   plan_gemm(go, part, plan);
@@ -1037,27 +1026,6 @@ int validate_mlp_bwd(const MlpBwdArgs& a, bool with_ptrs) {
                     !aligned16(a.db1) || !aligned16(a.db2) || !aligned16(a.Z)))
     return fail(PARTIR_E_LAYOUT, "tensors must be 16-byte aligned");
   return PARTIR_OK;
-}
-
-void plan_transpose(const void* in, void* out, int64_t rows, int64_t cols, const char* name, Plan& plan) {
-  Launch L;
-  L.kind = L_TRANSPOSE;
-  L.name = name;
-  L.tr.in = (const uint16_t*)in; L.tr.out = (uint16_t*)out;
-  L.tr.ldi = cols; L.tr.ldo = rows; L.tr.rows = (int)rows; L.tr.cols = (int)cols;
-  char buf[160];
-  snprintf(buf, sizeof buf, "transpose: [%lld,%lld] -> [%lld,%lld] bf16", (long long)rows, (long long)cols,
-           (long long)cols, (long long)rows);
-  L.text = buf;
-  plan.launches.push_back(L);
-}
-
-// out[c][r] = in[r][c] with explicit leading dims (a column block of a wider output)
-void plan_transpose_ld(const void* in, int64_t ldi, void* out, int64_t ldo, int64_t rows, int64_t cols,
-                       const char* name, Plan& plan) {
-  plan_transpose(in, out, rows, cols, name, plan);
-  plan.launches.back().tr.ldi = ldi;
-  plan.launches.back().tr.ldo = ldo;
 }
 
 void plan_colsum(const void* in, void* partial, void* out, int64_t rows, int64_t cols, bool partial_ready,
@@ -1102,20 +1070,14 @@ void plan_mlp_bwd(const MlpBwdArgs& a, void* ws, Plan& plan) {
   void* Z = a.Z ? (void*)a.Z : take(tf);
   void* dH = take(tf);
   void* dZ = take(tf);
-  void* Ht = take(tf);
-  void* dZt = take(tf);
-  void* Xt = take(td);
-  void* dYt = take(td);
-  void* W1 = take(df);
-  void* W2 = take(df);
+  void* H = take(tf);
   void* csp = take(cs_bytes);
   void* part = base ? base + off : nullptr;
+  // Every operand is read where it lies: W1^T and W2^T are the [K, N] right
+  // operands of dX and dH, and the activations the [K, M] / [K, N] operands
+  // of the weight gradients (no transposed copies).
   GemmSpec gz, gh, g2, g1, gx;
   if (live) {
-    plan_transpose(a.X, Xt, T, D, "bwd.transpose", plan);
-    plan_transpose(a.dY, dYt, T, D, "bwd.transpose", plan);
-    plan_transpose(a.W1t, W1, F, D, "bwd.transpose", plan);
-    plan_transpose(a.W2t, W2, D, F, "bwd.transpose", plan);
     if (!a.Z) {
       gz.A = a.X; gz.B[0] = a.W1t; gz.C[0] = Z; gz.bias[0] = (const float*)a.b1;
       gz.lda = D; gz.ldb = D; gz.ldc = F; gz.M = T; gz.N = F; gz.K = D;
@@ -1123,8 +1085,8 @@ void plan_mlp_bwd(const MlpBwdArgs& a, void* ws, Plan& plan) {
       gz.name = "mlp.bwd.z"; gz.label = "bwd.z  Z = slice 0 X[b] . slice 1 W1[m] (recomputed)";
       plan_gemm(gz, nullptr, plan);
     }
-    gh.A = a.dY; gh.B[0] = W2; gh.C[0] = dH;
-    gh.lda = D; gh.ldb = D; gh.ldc = F; gh.M = T; gh.N = F; gh.K = D;
+    gh.A = a.dY; gh.B[0] = a.W2t; gh.b_nk = 0; gh.C[0] = dH;
+    gh.lda = D; gh.ldb = F; gh.ldc = F; gh.M = T; gh.N = F; gh.K = D;
     gh.c_dtype = PARTIR_BF16; gh.rm = a.Rb; gh.rn = a.Rm;
     gh.name = "mlp.bwd.dh"; gh.label = "bwd.dh dH = slice 0 dY[b] . (slice 0 W2[m])^T";
     plan_gemm(gh, nullptr, plan);
@@ -1132,23 +1094,23 @@ void plan_mlp_bwd(const MlpBwdArgs& a, void* ws, Plan& plan) {
     E.kind = L_ACT_BWD;
     E.name = "mlp.bwd.act";
     E.act.Z = (const uint16_t*)Z; E.act.dH = (const uint16_t*)dH; E.act.dZ = (uint16_t*)dZ;
-    E.act.Ht = (uint16_t*)Ht; E.act.dZt = (uint16_t*)dZt; E.act.ld = F; E.act.ldt = T;
+    E.act.H = (uint16_t*)H; E.act.ld = F;
     E.act.colpart = a.db1 ? (float*)csp : nullptr;   // db1's block sums, fused
     E.act.rows = (int)T; E.act.cols = (int)F; E.act.act = a.act;
-    E.text = a.act ? "act_backward: dZ = dH * gelu'(Z); H^T, dZ^T" : "act_backward: dZ = dH; H^T, dZ^T";
+    E.text = a.act ? "act_backward: dZ = dH * gelu'(Z); H = gelu(Z)" : "act_backward: dZ = dH; H = Z";
     plan.launches.push_back(E);
-    g2.A = dYt; g2.B[0] = Ht; g2.C[0] = a.dW2t;
-    g2.lda = T; g2.ldb = T; g2.ldc = F; g2.M = D; g2.N = F; g2.K = T;
+    g2.A = a.dY; g2.a_mn = true; g2.B[0] = H; g2.b_nk = 0; g2.C[0] = a.dW2t;
+    g2.lda = D; g2.ldb = F; g2.ldc = F; g2.M = D; g2.N = F; g2.K = T;
     g2.ab_dtype = PARTIR_BF16; g2.c_dtype = PARTIR_F32; g2.rn = a.Rm; g2.rk = a.Rb;
     g2.name = "mlp.bwd.dw2"; g2.label = "bwd.dw2 dW2^T = sum_b (slice 0 dY[b])^T . H[b][:, m]";
     plan_gemm(g2, part, plan);
-    g1.A = dZt; g1.B[0] = Xt; g1.C[0] = a.dW1t;
-    g1.lda = T; g1.ldb = T; g1.ldc = D; g1.M = F; g1.N = D; g1.K = T;
+    g1.A = dZ; g1.a_mn = true; g1.B[0] = a.X; g1.b_nk = 0; g1.C[0] = a.dW1t;
+    g1.lda = F; g1.ldb = D; g1.ldc = D; g1.M = F; g1.N = D; g1.K = T;
     g1.c_dtype = PARTIR_F32; g1.rm = a.Rm; g1.rk = a.Rb;
     g1.name = "mlp.bwd.dw1"; g1.label = "bwd.dw1 dW1^T = sum_b dZ[b][:, m]^T . slice 0 X[b]";
     plan_gemm(g1, part, plan);
-    gx.A = dZ; gx.B[0] = W1; gx.C[0] = a.dX;
-    gx.lda = F; gx.ldb = F; gx.ldc = D; gx.M = T; gx.N = D; gx.K = F;
+    gx.A = dZ; gx.B[0] = a.W1t; gx.b_nk = 0; gx.C[0] = a.dX;
+    gx.lda = F; gx.ldb = D; gx.ldc = D; gx.M = T; gx.N = D; gx.K = F;
     gx.c_dtype = PARTIR_F32; gx.rm = a.Rb; gx.rk = a.Rm;
     gx.name = "mlp.bwd.dx"; gx.label = "bwd.dx dX = sum_m dZ[b][:, m] . (slice 1 W1[m])^T";
     plan_gemm(gx, part, plan);

@@ -350,7 +350,9 @@ def test_mlp_backward_plans():
     t = p["text"]
     assert p["n_virtual_shards"] == 16 and p["n_tile_loops"] == 2 and p["n_sum_loops"] == 3
     assert p["flops"] == 10.0 * T * D * F
-    assert t.count("transpose") == 4 and "act_backward" in t
+    # no transposed copies: W1^T, W2^T and the activations are read in place
+    assert "transpose" not in t and "act_backward" in t and t.count("read in place") == 4
+    assert t.count("A as [K, M] B as [K, N]") == 2
     # the batch #sum of the weight gradients runs over K = tokens, 2 shards
     assert "dW2^T = sum_b" in t and "#sum K x2 (4096/shard)" in t
     # the model #sum of dX runs over K = F, 8 shards
@@ -518,3 +520,17 @@ def test_last_wave_tail_split(M, N, K, tail, parts):
         assert ".fixup" not in t and p["n_launches"] == 1 and p["workspace_bytes"] == 0
     assert P.lib().partir_loop_matmul_workspace(M, N, K, P.BF16, P.BF16, P.B_NK, -1, -1, 1, P.SUM_AUTO) == \
         p["workspace_bytes"]
+
+
+def test_attn_block_backward_plan_reads_operands_in_place():
+    """No transposed copies: Wo^T and W{q,k,v}^T are the [K, N] right operands
+    of dA and dX (the three stacked along K), and dY, dQ|dK|dV, X and the
+    attention output the [K, M] / [K, N] operands of the weight gradients."""
+    B, S, D, H = 4, 2048, 4096, 32
+    p = P.plan_attn_block_backward(B, S, D, H, R_batch=2, R_model=8)
+    t = p["text"]
+    assert "transpose" not in t
+    assert t.count("B as [K, N] stacked from 3 arrays") == 1            # dX
+    assert t.count("A as [K, M] B as [K, N]") == 4                      # dWq, dWk, dWv, dWo
+    assert t.count("read in place") == 6                                # + dA
+    assert P.lib().partir_attn_block_backward_workspace(B, S, D, H, 128, 2, 8) == p["workspace_bytes"]
