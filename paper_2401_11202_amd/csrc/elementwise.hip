@@ -39,6 +39,9 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(ReduceParams p) {
   }
 }
 
+// rows up to 256 * RMS_REG_CHUNKS wide are held in registers
+constexpr int RMS_REG_CHUNKS = 24;
+
 // One wave per row: fp32 sum of squares over D, then y = bf16(g * x * rstd).
 // With parts, row r of x lives in the part r / rows_part (device-local arrays).
 template <int PARTS>
@@ -51,22 +54,45 @@ __device__ __forceinline__ void rmsnorm_body(const RmsParams& p, const RmsParts*
     const int part = row / t->rows_part;
     x = t->x[part] + (int64_t)(row - part * t->rows_part) * p.ldx;
   }
+  uint16_t* y = p.y + (int64_t)row * p.ldy;
+  auto store = [&](int c, const f32x4& v, float rstd) {
+    const f32x4 g = *(const f32x4*)(p.g + c);
+    bf16x4 o = {(__bf16)(g[0] * (v[0] * rstd)), (__bf16)(g[1] * (v[1] * rstd)),
+                (__bf16)(g[2] * (v[2] * rstd)), (__bf16)(g[3] * (v[3] * rstd))};
+    *(bf16x4*)(y + c) = o;
+  };
+  auto rstd_of = [&](float ss) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) ss += __shfl_xor(ss, o);
+    return 1.0f / sqrtf(ss / (float)p.D + p.eps);
+  };
+  if (p.D <= 256 * RMS_REG_CHUNKS) {
+    // the row stays in registers: every load issued before the first use,
+    // one HBM read of x
+    f32x4 v[RMS_REG_CHUNKS];
+#pragma unroll
+    for (int i = 0; i < RMS_REG_CHUNKS; ++i) {
+      const int c = lane * 4 + 256 * i;
+      v[i] = c < p.D ? *(const f32x4*)(x + c) : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+    }
+    float ss = 0.0f;
+#pragma unroll
+    for (int i = 0; i < RMS_REG_CHUNKS; ++i) ss += v[i][0] * v[i][0] + v[i][1] * v[i][1] + v[i][2] * v[i][2] + v[i][3] * v[i][3];
+    const float rstd = rstd_of(ss);
+#pragma unroll
+    for (int i = 0; i < RMS_REG_CHUNKS; ++i) {
+      const int c = lane * 4 + 256 * i;
+      if (c < p.D) store(c, v[i], rstd);
+    }
+    return;
+  }
   float ss = 0.0f;
   for (int c = lane * 4; c < p.D; c += 256) {
     const f32x4 v = *(const f32x4*)(x + c);
     ss += v[0] * v[0] + v[1] * v[1] + v[2] * v[2] + v[3] * v[3];
   }
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) ss += __shfl_xor(ss, o);
-  const float rstd = 1.0f / sqrtf(ss / (float)p.D + p.eps);
-  uint16_t* y = p.y + (int64_t)row * p.ldy;
-  for (int c = lane * 4; c < p.D; c += 256) {
-    const f32x4 v = *(const f32x4*)(x + c);
-    const f32x4 g = *(const f32x4*)(p.g + c);
-    bf16x4 o = {(__bf16)(g[0] * (v[0] * rstd)), (__bf16)(g[1] * (v[1] * rstd)),
-                (__bf16)(g[2] * (v[2] * rstd)), (__bf16)(g[3] * (v[3] * rstd))};
-    *(bf16x4*)(y + c) = o;
-  }
+  const float rstd = rstd_of(ss);
+  for (int c = lane * 4; c < p.D; c += 256) store(c, *(const f32x4*)(x + c), rstd);
 }
 
 __global__ __launch_bounds__(256) void rmsnorm_kernel(RmsParams p) { rmsnorm_body<0>(p, nullptr); }
