@@ -99,12 +99,20 @@ __device__ __forceinline__ bf16x8 row_frag(const char* tile, int r0, int col, in
   return *(const bf16x8*)(tile + toff(r0 + col, (2 * ds + h) * 16));
 }
 
+// ds_read_b64_tr_b16 through a restrict pointer: the alias scope this gives
+// the read keeps the wait insertion from making it wait for every LDS DMA in
+// flight (the next block's loads; the loops order their stages by explicit
+// vmcnt waits and barriers).
+__device__ __forceinline__ i16x4 lds_read_tr16(const char* __restrict__ p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)p);
+}
+
 // A operand X^T[d rows 32 dt.., positions 16 u..] of a tile X [positions x d],
 // the positions permuted as the score registers are (see the forward kernel).
 __device__ __forceinline__ bf16x8 tr_frag(const char* tile, int u, int dt, int v_row, int v_colb) {
   const int row = 16 * u + v_row, colb = 64 * dt + v_colb;
-  const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(tile + toff(row, colb)));
-  const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(tile + toff(row + 8, colb)));
+  const i16x4 lo = lds_read_tr16(tile + toff(row, colb));
+  const i16x4 hi = lds_read_tr16(tile + toff(row + 8, colb));
   return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
 }
 
