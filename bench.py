@@ -351,7 +351,7 @@ def kernel_source_hash():
 def main():
     args = parse()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on exactly one GPU; --gpus must be 1",
+        print(json.dumps({"error": "this benchmark runs on exactly one GPU (every virtual shard on it); --gpus must be 1",
                           "n_gpus": args.gpus}))
         log("bench.py: only --gpus 1 is supported (a single MI355X evaluates every virtual shard)")
         sys.exit(2)

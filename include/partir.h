@@ -71,7 +71,7 @@ typedef enum partir_status {
   PARTIR_E_LAYOUT = 6,       /* leading dim < cols, or 16-byte misalignment      */
   PARTIR_E_WORKSPACE = 7,    /* workspace smaller than the query returns         */
   PARTIR_E_HIP = 8,          /* a HIP runtime call or kernel launch failed       */
-  PARTIR_E_UNSUPPORTED = 9   /* R < 1, or an option this build does not provide  */
+  PARTIR_E_UNSUPPORTED = 9   /* R < 1, or an option the library does not provide */
 } partir_status;
 
 typedef enum partir_dtype { PARTIR_F32 = 0, PARTIR_BF16 = 1 } partir_dtype;
