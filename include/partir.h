@@ -294,8 +294,9 @@ size_t partir_mlp_block_backward_workspace(int64_t T, int64_t D, int64_t F, int 
  * [h*d_head, (h+1)*d_head) of Q, K and V.  Batch shards hold whole sequences.
  * scale <= 0 selects 1/sqrt(d_head).  Y: [B*S, D], out_dtype F32 or BF16.
  * The workspace holds Q, K, V and the attention output (bf16, [B*S, D] each).
- * Constraints: d_head == 128, S a multiple of 128.  B = 0 or S = 0 (no
- * tokens) launches nothing.
+ * Constraints: d_head == 128, S a multiple of 128, S*D*2 < 4 GiB (one
+ * sequence's rows of an [S, D] bf16 array).  B = 0 or S = 0 (no tokens)
+ * launches nothing.
  * Errors: E_NULL, E_SHAPE (n_heads*d_head != D, or d_head / S outside the
  * constraints), E_DIVISIBILITY (R_batch does not divide B or R_model does not
  * divide n_heads), E_DTYPE, E_LAYOUT, E_WORKSPACE, E_UNSUPPORTED, E_HIP.
@@ -369,7 +370,7 @@ size_t partir_attn_block_backward_workspace(int64_t B, int64_t S, int64_t D, int
  * Q, K, V, O: [B*S, n_heads*d_head] bf16 row-major (ld = n_heads*d_head),
  * sequence-major; head h owns columns [h*d_head, (h+1)*d_head).
  * scale <= 0 selects 1/sqrt(d_head).  Constraints: d_head == 128, S a
- * multiple of 128, R_kv dividing S/64.  Workspace (R_kv > 1): the shards'
+ * multiple of 128, S*n_heads*d_head*2 < 4 GiB, R_kv dividing S/64.  Workspace (R_kv > 1): the shards'
  * fp32 o (R_kv*B*S*n_heads*d_head) and m, l (R_kv*B*S*n_heads each).
  * Errors: E_NULL, E_SHAPE, E_DIVISIBILITY (R_kv does not divide S/64),
  * E_LAYOUT, E_WORKSPACE, E_UNSUPPORTED (R_kv < 1), E_HIP.

@@ -559,6 +559,9 @@ int validate_attn_shapes(int64_t B, int64_t S, int64_t D, int64_t H, int64_t dh,
   if (H * dh != D) return fail(PARTIR_E_SHAPE, "n_heads*d_head = %lld != D = %lld", (long long)(H * dh), (long long)D);
   if (dh != 128) return fail(PARTIR_E_SHAPE, "d_head must be 128 (got %lld)", (long long)dh);
   if (S % 128) return fail(PARTIR_E_SHAPE, "S must be a multiple of 128 (got %lld)", (long long)S);
+  // the attention kernels address one sequence's rows of Q, K, V by 32-bit byte offsets
+  if (S * D * 2 > ((int64_t)1 << 32) - 1)
+    return fail(PARTIR_E_SHAPE, "one sequence of S=%lld rows of D=%lld bf16 exceeds 4 GiB", (long long)S, (long long)D);
   if (Rb < 1 || Rm < 1) return fail(PARTIR_E_UNSUPPORTED, "R_batch and R_model must be >= 1");
   if (B % Rb) return fail(PARTIR_E_DIVISIBILITY, "R_batch=%d does not divide B=%lld (batch shards hold whole sequences)", Rb, (long long)B);
   if (H % Rm) return fail(PARTIR_E_DIVISIBILITY, "R_model=%d does not divide n_heads=%lld", Rm, (long long)H);

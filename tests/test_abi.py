@@ -297,6 +297,7 @@ def test_attention_core_plans():
     (dict(R=0), "PARTIR_E_UNSUPPORTED"),
     (dict(S=200), "PARTIR_E_SHAPE"),
     (dict(dh=64), "PARTIR_E_SHAPE"),
+    (dict(S=1 << 20, H=16), "PARTIR_E_SHAPE"),  # one sequence's K: 2^20 x 2048 bf16 = 4 GiB
     (dict(Q=NULL), "PARTIR_E_NULL"),
     (dict(Q=DUMMY_ODD), "PARTIR_E_LAYOUT"),
     (dict(ws_bytes=0), "PARTIR_E_WORKSPACE"),
