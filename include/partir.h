@@ -365,13 +365,19 @@ size_t partir_attn_block_backward_workspace(int64_t B, int64_t S, int64_t D, int
  * (M, 2^(m-M) l + 2^(m'-M) l', 2^(m-M) o + 2^(m'-M) o'), M = max(m, m'),
  * which is associative and commutative; the shards are folded in order
  * s = 0..R_kv-1 and O = o / l.  With causal masking a query sees keys at
- * positions <= its own, so shards past it contribute (-inf, 0, 0).  R_kv = 1
- * is plain attention (no workspace).
+ * positions <= its own, so shards past it contribute (-inf, 0, 0) and are
+ * skipped.  With a causal mask and a grid too small to fill the device several
+ * times over, each shard of at least 2048 keys is evaluated as 2 or 4 ordered
+ * parts of at least 1024 keys, folded in the same order (the plan text names
+ * them).  R_kv = 1 is plain attention (no workspace).
  * Q, K, V, O: [B*S, n_heads*d_head] bf16 row-major (ld = n_heads*d_head),
  * sequence-major; head h owns columns [h*d_head, (h+1)*d_head).
  * scale <= 0 selects 1/sqrt(d_head).  Constraints: d_head == 128, S a
- * multiple of 128, S*n_heads*d_head*2 < 4 GiB, R_kv dividing S/64.  Workspace (R_kv > 1): the shards'
- * fp32 o (R_kv*B*S*n_heads*d_head) and m, l (R_kv*B*S*n_heads each).
+ * multiple of 128, S*n_heads*d_head*2 < 4 GiB, R_kv dividing S/64.
+ * Workspace (R_kv > 1): the parts' fp32 o (P*B*S*n_heads*d_head) and m, l
+ * (P*B*S*n_heads each), P = R_kv times the parts per shard;
+ * partir_attention_workspace gives the size for a causal mask, which is also
+ * enough without one.
  * Errors: E_NULL, E_SHAPE, E_DIVISIBILITY (R_kv does not divide S/64),
  * E_LAYOUT, E_WORKSPACE, E_UNSUPPORTED (R_kv < 1), E_HIP.
  */

@@ -58,13 +58,23 @@ void attention_kernel(AttnParams p) {
   // index; with a split key axis, the shards of one query block are adjacent
   const int nqb = p.S / BQ;
   const int nbh = p.B * p.H;
-  const int qs = blockIdx.x / nbh;
-  const int qb = nqb - 1 - qs / p.nsplit;
-  const int split = qs % p.nsplit;
-  const int bh = blockIdx.x % nbh;
+  const int per_qb = nbh * p.nsplit;
+  const int qs = blockIdx.x / per_qb;
+  const int qb = nqb - 1 - qs;
+  // Workgroup i runs on XCD i mod 8.  Under a causal mask the shards of early
+  // keys carry most of the work, so (shard, head) must not stay tied to one
+  // XCD: rotating it by the query block spreads every shard over all XCDs.
+  int inner = blockIdx.x - qs * per_qb;
+  if (p.nsplit > 1) inner = (inner + qs) % per_qb;
+  const int split = inner / nbh;
+  const int bh = inner - split * nbh;
   const int b = bh / p.H, head = bh - b * p.H;
   const int q0 = qb * BQ;
   const int64_t tok0 = (int64_t)b * p.S;
+  // causal: a key shard that starts past this query block's last query holds
+  // nothing for it; the combine does not read such a shard, so it is skipped
+  // (workgroup-uniform, before any barrier)
+  if (p.nsplit > 1 && p.causal && split * p.kb_per * BKV > q0 + BQ - 1) return;
 
   // ---- this lane's query fragments (B operand of S^T = K Q^T), kept in VGPRs
   const int qi = q0 + 32 * w + col;      // query position of this lane's column
@@ -265,11 +275,15 @@ __global__ __launch_bounds__(256) void attention_combine_kernel(AttnParams p) {
   const int64_t t = th / p.H;
   const int head = (int)(th - t * p.H);
   const int64_t sstride = T * p.H;
+  // with a causal mask, shard s holds keys for this row only if its first key
+  // s * kb_per * 64 is at or before the row's position; the later shards were
+  // not written (their share of the sum is zero)
+  const int nparts = p.causal ? min(p.nsplit, (int)(t % p.S) / (p.kb_per * 64) + 1) : p.nsplit;
   float M = -3.0e38f;
-  for (int s = 0; s < p.nsplit; ++s) M = fmaxf(M, p.Mpart[s * sstride + th]);
+  for (int s = 0; s < nparts; ++s) M = fmaxf(M, p.Mpart[s * sstride + th]);
   float L = 0.0f;
   f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
-  for (int s = 0; s < p.nsplit; ++s) {
+  for (int s = 0; s < nparts; ++s) {
     const float w = __builtin_amdgcn_exp2f(p.Mpart[s * sstride + th] - M);
     L += w * p.Lpart[s * sstride + th];
     acc += w * *(const f32x4*)(p.Opart + (s * T + t) * (int64_t)(p.H * DH) + head * DH + 4 * c4);

@@ -136,7 +136,8 @@ struct AttnParams {
   float scale_log2;  // scale * log2(e)
   // key axis as a loop of nsplit shards (a custom associative #sum): shard s
   // covers key blocks [s * kb_per, (s + 1) * kb_per) of 64 keys and writes its
-  // unnormalised output and softmax statistics instead of O
+  // unnormalised output and softmax statistics instead of O.  With a causal
+  // mask a shard is written only for the rows at or after its first key.
   int nsplit = 1;
   int kb_per = 0;
   float* Opart = nullptr;   // [nsplit][B*S][H*128] fp32, sum_j 2^(s_j c - m) v_j

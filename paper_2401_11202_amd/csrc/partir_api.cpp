@@ -798,6 +798,26 @@ int validate_attn_core(const AttnCoreArgs& a, bool with_ptrs) {
   return PARTIR_OK;
 }
 
+// Parts per key shard of the causal attention core.  A query block needs the
+// key blocks up to its own, so under a causal mask the (query block, shard)
+// workgroups range from empty to a whole shard; when the grid alone does not
+// fill the chip several times over (256 CUs, two attention workgroups each),
+// the longest workgroup sets the time.  Each shard of at least 2 x 16 key
+// blocks then runs as 2 (or 4) ordered parts of at least 16 blocks, folded in
+// key order by the combine like the shards themselves: the same #sum, in
+// smaller pieces.  The combine reads, for each row, only the parts whose
+// first key is at or before it.
+int attn_core_parts(int64_t B, int64_t S, int64_t H, int causal, int Rkv) {
+  constexpr int64_t kFillWorkgroups = 4 * 256 * 2;
+  constexpr int64_t kMinPartBlocks = 16;
+  if (!causal || Rkv < 2) return 1;
+  const int64_t kbs = S / 64 / Rkv, wgs = (S / 128) * B * H * Rkv;
+  int parts = 1;
+  while (parts < 4 && wgs * parts < kFillWorkgroups && kbs % (2 * parts) == 0 && kbs / (2 * parts) >= kMinPartBlocks)
+    parts *= 2;
+  return parts;
+}
+
 void plan_attn_core(const AttnCoreArgs& a, void* ws, Plan& plan) {
   const int64_t T = a.B * a.S, D = a.H * a.dh;
   plan.n_shards = a.Rkv;
@@ -805,7 +825,9 @@ void plan_attn_core(const AttnCoreArgs& a, void* ws, Plan& plan) {
   const double pairs = a.causal ? (double)a.S * (a.S + 1) / 2 : (double)a.S * a.S;
   plan.flops = 4.0 * a.B * a.H * pairs * a.dh;
   if (T == 0) return;
-  const size_t o_bytes = align_up((size_t)a.Rkv * T * D * 4), ml_bytes = align_up((size_t)a.Rkv * T * a.H * 4);
+  const int parts = attn_core_parts(a.B, a.S, a.H, a.causal, a.Rkv);
+  const int nsplit = a.Rkv * parts;
+  const size_t o_bytes = align_up((size_t)nsplit * T * D * 4), ml_bytes = align_up((size_t)nsplit * T * a.H * 4);
   if (a.Rkv > 1) {
     plan.ws_bytes = o_bytes + 2 * ml_bytes;
     plan.n_sum_loops = 1;
@@ -820,17 +842,18 @@ void plan_attn_core(const AttnCoreArgs& a, void* ws, Plan& plan) {
   p.B = (int)a.B; p.S = (int)a.S; p.H = (int)a.H; p.causal = a.causal;
   const float sc = a.scale > 0 ? a.scale : 1.0f / std::sqrt((float)a.dh);
   p.scale_log2 = sc * 1.4426950408889634f;
-  p.nsplit = a.Rkv;
-  p.kb_per = (int)(a.S / 64 / a.Rkv);
+  p.nsplit = nsplit;
+  p.kb_per = (int)(a.S / 64 / nsplit);
   char* base = (char*)ws;
   p.Opart = base ? (float*)base : nullptr;
   p.Mpart = base ? (float*)(base + o_bytes) : nullptr;
   p.Lpart = base ? (float*)(base + o_bytes + ml_bytes) : nullptr;
   p.lse = a.lse;
-  char buf[256];
-  snprintf(buf, sizeof buf, "attention: loop h [#tile<1>](%lld heads) x loop s [#sum softmax](%d key shards of %d) over "
-           "%lld sequences, S=%lld, %s", (long long)a.H, a.Rkv, p.kb_per * 64, (long long)a.B, (long long)a.S,
-           a.causal ? "causal" : "full");
+  char buf[320], part[64] = "";
+  if (parts > 1) snprintf(part, sizeof part, ", each as %d ordered parts of %d", parts, p.kb_per * 64);
+  snprintf(buf, sizeof buf, "attention: loop h [#tile<1>](%lld heads) x loop s [#sum softmax](%d key shards of %d%s) "
+           "over %lld sequences, S=%lld, %s", (long long)a.H, a.Rkv, p.kb_per * 64 * parts, part, (long long)a.B,
+           (long long)a.S, a.causal ? "causal" : "full");
   L.text = buf;
   plan.launches.push_back(L);
   if (a.Rkv > 1) {

@@ -292,6 +292,27 @@ def test_attention_core_plans():
     assert P.lib().partir_attention_workspace(2, 2048, 8, 128, 4) == four["workspace_bytes"]
 
 
+def test_attention_core_causal_parts():
+    """A causal grid too small to fill the device runs each shard of >= 2048
+    keys as ordered parts of >= 1024 keys; full attention, R_kv = 1 and large
+    grids keep one part per shard."""
+    B, S, H, R = 1, 8192, 2, 4
+    T, D = B * S, H * 128
+    causal = P.plan_attention(B, S, H, 128, True, R)
+    assert "each as 2 ordered parts of 1024" in causal["text"] and "4 key shards of 2048" in causal["text"]
+    assert causal["workspace_bytes"] == 8 * T * D * 4 + 2 * 8 * T * H * 4
+    assert causal["n_virtual_shards"] == 4 and causal["n_launches"] == 2
+    full = P.plan_attention(B, S, H, 128, False, R)
+    assert "ordered parts" not in full["text"] and full["workspace_bytes"] == 4 * T * D * 4 + 2 * 4 * T * H * 4
+    assert P.lib().partir_attention_workspace(B, S, H, 128, R) == causal["workspace_bytes"]
+    assert "ordered parts" not in P.plan_attention(B, S, H, 128, True, 1)["text"]
+    assert "ordered parts" not in P.plan_attention(4, S, 32, 128, True, R)["text"]      # 8192 workgroups
+    four = P.plan_attention(1, 32768, 1, 128, True, 4)       # 128 key blocks a shard, 1024 workgroups
+    assert "each as 2 ordered parts of 4096" in four["text"]
+    eight = P.plan_attention(1, 32768, 1, 128, True, 2)      # 256 key blocks a shard, 512 workgroups
+    assert "each as 4 ordered parts of 4096" in eight["text"]
+
+
 @pytest.mark.parametrize("kwargs,status", [
     (dict(R=3), "PARTIR_E_DIVISIBILITY"),     # 32 key blocks of 64
     (dict(R=0), "PARTIR_E_UNSUPPORTED"),

@@ -90,6 +90,35 @@ def test_split_kv_long_sequence_sampled_rows():
     assert err <= TOL_BF16
 
 
+@pytest.mark.parametrize("B,S,H,R", [(1, 8192, 2, 4), (1, 4096, 1, 2)])
+def test_split_kv_causal_parts_sampled_rows(B, S, H, R):
+    """Shards of >= 2048 keys on a small causal grid run as ordered parts
+    (8192 keys, 2 heads, R_kv = 4: the long-sequence benchmark shape; 4096
+    keys, R_kv = 2: four parts of 1024); rows on both sides of every part
+    boundary, the last row and seeded rows match the oracle, and the
+    log-sum-exp matches the unsplit kernel's."""
+    info = P.plan_attention(B, S, H, DH, True, R)
+    assert "ordered parts" in info["text"], info["text"]
+    part = int(info["text"].split("ordered parts of ")[1].split(")")[0])
+    Q, K, V = make_qkv(124, B, S, H)
+    rng = np.random.default_rng(124)
+    edges = [e for j in range(S // part) for e in (j * part - 1, j * part) if e >= 0]
+    rows = np.unique(np.concatenate([edges, [S - 1], rng.choice(S, 24, replace=False)]))
+    say(f"attention B={B} S={S} H={H} R_kv={R}, parts of {part} keys: {len(rows)} sampled rows")
+    q, k, v = Q.to_device(), K.to_device(), V.to_device()
+    o, lse = P.attention_train(q, k, v, B=B, S=S, n_heads=H, causal=True, R_kv=R)
+    _, lse1 = P.attention_train(q, k, v, B=B, S=S, n_heads=H, causal=True, R_kv=1)
+    torch.cuda.synchronize()
+    ref, nrm = reference(Q, K, V, B, S, H, True, rows)
+    err = O.normalised_error(host(o)[rows], ref, nrm)
+    lse_err = float((lse - lse1).abs().max())
+    say(f"    max normalised error {err:.3e}, lse against the unsplit kernel {lse_err:.2e}")
+    assert err <= TOL_BF16 and lse_err < 1e-4
+    again = P.attention(q, k, v, B=B, S=S, n_heads=H, causal=True, R_kv=R)
+    torch.cuda.synchronize()
+    assert torch.equal(o, again)
+
+
 def test_split_kv_matches_single_shard_and_is_deterministic():
     B, S, H = 2, 512, 4
     Q, K, V = make_qkv(123, B, S, H)
