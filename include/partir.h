@@ -378,8 +378,9 @@ size_t partir_attn_block_backward_workspace(int64_t B, int64_t S, int64_t D, int
  * (P*B*S*n_heads each), P = R_kv times the parts per shard;
  * partir_attention_workspace gives the size for a causal mask, which is also
  * enough without one.
- * Errors: E_NULL, E_SHAPE, E_DIVISIBILITY (R_kv does not divide S/64),
- * E_LAYOUT, E_WORKSPACE, E_UNSUPPORTED (R_kv < 1), E_HIP.
+ * Errors: E_NULL, E_SHAPE (also when (S/128)*B*n_heads*R_kv exceeds 2^29),
+ * E_DIVISIBILITY (R_kv does not divide S/64), E_LAYOUT, E_WORKSPACE,
+ * E_UNSUPPORTED (R_kv < 1), E_HIP.
  */
 int partir_attention(const void* Q, const void* K, const void* V, void* O,
                      int64_t B, int64_t S, int64_t n_heads, int64_t d_head,

@@ -791,6 +791,9 @@ int validate_attn_core(const AttnCoreArgs& a, bool with_ptrs) {
   if ((a.S / 64) % a.Rkv)
     return fail(PARTIR_E_DIVISIBILITY, "R_kv=%d does not divide the %lld key blocks of 64 (S=%lld)", a.Rkv,
                 (long long)(a.S / 64), (long long)a.S);
+  // one workgroup per (128-query block, sequence, head, part), up to 4 parts a shard
+  if ((a.S / 128) * a.B * a.H * a.Rkv > ((int64_t)1 << 29))
+    return fail(PARTIR_E_SHAPE, "R_kv=%d gives more than 2^29 (query block, head, shard) workgroups", a.Rkv);
   if (with_ptrs && a.B * a.S > 0 && (!a.Q || !a.K || !a.V || !a.O))
     return fail(PARTIR_E_NULL, "Q, K, V and O must be non-NULL");
   if (with_ptrs && (!aligned16(a.Q) || !aligned16(a.K) || !aligned16(a.V) || !aligned16(a.O)))

@@ -319,6 +319,7 @@ def test_attention_core_causal_parts():
     (dict(S=200), "PARTIR_E_SHAPE"),
     (dict(dh=64), "PARTIR_E_SHAPE"),
     (dict(S=1 << 20, H=16), "PARTIR_E_SHAPE"),  # one sequence's K: 2^20 x 2048 bf16 = 4 GiB
+    (dict(B=256, S=1 << 16, H=8, R=1024), "PARTIR_E_SHAPE"),  # 2^30 workgroups
     (dict(Q=NULL), "PARTIR_E_NULL"),
     (dict(Q=DUMMY_ODD), "PARTIR_E_LAYOUT"),
     (dict(ws_bytes=0), "PARTIR_E_WORKSPACE"),
