@@ -90,20 +90,21 @@ def test_split_kv_long_sequence_sampled_rows():
     assert err <= TOL_BF16
 
 
-@pytest.mark.parametrize("B,S,H,R", [(1, 8192, 2, 4), (1, 4096, 1, 2)])
+@pytest.mark.parametrize("B,S,H,R", [(1, 8192, 2, 4), (1, 4096, 1, 2), (2, 4096, 1, 2)])
 def test_split_kv_causal_parts_sampled_rows(B, S, H, R):
     """Shards of >= 2048 keys on a small causal grid run as ordered parts
     (8192 keys, 2 heads, R_kv = 4: the long-sequence benchmark shape; 4096
-    keys, R_kv = 2: four parts of 1024); rows on both sides of every part
-    boundary, the last row and seeded rows match the oracle, and the
-    log-sum-exp matches the unsplit kernel's."""
+    keys, R_kv = 2: four parts of 1024, also over two sequences, where a
+    row's parts follow from its position in its own sequence); rows on both
+    sides of every part boundary of every sequence, the last row and seeded
+    rows match the oracle, and the log-sum-exp matches the unsplit kernel's."""
     info = P.plan_attention(B, S, H, DH, True, R)
     assert "ordered parts" in info["text"], info["text"]
     part = int(info["text"].split("ordered parts of ")[1].split(")")[0])
     Q, K, V = make_qkv(124, B, S, H)
     rng = np.random.default_rng(124)
-    edges = [e for j in range(S // part) for e in (j * part - 1, j * part) if e >= 0]
-    rows = np.unique(np.concatenate([edges, [S - 1], rng.choice(S, 24, replace=False)]))
+    edges = [b * S + e for b in range(B) for j in range(S // part) for e in (j * part - 1, j * part) if e >= 0]
+    rows = np.unique(np.concatenate([edges, [B * S - 1], rng.choice(B * S, 24, replace=False)]))
     say(f"attention B={B} S={S} H={H} R_kv={R}, parts of {part} keys: {len(rows)} sampled rows")
     q, k, v = Q.to_device(), K.to_device(), V.to_device()
     o, lse = P.attention_train(q, k, v, B=B, S=S, n_heads=H, causal=True, R_kv=R)
