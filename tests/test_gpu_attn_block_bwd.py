@@ -40,7 +40,7 @@ def run(w, x, dY, Rb, Rm):
     return out
 
 
-@pytest.mark.parametrize("Rb,Rm", [(1, 8), (2, 4)])
+@pytest.mark.parametrize("Rb,Rm", [(1, 8), (2, 4), (1, 1), (2, 8)])
 def test_attn_block_backward_small_every_element(Rb, Rm):
     w = W.WORKLOADS["attn_block_small"]
     x = W.make_inputs(w)
@@ -50,6 +50,28 @@ def test_attn_block_backward_small_every_element(Rb, Rm):
     ref, nrm = O.attn_block_backward(x["X"].f64(), x["Wq"].f64(), x["Wk"].f64(), x["Wv"].f64(), x["Wo"].f64(),
                                      dY.f64(), w["B"], w["S"], w["H"], w["dh"], True, None, Rb, Rm,
                                      return_norm=True)
+    for k in KEYS:
+        err = O.normalised_error(got[k], ref[k], nrm[k])
+        fro = rel_fro(got[k], ref[k])
+        say(f"    {k}: max normalised error {err:.3e}, relative Frobenius {fro:.3e}")
+        assert err <= TOL_BF16 and fro <= TOL_REL_FRO, k
+
+
+def test_attn_block_backward_one_sequence_one_head_per_shard():
+    """Three sequences of the minimum length (128, one query block), three
+    heads, mesh 3 x 3: every shard holds one sequence and one head, and the
+    model #sum folds three single-head partials; every element."""
+    B, S, H, dh = 3, 128, 3, 128
+    D = H * dh
+    w = {"B": B, "S": S, "D": D, "H": H}
+    x = {"X": I.gaussian(133, 0, (B * S, D), 1.0)}
+    for i, k in enumerate(("Wq", "Wk", "Wv", "Wo")):
+        x[k] = I.gaussian(133, 1 + i, (D, D), D ** -0.5)
+    dY = I.gaussian(133, 9, (B * S, D), 1.0)
+    say(f"attn block backward B={B} S={S} H={H} R_batch=3 R_model=3")
+    got = run(w, x, dY, 3, 3)
+    ref, nrm = O.attn_block_backward(x["X"].f64(), x["Wq"].f64(), x["Wk"].f64(), x["Wv"].f64(), x["Wo"].f64(),
+                                     dY.f64(), B, S, H, dh, True, None, 3, 3, return_norm=True)
     for k in KEYS:
         err = O.normalised_error(got[k], ref[k], nrm[k])
         fro = rel_fro(got[k], ref[k])
