@@ -214,6 +214,23 @@ def test_decoder_small_full_output():
     assert err <= TOL_BF16
 
 
+@pytest.mark.parametrize("Rb,Rm", [(1, 1), (1, 8), (2, 2)])
+def test_decoder_small_other_partitions(Rb, Rm):
+    """The small decoder under other nests of batch #tile and model #tile /
+    #sum (unpartitioned; one head per model shard with F/R = 216; 2 x 2),
+    every element against the oracle's shard interpreter for that nest."""
+    w = W.WORKLOADS["decoder_2layer_small"]
+    x = W.make_inputs(w)
+    nest = dict(w.dims, R_batch=Rb, R_model=Rm)
+    say(f"decoder small R_batch={Rb} R_model={Rm}")
+    out = run_decoder(nest, x)
+    ref, norm = O.decoder(x["x"].f64(), oracle_layers(x), w["B"], w["S"], w["H"], w["dh"], 1e-6, Rb, Rm,
+                          return_norm=True)
+    err = O.normalised_error(host(out), ref, norm)
+    say(f"    max normalised error {err:.3e}")
+    assert err <= TOL_BF16
+
+
 def test_decoder_small_random_gains():
     w = W.WORKLOADS["decoder_2layer_small"]
     x = W.make_inputs(w)
