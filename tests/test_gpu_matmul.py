@@ -63,6 +63,22 @@ def test_f32_modes_ragged(tile, summ, R, b_layout):
 
 
 @pytest.mark.parametrize("out", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("tile,summ,R", [("M", None, 3), ("N", None, 3), (None, "K", 3), (None, "K", 5),
+                                         ("M", "K", 5), ("N", "K", 3)])
+def test_bf16_odd_shard_counts(tile, summ, R, out):
+    """Odd loop sizes: shards of 200 / 120 rows, 176 columns, 160 / 96 keys
+    (none a multiple of the 256-wide tiles), fused and split-K sums."""
+    M, N, K = 600, 528, 480
+    A = I.gaussian(105, 0, (M, K), 1.0, "bf16")
+    B = I.gaussian(105, 1, (K, N), K ** -0.5, "bf16")
+    for impl in ("fused", "splitk"):
+        say(f"bf16 {M}x{N}x{K} tile={tile} sum={summ} R={R} out={out} {impl}")
+        C = run(A, B, tile, summ, R, "nk", out_dtype=out, sum_impl=impl)
+        err = check(A, B, C, tile, summ, R, TOL_BF16)
+        assert err <= accum_bound(K) + (2.0 ** -8 if out == torch.bfloat16 else 0.0)
+
+
+@pytest.mark.parametrize("out", [torch.float32, torch.bfloat16])
 @pytest.mark.parametrize("tile,summ,R", [(None, None, 1), ("M", None, 4), ("N", None, 4), (None, "K", 4),
                                          ("M", "K", 4), ("N", "K", 2), (None, "K", 8)])
 def test_bf16_modes_ragged(tile, summ, R, out):
