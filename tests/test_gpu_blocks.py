@@ -104,6 +104,21 @@ def test_mlp_integer_exact(Rb, Rm):
     assert np.array_equal(host(Y), ref)
 
 
+@pytest.mark.parametrize("Rb,Rm", [(3, 3), (3, 5), (1, 5)])
+def test_mlp_integer_exact_odd_nests(Rb, Rm):
+    """Odd loop sizes (batch shards of 256 rows, model shards of 320 / 192
+    hidden units), act = none, entries in {-1, 0, 1}: exact for every nest."""
+    T, D, F = 768, 256, 960
+    X = I.small_ints(113, 0, (T, D), -1, 1)
+    W1 = I.small_ints(113, 1, (D, F), -1, 1)
+    W2 = I.small_ints(113, 2, (F, D), -1, 1)
+    Y = P.mlp_block(X.to_device(), dev_t(W1), dev_t(W2), R_batch=Rb, R_model=Rm, act="none",
+                    out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    ref = O.mlp_block(X.f64(), W1.f64(), W2.f64(), act="none", R_batch=Rb, R_model=Rm)
+    assert np.array_equal(host(Y), ref)
+
+
 @pytest.mark.slow
 @pytest.mark.parametrize("name", ["mlp_megatron", "mlp_batch_x_megatron"])
 def test_mlp_full_size_sampled_rows(name):
