@@ -49,7 +49,7 @@ def oracle_params(p, g1, g2):
     return q
 
 
-@pytest.mark.parametrize("RB,RM", [(2, 4), (1, 2)])
+@pytest.mark.parametrize("RB,RM", [(2, 4), (1, 2), (1, 1), (2, 2), (2, 8)])
 def test_decoder_sharded_small_every_part(RB, RM):
     B, S, H, F = 2, 256, 8, 2048
     D = H * 128
