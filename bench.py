@@ -5,10 +5,16 @@
 
 A step is one call of the partitioned program over one batch of seeded
 synthetic input already resident in HBM (all virtual shards, every #tile and
-#sum of the nest).  Prints one JSON line with the achieved TFLOP/s, the
-roofline of the dominant kernel (its average launch time measured with HIP
-events on the launch stream during the timed steps) and the CPU oracle timed
-on a bounded sample of the same workload.
+#sum of the nest).  The default workload is the largest single-GPU one: the
+batch #tile (4) x Megatron (8) MLP block, X [16384, 8192], W1 [8192, 32768],
+W2 [32768, 8192], 32 virtual shards.  After W warm-up steps, K steps are
+timed three times (each trial bracketed by device synchronisations); the line
+reports the median trial and the minimum.  Prints one JSON line with the
+achieved TFLOP/s, the roofline of the dominant kernel (its average launch time
+measured with HIP events on the launch stream during the timed steps), the
+MFMA utilisation read from the committed rocprofv3 counter summary of the
+same kernel sources, and the CPU oracle timed on a bounded sample of the same
+workload.
 
 --copy-calib BYTES runs only a device-to-device copy of that size (the
 reference kernel for scaling HBM counters) and exits.
@@ -41,7 +47,8 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="mlp_megatron")
+    ap.add_argument("--workload", default="mlp_batch_x_megatron")
+    ap.add_argument("--trials", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="target CPU work of the oracle sample")
     ap.add_argument("--copy-calib", type=int, default=0)
@@ -55,7 +62,7 @@ def setup(w, P, I):
     import torch
     from paper_2401_11202_amd import workloads as W
     x = W.make_inputs(w)
-    dev_t = lambda t: I.transposed(t).to_device()
+    dev = lambda t: t.to_device()   # weights are [fan_in, fan_out], as the entry points take them
     if w.kind == "matmul":
         A = x["A"].to_device()
         B = x["B"].to_device()
@@ -70,18 +77,18 @@ def setup(w, P, I):
         return x, step, roles, "mfma_f32"
     if w.kind == "mlp":
         T, D, F = w["T"], w["D"], w["F"]
-        X, W1t, W2t = x["X"].to_device(), dev_t(x["W1"]), dev_t(x["W2"])
+        X, W1, W2 = x["X"].to_device(), dev(x["W1"]), dev(x["W2"])
         Y = torch.empty((T, D), dtype=torch.float32, device="cuda")
         ws = torch.empty(P.mlp_block_workspace(T, D, F, P.F32, w["R_batch"], w["R_model"]),
                          dtype=torch.uint8, device="cuda")
-        step = lambda: P.mlp_block(X, W1t, W2t, R_batch=w["R_batch"], R_model=w["R_model"], out=Y, workspace=ws)
+        step = lambda: P.mlp_block(X, W1, W2, R_batch=w["R_batch"], R_model=w["R_model"], out=Y, workspace=ws)
         roles = {"mlp.up": 2.0 * T * D * F, "mlp.down": 2.0 * T * D * F}
         return x, step, roles, "mfma_bf16"
     if w.kind == "attn_train":
         B, S, D, H, dh, Rb, Rm = w["B"], w["S"], w["D"], w["H"], w["dh"], w["R_batch"], w["R_model"]
         T = B * S
         X, dY = x["X"].to_device(), x["dY"].to_device()
-        Ws = [dev_t(x[k]) for k in ("Wq", "Wk", "Wv", "Wo")]
+        Ws = [dev(x[k]) for k in ("Wq", "Wk", "Wv", "Wo")]
         Y = torch.empty((T, D), dtype=torch.float32, device="cuda")
         saved = torch.empty(P.lib().partir_attn_block_saved_bytes(B, S, D, H), dtype=torch.uint8, device="cuda")
         wsf = torch.empty(P.attn_block_workspace(B, S, D, H, dh, Rb, Rm), dtype=torch.uint8, device="cuda")
@@ -103,7 +110,7 @@ def setup(w, P, I):
         return x, step, roles, "mfma_bf16"
     if w.kind == "mlp_z3":
         T, D, F, Rb, Rm = w["T"], w["D"], w["F"], w["R_batch"], w["R_model"]
-        xs, w1s, w2s = P.z3_device_arrays(x["X"].to_device(), dev_t(x["W1"]), dev_t(x["W2"]), Rb, Rm)
+        xs, w1s, w2s = P.z3_device_arrays(x["X"].to_device(), dev(x["W1"]), dev(x["W2"]), Rb, Rm)
         b1, b2 = x["b1"].to_device(), x["b2"].to_device()
         ys = [torch.empty((T // (Rb * Rm), D), dtype=torch.float32, device="cuda") for _ in range(Rb * Rm)]
         ws = torch.empty(P.lib().partir_mlp_block_sharded_workspace(T, D, F, Rb, Rm), dtype=torch.uint8,
@@ -114,7 +121,7 @@ def setup(w, P, I):
         return x, step, roles, "mfma_bf16"
     if w.kind == "mlp_train":
         T, D, F, Rb, Rm = w["T"], w["D"], w["F"], w["R_batch"], w["R_model"]
-        X, W1t, W2t, dY, b1 = x["X"].to_device(), dev_t(x["W1"]), dev_t(x["W2"]), x["dY"].to_device(), \
+        X, W1, W2, dY, b1 = x["X"].to_device(), dev(x["W1"]), dev(x["W2"]), x["dY"].to_device(), \
             x["b1"].to_device()
         Y = torch.empty((T, D), dtype=torch.float32, device="cuda")
         Z = torch.empty((T, F), dtype=torch.bfloat16, device="cuda")
@@ -123,14 +130,14 @@ def setup(w, P, I):
                           dtype=torch.uint8, device="cuda")
 
         f32 = dict(dtype=torch.float32, device="cuda")
-        grads = (torch.empty((T, D), **f32), torch.empty((F, D), **f32), torch.empty((D, F), **f32),
+        grads = (torch.empty((T, D), **f32), torch.empty((D, F), **f32), torch.empty((F, D), **f32),
                  torch.empty((F,), **f32), torch.empty((D,), **f32))
 
         def step():
             # forward, then every gradient of the same nest (a training step
             # without the optimizer update, which is elementwise)
-            P.mlp_block_train(X, W1t, W2t, b1=b1, R_batch=Rb, R_model=Rm, out=Y, Z=Z, workspace=wsf)
-            P.mlp_block_backward(X, W1t, W2t, dY, b1=b1, Z=Z, R_batch=Rb, R_model=Rm, bias_grads=True, out=grads,
+            P.mlp_block_train(X, W1, W2, b1=b1, R_batch=Rb, R_model=Rm, out=Y, Z=Z, workspace=wsf)
+            P.mlp_block_backward(X, W1, W2, dY, b1=b1, Z=Z, R_batch=Rb, R_model=Rm, bias_grads=True, out=grads,
                                  workspace=wsb)
         f = 2.0 * T * D * F
         roles = {"mlp.up": f, "mlp.down": f, "mlp.bwd.dh": f, "mlp.bwd.dw2": f, "mlp.bwd.dw1": f,
@@ -140,7 +147,7 @@ def setup(w, P, I):
         B, S, D, H = w["B"], w["S"], w["D"], w["H"]
         T = B * S
         X = x["X"].to_device()
-        Ws = [dev_t(x[k]) for k in ("Wq", "Wk", "Wv", "Wo")]
+        Ws = [dev(x[k]) for k in ("Wq", "Wk", "Wv", "Wo")]
         Y = torch.empty((T, D), dtype=torch.float32, device="cuda")
         ws = torch.empty(P.attn_block_workspace(B, S, D, H, w["dh"], w["R_batch"], w["R_model"]),
                          dtype=torch.uint8, device="cuda")
@@ -155,7 +162,7 @@ def setup(w, P, I):
         x0 = x["x"].to_device()
         xs = torch.empty_like(x0)
         layers = [dict(g1=p["g1"].to_device(), g2=p["g2"].to_device(),
-                       W=[dev_t(p[k]) for k in ("Wq", "Wk", "Wv", "Wo", "W1", "W2")]) for p in x["layers"]]
+                       W=[dev(p[k]) for k in ("Wq", "Wk", "Wv", "Wo", "W1", "W2")]) for p in x["layers"]]
         ws = torch.empty(P.decoder_layer_workspace(B, S, D, H, w["dh"], F, w["R_batch"], w["R_model"]),
                          dtype=torch.uint8, device="cuda")
 
@@ -177,7 +184,7 @@ def setup(w, P, I):
         xs = [t.clone() for t in x0]
         layers = []
         for p in x["layers"]:
-            _, parts = P.z3_decoder_arrays(x0[0], {k: dev_t(p[k]) for k in ("Wq", "Wk", "Wv", "Wo", "W1", "W2")},
+            _, parts = P.z3_decoder_arrays(x0[0], {k: dev(p[k]) for k in ("Wq", "Wk", "Wv", "Wo", "W1", "W2")},
                                            Rb, Rm)
             layers.append(dict(g1=p["g1"].to_device(), g2=p["g2"].to_device(), parts=parts))
         ws = torch.empty(P.lib().partir_decoder_layer_sharded_workspace(B, S, D, H, w["dh"], F, Rb, Rm),
@@ -209,15 +216,45 @@ def setup(w, P, I):
 # ---------------------------------------------------------------------------
 # CPU baseline: the oracle on a bounded sample of the same workload
 # ---------------------------------------------------------------------------
+def host_description():
+    """CPU model, cores this process may run on, and the thread counts the
+    oracle's BLAS and OpenMP use."""
+    model = None
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    affinity = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
+    blas = None
+    try:
+        from threadpoolctl import threadpool_info
+        blas = max(i.get("num_threads", 1) for i in threadpool_info()) or None
+    except Exception:
+        pass
+    return {"cpu_model": model, "affinity_cores": affinity, "omp_num_threads": os.environ.get("OMP_NUM_THREADS"),
+            "blas_threads": blas}
+
+
 def cpu_baseline(w, x, target_s):
+    """The oracle on a bounded sample, its rate, the host it ran on, and the
+    time the full output would take at that rate (an extrapolation, labelled
+    as such: the oracle is never run on the whole workload here)."""
+    from paper_2401_11202_amd import workloads as W
+    info = host_description()
+    r = _cpu_sample(w, x, target_s, info["blas_threads"] or info["affinity_cores"] or 1)
+    r.update(info)
+    r["extrapolated_full_output_s"] = round(W.flops(w) / (r["value"] * 1e12), 1)
+    r["extrapolation"] = "full-output oracle time = the workload's algorithmic FLOPs / the sample's rate"
+    return r
+
+
+def _cpu_sample(w, x, target_s, cores):
     import numpy as np
     from oracle import partir_oracle as O
     from paper_2401_11202_amd import workloads as W
-    try:
-        from threadpoolctl import threadpool_info
-        cores = max(i.get("num_threads", 1) for i in threadpool_info()) or 1
-    except Exception:
-        cores = os.cpu_count() or 1
     if w.kind == "matmul":
         A, B = x["A"].f64(), x["B"].f64()
         t0 = time.perf_counter()
@@ -339,6 +376,21 @@ def traffic_from_profile(workload, role):
     return float(m.group(1))
 
 
+def mfma_busy_from_profile(workload, role):
+    """MFMA busy fraction of `role`'s kernel from the committed rocprofv3
+    counter summary (SQ_VALU_MFMA_BUSY_CYCLES over the dispatch's cycles),
+    valid only while the kernel source is unchanged."""
+    path = os.path.join(ROOT, "profiles", f"mfma_util_{workload}.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    h = re.search(r"kernel_source_sha256:\s*([0-9a-f]+)", text)
+    m = re.search(r"mfma_busy\s+" + re.escape(role) + r":\s*([0-9.]+)", text)
+    if not m or not h or h.group(1) != kernel_source_hash():
+        return None
+    return float(m.group(1))
+
+
 def kernel_source_hash():
     d = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2401_11202_amd", "csrc")
@@ -381,15 +433,19 @@ def main():
 
     P.trace_reset()
     P.trace_enable(True)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step()
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
+    trials = []
+    for _ in range(max(1, args.trials)):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            step()
+        torch.cuda.synchronize()
+        trials.append(time.perf_counter() - t0)
+        log(f"bench: {args.steps} steps in {trials[-1] * 1e3:.2f} ms")
     P.trace_enable(False)
     trace = P.trace_read()
-    log(f"bench: {args.steps} steps in {elapsed * 1e3:.2f} ms; trace {trace}")
+    log(f"bench: trace {trace}")
+    elapsed = sorted(trials)[len(trials) // 2]      # the median trial
 
     flops = W.flops(w)
     value = flops * args.steps / elapsed / 1e12
@@ -399,10 +455,11 @@ def main():
     launches, total_ms = trace[dom]
     avg_s = total_ms / launches / 1e3
     achieved = roles[dom] / avg_s / 1e12
+    busy = mfma_busy_from_profile(w.name, dom)
     roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
                 "frac": round(achieved / peak, 4), "traffic": traffic_from_profile(w.name, dom),
                 "kernel": dom, "avg_launch_ms": round(avg_s * 1e3, 4),
-                "flops_per_launch": roles[dom]}
+                "flops_per_launch": roles[dom], "mfma_busy": busy}
     kernels = {k: {"launches": v[0], "avg_ms": round(v[1] / v[0], 4),
                    "tflops": round(roles[k] / (v[1] / v[0] / 1e3) / 1e12, 1) if k in roles else None}
                for k, v in trace.items()}
@@ -414,11 +471,18 @@ def main():
 
     out = {"metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1,
            "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(elapsed / args.steps * 1e3, 4),
+           "trials": len(trials), "ms_per_step_trials": [round(t / args.steps * 1e3, 4) for t in trials],
+           "ms_per_step_min": round(min(trials) / args.steps * 1e3, 4),
+           "value_at_min": round(flops * args.steps / min(trials) / 1e12, 2),
            "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
            "dtype": "f32" if unit_kind == "mfma_f32" else "bf16",
            "data": "synthetic (seeded Gaussian, weights scaled 1/sqrt(fan_in))",
            "config": {"workload": w.name, **w.dims, "parallelism": "virtual shards on 1 GPU"},
-           "mfma_util_pct_of_peak": round(100.0 * value / peak, 2),
+           # achieved TFLOP/s over the published dense peak (not a counter)
+           "frac_of_peak": round(value / peak, 4),
+           # the dominant kernel's MFMA busy fraction, a rocprofv3 counter
+           # reading from profiles/ for these kernel sources (null if stale)
+           "mfma_busy_dominant_kernel": busy,
            "roofline": roofline, "kernels": kernels, "cpu_baseline": cpu}
     print(json.dumps(out), flush=True)
 

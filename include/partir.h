@@ -121,8 +121,12 @@ typedef enum partir_act { PARTIR_ACT_NONE = 0, PARTIR_ACT_GELU_ERF = 1 } partir_
  * b_layout: partir_b_layout.  sum_impl: partir_sum_impl (ignored without a
  * #sum).  ws / ws_bytes: workspace of at least partir_loop_matmul_workspace().
  * M, N or K may be 0: M = 0 or N = 0 launches nothing; K = 0 writes zeros.
+ * Limits: bf16 operands address each block of 64 rows (K-contiguous) or 64
+ * K rows (B as [K, N]) through a 32-bit byte range, so lda and ldb are at
+ * most 2^24 elements; the output tiles (64 x 64 counted per shard) times R
+ * must stay below 2^31.
  * Errors: E_NULL (a non-empty A, B or C NULL, or ws NULL with ws_bytes
- * short), E_SHAPE (a size < 0 or above 2^30),
+ * short), E_SHAPE (a size < 0 or above 2^30, or beyond the limits above),
  * E_DIVISIBILITY (R does not divide the tiled or summed dim), E_AXIS,
  * E_DTYPE, E_LAYOUT, E_WORKSPACE, E_UNSUPPORTED (R < 1), E_HIP.
  */
@@ -148,9 +152,11 @@ size_t partir_loop_matmul_workspace(int64_t M, int64_t N, int64_t K,
  *       loop m [#sum](R_model) {
  *         act(slice 0 X[b] @ slice 1 W1[m] + slice 0 b1[m]) @ slice 0 W2[m] }
  *       + b2 }
- * X: [T, D] bf16 row-major (ld = D).  W1t: W1^T, [F, D] bf16.  W2t: W2^T,
- * [D, F] bf16.  b1: [F] f32 or NULL (tiled with W1's columns).  b2: [D] f32
- * or NULL, added once after the #sum.  Y: [T, D], out_dtype F32 or BF16.
+ * X: [T, D] bf16 row-major (ld = D).  W1: [D, F] bf16 and W2: [F, D] bf16,
+ * row-major [fan_in, fan_out] (slice 1 W1[m] is a column block, slice 0
+ * W2[m] a row block; both are read in place).  b1: [F] f32 or NULL (tiled
+ * with W1's columns).  b2: [D] f32 or NULL, added once after the #sum.
+ * Y: [T, D], out_dtype F32 or BF16.
  * act: partir_act applied to the first product.  The intermediate
  * H = act(X W1 + b1) ([T, F], stored bf16) lives in the workspace; each model
  * shard m writes its columns [m F/R_model, (m+1) F/R_model) and the second
@@ -160,8 +166,8 @@ size_t partir_loop_matmul_workspace(int64_t M, int64_t N, int64_t K,
  * R_model does not divide F), E_DTYPE (in_dtype other than BF16), E_LAYOUT,
  * E_WORKSPACE, E_UNSUPPORTED (R < 1), E_HIP.
  */
-int partir_mlp_block(const void* X, const void* W1t, const void* b1,
-                     const void* W2t, const void* b2, void* Y,
+int partir_mlp_block(const void* X, const void* W1, const void* b1,
+                     const void* W2, const void* b2, void* Y,
                      int64_t T, int64_t D, int64_t F,
                      int in_dtype, int out_dtype, int act,
                      int R_batch, int R_model,
@@ -213,7 +219,8 @@ size_t partir_mlp_block_sharded_workspace(int64_t T, int64_t D, int64_t F, int R
  * row block is added into its owner's residual part (reduce_scatter).  The
  * result equals partir_decoder_layer on the concatenated x.  Constraints:
  * those of partir_decoder_layer, T/(R_batch R_model) a multiple of 16,
- * D/R_batch and F/R_model multiples of 64, at most 64 devices.
+ * D/R_batch and F/R_model multiples of 64, at most 21 devices (the Q|K|V
+ * projection reads three weights' blocks through one table of 64 parts).
  * Errors: E_NULL, E_SHAPE, E_DIVISIBILITY, E_LAYOUT, E_WORKSPACE,
  * E_UNSUPPORTED, E_HIP. */
 int partir_decoder_layer_sharded(void* const* x_parts, const void* g1, const void* g2, float eps,
@@ -231,8 +238,8 @@ size_t partir_decoder_layer_sharded_workspace(int64_t B, int64_t S, int64_t D, i
  * by the same up-projection tiles) that partir_mlp_block_backward reads
  * instead of recomputing it.  Same workspace as partir_mlp_block.  Z must be
  * non-NULL when T, D and F are all non-zero; errors as partir_mlp_block. */
-int partir_mlp_block_train(const void* X, const void* W1t, const void* b1,
-                           const void* W2t, const void* b2, void* Y, void* Z,
+int partir_mlp_block_train(const void* X, const void* W1, const void* b1,
+                           const void* W2, const void* b2, void* Y, void* Z,
                            int64_t T, int64_t D, int64_t F,
                            int in_dtype, int out_dtype, int act,
                            int R_batch, int R_model,
@@ -255,22 +262,21 @@ size_t partir_mlp_block_workspace(int64_t T, int64_t D, int64_t F, int out_dtype
  *   dW1 = X^T dZ       loop m [#tile<1>] { loop b [#sum] }
  *   dX  = dZ W1^T      loop b [#tile<0>] { loop m [#sum] }   the model-parallel sum
  *   db1 = sum_t dZ, db2 = sum_t dY  (in fixed row-block order)
- * X, W1t, W2t, b1 as in partir_mlp_block; dY: [T, D] bf16.  Outputs fp32:
- * dX [T, D]; dW1t = dW1^T [F, D] and dW2t = dW2^T [D, F] (the weights'
- * stored layout); db1 [F], db2 [D] (either may be NULL: not computed).
+ * X, W1, W2, b1 as in partir_mlp_block; dY: [T, D] bf16.  Outputs fp32:
+ * dX [T, D]; dW1 [D, F] and dW2 [F, D] (the weights' layout); db1 [F],
+ * db2 [D] (either may be NULL: not computed).
  * Z: the pre-activation X W1 + b1 [T, F] bf16 kept by partir_mlp_block_train
  * (read only), or NULL: then it is recomputed into the workspace.
- * Intermediates dH, dZ are bf16 in the workspace, which also holds the
- * transposes the token-contracting products read (X^T, dY^T, H^T, dZ^T,
- * W1, W2); the workspace query assumes Z is recomputed (an upper bound
- * otherwise).  Constraints: D, F/R_model and T/R_batch multiples of 8.  A
+ * Intermediates Z (when recomputed), dH, dZ and H = act(Z) are bf16 in the
+ * workspace; every operand is read in place (no transposed copies).  The
+ * workspace query assumes Z is recomputed (an upper bound otherwise).  Constraints: D, F/R_model and T/R_batch multiples of 8.  A
  * size of 0 gives empty sums (zeros) for every non-empty gradient.
  * Errors: E_NULL, E_SHAPE, E_DIVISIBILITY, E_LAYOUT, E_WORKSPACE,
  * E_UNSUPPORTED (R < 1, unknown act), E_HIP.
  */
-int partir_mlp_block_backward(const void* X, const void* W1t, const void* b1,
-                              const void* W2t, const void* dY, const void* Z,
-                              void* dX, void* dW1t, void* db1, void* dW2t, void* db2,
+int partir_mlp_block_backward(const void* X, const void* W1, const void* b1,
+                              const void* W2, const void* dY, const void* Z,
+                              void* dX, void* dW1, void* db1, void* dW2, void* db2,
                               int64_t T, int64_t D, int64_t F, int act,
                               int R_batch, int R_model,
                               void* ws, size_t ws_bytes, void* stream);
@@ -280,7 +286,10 @@ size_t partir_mlp_block_backward_workspace(int64_t T, int64_t D, int64_t F, int 
                                            int with_bias_grads, int R_batch, int R_model);
 
 /* ------------------------------------------------------------------------ */
-/* Attention block: heads #tile inside a Megatron #sum, in a batch #tile.     */
+/* Attention block: heads #tile inside a Megatron #sum, in a batch #tile     */
+/* (Megatron model parallelism of attention, Sec. 2.3; the MP tactic shards   */
+/* the QKV weights on their heads dim and the output weight on its rows,      */
+/* Sec. 3; the batch tile of BP, Sec. 3; TMR matmul forms, Sec. 5.2.1).       */
 /* ------------------------------------------------------------------------ */
 /*
  * Y = loop b [#tile<0>](R_batch) {
@@ -289,9 +298,10 @@ size_t partir_mlp_block_backward_workspace(int64_t T, int64_t D, int64_t F, int 
  *             attn(Q_h, K_h, V_h) }) @ slice 0 Wo[m] } }
  * with Q = slice 0 X[b] @ slice 1 Wq[m] (K, V likewise) and, per sequence
  * and head, attn = softmax(scale * Q K^T, keys j <= query i when causal) V.
- * X: [B*S, D] bf16, sequence-major (token t = s*S + position).  Wq_t, Wk_t,
- * Wv_t, Wo_t: transposed [D, D] bf16 weights; head h owns columns
- * [h*d_head, (h+1)*d_head) of Q, K and V.  Batch shards hold whole sequences.
+ * X: [B*S, D] bf16, sequence-major (token t = s*S + position).  Wq, Wk, Wv,
+ * Wo: [D, D] bf16 row-major [fan_in, fan_out], read in place; head h owns
+ * columns [h*d_head, (h+1)*d_head) of Wq, Wk, Wv (so of Q, K and V) and rows
+ * [h*d_head, (h+1)*d_head) of Wo.  Batch shards hold whole sequences.
  * scale <= 0 selects 1/sqrt(d_head).  Y: [B*S, D], out_dtype F32 or BF16.
  * The workspace holds Q, K, V and the attention output (bf16, [B*S, D] each).
  * Constraints: d_head == 128, S a multiple of 128, S*D*2 < 4 GiB (one
@@ -301,8 +311,8 @@ size_t partir_mlp_block_backward_workspace(int64_t T, int64_t D, int64_t F, int 
  * constraints), E_DIVISIBILITY (R_batch does not divide B or R_model does not
  * divide n_heads), E_DTYPE, E_LAYOUT, E_WORKSPACE, E_UNSUPPORTED, E_HIP.
  */
-int partir_attn_block(const void* X, const void* Wq_t, const void* Wk_t,
-                      const void* Wv_t, const void* Wo_t, void* Y,
+int partir_attn_block(const void* X, const void* Wq, const void* Wk,
+                      const void* Wv, const void* Wo, void* Y,
                       int64_t B, int64_t S, int64_t D, int64_t n_heads, int64_t d_head,
                       int causal, float scale, int in_dtype, int out_dtype,
                       int R_batch, int R_model,
@@ -318,8 +328,8 @@ size_t partir_attn_block_workspace(int64_t B, int64_t S, int64_t D, int64_t n_he
  * partir_attn_block_backward.  Workspace: that of partir_attn_block minus the
  * Q, K, V, A it no longer holds (partir_attn_block_workspace is an upper
  * bound). */
-int partir_attn_block_train(const void* X, const void* Wq_t, const void* Wk_t,
-                            const void* Wv_t, const void* Wo_t, void* Y, void* saved,
+int partir_attn_block_train(const void* X, const void* Wq, const void* Wk,
+                            const void* Wv, const void* Wo, void* Y, void* saved,
                             int64_t B, int64_t S, int64_t D, int64_t n_heads, int64_t d_head,
                             int causal, float scale, int in_dtype, int out_dtype,
                             int R_batch, int R_model,
@@ -335,16 +345,16 @@ size_t partir_attn_block_saved_bytes(int64_t B, int64_t S, int64_t D, int64_t n_
  *                                      the sum over the three projections
  *   dW{q,k,v} = X^T d{Q,K,V}       loop m [#tile<1>] { loop b [#sum] }
  *   dWo = A^T dY                   loop m [#tile<0>] { loop b [#sum] }
- * Weights and their gradients in the stored layout W^T [out, in] (dW*_t
- * fp32 [D, D]); dX fp32 [B*S, D]; `saved` from partir_attn_block_train.  The
- * workspace holds dA, [dQ dK dV], the transposes the token-contracting
- * products read and the transposed weights.  Constraints as
+ * Weights as in partir_attn_block and their gradients in the same
+ * [fan_in, fan_out] layout (dW* fp32 [D, D]); dX fp32 [B*S, D]; `saved` from
+ * partir_attn_block_train.  The workspace holds dA, [dQ dK dV] and the
+ * rowsums; every operand is read in place.  Constraints as
  * partir_attn_block.  Errors: E_NULL, E_SHAPE, E_DIVISIBILITY, E_LAYOUT,
  * E_WORKSPACE, E_UNSUPPORTED, E_HIP. */
-int partir_attn_block_backward(const void* X, const void* Wq_t, const void* Wk_t,
-                               const void* Wv_t, const void* Wo_t, const void* saved,
-                               const void* dY, void* dX, void* dWq_t, void* dWk_t,
-                               void* dWv_t, void* dWo_t,
+int partir_attn_block_backward(const void* X, const void* Wq, const void* Wk,
+                               const void* Wv, const void* Wo, const void* saved,
+                               const void* dY, void* dX, void* dWq, void* dWk,
+                               void* dWv, void* dWo,
                                int64_t B, int64_t S, int64_t D, int64_t n_heads, int64_t d_head,
                                int causal, float scale, int R_batch, int R_model,
                                void* ws, size_t ws_bytes, void* stream);
@@ -420,7 +430,10 @@ int partir_attention_backward(const void* Q, const void* K, const void* V, const
 size_t partir_attention_backward_workspace(int64_t B, int64_t S, int64_t n_heads, int64_t d_head);
 
 /* ------------------------------------------------------------------------ */
-/* Pre-norm decoder layer on an fp32 residual stream, in place.               */
+/* Pre-norm decoder layer on an fp32 residual stream, in place: the          */
+/* transformer layer the evaluation partitions (Sec. 7.1, with its           */
+/* additional normalisation), under BP + MP (Sec. 3) as a batch #tile over   */
+/* the attention and MLP nests above.                                         */
 /* ------------------------------------------------------------------------ */
 /*
  * x = loop b [#tile<0>](R_batch) { xb = slice 0 x[b];
@@ -428,8 +441,8 @@ size_t partir_attention_backward_workspace(int64_t B, int64_t S, int64_t n_heads
  *       h  + loop m [#sum](R_model) { gelu(rmsnorm(h, g2) @ slice 1 W1[m]) @ slice 0 W2[m] } }
  * rmsnorm(x, g) = g * x / sqrt(mean(x^2) + eps) over the D features of a row;
  * attention is causal with scale 1/sqrt(d_head).
- * x: [B*S, D] f32, updated in place.  g1, g2: [D] f32.  Wq_t..Wo_t as in
- * partir_attn_block; W1t: [F, D] bf16; W2t: [D, F] bf16.
+ * x: [B*S, D] f32, updated in place.  g1, g2: [D] f32.  Wq..Wo as in
+ * partir_attn_block; W1: [D, F] bf16; W2: [F, D] bf16 ([fan_in, fan_out]).
  * Workspace: normalised activations, Q, K, V, attention output and the
  * [B*S, F] FFN intermediate, all bf16.
  * F = 0 leaves out the FFN half (it adds the empty sum); B = 0 or S = 0
@@ -438,8 +451,8 @@ size_t partir_attention_backward_workspace(int64_t B, int64_t S, int64_t n_heads
  * divide F.
  */
 int partir_decoder_layer(void* x, const void* g1, const void* g2, float eps,
-                         const void* Wq_t, const void* Wk_t, const void* Wv_t,
-                         const void* Wo_t, const void* W1t, const void* W2t,
+                         const void* Wq, const void* Wk, const void* Wv,
+                         const void* Wo, const void* W1, const void* W2,
                          int64_t B, int64_t S, int64_t D, int64_t n_heads,
                          int64_t d_head, int64_t F, int R_batch, int R_model,
                          void* ws, size_t ws_bytes, void* stream);

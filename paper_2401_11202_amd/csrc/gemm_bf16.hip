@@ -230,18 +230,7 @@ __device__ __forceinline__ void gemm_body(const GemmParams& p, const GemmParts* 
       char* base = smem + stage * STAGE + lds_w;
       __amdgpu_buffer_rsrc_t rma, rmb;
       if (AMN) rma = make_rsrc(p.A + (int64_t)kb * p.lda + row0, kvalid * (uint32_t)p.lda * 2);
-      if (BMN) {
-        // B stacked along K from p.B[0..2] (b_kpart_rows rows each; a k tile
-        // never straddles two of them), or one array
-        const uint16_t* bs = Bg;
-        int krow = kb;
-        if (p.b_kpart_rows) {
-          const int part = kb / p.b_kpart_rows;
-          bs = pick3(part, p.B[0], p.B[1], p.B[2]);
-          krow = kb - part * p.b_kpart_rows;
-        }
-        rmb = make_rsrc(bs + (int64_t)krow * p.ldb + col0, kvalid * (uint32_t)p.ldb * 2);
-      }
+      if (BMN) rmb = make_rsrc(Bg + (int64_t)kb * p.ldb + col0, kvalid * (uint32_t)p.ldb * 2);
       const uint32_t kmask = (kb + lchunk * 8 < k_end) ? 0u : OOB;
       const uint32_t so = (uint32_t)kb * 2;
 #pragma unroll
@@ -566,9 +555,9 @@ template <int EPI, int ACT>
 __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void gemm_bf16_fixup_kernel(GemmParams p) { gemm_body<EPI, ACT, 0, 1>(p, nullptr); }
 
-template <int EPI, int AMN, int BMN>
+template <int EPI, int ACT, int AMN, int BMN>
 __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2)))
-void gemm_bf16_mn_kernel(GemmParams p) { gemm_body<EPI, 0, 0, 0, AMN, BMN>(p, nullptr); }
+void gemm_bf16_mn_kernel(GemmParams p) { gemm_body<EPI, ACT, 0, 0, AMN, BMN>(p, nullptr); }
 
 template <int EPI, int ACT>
 __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2)))
@@ -617,33 +606,44 @@ hipError_t launch_parts(const GemmParams& p, const GemmParts& t, hipStream_t s) 
   return hipGetLastError();
 }
 
-template <int EPI, int AMN, int BMN>
+template <int EPI, int ACT, int AMN, int BMN>
 hipError_t launch_mn(const GemmParams& p, hipStream_t s) {
   if (p.tail_parts > 1 && !tail_ok(p)) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((gemm_bf16_mn_kernel<EPI, AMN, BMN>), dim3((unsigned)main_grid(p)), dim3(NT), 0, s, p);
+  hipLaunchKernelGGL((gemm_bf16_mn_kernel<EPI, ACT, AMN, BMN>), dim3((unsigned)main_grid(p)), dim3(NT), 0, s, p);
   return hipGetLastError();
 }
 
-// MN-major operands: no activation (the products that read them are backward
-// passes and plain matmuls); the fixup launch is the common one.
+// MN-major operands; the fixup launch is the common one.  An activation (and
+// the kept pre-activation) only with A K-contiguous and B stored [K, N]: the
+// forward products of the blocks, whose weights are [fan_in, fan_out].
 template <int AMN, int BMN>
 hipError_t dispatch_mn(const GemmParams& p, hipStream_t s) {
-  if (p.act) return hipErrorInvalidValue;
-  switch (p.epi) {
-    case EPI_BF16: return launch_mn<EPI_BF16, AMN, BMN>(p, s);
-    case EPI_F32: return launch_mn<EPI_F32, AMN, BMN>(p, s);
-    case EPI_PARTIAL: return launch_mn<EPI_PARTIAL, AMN, BMN>(p, s);
-    case EPI_RESID_F32: return launch_mn<EPI_RESID_F32, AMN, BMN>(p, s);
-    default: return hipErrorInvalidValue;
+  if constexpr (AMN == 0 && BMN == 1) {
+    switch (p.epi * 2 + (p.act ? 1 : 0)) {
+      case EPI_BF16 * 2 + 0: return launch_mn<EPI_BF16, 0, 0, 1>(p, s);
+      case EPI_BF16 * 2 + 1: return launch_mn<EPI_BF16, 1, 0, 1>(p, s);
+      case EPI_F32 * 2 + 0: return launch_mn<EPI_F32, 0, 0, 1>(p, s);
+      case EPI_F32 * 2 + 1: return launch_mn<EPI_F32, 1, 0, 1>(p, s);
+      case EPI_PARTIAL * 2 + 0: return launch_mn<EPI_PARTIAL, 0, 0, 1>(p, s);
+      case EPI_RESID_F32 * 2 + 0: return launch_mn<EPI_RESID_F32, 0, 0, 1>(p, s);
+      case EPI_BF16_SAVE * 2 + 0: return launch_mn<EPI_BF16_SAVE, 0, 0, 1>(p, s);
+      case EPI_BF16_SAVE * 2 + 1: return launch_mn<EPI_BF16_SAVE, 1, 0, 1>(p, s);
+      default: return hipErrorInvalidValue;
+    }
+  } else {
+    if (p.act) return hipErrorInvalidValue;
+    switch (p.epi) {
+      case EPI_BF16: return launch_mn<EPI_BF16, 0, AMN, BMN>(p, s);
+      case EPI_F32: return launch_mn<EPI_F32, 0, AMN, BMN>(p, s);
+      case EPI_PARTIAL: return launch_mn<EPI_PARTIAL, 0, AMN, BMN>(p, s);
+      case EPI_RESID_F32: return launch_mn<EPI_RESID_F32, 0, AMN, BMN>(p, s);
+      default: return hipErrorInvalidValue;
+    }
   }
 }
 
 template <int FIX>
 hipError_t dispatch(const GemmParams& p, hipStream_t s) {
-  // B stacked along K: whole 64-row k tiles inside one of the three arrays
-  if (p.b_kpart_rows && (!p.b_mn || p.ngroups != 1 || p.b_kpart_rows % BK || p.K > 3 * p.b_kpart_rows ||
-                         (p.nsplit > 1 && p.ks % BK)))
-    return hipErrorInvalidValue;
   if (!FIX && (p.a_mn || p.b_mn)) {
     if (p.a_mn && p.b_mn) return dispatch_mn<1, 1>(p, s);
     return p.a_mn ? dispatch_mn<1, 0>(p, s) : dispatch_mn<0, 1>(p, s);

@@ -52,9 +52,6 @@ struct GemmParams {
   // (A stored [K, M] with leading dim lda, B stored [K, N] with leading dim
   // ldb).  MN-major operands take no activation.
   int a_mn, b_mn;
-  // MN-major B only, one group: B is B[0], B[1], B[2] stacked along K,
-  // b_kpart_rows rows each (a multiple of 64); 0: B[group] alone.
-  int b_kpart_rows;
 };
 
 hipError_t launch_gemm_bf16(const GemmParams& p, hipStream_t s);

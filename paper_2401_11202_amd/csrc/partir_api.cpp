@@ -123,7 +123,6 @@ struct GemmSpec {
   void* aux = nullptr;          // bf16 pre-activation output (kept for a backward pass)
   bool tail_ok = false;         // the caller's workspace region holds gemm_ws_bytes (tail split allowed)
   bool a_mn = false;            // bf16 A stored [K, M] (leading dim lda) instead of [M, K]
-  int b_kstack = 0;             // B stored [K, N] as B[0], B[1], B[2] stacked along K, this many rows each
   const char* name = "gemm";    // role, used as the trace name
   const char* label = "gemm";   // loop nest, for the plan text
 };
@@ -179,7 +178,7 @@ std::string describe_gemm(const GemmSpec& g, int64_t grid, bool split) {
   if (g.ab_dtype == PARTIR_BF16 && (g.a_mn || !g.b_nk)) {
     t += "; read in place:";
     if (g.a_mn) t += " A as [K, M]";
-    if (!g.b_nk) t += g.b_kstack ? " B as [K, N] stacked from 3 arrays" : " B as [K, N]";
+    if (!g.b_nk) t += " B as [K, N]";
   }
   return t;
 }
@@ -223,7 +222,6 @@ int plan_gemm(const GemmSpec& g, void* ws, Plan& plan) {
     p.epi = split ? EPI_PARTIAL : (g.aux ? EPI_BF16_SAVE : epi_store);
     p.a_mn = g.a_mn;
     p.b_mn = !g.b_nk;   // B stored [K, N]
-    p.b_kpart_rows = g.b_kstack;
     int64_t tail_base;
     p.tail_parts = gemm_tail_parts(g, &tail_base);
     p.tail_base = (int)tail_base;
@@ -376,6 +374,8 @@ struct MatmulArgs {
   int ab, c, b_layout, tile_axis, sum_axis, R, sum_impl;
 };
 
+constexpr int64_t kBf16MaxLd = (int64_t)1 << 24;
+
 int validate_matmul(const MatmulArgs& a, bool with_ptrs) {
   // Empty operands are legal: a zero-size dim slices into R empty shards
   // (n_d = 0 satisfies TSlice), and a #sum over K = 0 is the empty sum.
@@ -415,6 +415,18 @@ int validate_matmul(const MatmulArgs& a, bool with_ptrs) {
   const int rk = a.sum_axis == PARTIR_AXIS_K ? a.R : 1;
   const int rn = a.tile_axis == PARTIR_AXIS_N ? a.R : 1;
   if ((a.K / rk) % vec) return fail(PARTIR_E_LAYOUT, "K/R must be a multiple of %d (16-byte shard views)", vec);
+  // The bf16 kernel addresses each 64-row block of an operand (64 K rows of
+  // an MN-major one) through a buffer descriptor whose byte range is a 32-bit
+  // number, and masks a lane with offset bit 31: 128 * ld bytes must stay
+  // within 2^31.
+  if (a.ab == PARTIR_BF16 && ((a_used && a.lda > kBf16MaxLd) || (b_used && a.ldb > kBf16MaxLd)))
+    return fail(PARTIR_E_SHAPE, "bf16 operands: leading dims above 2^24 elements are not addressable");
+  // output tiles (64 x 64 at the smallest, never straddling a shard) times
+  // K shards index the grid in 32 bits
+  const int64_t rm = a.tile_axis == PARTIR_AXIS_M ? a.R : 1;
+  if (c_used && rm * cdiv(a.M / rm, 64) * rn * cdiv(a.N / rn, 64) * (int64_t)rk > ((int64_t)1 << 31) - 1)
+    return fail(PARTIR_E_SHAPE, "C[%lld,%lld] with R=%d has more output tiles than a launch can index",
+                (long long)a.M, (long long)a.N, a.R);
   if ((a.N / rn) % 4) return fail(PARTIR_E_LAYOUT, "N/R must be a multiple of 4 (16-byte shard views)");
   if (a.ab == PARTIR_BF16 && a.b_layout == PARTIR_B_KN && ((a.N % 8) || ((a.N / rn) % 8)))
     return fail(PARTIR_E_LAYOUT, "bf16 B as [K, N]: N and N/R must be multiples of 8 (16-byte rows of B)");
@@ -479,7 +491,7 @@ void plan_matmul(const MatmulArgs& a, void* ws, Plan& plan) {
 // partir_mlp_block
 // ---------------------------------------------------------------------------
 struct MlpArgs {
-  const void *X = nullptr, *W1t = nullptr, *b1 = nullptr, *W2t = nullptr, *b2 = nullptr;
+  const void *X = nullptr, *W1 = nullptr, *b1 = nullptr, *W2 = nullptr, *b2 = nullptr;
   void* Y = nullptr;
   int64_t T, D, F;
   int in, out, act, Rb, Rm;
@@ -489,9 +501,9 @@ struct MlpArgs {
 int validate_mlp(const MlpArgs& a, bool with_ptrs) {
   if (a.T < 0 || a.D < 0 || a.F < 0) return fail(PARTIR_E_SHAPE, "T, D, F must be >= 0");
   // an operand must be present only if it will be read (or written)
-  if (with_ptrs && ((a.T * a.D > 0 && a.F > 0 && !a.X) || (a.T * a.D * a.F > 0 && (!a.W1t || !a.W2t)) ||
+  if (with_ptrs && ((a.T * a.D > 0 && a.F > 0 && !a.X) || (a.T * a.D * a.F > 0 && (!a.W1 || !a.W2)) ||
                     (a.T * a.D > 0 && !a.Y)))
-    return fail(PARTIR_E_NULL, "X, W1t, W2t and Y must be non-NULL (unless empty)");
+    return fail(PARTIR_E_NULL, "X, W1, W2 and Y must be non-NULL (unless empty)");
   if (a.T > (1 << 30) || a.D > (1 << 20) || a.F > (1 << 22)) return fail(PARTIR_E_SHAPE, "dims too large");
   if (a.Rb < 1 || a.Rm < 1) return fail(PARTIR_E_UNSUPPORTED, "R_batch and R_model must be >= 1");
   if (a.in != PARTIR_BF16) return fail(PARTIR_E_DTYPE, "in_dtype must be BF16");
@@ -500,7 +512,7 @@ int validate_mlp(const MlpArgs& a, bool with_ptrs) {
   if (a.T % a.Rb) return fail(PARTIR_E_DIVISIBILITY, "R_batch=%d does not divide T=%lld", a.Rb, (long long)a.T);
   if (a.F % a.Rm) return fail(PARTIR_E_DIVISIBILITY, "R_model=%d does not divide F=%lld", a.Rm, (long long)a.F);
   if (a.D % 8 || (a.F / a.Rm) % 8) return fail(PARTIR_E_LAYOUT, "D and F/R_model must be multiples of 8");
-  if (with_ptrs && (!aligned16(a.X) || !aligned16(a.W1t) || !aligned16(a.W2t) || !aligned16(a.Y) ||
+  if (with_ptrs && (!aligned16(a.X) || !aligned16(a.W1) || !aligned16(a.W2) || !aligned16(a.Y) ||
                     !aligned16(a.b1) || !aligned16(a.b2) || !aligned16(a.Z)))
     return fail(PARTIR_E_LAYOUT, "tensors must be 16-byte aligned");
   return PARTIR_OK;
@@ -510,16 +522,17 @@ void plan_mlp(const MlpArgs& a, void* ws, Plan& plan) {
   const size_t h_bytes = align_up((size_t)a.T * a.F * 2);
   char* base = (char*)ws;
   void* H = base;
+  // W1 [D, F] and W2 [F, D] are the products' [K, N] right operands, read in place
   GemmSpec g1;
-  g1.A = a.X; g1.B[0] = a.W1t; g1.C[0] = H; g1.bias[0] = (const float*)a.b1;
-  g1.lda = a.D; g1.ldb = a.D; g1.ldc = a.F;
+  g1.A = a.X; g1.B[0] = a.W1; g1.b_nk = 0; g1.C[0] = H; g1.bias[0] = (const float*)a.b1;
+  g1.lda = a.D; g1.ldb = a.F; g1.ldc = a.F;
   g1.M = a.T; g1.N = a.F; g1.K = a.D;
   g1.c_dtype = PARTIR_BF16; g1.rm = a.Rb; g1.rn = a.Rm; g1.act = a.act; g1.aux = a.Z;
   g1.name = "mlp.up";
   g1.label = "mlp.up   H = act(slice 0 X[b] . slice 1 W1[m])";
   GemmSpec g2;
-  g2.A = H; g2.B[0] = a.W2t; g2.C[0] = a.Y; g2.bias[0] = (const float*)a.b2;
-  g2.lda = a.F; g2.ldb = a.F; g2.ldc = a.D;
+  g2.A = H; g2.B[0] = a.W2; g2.b_nk = 0; g2.C[0] = a.Y; g2.bias[0] = (const float*)a.b2;
+  g2.lda = a.F; g2.ldb = a.D; g2.ldc = a.D;
   g2.M = a.T; g2.N = a.D; g2.K = a.F;
   g2.c_dtype = a.out; g2.rm = a.Rb; g2.rk = a.Rm;
   g2.name = "mlp.down";
@@ -590,7 +603,7 @@ GemmSpec qkv_spec(const void* Xn, const void* Wq, const void* Wk, const void* Wv
                   int64_t D, int Rb, int Rm) {
   const size_t one = align_up((size_t)T * D * 2);
   GemmSpec g;
-  g.A = Xn; g.B[0] = Wq; g.B[1] = Wk; g.B[2] = Wv;
+  g.A = Xn; g.B[0] = Wq; g.B[1] = Wk; g.B[2] = Wv; g.b_nk = 0;   // W{q,k,v} [D, D] as [K, N]
   g.C[0] = qkvo; g.C[1] = qkvo ? qkvo + one : nullptr; g.C[2] = qkvo ? qkvo + 2 * one : nullptr;
   g.ngroups = 3;
   g.lda = D; g.ldb = D; g.ldc = D;
@@ -659,7 +672,7 @@ void plan_attn(const AttnArgs& a, void* ws, Plan& plan) {
                       lse);
   GemmSpec g;
   g.A = qkvo ? qkvo + 3 * align_up((size_t)T * a.D * 2) : nullptr;
-  g.B[0] = a.Wo; g.C[0] = a.Y;
+  g.B[0] = a.Wo; g.b_nk = 0; g.C[0] = a.Y;
   g.lda = a.D; g.ldb = a.D; g.ldc = a.D;
   g.M = T; g.N = a.D; g.K = a.D;
   g.c_dtype = a.out; g.rm = a.Rb; g.rk = a.Rm;
@@ -735,7 +748,7 @@ void plan_dec(const DecArgs& a, void* ws, Plan& plan) {
                       true, part);
   GemmSpec go;
   go.A = qkvo ? qkvo + 3 * align_up((size_t)T * a.D * 2) : nullptr;
-  go.B[0] = a.Wo; go.C[0] = a.x; go.resid = (const float*)a.x; go.resid_add = true;
+  go.B[0] = a.Wo; go.b_nk = 0; go.C[0] = a.x; go.resid = (const float*)a.x; go.resid_add = true;
   go.lda = a.D; go.ldb = a.D; go.ldc = a.D; go.ldr = a.D;
   go.M = T; go.N = a.D; go.K = a.D;
   go.c_dtype = PARTIR_F32; go.rm = a.Rb; go.rk = a.Rm; go.tail_ok = true;
@@ -749,16 +762,16 @@ void plan_dec(const DecArgs& a, void* ws, Plan& plan) {
   if (a.F == 0) return;       // an FFN of width 0 adds the empty sum: x is unchanged
   plan_rmsnorm((const float*)a.x, (const float*)a.g2, xn, T, a.D, a.eps, a.Rb, plan);
   GemmSpec g1;
-  g1.A = xn; g1.B[0] = a.W1; g1.C[0] = Hf;
-  g1.lda = a.D; g1.ldb = a.D; g1.ldc = a.F;
+  g1.A = xn; g1.B[0] = a.W1; g1.b_nk = 0; g1.C[0] = Hf;
+  g1.lda = a.D; g1.ldb = a.F; g1.ldc = a.F;
   g1.M = T; g1.N = a.F; g1.K = a.D;
   g1.c_dtype = PARTIR_BF16; g1.rm = a.Rb; g1.rn = a.Rm; g1.act = 1;
   g1.name = "mlp.up";
   g1.label = "dec.ffn_up H = gelu(slice 0 xn[b] . slice 1 W1[m])";
   plan_gemm(g1, nullptr, plan);
   GemmSpec g2;
-  g2.A = Hf; g2.B[0] = a.W2; g2.C[0] = a.x; g2.resid = (const float*)a.x; g2.resid_add = true;
-  g2.lda = a.F; g2.ldb = a.F; g2.ldc = a.D; g2.ldr = a.D;
+  g2.A = Hf; g2.B[0] = a.W2; g2.b_nk = 0; g2.C[0] = a.x; g2.resid = (const float*)a.x; g2.resid_add = true;
+  g2.lda = a.F; g2.ldb = a.D; g2.ldc = a.D; g2.ldr = a.D;
   g2.M = T; g2.N = a.D; g2.K = a.F;
   g2.c_dtype = PARTIR_F32; g2.rm = a.Rb; g2.rk = a.Rm; g2.tail_ok = true;
   g2.name = "mlp.down";
@@ -923,7 +936,7 @@ void plan_attn_bwd(const AttnBwdArgs& a, void* ws, Plan& plan) {
 // attention block backward
 // ---------------------------------------------------------------------------
 struct AttnBlockBwdArgs {
-  const void *X = nullptr, *Wq = nullptr, *Wk = nullptr, *Wv = nullptr, *Wo = nullptr;   // stored W^T [out, in]
+  const void *X = nullptr, *Wq = nullptr, *Wk = nullptr, *Wv = nullptr, *Wo = nullptr;   // [fan_in, fan_out]
   const void* saved = nullptr;                                                         // from the training forward
   const void* dY = nullptr;
   void *dX = nullptr, *dWq = nullptr, *dWk = nullptr, *dWv = nullptr, *dWo = nullptr;
@@ -945,13 +958,13 @@ int validate_attn_block_bwd(const AttnBlockBwdArgs& a, bool with_ptrs) {
   return PARTIR_OK;
 }
 
-// Gradients of the attention block (same nest as partir_attn_block), Wo etc.
-// in their stored layout W^T [out, in]:
+// Gradients of the attention block (same nest as partir_attn_block); every
+// weight and its gradient is [fan_in, fan_out] = [D, D]:
 //   dA = dY Wo^T                  loop b [#tile<0>] loop m [#tile<1>] (heads)
 //   dQ|dK|dV = attention backward per head
 //   dX = [dQ dK dV] [Wq Wk Wv]^T  loop b [#tile<0>] loop m [#sum], and the sum over q, k, v
-//   dW{q,k,v}^T = dQKV^T X        loop m [#tile<0>] loop b [#sum]
-//   dWo^T = dY^T A                loop m [#tile<1>] loop b [#sum]
+//   dW{q,k,v} = X^T dQKV          loop m [#tile<1>] loop b [#sum]
+//   dWo = A^T dY                  loop m [#tile<0>] loop b [#sum]
 void plan_attn_block_bwd(const AttnBlockBwdArgs& a, void* ws, Plan& plan) {
   const int64_t T = a.B * a.S, D = a.D;
   plan.n_shards = a.Rb * a.Rm;
@@ -974,11 +987,11 @@ void plan_attn_block_bwd(const AttnBlockBwdArgs& a, void* ws, Plan& plan) {
   void* dQKV = take(3 * td);
   void* Dst = take(align_up((size_t)T * a.H * 4));
   void* part = base ? base + off : nullptr;
-  // Every operand is read where it lies: the stored W^T arrays are the
-  // [K, N] right operands of dA and dX, and the activations are the [K, M] /
+  // Every operand is read where it lies: the weights are the K-contiguous
+  // transposed right operands of dA and dX, and the activations the [K, M] /
   // [K, N] operands of the weight gradients (no transposed copies).
   GemmSpec ga;
-  ga.A = a.dY; ga.B[0] = a.Wo; ga.b_nk = 0; ga.C[0] = dA;
+  ga.A = a.dY; ga.B[0] = a.Wo; ga.C[0] = dA;
   ga.lda = D; ga.ldb = D; ga.ldc = D; ga.M = T; ga.N = D; ga.K = D;
   ga.c_dtype = PARTIR_BF16; ga.rm = a.Rb; ga.rn = a.Rm;
   ga.name = "attn.bwd.da"; ga.label = "bwd.da dA = slice 0 dY[b] . (slice 0 Wo[m])^T";
@@ -992,31 +1005,45 @@ void plan_attn_block_bwd(const AttnBlockBwdArgs& a, void* ws, Plan& plan) {
   Launch L = core.launches.back();
   L.attn_bwd.lddq = L.attn_bwd.lddk = L.attn_bwd.lddv = 3 * D;   // [dQ | dK | dV] side by side
   plan.launches.push_back(L);
+  // dX: the right operand [Wq Wk Wv]^T is K-contiguous and split along K
+  // over the three weights, read through a table of three K parts (whole-K
+  // accumulation in q, k, v order)
   GemmSpec gx;
-  gx.A = dQKV; gx.B[0] = a.Wq; gx.B[1] = a.Wk; gx.B[2] = a.Wv; gx.b_nk = 0; gx.b_kstack = (int)D;
-  gx.C[0] = a.dX;
+  gx.A = dQKV; gx.C[0] = a.dX;
   gx.lda = 3 * D; gx.ldb = D; gx.ldc = D; gx.M = T; gx.N = D; gx.K = 3 * D;
   gx.c_dtype = PARTIR_F32; gx.rm = a.Rb;
   gx.name = "attn.bwd.dx"; gx.label = "bwd.dx dX = sum over m and q|k|v of dQKV[b][:, m] . W{q,k,v}[:, m]^T";
-  plan_gemm(gx, part, plan);
-  const char* wnames[3] = {"bwd.dwq dWq^T = sum_b dQ[b][:, m]^T . slice 0 X[b]",
-                           "bwd.dwk dWk^T = sum_b dK[b][:, m]^T . slice 0 X[b]",
-                           "bwd.dwv dWv^T = sum_b dV[b][:, m]^T . slice 0 X[b]"};
+  {
+    const size_t first = plan.launches.size();
+    plan_gemm(gx, part, plan);
+    std::shared_ptr<GemmParts> t(new GemmParts{});
+    t->b_nrows = (int)D; t->b_kcols = (int)D; t->b_nk = 3; t->b_gstride = 0;
+    t->b[0] = (const uint16_t*)a.Wq; t->b[1] = (const uint16_t*)a.Wk; t->b[2] = (const uint16_t*)a.Wv;
+    for (size_t i = first; i < plan.launches.size(); ++i) {
+      Launch& L = plan.launches[i];
+      L.kind = L.kind == L_GEMM_BF16_FIXUP ? L_GEMM_BF16_PARTS_FIXUP : L_GEMM_BF16_PARTS;
+      L.parts = t;
+      if (i == first) L.text += "; B^T read as K parts Wq | Wk | Wv";
+    }
+  }
+  const char* wnames[3] = {"bwd.dwq dWq = sum_b (slice 0 X[b])^T . dQ[b][:, m]",
+                           "bwd.dwk dWk = sum_b (slice 0 X[b])^T . dK[b][:, m]",
+                           "bwd.dwv dWv = sum_b (slice 0 X[b])^T . dV[b][:, m]"};
   void* dW[3] = {a.dWq, a.dWk, a.dWv};
   for (int i = 0; i < 3; ++i) {
     GemmSpec gw;
-    gw.A = dQKV ? (char*)dQKV + i * D * 2 : nullptr; gw.a_mn = true;
-    gw.B[0] = a.X; gw.b_nk = 0; gw.C[0] = dW[i];
-    gw.lda = 3 * D; gw.ldb = D; gw.ldc = D; gw.M = D; gw.N = D; gw.K = T;
-    gw.c_dtype = PARTIR_F32; gw.rm = a.Rm; gw.rk = a.Rb; gw.sum_impl = PARTIR_SUM_FUSED;
+    gw.A = a.X; gw.a_mn = true;
+    gw.B[0] = dQKV ? (char*)dQKV + i * D * 2 : nullptr; gw.b_nk = 0; gw.C[0] = dW[i];
+    gw.lda = D; gw.ldb = 3 * D; gw.ldc = D; gw.M = D; gw.N = D; gw.K = T;
+    gw.c_dtype = PARTIR_F32; gw.rn = a.Rm; gw.rk = a.Rb; gw.sum_impl = PARTIR_SUM_FUSED;
     gw.name = "attn.bwd.dwqkv"; gw.label = wnames[i];
     plan_gemm(gw, nullptr, plan);
   }
   GemmSpec go;
-  go.A = a.dY; go.a_mn = true; go.B[0] = Ao; go.b_nk = 0; go.C[0] = a.dWo;
+  go.A = Ao; go.a_mn = true; go.B[0] = a.dY; go.b_nk = 0; go.C[0] = a.dWo;
   go.lda = D; go.ldb = D; go.ldc = D; go.M = D; go.N = D; go.K = T;
-  go.c_dtype = PARTIR_F32; go.rn = a.Rm; go.rk = a.Rb;
-  go.name = "attn.bwd.dwo"; go.label = "bwd.dwo dWo^T = sum_b (slice 0 dY[b])^T . A[b][:, m]";
+  go.c_dtype = PARTIR_F32; go.rm = a.Rm; go.rk = a.Rb;
+  go.name = "attn.bwd.dwo"; go.label = "bwd.dwo dWo = sum_b A[b][:, m]^T . slice 0 dY[b]";
   plan_gemm(go, part, plan);
   plan.n_sum_loops = 4;
   plan.ws_bytes = off + std::max(gemm_ws_bytes(gx), gemm_ws_bytes(go));
@@ -1026,9 +1053,9 @@ void plan_attn_block_bwd(const AttnBlockBwdArgs& a, void* ws, Plan& plan) {
 // partir_mlp_block_backward
 // ---------------------------------------------------------------------------
 struct MlpBwdArgs {
-  const void *X = nullptr, *W1t = nullptr, *b1 = nullptr, *W2t = nullptr, *dY = nullptr;
+  const void *X = nullptr, *W1 = nullptr, *b1 = nullptr, *W2 = nullptr, *dY = nullptr;
   const void* Z = nullptr;   // kept pre-activation; NULL: recomputed
-  void *dX = nullptr, *dW1t = nullptr, *db1 = nullptr, *dW2t = nullptr, *db2 = nullptr;
+  void *dX = nullptr, *dW1 = nullptr, *db1 = nullptr, *dW2 = nullptr, *db2 = nullptr;
   int64_t T, D, F;
   int act, Rb, Rm;
 };
@@ -1045,13 +1072,13 @@ int validate_mlp_bwd(const MlpBwdArgs& a, bool with_ptrs) {
     return fail(PARTIR_E_LAYOUT, "D, F/R_model and T/R_batch must be multiples of 8 (16-byte runs; the weight "
                 "gradients contract over tokens)");
   const bool live = a.T * a.D * a.F > 0;
-  if (with_ptrs && live && (!a.X || !a.W1t || !a.W2t || !a.dY))
-    return fail(PARTIR_E_NULL, "X, W1t, W2t and dY must be non-NULL");
-  if (with_ptrs && ((a.T * a.D > 0 && !a.dX) || (a.F * a.D > 0 && (!a.dW1t || !a.dW2t))))
-    return fail(PARTIR_E_NULL, "dX, dW1t and dW2t must be non-NULL when they hold elements");
+  if (with_ptrs && live && (!a.X || !a.W1 || !a.W2 || !a.dY))
+    return fail(PARTIR_E_NULL, "X, W1, W2 and dY must be non-NULL");
+  if (with_ptrs && ((a.T * a.D > 0 && !a.dX) || (a.F * a.D > 0 && (!a.dW1 || !a.dW2))))
+    return fail(PARTIR_E_NULL, "dX, dW1 and dW2 must be non-NULL when they hold elements");
   if (with_ptrs && a.db2 && a.T * a.D > 0 && !a.dY) return fail(PARTIR_E_NULL, "db2 needs dY");
-  if (with_ptrs && (!aligned16(a.X) || !aligned16(a.W1t) || !aligned16(a.W2t) || !aligned16(a.dY) ||
-                    !aligned16(a.dX) || !aligned16(a.dW1t) || !aligned16(a.dW2t) || !aligned16(a.b1) ||
+  if (with_ptrs && (!aligned16(a.X) || !aligned16(a.W1) || !aligned16(a.W2) || !aligned16(a.dY) ||
+                    !aligned16(a.dX) || !aligned16(a.dW1) || !aligned16(a.dW2) || !aligned16(a.b1) ||
                     !aligned16(a.db1) || !aligned16(a.db2) || !aligned16(a.Z)))
     return fail(PARTIR_E_LAYOUT, "tensors must be 16-byte aligned");
   return PARTIR_OK;
@@ -1080,7 +1107,7 @@ void plan_colsum(const void* in, void* partial, void* out, int64_t rows, int64_t
 //   dW1 = X^T dZ     loop m [#tile<1>] loop b [#sum]
 //   dX = dZ W1^T     loop b [#tile<0>] loop m [#sum]   (the model-parallel reduction)
 //   db1 = sum_t dZ, db2 = sum_t dY
-// Weight gradients are written in the weights' stored (transposed) layout.
+// Weights and their gradients are [fan_in, fan_out]: W1, dW1 [D, F]; W2, dW2 [F, D].
 void plan_mlp_bwd(const MlpBwdArgs& a, void* ws, Plan& plan) {
   const int64_t T = a.T, D = a.D, F = a.F;
   plan.n_shards = a.Rb * a.Rm;
@@ -1102,20 +1129,21 @@ void plan_mlp_bwd(const MlpBwdArgs& a, void* ws, Plan& plan) {
   void* H = take(tf);
   void* csp = take(cs_bytes);
   void* part = base ? base + off : nullptr;
-  // Every operand is read where it lies: W1^T and W2^T are the [K, N] right
-  // operands of dX and dH, and the activations the [K, M] / [K, N] operands
-  // of the weight gradients (no transposed copies).
+  // Every operand is read where it lies: W1 is the [K, N] right operand of
+  // Z and, K-contiguous, the transposed right operand of dX (W2 likewise of
+  // dH); the activations are the [K, M] / [K, N] operands of the weight
+  // gradients (no transposed copies).
   GemmSpec gz, gh, g2, g1, gx;
   if (live) {
     if (!a.Z) {
-      gz.A = a.X; gz.B[0] = a.W1t; gz.C[0] = Z; gz.bias[0] = (const float*)a.b1;
-      gz.lda = D; gz.ldb = D; gz.ldc = F; gz.M = T; gz.N = F; gz.K = D;
+      gz.A = a.X; gz.B[0] = a.W1; gz.b_nk = 0; gz.C[0] = Z; gz.bias[0] = (const float*)a.b1;
+      gz.lda = D; gz.ldb = F; gz.ldc = F; gz.M = T; gz.N = F; gz.K = D;
       gz.c_dtype = PARTIR_BF16; gz.rm = a.Rb; gz.rn = a.Rm;
       gz.name = "mlp.bwd.z"; gz.label = "bwd.z  Z = slice 0 X[b] . slice 1 W1[m] (recomputed)";
       plan_gemm(gz, nullptr, plan);
     }
-    gh.A = a.dY; gh.B[0] = a.W2t; gh.b_nk = 0; gh.C[0] = dH;
-    gh.lda = D; gh.ldb = F; gh.ldc = F; gh.M = T; gh.N = F; gh.K = D;
+    gh.A = a.dY; gh.B[0] = a.W2; gh.C[0] = dH;
+    gh.lda = D; gh.ldb = D; gh.ldc = F; gh.M = T; gh.N = F; gh.K = D;
     gh.c_dtype = PARTIR_BF16; gh.rm = a.Rb; gh.rn = a.Rm;
     gh.name = "mlp.bwd.dh"; gh.label = "bwd.dh dH = slice 0 dY[b] . (slice 0 W2[m])^T";
     plan_gemm(gh, nullptr, plan);
@@ -1128,18 +1156,18 @@ void plan_mlp_bwd(const MlpBwdArgs& a, void* ws, Plan& plan) {
     E.act.rows = (int)T; E.act.cols = (int)F; E.act.act = a.act;
     E.text = a.act ? "act_backward: dZ = dH * gelu'(Z); H = gelu(Z)" : "act_backward: dZ = dH; H = Z";
     plan.launches.push_back(E);
-    g2.A = a.dY; g2.a_mn = true; g2.B[0] = H; g2.b_nk = 0; g2.C[0] = a.dW2t;
-    g2.lda = D; g2.ldb = F; g2.ldc = F; g2.M = D; g2.N = F; g2.K = T;
-    g2.ab_dtype = PARTIR_BF16; g2.c_dtype = PARTIR_F32; g2.rn = a.Rm; g2.rk = a.Rb;
-    g2.name = "mlp.bwd.dw2"; g2.label = "bwd.dw2 dW2^T = sum_b (slice 0 dY[b])^T . H[b][:, m]";
+    g2.A = H; g2.a_mn = true; g2.B[0] = a.dY; g2.b_nk = 0; g2.C[0] = a.dW2;
+    g2.lda = F; g2.ldb = D; g2.ldc = D; g2.M = F; g2.N = D; g2.K = T;
+    g2.ab_dtype = PARTIR_BF16; g2.c_dtype = PARTIR_F32; g2.rm = a.Rm; g2.rk = a.Rb;
+    g2.name = "mlp.bwd.dw2"; g2.label = "bwd.dw2 dW2 = sum_b H[b][:, m]^T . slice 0 dY[b]";
     plan_gemm(g2, part, plan);
-    g1.A = dZ; g1.a_mn = true; g1.B[0] = a.X; g1.b_nk = 0; g1.C[0] = a.dW1t;
-    g1.lda = F; g1.ldb = D; g1.ldc = D; g1.M = F; g1.N = D; g1.K = T;
-    g1.c_dtype = PARTIR_F32; g1.rm = a.Rm; g1.rk = a.Rb;
-    g1.name = "mlp.bwd.dw1"; g1.label = "bwd.dw1 dW1^T = sum_b dZ[b][:, m]^T . slice 0 X[b]";
+    g1.A = a.X; g1.a_mn = true; g1.B[0] = dZ; g1.b_nk = 0; g1.C[0] = a.dW1;
+    g1.lda = D; g1.ldb = F; g1.ldc = F; g1.M = D; g1.N = F; g1.K = T;
+    g1.c_dtype = PARTIR_F32; g1.rn = a.Rm; g1.rk = a.Rb;
+    g1.name = "mlp.bwd.dw1"; g1.label = "bwd.dw1 dW1 = sum_b (slice 0 X[b])^T . dZ[b][:, m]";
     plan_gemm(g1, part, plan);
-    gx.A = dZ; gx.B[0] = a.W1t; gx.b_nk = 0; gx.C[0] = a.dX;
-    gx.lda = F; gx.ldb = D; gx.ldc = D; gx.M = T; gx.N = D; gx.K = F;
+    gx.A = dZ; gx.B[0] = a.W1; gx.C[0] = a.dX;
+    gx.lda = F; gx.ldb = F; gx.ldc = D; gx.M = T; gx.N = D; gx.K = F;
     gx.c_dtype = PARTIR_F32; gx.rm = a.Rb; gx.rk = a.Rm;
     gx.name = "mlp.bwd.dx"; gx.label = "bwd.dx dX = sum_m dZ[b][:, m] . (slice 1 W1[m])^T";
     plan_gemm(gx, part, plan);
@@ -1152,8 +1180,8 @@ void plan_mlp_bwd(const MlpBwdArgs& a, void* ws, Plan& plan) {
     // (zeros), except db2 = sum_t dY when only F is 0
     if (T * D > 0) plan_empty_sum(a.dX, T, D, D, false, nullptr, nullptr, 0, false, "mlp.bwd.dx", plan);
     if (F * D > 0) {
-      plan_empty_sum(a.dW1t, F, D, D, false, nullptr, nullptr, 0, false, "mlp.bwd.dw1", plan);
-      plan_empty_sum(a.dW2t, D, F, F, false, nullptr, nullptr, 0, false, "mlp.bwd.dw2", plan);
+      plan_empty_sum(a.dW1, D, F, F, false, nullptr, nullptr, 0, false, "mlp.bwd.dw1", plan);
+      plan_empty_sum(a.dW2, F, D, D, false, nullptr, nullptr, 0, false, "mlp.bwd.dw2", plan);
     }
     if (a.db1 && F > 0) plan_empty_sum(a.db1, 1, F, F, false, nullptr, nullptr, 0, false, "mlp.bwd.db", plan);
     if (a.db2 && D > 0) plan_colsum(a.dY, csp, a.db2, T, D, false, "mlp.bwd.db", plan);
@@ -1269,10 +1297,10 @@ int partir_plan_mlp_block(int64_t T, int64_t D, int64_t F, int out_dtype, int R_
   return PARTIR_OK;
 }
 
-int partir_mlp_block(const void* X, const void* W1t, const void* b1, const void* W2t, const void* b2, void* Y,
+int partir_mlp_block(const void* X, const void* W1, const void* b1, const void* W2, const void* b2, void* Y,
                      int64_t T, int64_t D, int64_t F, int in_dtype, int out_dtype, int act,
                      int R_batch, int R_model, void* ws, size_t ws_bytes, void* stream) {
-  MlpArgs a{X, W1t, b1, W2t, b2, Y, T, D, F, in_dtype, out_dtype, act, R_batch, R_model};
+  MlpArgs a{X, W1, b1, W2, b2, Y, T, D, F, in_dtype, out_dtype, act, R_batch, R_model};
   int st = validate_mlp(a, true);
   if (st) return st;
   Plan probe;
@@ -1284,10 +1312,10 @@ int partir_mlp_block(const void* X, const void* W1t, const void* b1, const void*
   return execute(plan, stream);
 }
 
-int partir_mlp_block_train(const void* X, const void* W1t, const void* b1, const void* W2t, const void* b2,
+int partir_mlp_block_train(const void* X, const void* W1, const void* b1, const void* W2, const void* b2,
                            void* Y, void* Z, int64_t T, int64_t D, int64_t F, int in_dtype, int out_dtype,
                            int act, int R_batch, int R_model, void* ws, size_t ws_bytes, void* stream) {
-  MlpArgs a{X, W1t, b1, W2t, b2, Y, T, D, F, in_dtype, out_dtype, act, R_batch, R_model, Z};
+  MlpArgs a{X, W1, b1, W2, b2, Y, T, D, F, in_dtype, out_dtype, act, R_batch, R_model, Z};
   if (T * D * F > 0 && !Z) return fail(PARTIR_E_NULL, "Z must be non-NULL (unless empty)");
   int st = validate_mlp(a, true);
   if (st) return st;
@@ -1426,7 +1454,9 @@ int validate_dec_sharded(const DecShardedArgs& a, bool with_ptrs) {
   if (st) return st;
   const int nd = a.Rb * a.Rm;
   const int64_t T = a.B * a.S;
-  if (nd > kMaxParts) return fail(PARTIR_E_UNSUPPORTED, "at most %d devices (R_batch * R_model)", kMaxParts);
+  // the Q|K|V projection reads three weights' blocks through one part table
+  if (3 * nd > kMaxParts)
+    return fail(PARTIR_E_UNSUPPORTED, "at most %d devices (R_batch * R_model) for the decoder layer", kMaxParts / 3);
   if (a.F < 0 || a.F > (1 << 22)) return fail(PARTIR_E_SHAPE, "F out of range");
   if (!(a.eps >= 0.0f)) return fail(PARTIR_E_SHAPE, "eps must be >= 0");
   if (a.F % a.Rm) return fail(PARTIR_E_DIVISIBILITY, "R_model=%d does not divide F=%lld", a.Rm, (long long)a.F);
@@ -1676,10 +1706,10 @@ int partir_plan_attn_block(int64_t B, int64_t S, int64_t D, int64_t n_heads, int
   return PARTIR_OK;
 }
 
-int partir_attn_block(const void* X, const void* Wq_t, const void* Wk_t, const void* Wv_t, const void* Wo_t, void* Y,
+int partir_attn_block(const void* X, const void* Wq, const void* Wk, const void* Wv, const void* Wo, void* Y,
                       int64_t B, int64_t S, int64_t D, int64_t n_heads, int64_t d_head, int causal, float scale,
                       int in_dtype, int out_dtype, int R_batch, int R_model, void* ws, size_t ws_bytes, void* stream) {
-  AttnArgs a{X, Wq_t, Wk_t, Wv_t, Wo_t, Y, B, S, D, n_heads, d_head, causal ? 1 : 0, scale,
+  AttnArgs a{X, Wq, Wk, Wv, Wo, Y, B, S, D, n_heads, d_head, causal ? 1 : 0, scale,
              in_dtype, out_dtype, R_batch, R_model};
   int st = validate_attn(a, true);
   if (st) return st;
@@ -1697,11 +1727,11 @@ size_t partir_attn_block_saved_bytes(int64_t B, int64_t S, int64_t D, int64_t n_
   return attn_core_bytes(B * S, D) + align_up((size_t)(B * S * n_heads) * 4);
 }
 
-int partir_attn_block_train(const void* X, const void* Wq_t, const void* Wk_t, const void* Wv_t, const void* Wo_t,
+int partir_attn_block_train(const void* X, const void* Wq, const void* Wk, const void* Wv, const void* Wo,
                             void* Y, void* saved, int64_t B, int64_t S, int64_t D, int64_t n_heads, int64_t d_head,
                             int causal, float scale, int in_dtype, int out_dtype, int R_batch, int R_model,
                             void* ws, size_t ws_bytes, void* stream) {
-  AttnArgs a{X, Wq_t, Wk_t, Wv_t, Wo_t, Y, B, S, D, n_heads, d_head, causal ? 1 : 0, scale,
+  AttnArgs a{X, Wq, Wk, Wv, Wo, Y, B, S, D, n_heads, d_head, causal ? 1 : 0, scale,
              in_dtype, out_dtype, R_batch, R_model, saved};
   int st = validate_attn(a, true);
   if (st) return st;
@@ -1739,14 +1769,14 @@ int partir_plan_attn_block_backward(int64_t B, int64_t S, int64_t D, int64_t n_h
   return PARTIR_OK;
 }
 
-int partir_attn_block_backward(const void* X, const void* Wq_t, const void* Wk_t, const void* Wv_t,
-                               const void* Wo_t, const void* saved, const void* dY, void* dX, void* dWq_t,
-                               void* dWk_t, void* dWv_t, void* dWo_t, int64_t B, int64_t S, int64_t D,
+int partir_attn_block_backward(const void* X, const void* Wq, const void* Wk, const void* Wv,
+                               const void* Wo, const void* saved, const void* dY, void* dX, void* dWq,
+                               void* dWk, void* dWv, void* dWo, int64_t B, int64_t S, int64_t D,
                                int64_t n_heads, int64_t d_head, int causal, float scale, int R_batch, int R_model,
                                void* ws, size_t ws_bytes, void* stream) {
   AttnBlockBwdArgs a;
-  a.X = X; a.Wq = Wq_t; a.Wk = Wk_t; a.Wv = Wv_t; a.Wo = Wo_t; a.saved = saved; a.dY = dY;
-  a.dX = dX; a.dWq = dWq_t; a.dWk = dWk_t; a.dWv = dWv_t; a.dWo = dWo_t;
+  a.X = X; a.Wq = Wq; a.Wk = Wk; a.Wv = Wv; a.Wo = Wo; a.saved = saved; a.dY = dY;
+  a.dX = dX; a.dWq = dWq; a.dWk = dWk; a.dWv = dWv; a.dWo = dWo;
   a.B = B; a.S = S; a.D = D; a.H = n_heads; a.dh = d_head; a.causal = causal ? 1 : 0; a.scale = scale;
   a.Rb = R_batch; a.Rm = R_model;
   int st = validate_attn_block_bwd(a, true);
@@ -1786,13 +1816,13 @@ int partir_plan_mlp_block_backward(int64_t T, int64_t D, int64_t F, int act, int
   return PARTIR_OK;
 }
 
-int partir_mlp_block_backward(const void* X, const void* W1t, const void* b1, const void* W2t, const void* dY,
-                              const void* Z, void* dX, void* dW1t, void* db1, void* dW2t, void* db2, int64_t T,
+int partir_mlp_block_backward(const void* X, const void* W1, const void* b1, const void* W2, const void* dY,
+                              const void* Z, void* dX, void* dW1, void* db1, void* dW2, void* db2, int64_t T,
                               int64_t D, int64_t F, int act, int R_batch, int R_model, void* ws, size_t ws_bytes,
                               void* stream) {
   MlpBwdArgs a;
-  a.X = X; a.W1t = W1t; a.b1 = b1; a.W2t = W2t; a.dY = dY; a.Z = Z;
-  a.dX = dX; a.dW1t = dW1t; a.db1 = db1; a.dW2t = dW2t; a.db2 = db2;
+  a.X = X; a.W1 = W1; a.b1 = b1; a.W2 = W2; a.dY = dY; a.Z = Z;
+  a.dX = dX; a.dW1 = dW1; a.db1 = db1; a.dW2 = dW2; a.db2 = db2;
   a.T = T; a.D = D; a.F = F; a.act = act; a.Rb = R_batch; a.Rm = R_model;
   int st = validate_mlp_bwd(a, true);
   if (st) return st;
@@ -1921,12 +1951,12 @@ int partir_plan_decoder_layer(int64_t B, int64_t S, int64_t D, int64_t n_heads, 
   return PARTIR_OK;
 }
 
-int partir_decoder_layer(void* x, const void* g1, const void* g2, float eps, const void* Wq_t, const void* Wk_t,
-                         const void* Wv_t, const void* Wo_t, const void* W1t, const void* W2t, int64_t B, int64_t S,
+int partir_decoder_layer(void* x, const void* g1, const void* g2, float eps, const void* Wq, const void* Wk,
+                         const void* Wv, const void* Wo, const void* W1, const void* W2, int64_t B, int64_t S,
                          int64_t D, int64_t n_heads, int64_t d_head, int64_t F, int R_batch, int R_model,
                          void* ws, size_t ws_bytes, void* stream) {
   DecArgs a;
-  a.x = x; a.g1 = g1; a.g2 = g2; a.Wq = Wq_t; a.Wk = Wk_t; a.Wv = Wv_t; a.Wo = Wo_t; a.W1 = W1t; a.W2 = W2t;
+  a.x = x; a.g1 = g1; a.g2 = g2; a.Wq = Wq; a.Wk = Wk; a.Wv = Wv; a.Wo = Wo; a.W1 = W1; a.W2 = W2;
   a.eps = eps; a.B = B; a.S = S; a.D = D; a.H = n_heads; a.dh = d_head; a.F = F; a.Rb = R_batch; a.Rm = R_model;
   int st = validate_dec(a, true);
   if (st) return st;

@@ -68,6 +68,19 @@ def sample_rows(T: int, R_batch: int, n: int, seed: int, S: int | None = None,
     return sorted(rows)
 
 
+def every_block_rows(B: int, S: int, seqs, seed: int, block: int = 128):
+    """One seeded row in every `block`-query block of each sequence in
+    `seqs` (so late blocks with long causal key loops are compared too), plus
+    positions 0 and S-1 of those sequences and position 0 of every sequence."""
+    rng = np.random.default_rng(seed)
+    rows = {s * S for s in range(B)}
+    for s in seqs:
+        rows.update((s * S, s * S + S - 1))
+        for b0 in range(0, S, block):
+            rows.add(s * S + b0 + int(rng.integers(0, block)))
+    return sorted(rows)
+
+
 def accum_bound(K: int) -> float:
     """Higham-style bound for fp32 accumulation of K exact products."""
     u = 2.0 ** -24

@@ -95,6 +95,32 @@ def test_loop_matmul_validation(kwargs, status):
     assert P.lib().partir_last_error().decode().startswith(status)
 
 
+@pytest.mark.parametrize("kwargs,status", [
+    # a bf16 operand addresses a 64-row block through a 32-bit byte range: at
+    # lda = 2^25 that range (64 * lda * 2 = 2^32) wraps, so it is refused
+    (dict(M=64, N=8, K=2 ** 25), "PARTIR_E_SHAPE"),
+    (dict(M=64, N=8, K=2 ** 26), "PARTIR_E_SHAPE"),
+    (dict(M=64, N=8, K=2 ** 24 + 8), "PARTIR_E_SHAPE"),
+    (dict(M=64, N=8, K=2 ** 24), "PARTIR_E_HIP"),                    # the largest addressable K
+    (dict(M=64, N=8, K=64, lda=2 ** 24 + 8), "PARTIR_E_SHAPE"),      # a long leading dim alone
+    (dict(M=64, N=2 ** 24 + 8, K=64, bl=P.B_KN, ldc=2 ** 24 + 8), "PARTIR_E_SHAPE"),   # B [K, N] rows
+    (dict(M=2 ** 24 + 8, N=8, K=64, bl=P.B_NK, ldb=2 ** 24 + 8), "PARTIR_E_SHAPE"),    # B^T rows
+    # 2^24 x 2^8 output tiles of 64 x 64: more than a grid indexes
+    (dict(M=2 ** 30, N=2 ** 14, K=64), "PARTIR_E_SHAPE"),
+    (dict(M=2 ** 30, N=2 ** 12, K=64), "PARTIR_E_HIP"),
+])
+def test_loop_matmul_bf16_addressing_limits(kwargs, status):
+    args = dict(ab=P.BF16, c=P.BF16, bl=P.B_NK, summ=P.AXIS_NONE, R=1, ws=NULL, ws_bytes=0)
+    args.update(kwargs)
+    st = mm(**args)
+    assert P.STATUS[st] == status, P.lib().partir_last_error().decode()
+    if status == "PARTIR_E_SHAPE" and not {"lda", "ldb", "ldc"} & set(kwargs):
+        # the size query (leading dims = row lengths) refuses the same shapes
+        assert P.lib().partir_loop_matmul_workspace(args["M"], args["N"], args["K"], P.BF16, P.BF16, args["bl"],
+                                                    args.get("tile", P.AXIS_NONE), P.AXIS_NONE, args["R"],
+                                                    P.SUM_AUTO) == ctypes.c_size_t(-1).value
+
+
 def test_valid_call_reaches_launch(monkeypatch):
     monkeypatch.setenv("PARTIR_FAIL_LAUNCH", "1")
     assert P.STATUS[mm()] == "PARTIR_E_HIP"
@@ -373,11 +399,13 @@ def test_mlp_backward_plans():
     t = p["text"]
     assert p["n_virtual_shards"] == 16 and p["n_tile_loops"] == 2 and p["n_sum_loops"] == 3
     assert p["flops"] == 10.0 * T * D * F
-    # no transposed copies: W1^T, W2^T and the activations are read in place
-    assert "transpose" not in t and "act_backward" in t and t.count("read in place") == 4
-    assert t.count("A as [K, M] B as [K, N]") == 2
+    # no transposed copies: W1 (as [K, N] for the recomputed Z) and the
+    # activations are read in place; W1 and W2 are the K-contiguous
+    # transposed operands of dX and dH
+    assert "transpose" not in t and "act_backward" in t and t.count("read in place") == 3
+    assert t.count("A as [K, M] B as [K, N]") == 2 and t.count("read in place: B as [K, N]") == 1
     # the batch #sum of the weight gradients runs over K = tokens, 2 shards
-    assert "dW2^T = sum_b" in t and "#sum K x2 (4096/shard)" in t
+    assert "dW2 = sum_b" in t and "dW1 = sum_b" in t and "#sum K x2 (4096/shard)" in t
     # the model #sum of dX runs over K = F, 8 shards
     assert "dX = sum_m" in t and "#sum K x8 (2048/shard)" in t
     assert P.lib().partir_mlp_block_backward_workspace(T, D, F, P.ACT_GELU, 0, 2, 8) == p["workspace_bytes"]
@@ -511,6 +539,29 @@ def test_decoder_sharded_validation(kwargs, status):
     assert P.STATUS[dec_sharded(**kwargs)] == status, P.lib().partir_last_error().decode()
 
 
+@pytest.mark.parametrize("Rb,Rm", [(4, 8), (8, 8), (2, 11), (3, 8)])
+def test_decoder_sharded_meshes_beyond_the_part_table_are_refused(Rb, Rm):
+    """The Q|K|V projection reads the three weights' blocks through one table
+    of 64 parts, so meshes of more than 21 devices are refused before any plan
+    is built (the size and plan queries included)."""
+    B, S, H = 2 * Rb, 128 * Rm, 2 * Rm
+    D, F = H * 128, 64 * Rb * Rm
+    assert P.STATUS[dec_sharded(B=B, S=S, D=D, H=H, F=F, Rb=Rb, Rm=Rm)] == "PARTIR_E_UNSUPPORTED"
+    assert "at most 21 devices" in P.lib().partir_last_error().decode()
+    assert P.lib().partir_decoder_layer_sharded_workspace(B, S, D, H, 128, F, Rb, Rm) == ctypes.c_size_t(-1).value
+    with pytest.raises(P.PartirError, match="UNSUPPORTED"):
+        P.plan_decoder_layer_sharded(B, S, D, H, 128, F, R_batch=Rb, R_model=Rm)
+
+
+def test_decoder_sharded_largest_mesh_plans():
+    """21 devices (3 x 7) fill 63 entries of the part table: accepted."""
+    Rb, Rm = 3, 7
+    B, S, H = 3, 128 * 7, 21
+    D, F = H * 128, 64 * 21
+    assert P.STATUS[dec_sharded(B=B, S=S, D=D, H=H, F=F, Rb=Rb, Rm=Rm)] == "PARTIR_E_HIP"
+    assert P.plan_decoder_layer_sharded(B, S, D, H, 128, F, R_batch=Rb, R_model=Rm)["n_virtual_shards"] == 21
+
+
 def test_decoder_sharded_plan():
     p = P.plan_decoder_layer_sharded(4, 2048, 5120, 40, 128, 13824, R_batch=2, R_model=4)
     t = p["text"]
@@ -546,14 +597,15 @@ def test_last_wave_tail_split(M, N, K, tail, parts):
 
 
 def test_attn_block_backward_plan_reads_operands_in_place():
-    """No transposed copies: Wo^T and W{q,k,v}^T are the [K, N] right operands
-    of dA and dX (the three stacked along K), and dY, dQ|dK|dV, X and the
-    attention output the [K, M] / [K, N] operands of the weight gradients."""
+    """No transposed copies: Wo and W{q,k,v} are the K-contiguous transposed
+    right operands of dA and dX (the three as K parts of one product), and
+    dY, dQ|dK|dV, X and the attention output the [K, M] / [K, N] operands of
+    the weight gradients."""
     B, S, D, H = 4, 2048, 4096, 32
     p = P.plan_attn_block_backward(B, S, D, H, R_batch=2, R_model=8)
     t = p["text"]
     assert "transpose" not in t
-    assert t.count("B as [K, N] stacked from 3 arrays") == 1            # dX
+    assert t.count("B^T read as K parts Wq | Wk | Wv") == 1             # dX
     assert t.count("A as [K, M] B as [K, N]") == 4                      # dWq, dWk, dWv, dWo
-    assert t.count("read in place") == 6                                # + dA
+    assert t.count("read in place") == 4
     assert P.lib().partir_attn_block_backward_workspace(B, S, D, H, 128, 2, 8) == p["workspace_bytes"]

@@ -21,14 +21,10 @@ pytestmark = pytest.mark.gpu
 KEYS = ("dX", "dWq", "dWk", "dWv", "dWo")
 
 
-def dev_t(t: I.HostTensor):
-    return I.transposed(t).to_device()
-
-
 def run(w, x, dY, Rb, Rm):
     B, S, D, H = w["B"], w["S"], w["D"], w["H"]
     Xd = x["X"].to_device()
-    Ws = [dev_t(x[k]) for k in ("Wq", "Wk", "Wv", "Wo")]
+    Ws = [x[k].to_device() for k in ("Wq", "Wk", "Wv", "Wo")]
     Y, saved = P.attn_block_train(Xd, *Ws, B=B, S=S, n_heads=H, R_batch=Rb, R_model=Rm)
     Y0 = P.attn_block(Xd, *Ws, B=B, S=S, n_heads=H, R_batch=Rb, R_model=Rm)
     g = P.attn_block_backward(Xd, *Ws, saved, dY.to_device(), B=B, S=S, n_heads=H, R_batch=Rb, R_model=Rm)
@@ -36,7 +32,7 @@ def run(w, x, dY, Rb, Rm):
     assert torch.equal(Y, Y0)          # the training forward computes the same Y
     out = {"dX": host(g[0])}
     for k, t in zip(KEYS[1:], g[1:]):
-        out[k] = host(t).T             # stored W^T -> logical orientation
+        out[k] = host(t)               # [fan_in, fan_out], as the weights
     return out
 
 

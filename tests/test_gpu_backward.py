@@ -22,21 +22,17 @@ pytestmark = pytest.mark.gpu
 KEYS = ("dX", "dW1", "dW2", "db1", "db2")
 
 
-def dev_t(t: I.HostTensor):
-    return I.transposed(t).to_device()
-
-
 def run(x, Rb, Rm, act="gelu", b1=True, bias_grads=True, keep_z=False):
     """The backward pass; with keep_z, after the training forward that keeps Z."""
-    X, W1t, W2t = x["X"].to_device(), dev_t(x["W1"]), dev_t(x["W2"])
+    X, W1, W2 = x["X"].to_device(), x["W1"].to_device(), x["W2"].to_device()
     b1 = x["b1"].to_device() if b1 else None
     Z = None
     if keep_z:
-        _, Z = P.mlp_block_train(X, W1t, W2t, b1=b1, R_batch=Rb, R_model=Rm, act=act)
-    g = P.mlp_block_backward(X, W1t, W2t, x["dY"].to_device(), b1=b1, Z=Z, R_batch=Rb, R_model=Rm, act=act,
+        _, Z = P.mlp_block_train(X, W1, W2, b1=b1, R_batch=Rb, R_model=Rm, act=act)
+    g = P.mlp_block_backward(X, W1, W2, x["dY"].to_device(), b1=b1, Z=Z, R_batch=Rb, R_model=Rm, act=act,
                              bias_grads=bias_grads)
     torch.cuda.synchronize()
-    out = {"dX": host(g[0]), "dW1": host(g[1]).T, "dW2": host(g[2]).T}
+    out = {"dX": host(g[0]), "dW1": host(g[1]), "dW2": host(g[2])}
     if bias_grads:
         out["db1"], out["db2"] = host(g[3]), host(g[4])
     return out
@@ -144,9 +140,9 @@ def test_training_forward_keeps_z(act):
     w = W.WORKLOADS["mlp_train_small"]
     x = W.make_inputs(w)
     Rb, Rm = w["R_batch"], w["R_model"]
-    X, W1t, W2t, b1 = x["X"].to_device(), dev_t(x["W1"]), dev_t(x["W2"]), x["b1"].to_device()
-    Y, Z = P.mlp_block_train(X, W1t, W2t, b1=b1, R_batch=Rb, R_model=Rm, act=act)
-    Y0 = P.mlp_block(X, W1t, W2t, b1=b1, R_batch=Rb, R_model=Rm, act=act)
+    X, W1, W2, b1 = x["X"].to_device(), x["W1"].to_device(), x["W2"].to_device(), x["b1"].to_device()
+    Y, Z = P.mlp_block_train(X, W1, W2, b1=b1, R_batch=Rb, R_model=Rm, act=act)
+    Y0 = P.mlp_block(X, W1, W2, b1=b1, R_batch=Rb, R_model=Rm, act=act)
     torch.cuda.synchronize()
     assert torch.equal(Y, Y0)
     zref = O.loop_tile(Rm, 1, lambda m: O.matmul(x["X"].f64(), O.slice_(x["W1"].f64(), 1, m, Rm))
@@ -165,10 +161,10 @@ def test_backward_empty_sizes():
     # no tokens: every weight and bias gradient is the empty #sum over the batch
     x = {"X": torch.empty((0, D), dtype=torch.bfloat16, device="cuda"),
          "dY": torch.empty((0, D), dtype=torch.bfloat16, device="cuda")}
-    W1t = torch.ones((F, D), dtype=torch.bfloat16, device="cuda")
-    W2t = torch.ones((D, F), dtype=torch.bfloat16, device="cuda")
+    W1 = torch.ones((D, F), dtype=torch.bfloat16, device="cuda")
+    W2 = torch.ones((F, D), dtype=torch.bfloat16, device="cuda")
     b1 = torch.ones((F,), **f32)
-    g = P.mlp_block_backward(x["X"], W1t, W2t, x["dY"], b1=b1, R_batch=2, R_model=4, bias_grads=True)
+    g = P.mlp_block_backward(x["X"], W1, W2, x["dY"], b1=b1, R_batch=2, R_model=4, bias_grads=True)
     torch.cuda.synchronize()
     assert g[0].shape == (0, D)
     for t in g[1:]:
@@ -176,11 +172,11 @@ def test_backward_empty_sizes():
     # no hidden units: dX is the empty #sum over the model loop; db2 = sum_t dY
     dY = I.gaussian(112, 0, (64, D), 1.0)
     X = I.gaussian(112, 1, (64, D), 1.0)
-    g = P.mlp_block_backward(X.to_device(), torch.empty((0, D), dtype=torch.bfloat16, device="cuda"),
-                             torch.empty((D, 0), dtype=torch.bfloat16, device="cuda"), dY.to_device(),
+    g = P.mlp_block_backward(X.to_device(), torch.empty((D, 0), dtype=torch.bfloat16, device="cuda"),
+                             torch.empty((0, D), dtype=torch.bfloat16, device="cuda"), dY.to_device(),
                              R_batch=2, R_model=4, bias_grads=True)
     torch.cuda.synchronize()
-    assert torch.count_nonzero(g[0]).item() == 0 and g[1].shape == (0, D) and g[2].shape == (D, 0)
+    assert torch.count_nonzero(g[0]).item() == 0 and g[1].shape == (D, 0) and g[2].shape == (0, D)
     ref = O.loop_sum(2, lambda b: np.sum(O.slice_(dY.f64(), 0, b, 2), axis=0))
     err = O.normalised_error(host(g[4]), ref, np.sum(np.abs(dY.f64()), axis=0))
     assert err <= 1e-6

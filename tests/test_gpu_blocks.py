@@ -15,21 +15,16 @@ from oracle import partir_oracle as O
 from paper_2401_11202_amd import inputs as I
 from paper_2401_11202_amd import partir as P
 from paper_2401_11202_amd import workloads as W
-from tests.gpu_common import TOL_BF16, host, sample_rows, say
+from tests.gpu_common import TOL_BF16, every_block_rows, host, sample_rows, say
 
 pytestmark = pytest.mark.gpu
-
-
-def dev_t(t: I.HostTensor):
-    """A weight stored output-major (its transpose) on the device."""
-    return I.transposed(t).to_device()
 
 
 # ---------------------------------------------------------------------------
 # MLP
 # ---------------------------------------------------------------------------
 def run_mlp(w, x, b1=None, b2=None, act="gelu", out_dtype=torch.float32):
-    return P.mlp_block(x["X"].to_device(), dev_t(x["W1"]), dev_t(x["W2"]),
+    return P.mlp_block(x["X"].to_device(), x["W1"].to_device(), x["W2"].to_device(),
                        b1=None if b1 is None else b1.to_device(), b2=None if b2 is None else b2.to_device(),
                        R_batch=w["R_batch"], R_model=w["R_model"], act=act, out_dtype=out_dtype)
 
@@ -97,7 +92,7 @@ def test_mlp_integer_exact(Rb, Rm):
     X = I.small_ints(110, 0, (T, D), -1, 1)
     W1 = I.small_ints(110, 1, (D, F), -1, 1)
     W2 = I.small_ints(110, 2, (F, D), -1, 1)
-    Y = P.mlp_block(X.to_device(), dev_t(W1), dev_t(W2), R_batch=Rb, R_model=Rm, act="none",
+    Y = P.mlp_block(X.to_device(), W1.to_device(), W2.to_device(), R_batch=Rb, R_model=Rm, act="none",
                     out_dtype=torch.float32)
     torch.cuda.synchronize()
     ref = O.mlp_block(X.f64(), W1.f64(), W2.f64(), act="none", R_batch=Rb, R_model=Rm)
@@ -112,7 +107,7 @@ def test_mlp_integer_exact_odd_nests(Rb, Rm):
     X = I.small_ints(113, 0, (T, D), -1, 1)
     W1 = I.small_ints(113, 1, (D, F), -1, 1)
     W2 = I.small_ints(113, 2, (F, D), -1, 1)
-    Y = P.mlp_block(X.to_device(), dev_t(W1), dev_t(W2), R_batch=Rb, R_model=Rm, act="none",
+    Y = P.mlp_block(X.to_device(), W1.to_device(), W2.to_device(), R_batch=Rb, R_model=Rm, act="none",
                     out_dtype=torch.float32)
     torch.cuda.synchronize()
     ref = O.mlp_block(X.f64(), W1.f64(), W2.f64(), act="none", R_batch=Rb, R_model=Rm)
@@ -140,7 +135,7 @@ def test_mlp_full_size_sampled_rows(name):
 # attention
 # ---------------------------------------------------------------------------
 def run_attn(w, x, causal=True, out_dtype=torch.float32, Rb=None, Rm=None):
-    return P.attn_block(x["X"].to_device(), dev_t(x["Wq"]), dev_t(x["Wk"]), dev_t(x["Wv"]), dev_t(x["Wo"]),
+    return P.attn_block(x["X"].to_device(), *(x[k].to_device() for k in ("Wq", "Wk", "Wv", "Wo")),
                         B=w["B"], S=w["S"], n_heads=w["H"], d_head=w["dh"], causal=causal,
                         R_batch=w["R_batch"] if Rb is None else Rb, R_model=w["R_model"] if Rm is None else Rm,
                         out_dtype=out_dtype)
@@ -192,7 +187,8 @@ def test_attn_full_size_sampled_rows():
     x = W.make_inputs(w)
     Y = run_attn(w, x)
     torch.cuda.synchronize()
-    rows = sample_rows(w["B"] * w["S"], w["R_batch"], 48, seed=w.wid, S=w["S"], max_pos=512, full_seq_rows=1)
+    # a row in every 128-query block of the first and the last sequence
+    rows = every_block_rows(w["B"], w["S"], (0, w["B"] - 1), seed=w.wid)
     say(f"attn_block: oracle on {len(rows)} rows")
     ref, norm = oracle_attn(w, x, rows=rows)
     err = O.normalised_error(host(Y[rows]), ref, norm)
@@ -206,8 +202,8 @@ def test_attn_full_size_sampled_rows():
 def run_decoder(w, x):
     xd = x["x"].to_device()
     for p in x["layers"]:
-        P.decoder_layer(xd, p["g1"].to_device(), p["g2"].to_device(), dev_t(p["Wq"]), dev_t(p["Wk"]),
-                        dev_t(p["Wv"]), dev_t(p["Wo"]), dev_t(p["W1"]), dev_t(p["W2"]),
+        P.decoder_layer(xd, p["g1"].to_device(), p["g2"].to_device(), p["Wq"].to_device(), p["Wk"].to_device(),
+                        p["Wv"].to_device(), p["Wo"].to_device(), p["W1"].to_device(), p["W2"].to_device(),
                         B=w["B"], S=w["S"], n_heads=w["H"], d_head=w["dh"], eps=1e-6,
                         R_batch=w["R_batch"], R_model=w["R_model"])
     torch.cuda.synchronize()
@@ -264,7 +260,9 @@ def test_decoder_full_size_sampled_rows():
     say("decoder_2layer: generating inputs")
     x = W.make_inputs(w)
     out = run_decoder(w, x)
-    rows = sample_rows(w["B"] * w["S"], w["R_batch"], 24, seed=w.wid, S=w["S"], max_pos=384, full_seq_rows=1)
+    # a row in every 128-query block of the first and the last sequence (one
+    # per batch shard)
+    rows = every_block_rows(w["B"], w["S"], (0, w["B"] - 1), seed=w.wid)
     say(f"decoder_2layer: oracle on {len(rows)} rows")
     ref, norm = O.decoder(x["x"].f64(), oracle_layers(x), w["B"], w["S"], w["H"], w["dh"], 1e-6,
                           w["R_batch"], w["R_model"], rows=rows, return_norm=True)
@@ -282,10 +280,10 @@ def test_mlp_with_empty_ffn_is_the_output_bias(out):
     T, D = 256, 512
     X = I.gaussian(108, 0, (T, D), 1.0, "bf16").to_device()
     b2 = I.gaussian(108, 1, (D,), 1.0, "f32")
-    W1t = torch.empty((0, D), dtype=torch.bfloat16, device="cuda")
-    W2t = torch.empty((D, 0), dtype=torch.bfloat16, device="cuda")
+    W1 = torch.empty((D, 0), dtype=torch.bfloat16, device="cuda")
+    W2 = torch.empty((0, D), dtype=torch.bfloat16, device="cuda")
     say(f"mlp F=0 out={out}")
-    Y = P.mlp_block(X, W1t, W2t, b2=b2.to_device(), R_model=4, out_dtype=out)
+    Y = P.mlp_block(X, W1, W2, b2=b2.to_device(), R_model=4, out_dtype=out)
     torch.cuda.synchronize()
     ref = O.mlp_block(np.zeros((T, D)), np.zeros((D, 0)), np.zeros((0, D)), None, b2.f64(), "gelu", 1, 4)
     if out == torch.bfloat16:
@@ -312,8 +310,8 @@ def test_decoder_with_empty_ffn_matches_oracle():
 def test_attention_with_no_tokens_is_a_no_op():
     X = torch.empty((0, 1024), dtype=torch.bfloat16, device="cuda")
     W_ = I.gaussian(109, 0, (1024, 1024), 1.0 / 32, "bf16")
-    Wt = dev_t(W_)
-    Y = P.attn_block(X, Wt, Wt, Wt, Wt, B=0, S=256, n_heads=8, R_model=8)
+    Wd = W_.to_device()
+    Y = P.attn_block(X, Wd, Wd, Wd, Wd, B=0, S=256, n_heads=8, R_model=8)
     torch.cuda.synchronize()
     assert tuple(Y.shape) == (0, 1024)
 
@@ -337,7 +335,7 @@ def test_planner_emitted_mlp_call_runs_and_matches_oracle():
     Rb, Rm = int(f["R_batch"]), int(f["R_model"])
     assert (Rb, Rm) == (2, 8)
     say(f"planner call: {call}")
-    Y = P.mlp_block(x["X"].to_device(), dev_t(x["W1"]), dev_t(x["W2"]), R_batch=Rb, R_model=Rm, act="gelu",
+    Y = P.mlp_block(x["X"].to_device(), x["W1"].to_device(), x["W2"].to_device(), R_batch=Rb, R_model=Rm, act="gelu",
                     out_dtype=torch.float32)
     torch.cuda.synchronize()
     ref, norm = O.mlp_block(x["X"].f64(), x["W1"].f64(), x["W2"].f64(), act="gelu", R_batch=Rb, R_model=Rm,

@@ -35,8 +35,8 @@ def gains(g):
 
 
 def run_sharded(x, p, g1, g2, B, S, H, RB, RM):
-    Wt = {k: I.transposed(v).to_device() for k, v in p.items()}
-    xs, parts = P.z3_decoder_arrays(x.to_device(), Wt, RB, RM)
+    Wd = {k: v.to_device() for k, v in p.items()}
+    xs, parts = P.z3_decoder_arrays(x.to_device(), Wd, RB, RM)
     G1, G2 = torch.from_numpy(gains(g1)).cuda(), torch.from_numpy(gains(g2)).cuda()
     P.decoder_layer_sharded(xs, G1, G2, parts, B=B, S=S, n_heads=H, R_batch=RB, R_model=RM)
     torch.cuda.synchronize()
@@ -73,9 +73,9 @@ def test_decoder_sharded_full_size_equals_whole_layer():
     say(f"decoder sharded B={B} S={S} D={D} F={F} mesh B={RB} M={RM}")
     got = run_sharded(x, p, g1, g2, B, S, H, RB, RM)
     xw = x.to_device()
-    Wt = [I.transposed(p[k]).to_device() for k in ("Wq", "Wk", "Wv", "Wo", "W1", "W2")]
+    Wd = [p[k].to_device() for k in ("Wq", "Wk", "Wv", "Wo", "W1", "W2")]
     G1, G2 = torch.from_numpy(gains(g1)).cuda(), torch.from_numpy(gains(g2)).cuda()
-    P.decoder_layer(xw, G1, G2, *Wt, B=B, S=S, n_heads=H, R_batch=RB, R_model=RM)
+    P.decoder_layer(xw, G1, G2, *Wd, B=B, S=S, n_heads=H, R_batch=RB, R_model=RM)
     torch.cuda.synchronize()
     assert np.array_equal(got, host(xw))
     rows = [0, 1, 200, S - 1]

@@ -20,12 +20,8 @@ from tests.gpu_common import TOL_BF16, host, say
 pytestmark = pytest.mark.gpu
 
 
-def dev_t(t: I.HostTensor):
-    return I.transposed(t).to_device()
-
-
 def run(x, RB, RM, act="gelu", out_dtype=torch.float32, biases=True):
-    xs, w1s, w2s = P.z3_device_arrays(x["X"].to_device(), dev_t(x["W1"]), dev_t(x["W2"]), RB, RM)
+    xs, w1s, w2s = P.z3_device_arrays(x["X"].to_device(), x["W1"].to_device(), x["W2"].to_device(), RB, RM)
     b1 = x["b1"].to_device() if biases else None
     b2 = x["b2"].to_device() if biases else None
     ys = P.mlp_block_sharded(xs, w1s, w2s, R_batch=RB, R_model=RM, b1=b1, b2=b2, act=act, out_dtype=out_dtype)
@@ -79,7 +75,7 @@ def test_sharded_full_size_rows_and_equal_to_whole_operands():
     T, RB, RM = w["T"], w["R_batch"], w["R_model"]
     say(f"mlp sharded {w.dims}")
     got = np.concatenate(run(x, RB, RM), axis=0)
-    whole = P.mlp_block(x["X"].to_device(), dev_t(x["W1"]), dev_t(x["W2"]), b1=x["b1"].to_device(),
+    whole = P.mlp_block(x["X"].to_device(), x["W1"].to_device(), x["W2"].to_device(), b1=x["b1"].to_device(),
                         b2=x["b2"].to_device(), R_batch=RB, R_model=RM)
     torch.cuda.synchronize()
     assert np.array_equal(got, host(whole))
