@@ -143,6 +143,26 @@ size_t partir_loop_matmul_workspace(int64_t M, int64_t N, int64_t K,
                                     int ab_dtype, int c_dtype, int b_layout,
                                     int tile_axis, int sum_axis, int R, int sum_impl);
 
+/* For callers that cannot allocate (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc): partir_loop_matmul with
+ * the same arguments except the workspace, which is instead a 64 MiB array
+ * in the library's device memory (one per GPU, held until the process
+ * ends).  The call allocates nothing (no hipMalloc or hipFree; with kernel
+ * tracing off it creates no events either).  A call whose
+ * partir_loop_matmul_workspace exceeds 64 MiB returns PARTIR_E_WORKSPACE
+ * before anything is enqueued; other errors as partir_loop_matmul.  Every
+ * split-K partial and tail part is written in full before it is read, so
+ * nothing is cleared between calls, but calls on one GPU share the array:
+ * calls that overlap in time on that GPU (different streams, or different
+ * host threads) race and must be ordered by the caller.  The current device
+ * must be the one `stream` belongs to. */
+int partir_loop_matmul_noalloc(const void* A, const void* B, void* C,
+                               int64_t M, int64_t N, int64_t K,
+                               int64_t lda, int64_t ldb, int64_t ldc,
+                               int ab_dtype, int c_dtype, int b_layout,
+                               int tile_axis, int sum_axis, int R, int sum_impl,
+                               void* stream);
+
 /* ------------------------------------------------------------------------ */
 /* Megatron MLP block nested in a batch #tile (Sec. 5.2.2 final listing,      */
 /* Sec. 2.3 on model parallelism).                                            */

@@ -1207,6 +1207,15 @@ void fill_info(const Plan& plan, partir_plan_info* info) {
 
 void set_last_error(const std::string& msg) { g_error = msg; }
 
+// partir_loop_matmul's argument checks alone (pointers included), for the
+// no-allocation variant, which must report them before it touches a device.
+int validate_loop_matmul_call(const void* A, const void* B, void* C, int64_t M, int64_t N, int64_t K,
+                              int64_t lda, int64_t ldb, int64_t ldc, int ab_dtype, int c_dtype, int b_layout,
+                              int tile_axis, int sum_axis, int R, int sum_impl) {
+  MatmulArgs a{A, B, C, M, N, K, lda, ldb, ldc, ab_dtype, c_dtype, b_layout, tile_axis, sum_axis, R, sum_impl};
+  return validate_matmul(a, true);
+}
+
 }  // namespace partir
 
 using namespace partir;

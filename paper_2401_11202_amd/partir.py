@@ -38,7 +38,8 @@ EXPORTS = ("partir_loop_matmul", "partir_loop_matmul_workspace", "partir_mlp_blo
            "partir_attention_backward_workspace", "partir_plan_attention_backward", "partir_attn_block_train",
            "partir_attn_block_saved_bytes", "partir_attn_block_backward", "partir_attn_block_backward_workspace",
            "partir_plan_attn_block_backward", "partir_decoder_layer_sharded",
-           "partir_decoder_layer_sharded_workspace", "partir_plan_decoder_layer_sharded")
+           "partir_decoder_layer_sharded_workspace", "partir_plan_decoder_layer_sharded",
+           "partir_loop_matmul_noalloc")
 
 
 class PartirError(RuntimeError):
@@ -76,6 +77,8 @@ def lib():
     sig = {
         "partir_loop_matmul": (I32, [P, P, P, I64, I64, I64, I64, I64, I64, I32, I32, I32, I32, I32, I32, I32, P, SZ, P]),
         "partir_loop_matmul_workspace": (SZ, [I64, I64, I64, I32, I32, I32, I32, I32, I32, I32]),
+        "partir_loop_matmul_noalloc": (I32, [P, P, P, I64, I64, I64, I64, I64, I64, I32, I32, I32, I32, I32, I32, I32,
+                                             P]),
         "partir_mlp_block": (I32, [P, P, P, P, P, P, I64, I64, I64, I32, I32, I32, I32, I32, P, SZ, P]),
         "partir_mlp_block_workspace": (SZ, [I64, I64, I64, I32, I32, I32]),
         "partir_attn_block": (I32, [P, P, P, P, P, P, I64, I64, I64, I64, I64, I32, F, I32, I32, I32, I32, P, SZ, P]),
@@ -300,6 +303,32 @@ def loop_matmul(A, B, *, tile: Optional[str] = None, sum: Optional[str] = None, 
     _check(lib().partir_loop_matmul(_ptr(A), _ptr(B), _ptr(out), M, N, K, lda, ldb,
                                     _rowmajor(out, "C"), ab, cd, bl, _axis(tile), _axis(sum), R, si,
                                     _ptr(ws), wsb, _stream(stream)))
+    return out
+
+
+def loop_matmul_noalloc(A, B, *, tile: Optional[str] = None, sum: Optional[str] = None, R: int = 1,
+                        b_layout: str = "kn", out_dtype=None, sum_impl: str = "auto", out, stream=None):
+    """loop_matmul without a workspace: the library's per-GPU scratch array
+    holds the #sum partials (see partir_loop_matmul_noalloc).  `out` must be
+    given (this call allocates nothing)."""
+    import torch
+    lda, ldb = _rowmajor(A, "A"), _rowmajor(B, "B")
+    M, K = A.shape
+    bl = B_KN if b_layout == "kn" else B_NK
+    Kb, N = (B.shape[0], B.shape[1]) if bl == B_KN else (B.shape[1], B.shape[0])
+    if Kb != K:
+        _bad("PARTIR_E_SHAPE", f"B holds K = {Kb}, A holds K = {K}")
+    ab = _dt(A)
+    if B.dtype != A.dtype:
+        _bad("PARTIR_E_DTYPE", f"A is {A.dtype}, B is {B.dtype}")
+    cd = ab if out_dtype is None else (BF16 if out_dtype == torch.bfloat16 else F32)
+    ldc = _rowmajor(out, "C")
+    if tuple(out.shape) != (M, N) or out.dtype != _tdt(cd):
+        _bad("PARTIR_E_LAYOUT", f"out is {tuple(out.shape)} {out.dtype}, expected [{M}, {N}] {_tdt(cd)}")
+    _gpu_all(A=A, B=B, out=out)
+    si = {"auto": SUM_AUTO, "fused": SUM_FUSED, "splitk": SUM_SPLITK}[sum_impl]
+    _check(lib().partir_loop_matmul_noalloc(_ptr(A), _ptr(B), _ptr(out), M, N, K, lda, ldb, ldc, ab, cd, bl,
+                                            _axis(tile), _axis(sum), R, si, _stream(stream)))
     return out
 
 

@@ -121,6 +121,30 @@ def test_loop_matmul_bf16_addressing_limits(kwargs, status):
                                                     P.SUM_AUTO) == ctypes.c_size_t(-1).value
 
 
+def mm_noalloc(M=256, N=256, K=512, ab=P.F32, c=P.F32, bl=P.B_KN, tile=P.AXIS_NONE, summ=P.AXIS_K, R=4,
+               impl=P.SUM_AUTO, A=DUMMY, B=DUMMY, C=DUMMY):
+    lda, ldb, ldc = K, (N if bl == P.B_KN else K), N
+    return P.lib().partir_loop_matmul_noalloc(A, B, C, M, N, K, lda, ldb, ldc, ab, c, bl, tile, summ, R, impl, None)
+
+
+@pytest.mark.parametrize("kwargs,status", [
+    # split-K partials of 8 x [2048, 2048] fp32 = 128 MiB: beyond the 64 MiB scratch
+    (dict(M=2048, N=2048, K=8192, ab=P.BF16, c=P.BF16, bl=P.B_NK, R=8), "PARTIR_E_WORKSPACE"),
+    (dict(M=4096, N=4096, K=4096, ab=P.BF16, c=P.F32, bl=P.B_NK, R=2, impl=P.SUM_SPLITK), "PARTIR_E_WORKSPACE"),
+    # invalid calls report partir_loop_matmul's own status
+    (dict(R=3), "PARTIR_E_DIVISIBILITY"),
+    (dict(A=NULL), "PARTIR_E_NULL"),
+    (dict(ab=P.F32, c=P.BF16), "PARTIR_E_DTYPE"),
+    # no scratch needed (no #sum): straight to the launch, which is forced to fail here
+    (dict(summ=P.AXIS_NONE, R=1), "PARTIR_E_HIP"),
+])
+def test_loop_matmul_noalloc_validation(kwargs, status):
+    st = mm_noalloc(**kwargs)
+    assert P.STATUS[st] == status, P.lib().partir_last_error().decode()
+    if status == "PARTIR_E_WORKSPACE":
+        assert "bytes of scratch" in P.lib().partir_last_error().decode()
+
+
 def test_valid_call_reaches_launch(monkeypatch):
     monkeypatch.setenv("PARTIR_FAIL_LAUNCH", "1")
     assert P.STATUS[mm()] == "PARTIR_E_HIP"
