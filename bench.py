@@ -362,42 +362,56 @@ def _cpu_sample(w, x, target_s, cores):
     raise ValueError(w.kind)
 
 
-def traffic_from_profile(workload, role):
-    """HBM bytes per launch of `role` from a committed rocprofv3 counter summary,
-    valid only while the kernel source is unchanged."""
-    path = os.path.join(ROOT, "profiles", f"traffic_{role.replace('.', '_')}_{workload}.md")
+# Sources that determine each kernel role's launches (the kernel itself, the
+# shared headers and the planner that sizes its grid): a committed counter
+# summary stays valid while these files are unchanged.
+_COMMON = ("kernels.h", "partir_api.cpp")
+_ROLE_SOURCES = {
+    "gemm": ("gemm_bf16.hip", "device_math.h") + _COMMON,
+    "attn.core": ("attention.hip",) + _COMMON,
+    "attn.bwd": ("attention_bwd.hip",) + _COMMON,
+    "loop_matmul.f32": ("gemm_f32.hip", "elementwise.hip") + _COMMON,
+}
+
+
+def role_sources(role):
+    if role in _ROLE_SOURCES:
+        return _ROLE_SOURCES[role]
+    return _ROLE_SOURCES["gemm"]   # every other role is a bf16 GEMM
+
+
+def kernel_source_hash(role):
+    d = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2401_11202_amd", "csrc")
+    for f in sorted(role_sources(role)):
+        d.update(f.encode())
+        d.update(open(os.path.join(csrc, f), "rb").read())
+    return d.hexdigest()
+
+
+def _profile_value(path, key, role):
     if not os.path.exists(path):
         return None
     text = open(path).read()
-    m = re.search(r"traffic_bytes_per_launch:\s*([0-9.eE+]+)", text)
-    h = re.search(r"kernel_source_sha256:\s*([0-9a-f]+)", text)
-    if not m or not h or h.group(1) != kernel_source_hash():
+    h = re.search(r"kernel_source_sha256 " + re.escape(role) + r":\s*([0-9a-f]+)", text)
+    m = re.search(key + r"\s+" + re.escape(role) + r":\s*([0-9.eE+]+)", text)
+    if not m or not h or h.group(1) != kernel_source_hash(role):
         return None
     return float(m.group(1))
+
+
+def traffic_from_profile(workload, role):
+    """HBM bytes per launch of `role` from the committed rocprofv3 counter
+    summary (FETCH_SIZE and WRITE_SIZE scaled by a plain copy's readings),
+    valid only while the role's kernel sources are unchanged."""
+    return _profile_value(os.path.join(ROOT, "profiles", f"traffic_{workload}.md"), "traffic_bytes_per_launch", role)
 
 
 def mfma_busy_from_profile(workload, role):
     """MFMA busy fraction of `role`'s kernel from the committed rocprofv3
-    counter summary (SQ_VALU_MFMA_BUSY_CYCLES over the dispatch's cycles),
-    valid only while the kernel source is unchanged."""
-    path = os.path.join(ROOT, "profiles", f"mfma_util_{workload}.md")
-    if not os.path.exists(path):
-        return None
-    text = open(path).read()
-    h = re.search(r"kernel_source_sha256:\s*([0-9a-f]+)", text)
-    m = re.search(r"mfma_busy\s+" + re.escape(role) + r":\s*([0-9.]+)", text)
-    if not m or not h or h.group(1) != kernel_source_hash():
-        return None
-    return float(m.group(1))
-
-
-def kernel_source_hash():
-    d = hashlib.sha256()
-    csrc = os.path.join(ROOT, "paper_2401_11202_amd", "csrc")
-    for f in sorted(os.listdir(csrc)):
-        if f.endswith((".hip", ".h", ".cpp")):
-            d.update(open(os.path.join(csrc, f), "rb").read())
-    return d.hexdigest()
+    counter summary (SQ_VALU_MFMA_BUSY_CYCLES over the dispatch's SIMD
+    cycles), valid only while the role's kernel sources are unchanged."""
+    return _profile_value(os.path.join(ROOT, "profiles", f"mfma_util_{workload}.md"), "mfma_busy", role)
 
 
 def main():

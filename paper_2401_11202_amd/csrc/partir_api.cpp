@@ -35,7 +35,11 @@ namespace {
 constexpr int kNumCU = 256;           // MI355X compute units: a grid below this underfills
 // Tile-order grouping for L2 reuse: consecutive workgroups walk group_m tile
 // rows before the next tile column; wide grids want shorter groups.
-int group_m_for(int tiles_n) { return std::min(8, std::max(2, 128 / std::max(1, tiles_n))); }
+// Tile-order grouping of the bf16 GEMM: consecutive tiles walk group_m tile
+// rows before moving to the next tile column, so the 32 tiles one XCD runs at
+// a time form a 4 x 8 block of the output, whose operands are 12 row blocks
+// (a 2 x 16 block needs 18): the least L2 -> fabric traffic per k step.
+int group_m_for(int /*tiles_n*/) { return 4; }
 constexpr size_t kWsAlign = 256;
 
 thread_local std::string g_error;
