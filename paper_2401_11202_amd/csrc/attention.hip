@@ -26,16 +26,25 @@ typedef int i32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int DH = 128, BQ = 128, BKV = 64, NT = 256;
-constexpr int KP = 256;                 // K tile row pitch (bytes), chunk-swizzled
-// V tile row pitch (bytes), padded: 320 = 256 + 64 puts consecutive rows 16
-// banks apart, so the 32 lanes of one ds_read_b64_tr_b16 half (4 rows x 2
-// column halves x 4 column quads, 8 B each) cover all 64 banks once
-constexpr int VP = 320;
-constexpr int KT_BYTES = BKV * KP;
-constexpr int VT_BYTES = BKV * VP;
-constexpr int STAGE = KT_BYTES + VT_BYTES;
+// K and V tiles: 64 rows of 256 B, written by direct-to-LDS buffer loads
+// (each wave load fills 1 KiB = 4 whole rows).  K: 16-byte chunk c of row r
+// at position c ^ (r & 15), so the 32 rows one S^T fragment read touches hit
+// all 64 banks.  V: 64-byte group g of row r at position g ^ (r & 3), so the
+// 4 rows x 64 B one half of a ds_read_b64_tr_b16 touches hit all 64 banks.
+constexpr int RP = 256;
+constexpr int T_BYTES = BKV * RP;
+constexpr int STAGE = 2 * T_BYTES;      // K tile, then V tile
 
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+typedef __attribute__((address_space(3))) void lds_void;
+
+// LDS reads through restrict pointers: the alias scope keeps the wait
+// insertion from making them wait on the next tiles' DMA (which writes the
+// other stage; the loop orders stages by explicit waits and barriers).
+__device__ __forceinline__ bf16x8 lds_read_b128(const char* __restrict__ p) { return *(const bf16x8*)p; }
+__device__ __forceinline__ i16x4 lds_read_tr16(const char* __restrict__ p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)p);
+}
 
 // Buffer descriptor of a workgroup-uniform base pointer (kept in SGPRs).
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint32_t bytes) {
@@ -85,36 +94,26 @@ void attention_kernel(AttnParams p) {
     for (int ds = 0; ds < 8; ++ds) qf[ds] = *(const bf16x8*)(qrow + 16 * ds);
   }
 
-  // ---- K / V tile loads: 64 rows x 256 B each, 4 + 4 chunks of 16 B per thread.
-  // Buffer loads: the per-thread row offsets are loop-invariant VGPRs and the
-  // key block enters as a scalar offset.
-  const int lr = tid >> 4, lc = tid & 15;
+  // ---- K / V tile loads straight into LDS: wave load i of wave w fills rows
+  // 16 i + 4 w .. +3 of a tile; lane L writes LDS chunk L % 16 of row
+  // 16 i + 4 w + L / 16, so it reads the global chunk that the tile's swizzle
+  // puts there.  The key block and the row block i enter as scalar offsets.
   const __amdgpu_buffer_rsrc_t krs = make_rsrc(p.K + tok0 * p.ldk + head * DH, (uint32_t)((p.S - 1) * p.ldk * 2 + DH * 2));
   const __amdgpu_buffer_rsrc_t vrs = make_rsrc(p.V + tok0 * p.ldv + head * DH, (uint32_t)((p.S - 1) * p.ldv * 2 + DH * 2));
-  uint32_t kvo[4], vvo[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    kvo[i] = (uint32_t)((lr + 16 * i) * p.ldk * 2 + lc * 16);
-    vvo[i] = (uint32_t)((lr + 16 * i) * p.ldv * 2 + lc * 16);
-  }
+  const int lrow = 4 * w + (lane >> 4), lch = lane & 15;   // row within a 16-row block; LDS chunk
+  const uint32_t kvo = (uint32_t)(lrow * p.ldk * 2 + ((lch ^ (lrow & 15)) << 4));
+  const uint32_t vvo = (uint32_t)(lrow * p.ldv * 2 + ((((lch >> 2) ^ (lrow & 3)) << 2 | (lch & 3)) << 4));
   const uint32_t kstep = (uint32_t)(BKV * p.ldk * 2), vstep = (uint32_t)(BKV * p.ldv * 2);
-  i32x4 rk[4], rv[4];
-  auto gload = [&](int kb) {
-    const uint32_t ks_off = (uint32_t)kb * kstep, vs_off = (uint32_t)kb * vstep;
+  const uint32_t krow16 = (uint32_t)(16 * p.ldk * 2), vrow16 = (uint32_t)(16 * p.ldv * 2);
+  auto gload = [&](int kb, int buf) {
+    char* ks = smem + buf * STAGE + w * 1024;
+    char* vs = ks + T_BYTES;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      rk[i] = __builtin_bit_cast(i32x4, __builtin_amdgcn_raw_buffer_load_b128(krs, kvo[i], ks_off, 0));
-      rv[i] = __builtin_bit_cast(i32x4, __builtin_amdgcn_raw_buffer_load_b128(vrs, vvo[i], vs_off, 0));
-    }
-  };
-  auto lstore = [&](int buf) {
-    char* ks = smem + buf * STAGE;
-    char* vs = ks + KT_BYTES;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int r = lr + 16 * i;
-      *(i32x4*)(ks + r * KP + ((lc ^ (r & 15)) << 4)) = rk[i];
-      *(i32x4*)(vs + r * VP + (lc << 4)) = rv[i];
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(krs, (lds_void*)(ks + i * 4096), 16, kvo,
+                                               (uint32_t)kb * kstep + i * krow16, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(vrs, (lds_void*)(vs + i * 4096), 16, vvo,
+                                               (uint32_t)kb * vstep + i * vrow16, 0, 0);
     }
   };
 
@@ -125,20 +124,20 @@ void attention_kernel(AttnParams p) {
     for (int v = 0; v < 16; ++v) oacc[d][v] = 0.0f;
   float m_run = -1e30f, l_run = 0.0f;
 
-  // ds_read_b64_tr_b16 addressing for the V^T operand (see header comment)
+  // ds_read_b64_tr_b16 addressing for the V^T operand (see header comment);
+  // row v_row (+ 16 u, + 8) keeps v_row & 3, so its 64-byte group d sits at
+  // d ^ v_sw
   const int j16 = lane & 15, G = lane >> 4, hh = G >> 1;
   const int v_row = 4 * hh + (j16 >> 2);
   const int v_colb = 2 * (16 * (G & 1) + 4 * (j16 & 3));
+  const int v_sw = v_row & 3;
 
   const int nkb_all = p.causal ? (q0 + BQ + BKV - 1) / BKV : p.S / BKV;
   const int kb_begin = p.nsplit > 1 ? split * p.kb_per : 0;
   const int nkb = p.nsplit > 1 ? min(nkb_all, kb_begin + p.kb_per) : nkb_all;   // one past the last block
   const int wave_last_q = q0 + 32 * w + 31;
 
-  if (kb_begin < nkb) {
-    gload(kb_begin);
-    lstore(0);
-  }
+  if (kb_begin < nkb) gload(kb_begin, 0);
   // Every load so far (the Q fragments included) has landed on every path
   // into the loop; without this the wait insertion cannot tell on the path
   // that skips the first block, and waits on the next block's prefetch
@@ -147,11 +146,12 @@ void attention_kernel(AttnParams p) {
   __syncthreads();
   for (int kb = kb_begin; kb < nkb; ++kb) {
     const int cur = (kb - kb_begin) & 1;
-    if (kb + 1 < nkb) gload(kb + 1);
+    // the other stage was finished with before the last barrier
+    if (kb + 1 < nkb) gload(kb + 1, cur ^ 1);
     const int k0 = kb * BKV;
     if (!p.causal || k0 <= wave_last_q) {
       const char* ks = smem + cur * STAGE;
-      const char* vs = ks + KT_BYTES;
+      const char* vs = ks + T_BYTES;
       // S^T = K Q^T for two 32-key sub-tiles
       f32x16 sacc[2];
 #pragma unroll
@@ -161,7 +161,7 @@ void attention_kernel(AttnParams p) {
         const int r = 32 * t + col;
 #pragma unroll
         for (int ds = 0; ds < 8; ++ds) {
-          const bf16x8 kf = *(const bf16x8*)(ks + r * KP + (((2 * ds + h) ^ (r & 15)) << 4));
+          const bf16x8 kf = lds_read_b128(ks + r * RP + (((2 * ds + h) ^ (r & 15)) << 4));
           sacc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ds], sacc[t], 0, 0, 0);
         }
       }
@@ -217,9 +217,9 @@ void attention_kernel(AttnParams p) {
       for (int u = 0; u < 4; ++u) {
 #pragma unroll
         for (int d = 0; d < 4; ++d) {
-          const char* base = vs + (16 * u + v_row) * VP + 64 * d + v_colb;
-          const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(base));
-          const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(base + 8 * VP));
+          const char* base = vs + (16 * u + v_row) * RP + 64 * (d ^ v_sw) + v_colb;
+          const i16x4 lo = lds_read_tr16(base);
+          const i16x4 hi = lds_read_tr16(base + 8 * RP);
           // whole-vector reinterpretation (per-element casts were lowered to
           // reads of the first dword only)
           const bf16x8 vf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
@@ -227,7 +227,7 @@ void attention_kernel(AttnParams p) {
         }
       }
     }
-    if (kb + 1 < nkb) lstore(cur ^ 1);
+    __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0): this wave's loads of the next tiles landed
     __syncthreads();
   }
 
