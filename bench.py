@@ -369,8 +369,15 @@ _COMMON = ("kernels.h", "partir_api.cpp")
 _ROLE_SOURCES = {
     "gemm": ("gemm_bf16.hip", "device_math.h") + _COMMON,
     "attn.core": ("attention.hip",) + _COMMON,
+    "attn.combine": ("attention.hip",) + _COMMON,
     "attn.bwd": ("attention_bwd.hip",) + _COMMON,
     "loop_matmul.f32": ("gemm_f32.hip", "elementwise.hip") + _COMMON,
+    "loop_matmul.f32.reduce": ("elementwise.hip",) + _COMMON,
+    "rmsnorm": ("elementwise.hip",) + _COMMON,
+    "mlp.bwd.act": ("backward.hip", "device_math.h") + _COMMON,
+    "mlp.bwd.db1": ("backward.hip",) + _COMMON,
+    "mlp.bwd.db2.partial": ("backward.hip",) + _COMMON,
+    "mlp.bwd.db2": ("backward.hip",) + _COMMON,
 }
 
 
