@@ -21,12 +21,13 @@
  * Conventions shared by all entry points
  * --------------------------------------
  * Layout.  Every matrix is row-major with an explicit leading dimension
- *   (elements between consecutive rows).  Weight matrices of the blocks are
- *   passed "output-major": a logical weight W of shape [fan_in, fan_out] is
- *   stored as its transpose W^T, a row-major [fan_out, fan_in] array (the
- *   nn.Linear layout), so that every MFMA operand is a contiguous run along
- *   the contraction dim.  `slice 1 W[m]` is then a block of rows of W^T and
- *   `slice 0 W[m]` a block of its columns; both are views.
+ *   (elements between consecutive rows).  The weights of partir_mlp_block,
+ *   partir_attn_block, partir_decoder_layer and their training and backward
+ *   calls are logical W [fan_in, fan_out], row-major: `slice 1 W[m]` is a
+ *   block of its columns and `slice 0 W[m]` a block of its rows, both views,
+ *   and the GEMMs read them in place (transposed LDS reads form the MFMA
+ *   operand).  The device-local entry points (*_sharded) take their weight
+ *   parts from W^T [fan_out, fan_in] instead, as each declaration states.
  * Memory.  All tensor pointers are device pointers owned by the caller, which
  *   also allocates the workspace (size from the matching *_workspace query;
  *   may be NULL when the query returns 0).  The library allocates no device

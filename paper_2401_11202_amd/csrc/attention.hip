@@ -13,6 +13,7 @@
 // and V sides (any order is exact for the contraction).
 // With causal masking a query sees keys at positions <= its own.
 #include "kernels.h"
+#include "lds_dma.h"
 
 namespace partir {
 namespace {
@@ -35,25 +36,10 @@ constexpr int RP = 256;
 constexpr int T_BYTES = BKV * RP;
 constexpr int STAGE = 2 * T_BYTES;      // K tile, then V tile
 
-typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
-typedef __attribute__((address_space(3))) void lds_void;
-
-// LDS reads through restrict pointers: the alias scope keeps the wait
-// insertion from making them wait on the next tiles' DMA (which writes the
-// other stage; the loop orders stages by explicit waits and barriers).
+// LDS reads of K fragments through a restrict pointer, for the same reason
+// as lds_read_tr16: the alias scope keeps the wait insertion from making them
+// wait on the next tiles' DMA (which writes the other stage).
 __device__ __forceinline__ bf16x8 lds_read_b128(const char* __restrict__ p) { return *(const bf16x8*)p; }
-__device__ __forceinline__ i16x4 lds_read_tr16(const char* __restrict__ p) {
-  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)p);
-}
-
-// Buffer descriptor of a workgroup-uniform base pointer (kept in SGPRs).
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint32_t bytes) {
-  const uint64_t a = (uint64_t)p;
-  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)a);
-  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(a >> 32));
-  void* u = (void*)(((uint64_t)hi << 32) | lo);
-  return __builtin_amdgcn_make_buffer_rsrc(u, (short)0, (int)__builtin_amdgcn_readfirstlane(bytes), 0x00020000);
-}
 
 __global__ __launch_bounds__(NT, 2)
 void attention_kernel(AttnParams p) {

@@ -21,6 +21,7 @@
 // All LDS tiles are 64 rows x 256 B with 16-byte chunks XOR-swizzled by row,
 // which serves both the row reads and the transposed reads.
 #include "kernels.h"
+#include "lds_dma.h"
 
 namespace partir {
 namespace {
@@ -31,29 +32,17 @@ typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef int i32x4 __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
 constexpr int DH = 128, NT = 256;
 constexpr int TR = 64;                 // rows of a streamed tile
 constexpr int TP = 256;                // tile row pitch (bytes)
 constexpr int TILE = TR * TP;          // 16 KiB
 
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint32_t bytes) {
-  const uint64_t a = (uint64_t)p;
-  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)a);
-  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(a >> 32));
-  void* u = (void*)(((uint64_t)hi << 32) | lo);
-  return __builtin_amdgcn_make_buffer_rsrc(u, (short)0, (int)__builtin_amdgcn_readfirstlane(bytes), 0x00020000);
-}
-
 // byte offset of (row, byte column) in a swizzled tile
 __device__ __forceinline__ int toff(int row, int colb) {
   return row * TP + ((((colb >> 4) ^ (row & 15))) << 4) + (colb & 15);
 }
 
-typedef __attribute__((address_space(3))) void lds_void;
-// s_waitcnt with only the vector-memory counter constrained (gfx9 encoding)
-#define WAIT_VMCNT(n) __builtin_amdgcn_s_waitcnt((((n) & 15) | (((n) >> 4) << 14)) | (0x7 << 4) | (0xF << 8))
 
 // Streams two [64 x 128] bf16 tiles (rows of X and Y, head columns) into a
 // swizzled LDS stage with buffer loads that write LDS directly: load j of
@@ -97,14 +86,6 @@ struct TileDma {
 // & 31), contraction (d) chunk 2 ds + h.
 __device__ __forceinline__ bf16x8 row_frag(const char* tile, int r0, int col, int h, int ds) {
   return *(const bf16x8*)(tile + toff(r0 + col, (2 * ds + h) * 16));
-}
-
-// ds_read_b64_tr_b16 through a restrict pointer: the alias scope this gives
-// the read keeps the wait insertion from making it wait for every LDS DMA in
-// flight (the next block's loads; the loops order their stages by explicit
-// vmcnt waits and barriers).
-__device__ __forceinline__ i16x4 lds_read_tr16(const char* __restrict__ p) {
-  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)p);
 }
 
 // A operand X^T[d rows 32 dt.., positions 16 u..] of a tile X [positions x d],

@@ -20,6 +20,7 @@
 //    its own fp32 partial; an ordered reduction (elementwise.hip) sums them.
 #include "kernels.h"
 #include "device_math.h"
+#include "lds_dma.h"
 
 namespace partir {
 namespace {
@@ -30,7 +31,6 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
 constexpr int BM = 256, BN = 256, NT = 512;
 constexpr int BK = 64, NS = 2;
@@ -51,29 +51,11 @@ constexpr uint32_t OOB = 0x80000000u;          // offset that reads as zero
 constexpr int PHI_N = 3072;
 constexpr float PHI_LO = -6.0f, PHI_SCALE = 256.0f;
 constexpr int PHI_BYTES = PHI_N * 8;
-typedef __attribute__((address_space(3))) void lds_void;
-
-// ds_read_b64_tr_b16 through a restrict pointer: the alias scope this gives
-// the read keeps the wait insertion from making it wait on every LDS DMA in
-// flight (the K loop orders its stages by explicit vmcnt waits and barriers).
-__device__ __forceinline__ i16x4 lds_read_tr16(const char* __restrict__ p) {
-  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)p);
-}
 
 // LDS reads to place after MFMA i of a k step that has nrd of them.
 template <int nrd>
 constexpr int lds_reads_after(int i) {
   return nrd <= 8 ? (i < nrd ? 1 : 0) : (i < nrd - 8 ? 2 : 1);
-}
-
-// Buffer descriptor of a workgroup-uniform base pointer (kept in SGPRs); any
-// offset at or beyond `bytes` reads as zero.
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint32_t bytes) {
-  const uint64_t a = (uint64_t)p;
-  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)a);
-  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(a >> 32));
-  void* u = (void*)(((uint64_t)hi << 32) | lo);
-  return __builtin_amdgcn_make_buffer_rsrc(u, (short)0, (int)__builtin_amdgcn_readfirstlane(bytes), 0x00020000);
 }
 
 template <typename T>
@@ -83,9 +65,6 @@ __device__ __forceinline__ T pick3(int g, T a, T b, T c) { return g == 0 ? a : (
 // c of row r sits at position c ^ swz(r), swz(r) = (r & 7) ^ ((r >> 3) & 1),
 // which spreads the 32 rows one MFMA operand read touches over all banks.
 __device__ __forceinline__ int swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
-
-// s_waitcnt with only the vector-memory counter constrained (gfx9 encoding)
-#define WAIT_VMCNT(n) __builtin_amdgcn_s_waitcnt((((n) & 15) | (((n) >> 4) << 14)) | (0x7 << 4) | (0xF << 8))
 
 // PARTS: operands in device-local arrays (`t`, a kernel argument); else the
 // plain pointers of `p` and t is unused.
@@ -103,7 +82,7 @@ __device__ __forceinline__ void gemm_body(const GemmParams& p, const GemmParts* 
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform: LDS bases and M0 in SGPRs
   const int wm = wave >> 2, wn = wave & 3;
 
   // ---- which tile of which virtual shard ----------------------------------
