@@ -151,6 +151,45 @@ def test_mlp_backward_norms_bound_the_gradients():
     assert np.allclose(n["dW2"], (np.abs(X) @ np.abs(W1) + np.abs(b1)).T @ np.abs(dY), rtol=1e-13, atol=0)
 
 
+def test_mlp_backward_norms_exact_on_nonnegative_operands():
+    """Two-sided pin of the GELU-case normalisers: with X, W1, b1, W2, dY >= 0
+    every |A||B| product equals AB, so each normaliser reduces to a closed
+    form written here from plain definitions (scipy's normal cdf and pdf for
+    GELU and its derivative): the dX, dW1, db1 normalisers exceed |grad| by
+    exactly the first-order term dH * Z carried through the same product,
+    and dW2's is (2 z Phi(z) + z^2 phi(z))^T dY.  An inflated or deflated
+    normaliser fails."""
+    from scipy.stats import norm
+    rng = np.random.default_rng(31)
+    T, D, F = 12, 6, 20
+    X = rng.uniform(0.0, 1.5, (T, D))
+    W1 = rng.uniform(0.0, 1.0, (D, F)) / math.sqrt(D)
+    W2 = rng.uniform(0.0, 1.0, (F, D)) / math.sqrt(F)
+    dY = rng.uniform(0.0, 1.0, (T, D))
+    b1 = rng.uniform(0.0, 0.5, F)
+    g, n = O.mlp_block_backward(X, W1, W2, dY, b1, "gelu", 2, 2, return_norm=True)
+    z = X @ W1 + b1                      # >= 0
+    dh = dY @ W2.T                       # >= 0
+    gp = norm.cdf(z) + z * norm.pdf(z)   # GELU'(z) > 0 for z >= 0
+    dz = dh * gp
+    extra = dh * z                       # |dH| nZ with nZ = Z here
+    assert np.allclose(g["dX"], dz @ W1.T, rtol=1e-12, atol=0)
+    assert np.allclose(n["dX"], (dz + extra) @ W1.T, rtol=1e-12, atol=0)
+    assert np.allclose(n["dW1"], X.T @ (dz + extra), rtol=1e-12, atol=0)
+    assert np.allclose(n["db1"], (dz + extra).sum(axis=0), rtol=1e-12, atol=0)
+    nh = 2.0 * z * norm.cdf(z) + z * z * norm.pdf(z)   # GELU'(z) z + GELU(z)
+    assert np.allclose(n["dW2"], nh.T @ dY, rtol=1e-12, atol=0)
+    assert np.allclose(n["db2"], dY.sum(axis=0), rtol=1e-13, atol=0)
+    # the sampled loop nests (the full-size GPU tests' reference) give the
+    # same normalisers at the rows and units they evaluate
+    rows, units = [0, 5, 11], [1, 7, 19]
+    _, sn = O.mlp_block_backward_sampled(X, W1, W2, dY, b1, "gelu", 2, 2, rows, units)
+    assert np.allclose(sn["dX"], ((dz + extra) @ W1.T)[rows], rtol=1e-12, atol=0)
+    assert np.allclose(sn["dW1"], (X.T @ (dz + extra))[:, units], rtol=1e-12, atol=0)
+    assert np.allclose(sn["db1"], (dz + extra).sum(axis=0)[units], rtol=1e-12, atol=0)
+    assert np.allclose(sn["dW2"], (nh.T @ dY)[units], rtol=1e-12, atol=0)
+
+
 def test_mlp_backward_empty_sizes():
     rng = np.random.default_rng(9)
     D, F = 8, 16
@@ -259,6 +298,27 @@ def test_attention_backward_norms_bound():
     (dq, dk, dv), (nq, nk, nv) = O.attention_backward(q, k, v, do, 0.35, True, return_norm=True)
     for g, n in ((dq, nq), (dk, nk), (dv, nv)):
         assert np.all(np.abs(g) <= n * (1 + 1e-12))
+
+
+@pytest.mark.parametrize("causal", [True, False])
+def test_attention_backward_norms_exact_on_nonnegative_operands(causal):
+    """Two-sided pin of the attention-backward normalisers: with q, k, v,
+    do >= 0 the magnitudes equal the values, so nv = dv exactly and nq, nk
+    exceed dq, dk by exactly 2 scale (P * D) K and 2 scale (P * D)^T Q, with
+    P = softmax(scale q k^T) (scipy) and D_i = sum_d do_id o_id, o = P v."""
+    from scipy.special import softmax
+    rng = np.random.default_rng(41)
+    n, dh, scale = 10, 4, 0.4
+    q, k, v, do = (rng.uniform(0.0, 1.0, (n, dh)) for _ in range(4))
+    (dq, dk, dv), (nq, nk, nv) = O.attention_backward(q, k, v, do, scale, causal, return_norm=True)
+    s = scale * (q @ k.T)
+    if causal:
+        s = np.where(np.tril(np.ones((n, n), bool)), s, -np.inf)
+    P = softmax(s, axis=1)
+    D = np.sum(do * (P @ v), axis=1, keepdims=True)
+    assert np.allclose(nv, dv, rtol=1e-12, atol=0)
+    assert np.allclose(nq, dq + 2.0 * scale * (P * D) @ k, rtol=1e-11, atol=1e-15)
+    assert np.allclose(nk, dk + 2.0 * scale * (P * D).T @ q, rtol=1e-11, atol=1e-15)
 
 
 # ---------------------------------------------------------------------------
