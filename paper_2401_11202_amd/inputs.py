@@ -89,6 +89,14 @@ def ones(shape, dtype: str = "f32") -> HostTensor:
     return _make(np.ones(shape, np.float32), dtype)
 
 
+def row_scaled(t: HostTensor, factors) -> HostTensor:
+    """t with row i multiplied by factors[i], stored again in t's dtype (a
+    ramp of magnitudes along the rows, e.g. keys whose scores grow with
+    their position)."""
+    x = (t.values * np.asarray(factors, np.float32)[:, None]).astype(np.float32)
+    return _make(x, t.dtype)
+
+
 def transposed(t: HostTensor) -> HostTensor:
     """The same tensor stored transposed (a row-major copy of t.T)."""
     v = np.ascontiguousarray(t.values.T)

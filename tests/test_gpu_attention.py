@@ -120,6 +120,51 @@ def test_split_kv_causal_parts_sampled_rows(B, S, H, R):
     assert torch.equal(o, again)
 
 
+@pytest.mark.parametrize("causal", [True, False])
+@pytest.mark.parametrize("ramp", ["rising", "falling"])
+@pytest.mark.parametrize("R", [1, 2])
+def test_score_ranges_that_move_the_running_maximum(causal, ramp, R):
+    """Keys whose magnitude ramps along the sequence (x0.25 .. x3) against
+    queries of scale 3: with a rising ramp the block maxima of the scores
+    climb by a few log2 units per 64-key block, so the running maximum moves
+    in some blocks and stays in others; with a falling ramp it is set in the
+    first block.  Outputs match the oracle, and the base-2 log-sum-exp
+    matches it within the fp32 accumulation bound of the scores,
+    gamma_128 c max_j sum_d |q_d k_jd| (c = scale log2 e), plus 2^-16."""
+    B, S, H = 1, 1024, 2
+    D = H * DH
+    Q = I.gaussian(811, 0, (B * S, D), 3.0, "bf16")
+    f = np.linspace(0.25, 3.0, S) if ramp == "rising" else np.linspace(3.0, 0.25, S)
+    K = I.row_scaled(I.gaussian(811, 1, (B * S, D), 1.0, "bf16"), np.tile(f, B))
+    V = I.gaussian(811, 2, (B * S, D), 1.0, "bf16")
+    say(f"attention B={B} S={S} H={H} causal={causal} R_kv={R}, {ramp} key magnitudes")
+    o, lse = P.attention_train(Q.to_device(), K.to_device(), V.to_device(), B=B, S=S, n_heads=H, causal=causal,
+                               R_kv=R)
+    torch.cuda.synchronize()
+    ref, nrm = reference(Q, K, V, B, S, H, causal)
+    err = O.normalised_error(host(o), ref, nrm)
+    scale = DH ** -0.5
+    c = scale * np.log2(np.e)
+    q, k = Q.f64(), K.f64()
+    lse_err = 0.0
+    for h in range(H):
+        cs = slice(h * DH, (h + 1) * DH)
+        s = scale * (q[:, cs] @ k[:, cs].T)
+        bound = np.abs(q[:, cs]) @ np.abs(k[:, cs]).T
+        if causal:
+            s = np.where(np.tril(np.ones((S, S), bool)), s, -np.inf)
+            bound = np.where(np.tril(np.ones((S, S), bool)), bound, 0.0)
+        mx = s.max(axis=1)
+        ref_lse = (mx + np.log(np.exp(s - mx[:, None]).sum(axis=1))) * np.log2(np.e)
+        gamma = DH * 2.0 ** -24 / (1 - DH * 2.0 ** -24)
+        tol = gamma * c * bound.max(axis=1) + 2.0 ** -16 * (1 + np.abs(ref_lse))
+        got = host(lse)[:, h].astype(np.float64)
+        assert np.all(np.abs(got - ref_lse) <= tol), (h, float(np.max(np.abs(got - ref_lse) - tol)))
+        lse_err = max(lse_err, float(np.max(np.abs(got - ref_lse))))
+    say(f"    max normalised error {err:.3e}, max lse error {lse_err:.2e} (log2 units)")
+    assert err <= TOL_BF16
+
+
 def test_split_kv_matches_single_shard_and_is_deterministic():
     B, S, H = 2, 512, 4
     Q, K, V = make_qkv(123, B, S, H)
