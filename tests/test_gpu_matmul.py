@@ -309,3 +309,29 @@ def test_bf16_b_kn_full_size_sampled_rows():
     err = O.normalised_error(C[rows], O.matmul(Ar, B.f64()), O.abs_product(Ar, B.f64()))
     say(f"    {len(rows)} rows, max normalised error {err:.3e}")
     assert err <= accum_bound(K)
+
+
+@pytest.mark.parametrize("summ,R", [(None, 1), ("K", 4)])
+def test_bf16_at_the_largest_leading_dimension(summ, R):
+    """K = lda = ldb = 2^24, the largest bf16 leading dimension the boundary
+    admits: a 64-row block of an operand then spans exactly 2^31 bytes, the
+    top of a buffer descriptor's range.  Entries in {-1, 0, 1} keep every
+    partial sum an integer below 2^24, so fp32 accumulation is exact and the
+    sampled outputs are compared bit for bit with fp64 dot products."""
+    M = N = 64
+    K = 1 << 24
+    g = torch.Generator(device="cuda").manual_seed(2024)
+    A = torch.randint(-1, 2, (M, K), generator=g, device="cuda", dtype=torch.int8).to(torch.bfloat16)
+    Bt = torch.randint(-1, 2, (N, K), generator=g, device="cuda", dtype=torch.int8).to(torch.bfloat16)
+    say(f"bf16 matmul {M}x{N}x{K} (lda = ldb = 2^24), sum={summ} R={R}")
+    C = P.loop_matmul(A, Bt, sum=summ, R=R, b_layout="nk", out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    c = host(C)
+    rng = np.random.default_rng(2024)
+    pairs = [(0, 0), (M - 1, N - 1), (M - 1, 0)] + [(int(rng.integers(M)), int(rng.integers(N))) for _ in range(5)]
+    a_rows = {i: A[i].float().cpu().numpy().astype(np.float64) for i, _ in pairs}
+    b_rows = {j: Bt[j].float().cpu().numpy().astype(np.float64) for _, j in pairs}
+    for i, j in pairs:
+        assert c[i, j] == float(np.dot(a_rows[i], b_rows[j])), (i, j)
+    del A, Bt, C
+    torch.cuda.empty_cache()
