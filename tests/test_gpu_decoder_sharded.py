@@ -66,6 +66,27 @@ def test_decoder_sharded_small_every_part(RB, RM):
     assert err <= TOL_BF16 and fro <= TOL_REL_FRO
 
 
+def test_decoder_sharded_largest_mesh_every_part():
+    """The largest mesh the boundary admits, {B: 3, M: 7} (21 devices, three
+    weight groups in the 64-slot part table): every residual part against the
+    oracle's lowered SPMD program.  Shapes are the smallest that divide over
+    it (tokens over 21 parts, heads and FFN over 7, d_model over 3)."""
+    RB, RM = 3, 7
+    B, S, H, F = 3, 896, 21, 2688
+    D = H * 128
+    x, p, g1, g2 = make(141, B, S, D, F)
+    say(f"decoder sharded B={B} S={S} D={D} F={F} mesh B={RB} M={RM}")
+    got = run_sharded(x, p, g1, g2, B, S, H, RB, RM)
+    q = oracle_params(p, g1, g2)
+    x_loc, p_loc = O.z3_local_decoder(x.f64(), q, RB, RM)
+    y = O.decoder_layer_z3(x_loc, p_loc, q["g1"], q["g2"], B, S, H, 128, 1e-6, RB, RM)
+    ref = np.concatenate([y[(b, m)] for b in range(RB) for m in range(RM)], axis=0)
+    _, norm = O.decoder_layer(x.f64(), q, B, S, H, 128, 1e-6, RB, RM, return_norm=True)
+    err, fro = O.normalised_error(got, ref, norm), rel_fro(got - x.f64(), ref - x.f64())
+    say(f"    max normalised error {err:.3e}, relative Frobenius of the update {fro:.3e}")
+    assert err <= TOL_BF16 and fro <= TOL_REL_FRO
+
+
 def test_decoder_sharded_full_size_equals_whole_layer():
     B, S, H, F, RB, RM = 4, 2048, 40, 13824, 2, 4
     D = H * 128
