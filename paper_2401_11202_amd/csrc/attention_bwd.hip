@@ -10,16 +10,22 @@
 // in a fixed order (no atomics: deterministic):
 //  * dq pass: workgroup = (sequence, head, 128 queries), 4 waves x 32
 //    queries; keys stream through LDS 64 at a time.  S^T = K Q^T and
-//    dP^T = V dO^T put one query per lane, dQ^T += K^T dS^T (K^T read with
-//    ds_read_b64_tr_b16).  It also writes D for the second pass.
+//    dP^T = V dO^T put one query per lane, dQ^T += K^T dS^T per 32 keys
+//    (K^T read with ds_read_b64_tr_b16).  It also writes D for the second
+//    pass.
 //  * dv and dk passes: workgroup = (sequence, head, 128 keys), 4 waves x 32
 //    keys; queries stream 64 at a time.  S = Q K^T and dP = dO V^T put one
 //    key per lane, dV^T += dO^T P (dv pass) and dK^T += Q^T dS (dk pass),
 //    from transposed reads of the dO and Q tiles.
 // Inside a 16-wide MFMA contraction step the order of the contracted
 // positions is permuted identically on both operands (exact for a sum).
-// All LDS tiles are 64 rows x 256 B with 16-byte chunks XOR-swizzled by row,
-// which serves both the row reads and the transposed reads.
+// All LDS tiles are 64 rows x 256 B with 16-byte chunks XOR-swizzled by row
+// (swz), so that both the row reads and the transposed reads hit every bank
+// once.  The causal mask costs VALU work only on blocks that cross a wave's
+// diagonal, and the block loops run two blocks per trip so that the LDS stage
+// of each is a constant (its offset folds into the LDS instructions).
+#include <type_traits>
+
 #include "kernels.h"
 #include "lds_dma.h"
 
@@ -28,6 +34,8 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -38,9 +46,27 @@ constexpr int TR = 64;                 // rows of a streamed tile
 constexpr int TP = 256;                // tile row pitch (bytes)
 constexpr int TILE = TR * TP;          // 16 KiB
 
+// The XOR applied to the 16-byte chunk index of a tile row: row 4 b + a of a
+// 16-row group (a, b < 4) gets 4 a + b.  A row read (16 lanes on 16
+// consecutive rows, one logical chunk) lands on 16 distinct chunks; half a
+// transposed read (4 consecutive rows x one aligned 64-byte group) does too,
+// since the row's low two bits move it to another 64-byte group.  (XOR with
+// the row's low four bits, which serves the row reads alone, put the four
+// rows of a transposed read on the same 16 banks.)
+__device__ __forceinline__ int swz(int row) { return ((row & 3) << 2) | ((row >> 2) & 3); }
+
 // byte offset of (row, byte column) in a swizzled tile
 __device__ __forceinline__ int toff(int row, int colb) {
-  return row * TP + ((((colb >> 4) ^ (row & 15))) << 4) + (colb & 15);
+  return row * TP + (((colb >> 4) ^ swz(row)) << 4) + (colb & 15);
+}
+
+// two fp32 values rounded to bf16 into elements i, i + 1 of x (one
+// v_cvt_pk_bf16_f32)
+__device__ __forceinline__ void put2(bf16x8& x, int i, float a, float b) {
+  const f32x2 f = {a, b};
+  const bf16x2 r = __builtin_convertvector(f, bf16x2);
+  x[i] = r[0];
+  x[i + 1] = r[1];
 }
 
 
@@ -48,8 +74,8 @@ __device__ __forceinline__ int toff(int row, int colb) {
 // swizzled LDS stage with buffer loads that write LDS directly: load j of
 // wave w fills tile rows 16 j + 4 w .. +4 (1 KiB, lane L at byte 16 L), so
 // lane L reads the global chunk that belongs at its LDS position,
-// (L % 16) ^ (row & 15), which does not depend on j (the row step enters as
-// a scalar offset).
+// (L % 16) ^ swz(row), which does not depend on j (the row step enters as a
+// scalar offset).
 struct TileDma {
   __amdgpu_buffer_rsrc_t rx, ry;
   uint32_t vx, vy;           // per-lane byte offsets of load 0
@@ -60,7 +86,7 @@ struct TileDma {
     w = tid >> 6;
     const int lane = tid & 63;
     const int row = 4 * w + (lane >> 4);
-    const int chunk = (lane & 15) ^ (row & 15);
+    const int chunk = (lane & 15) ^ swz(row);
     rx = make_rsrc(X, (uint32_t)((S - 1) * ldx * 2 + DH * 2));
     ry = make_rsrc(Y, (uint32_t)((S - 1) * ldy * 2 + DH * 2));
     vx = (uint32_t)(row * ldx * 2 + chunk * 16);
@@ -105,7 +131,7 @@ __device__ __forceinline__ void zero(f32x16& a) {
 // ---------------------------------------------------------------------------
 // dq pass
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(NT, 1)
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void attention_bwd_dq_kernel(AttnBwdParams p) {
   __shared__ __attribute__((aligned(1024))) char smem[2 * 2 * TILE];
   const int tid = threadIdx.x, lane = tid & 63;
@@ -156,20 +182,18 @@ void attention_bwd_dq_kernel(AttnBwdParams p) {
   const int nkb = p.causal ? (q0 + 128) / TR : p.S / TR;
   const int wave_last_q = q0 + 32 * w + 31;
   const float c = p.scale_log2;
-  kv.load(0, smem, smem + TILE);
-  WAIT_VMCNT(0);
-  __syncthreads();
-  for (int kb = 0; kb < nkb; ++kb) {
-    const int cur = kb & 1;
-    // the other stage was last read in the previous iteration, before its barrier
+  // Key block kb from LDS stage `stage`, block kb + 1 streaming into the
+  // other stage (last read in the previous iteration, before its barrier).
+  auto iter = [&](int kb, auto stage) {
+    const int cur = stage;
     if (kb + 1 < nkb) kv.load(kb + 1, smem + (cur ^ 1) * 2 * TILE, smem + (cur ^ 1) * 2 * TILE + TILE);
     const int k0 = kb * TR;
     if (!p.causal || k0 <= wave_last_q) {
       const char* ks = smem + cur * 2 * TILE;
       const char* vs = ks + TILE;
-      bf16x8 dsf[4];
 #pragma unroll
       for (int t = 0; t < 2; ++t) {
+        if (p.causal && k0 + 32 * t > wave_last_q) continue;   // wave-uniform: every key follows every query
         f32x16 s, dp;
         zero(s);
         zero(dp);
@@ -178,24 +202,36 @@ void attention_bwd_dq_kernel(AttnBwdParams p) {
           s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag(ks, 32 * t, col, h, ds), qf[ds], s, 0, 0, 0);
           dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag(vs, 32 * t, col, h, ds), gf[ds], dp, 0, 0, 0);
         }
-        const bool diag = p.causal && k0 + 32 * t + 31 > q0 + 32 * w;   // wave-uniform
+        float pr[16];
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int key = k0 + 32 * t + 8 * (v >> 2) + 4 * h + (v & 3);
-          float pr = __builtin_amdgcn_exp2f(__builtin_fmaf(s[v], c, -lse));
-          if (diag && key > qi) pr = 0.0f;
-          dsf[2 * t + (v >> 3)][v & 7] = (__bf16)(pr * (dp[v] - Dq));
+        for (int v = 0; v < 16; ++v) pr[v] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[v], c, -lse));
+        if (p.causal && k0 + 32 * t + 31 > q0 + 32 * w) {   // wave-uniform: keys past some query
+#pragma unroll
+          for (int v = 0; v < 16; ++v)
+            if (k0 + 32 * t + 8 * (v >> 2) + 4 * h + (v & 3) > qi) pr[v] = 0.0f;
         }
+        bf16x8 dsf[2];
+#pragma unroll
+        for (int v = 0; v < 16; v += 2)
+          put2(dsf[v >> 3], v & 7, pr[v] * (dp[v] - Dq), pr[v + 1] * (dp[v + 1] - Dq));
+        // dQ^T += K^T dS^T over these 32 keys, 2 steps of 16
+#pragma unroll
+        for (int uu = 0; uu < 2; ++uu)
+#pragma unroll
+          for (int d = 0; d < 4; ++d)
+            dq[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_frag(ks, 2 * t + uu, d, v_row, v_colb), dsf[uu], dq[d], 0,
+                                                            0, 0);
       }
-      // dQ^T += K^T dS^T over the 64 keys, 4 steps of 16
-#pragma unroll
-      for (int u = 0; u < 4; ++u)
-#pragma unroll
-        for (int d = 0; d < 4; ++d)
-          dq[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_frag(ks, u, d, v_row, v_colb), dsf[u], dq[d], 0, 0, 0);
     }
     WAIT_VMCNT(0);
     __syncthreads();
+  };
+  kv.load(0, smem, smem + TILE);
+  WAIT_VMCNT(0);
+  __syncthreads();
+  for (int kb = 0; kb < nkb; kb += 2) {
+    iter(kb, std::integral_constant<int, 0>{});
+    if (kb + 1 < nkb) iter(kb + 1, std::integral_constant<int, 1>{});
   }
 
   // dQ[query][d] = scale * dQ^T: lane holds rows d = 32 dt + 8 (v>>2) + 4 h + (v&3)
@@ -217,7 +253,7 @@ void attention_bwd_dq_kernel(AttnBwdParams p) {
 // recomputed, dK^T += Q^T dS).  One pass doing both needs 287 registers
 // (one wave per SIMD); the two passes recompute S once more but fit two
 // waves per SIMD, which more than pays (0.84 -> 0.74 ms for the whole
-// backward at 4 x 2048 tokens, 32 heads).
+// backward at 4 x 2048 tokens, 32 heads, when it was measured).
 template <int MODE>
 __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void attention_bwd_dkv_kernel(AttnBwdParams p) {
@@ -280,13 +316,11 @@ void attention_bwd_dkv_kernel(AttnBwdParams p) {
   const int nqb = p.S / TR;
   const int wave_first_k = k0 + 32 * w;
   const float c = p.scale_log2;
-  qg.load(qb_begin, smem, smem + TILE);
-  sload(qb_begin);
-  sstore(0);
-  WAIT_VMCNT(0);
-  __syncthreads();
-  for (int qb = qb_begin; qb < nqb; ++qb) {
-    const int cur = (qb - qb_begin) & 1;
+  // Query block qb from LDS stage `stage`, block qb + 1 and its statistics
+  // streaming into the other stage (last read in the previous iteration,
+  // before its barrier).
+  auto iter = [&](int qb, auto stage) {
+    const int cur = stage;
     if (qb + 1 < nqb) {
       qg.load(qb + 1, smem + (cur ^ 1) * 2 * TILE, smem + (cur ^ 1) * 2 * TILE + TILE);
       sload(qb + 1);
@@ -308,15 +342,23 @@ void attention_bwd_dkv_kernel(AttnBwdParams p) {
             dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag(gs, 32 * t, col, h, ds), vf[ds], dp, 0, 0, 0);
         }
         // lane: key kj; element v: query q0 + 32 t + 8 (v>>2) + 4 h + (v&3)
-        const bool diag = p.causal && q0 + 32 * t < wave_first_k + 31;   // wave-uniform
+        float pr[16];
+#pragma unroll
+        for (int v = 0; v < 16; ++v)
+          pr[v] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[v], c, -stat[cur][0][32 * t + 8 * (v >> 2) + 4 * h + (v & 3)]));
+        if (p.causal && q0 + 32 * t < wave_first_k + 31) {   // wave-uniform: queries before some key
+#pragma unroll
+          for (int v = 0; v < 16; ++v)
+            if (q0 + 32 * t + 8 * (v >> 2) + 4 * h + (v & 3) < kj) pr[v] = 0.0f;
+        }
         bf16x8 pf[2], dsf[2];
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int ql = 32 * t + 8 * (v >> 2) + 4 * h + (v & 3);
-          float pr = __builtin_amdgcn_exp2f(__builtin_fmaf(s[v], c, -stat[cur][0][ql]));
-          if (diag && q0 + ql < kj) pr = 0.0f;
-          if (DO_V) pf[v >> 3][v & 7] = (__bf16)pr;
-          if (DO_K) dsf[v >> 3][v & 7] = (__bf16)(pr * (dp[v] - stat[cur][1][ql]));
+        for (int v = 0; v < 16; v += 2) {
+          if (DO_V) put2(pf[v >> 3], v & 7, pr[v], pr[v + 1]);
+          if (DO_K) {
+            const int ql = 32 * t + 8 * (v >> 2) + 4 * h + (v & 3);   // v, v + 1: ql, ql + 1
+            put2(dsf[v >> 3], v & 7, pr[v] * (dp[v] - stat[cur][1][ql]), pr[v + 1] * (dp[v + 1] - stat[cur][1][ql + 1]));
+          }
         }
         // dV^T += dO^T P and dK^T += Q^T dS over these 32 queries (2 steps of 16)
 #pragma unroll
@@ -335,6 +377,15 @@ void attention_bwd_dkv_kernel(AttnBwdParams p) {
     if (qb + 1 < nqb) sstore(cur ^ 1);
     WAIT_VMCNT(0);
     __syncthreads();
+  };
+  qg.load(qb_begin, smem, smem + TILE);
+  sload(qb_begin);
+  sstore(0);
+  WAIT_VMCNT(0);
+  __syncthreads();
+  for (int qb = qb_begin; qb < nqb; qb += 2) {
+    iter(qb, std::integral_constant<int, 0>{});
+    if (qb + 1 < nqb) iter(qb + 1, std::integral_constant<int, 1>{});
   }
 
   uint16_t* okr = p.dK + tk * p.lddk + head * DH;
