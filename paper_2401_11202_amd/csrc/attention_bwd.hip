@@ -259,7 +259,7 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void attention_bwd_dkv_kernel(AttnBwdParams p) {
   constexpr bool DO_V = MODE == 1, DO_K = MODE == 2;
   __shared__ __attribute__((aligned(1024))) char smem[2 * 2 * TILE];
-  __shared__ float stat[2][2][TR];   // [stage][lse2, D][query]
+  __shared__ float stat[2][2][TR];   // [stage][-lse2 / c, -D][query]
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int h = lane >> 5, col = lane & 31;
@@ -287,6 +287,7 @@ void attention_bwd_dkv_kernel(AttnBwdParams p) {
   TileDma qg;
   qg.init(p.Q + tok0 * p.ldq + head * DH, p.ldq, p.dO + tok0 * p.ldg + head * DH, p.ldg, p.S, tid);
   float st_l = 0.0f, st_d = 0.0f;
+  const float inv_c = 1.0f / p.scale_log2;
   auto sload = [&](int blk) {
     if (tid < TR) {
       const int64_t t = tok0 + (int64_t)blk * TR + tid;
@@ -296,8 +297,8 @@ void attention_bwd_dkv_kernel(AttnBwdParams p) {
   };
   auto sstore = [&](int buf) {
     if (tid < TR) {
-      stat[buf][0][tid] = st_l;
-      stat[buf][1][tid] = st_d;
+      stat[buf][0][tid] = -st_l * inv_c;
+      stat[buf][1][tid] = -st_d;
     }
   };
 
@@ -332,9 +333,20 @@ void attention_bwd_dkv_kernel(AttnBwdParams p) {
 #pragma unroll
       for (int t = 0; t < 2; ++t) {
         if (p.causal && q0 + 32 * t + 31 < wave_first_k) continue;   // wave-uniform: sees none of these keys
+        // The accumulators start at -lse2 / c and -D of their rows (queries),
+        // so S - lse2 / c and dP - D come out of the products.
         f32x16 s, dp;
-        zero(s);
-        if (DO_K) zero(dp);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const f32x4 l4 = *(const f32x4*)&stat[cur][0][32 * t + 8 * i + 4 * h];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) s[4 * i + j] = l4[j];
+          if (DO_K) {
+            const f32x4 d4 = *(const f32x4*)&stat[cur][1][32 * t + 8 * i + 4 * h];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) dp[4 * i + j] = d4[j];
+          }
+        }
 #pragma unroll
         for (int ds = 0; ds < 8; ++ds) {
           s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag(qs, 32 * t, col, h, ds), kf[ds], s, 0, 0, 0);
@@ -345,7 +357,7 @@ void attention_bwd_dkv_kernel(AttnBwdParams p) {
         float pr[16];
 #pragma unroll
         for (int v = 0; v < 16; ++v)
-          pr[v] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[v], c, -stat[cur][0][32 * t + 8 * (v >> 2) + 4 * h + (v & 3)]));
+          pr[v] = __builtin_amdgcn_exp2f(s[v] * c);
         if (p.causal && q0 + 32 * t < wave_first_k + 31) {   // wave-uniform: queries before some key
 #pragma unroll
           for (int v = 0; v < 16; ++v)
@@ -355,10 +367,7 @@ void attention_bwd_dkv_kernel(AttnBwdParams p) {
 #pragma unroll
         for (int v = 0; v < 16; v += 2) {
           if (DO_V) put2(pf[v >> 3], v & 7, pr[v], pr[v + 1]);
-          if (DO_K) {
-            const int ql = 32 * t + 8 * (v >> 2) + 4 * h + (v & 3);   // v, v + 1: ql, ql + 1
-            put2(dsf[v >> 3], v & 7, pr[v] * (dp[v] - stat[cur][1][ql]), pr[v + 1] * (dp[v + 1] - stat[cur][1][ql + 1]));
-          }
+          if (DO_K) put2(dsf[v >> 3], v & 7, pr[v] * dp[v], pr[v + 1] * dp[v + 1]);
         }
         // dV^T += dO^T P and dK^T += Q^T dS over these 32 queries (2 steps of 16)
 #pragma unroll
