@@ -1,15 +1,18 @@
-// bf16 MFMA GEMM for gfx950: C = A . B^T with both operands K-contiguous.
+// bf16 MFMA GEMM for gfx950: C = A . B^T, A K-contiguous or stored [K, M],
+// B K-contiguous or stored [K, N].
 //
 // One workgroup computes a 256x256 output tile of one virtual shard with eight
 // waves (2 x 4, two per SIMD), each owning a 128x64 sub-tile as 4 x 2
-// accumulators of v_mfma_f32_32x32x16_bf16; while one wave of a SIMD waits on
-// memory the other keeps the matrix core busy.  K advances in 64-wide tiles
-// through two LDS stages of 64 KiB filled by buffer loads that write LDS
-// directly (no register staging): the loads for tile t+2 are issued in the
-// middle of tile t, after every wave has finished reading the stage they
-// overwrite.  Out-of-range lanes (ragged M / N / K edges, tiles past the end)
-// read as zeros.  The 256x256 tile is the largest whose fp32 accumulators fit
-// the register file, which keeps L2 -> LDS traffic per FLOP minimal.
+// accumulators of v_mfma_f32_32x32x16_bf16.  K advances in 64-wide tiles
+// through LDS buffers filled by buffer loads that write LDS directly (no
+// register staging).  With A K-contiguous (every forward product) the two
+// waves of a SIMD take turns: one runs a K tile's MFMAs on fragments already
+// in its registers while the other reads its next fragments and issues the
+// loads (the main loop below).  With A stored [K, M] (weight gradients) all
+// eight waves run in step through two 64 KiB stages.  Out-of-range lanes
+// (ragged M / N / K edges, tiles past the end) read as zeros.  The 256x256
+// tile is the largest whose fp32 accumulators fit the register file, which
+// keeps L2 -> LDS traffic per FLOP minimal.
 //
 // Loop semantics realised here (PartIR:Core, Sec. 5 / App. C):
 //  * #tile over M or N: the grid enumerates every shard's tiles; a tile never
@@ -34,6 +37,7 @@ typedef short i16x4 __attribute__((ext_vector_type(4)));
 
 constexpr int BM = 256, BN = 256, NT = 512;
 constexpr int BK = 64, NS = 2;
+constexpr int PP_LDS = 160 * 1024;   // LDS of the two-group main loop
 // Epilogue staging of the output tile in LDS (reusing the K stages): bf16
 // rows of 256 + 8 elements (528 B, 16-byte aligned rows), fp32 in two halves
 // of 128 rows of 256 + 4 floats (1040 B); the pads spread consecutive rows
@@ -78,7 +82,14 @@ __device__ __forceinline__ void gemm_body(const GemmParams& p, const GemmParts* 
   constexpr int CPR = BK / 8;   // 16-byte chunks per row
   constexpr int MAIN = (NS * STAGE > C_LDS) ? NS * STAGE : C_LDS;
   constexpr bool PHI_TAB = ACT && (EPI == EPI_BF16 || EPI == EPI_BF16_SAVE);
-  __shared__ __attribute__((aligned(1024))) char smem[MAIN + (PHI_TAB ? PHI_BYTES : 0)];
+  // PP: the two-group main loop below (every K-contiguous A); it uses all
+  // 160 KiB of LDS for its buffers and builds the Phi table after the loop,
+  // behind the epilogue's staging area
+  constexpr bool PP = !FIX && !AMN;
+  static_assert(C_LDS + PHI_BYTES <= PP_LDS, "epilogue staging and Phi table fit the PP buffers");
+  constexpr int PHI_OFF = PP ? C_LDS : MAIN;
+  constexpr int LDS_BYTES = PP ? PP_LDS : MAIN + (PHI_TAB ? PHI_BYTES : 0);
+  __shared__ __attribute__((aligned(1024))) char smem[LDS_BYTES];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -136,14 +147,16 @@ __device__ __forceinline__ void gemm_body(const GemmParams& p, const GemmParts* 
     k_end = min(p.K, k_begin + p.tail_kt * BK);
   }
 
-  if (PHI_TAB) {   // Phi table (read after the main loop's barriers)
-    float2* tab = (float2*)(smem + MAIN);
+  // Phi table (read after the main loop's barriers)
+  auto build_phi = [&] {
+    float2* tab = (float2*)(smem + PHI_OFF);
     for (int i = threadIdx.x; i < PHI_N; i += NT) {
       const float x0 = PHI_LO + (float)i / PHI_SCALE, x1 = PHI_LO + (float)(i + 1) / PHI_SCALE;
       const float p0 = phi_cdf(x0), p1 = phi_cdf(x1);
       tab[i] = make_float2(p0, p1 - p0);
     }
-  }
+  };
+  if (PHI_TAB && !PP) build_phi();
 
   // ---- global -> LDS loads ----------------------------------------------------
   // Per k tile each wave issues 4 + 4 wave-wide 16-byte loads; load j of wave
@@ -327,7 +340,7 @@ __device__ __forceinline__ void gemm_body(const GemmParams& p, const GemmParts* 
   // MFMAs run; then (tile kt+1 landed, every wave done with this stage) the
   // stage is refilled with tile kt+2 and the next tile's first fragments are
   // read during the last step.
-  if constexpr (!FIX) {
+  if constexpr (!FIX && !PP) {
 #pragma unroll
   for (int s = 0; s < NS; ++s) gload(s, s);
   WAIT_VMCNT(LPS * (NS - 1));
@@ -358,6 +371,195 @@ __device__ __forceinline__ void gemm_body(const GemmParams& p, const GemmParts* 
 #undef SLOTS
 #undef SLOT
 #undef SGB
+
+  // ---- main loop, A K-contiguous: two wave groups in ping-pong -------------
+  // Waves 0-3 (group 0) and 4-7 (group 1) sit one of each on every SIMD;
+  // group g computes rows 128 g .. 128 g + 127 of the tile, so it alone reads
+  // that half of the A tile, while both read the whole B tile.  LDS holds two
+  // buffers for each A half (16 KiB) and three for B (32 KiB): 160 KiB.
+  // Workgroup barriers cut time into phases of one K tile's MFMAs; in each
+  // phase one group multiplies a K tile whose fragments it already holds
+  // (32 MFMAs and nothing else, so nothing can hold them up) while the other
+  // group reads the fragments of its next K tile out of LDS and issues the
+  // loads.  Group 1 runs one phase behind:
+  //   phase 2t:   group 0 reads tile t, loads;  group 1 multiplies tile t-1
+  //   phase 2t+1: group 0 multiplies tile t;    group 1 reads tile t, loads
+  // The loads of a read phase of tile t: the group's A half of tile t+1 (into
+  // the A buffer of tile t-1) and the wave's half of its group's rows of B
+  // tile t+2 (into the B buffer of tile t-1, which both groups have read by
+  // then).  A wave waits for them at the end of its next MFMA phase, before
+  // the barrier after which the first of them is read.  Issuing the loads
+  // from the reading waves matters: an MFMA wave that issues a load while the
+  // address unit is busy stalls its matrix core (measured: 4-7% slower).
+  // Loads of tiles past the end of K read zeros into buffers no one reads
+  // any more, so the in-flight counts are fixed.
+  if constexpr (PP) {
+    constexpr int ABUF = 128 * BK * 2, BBUF = 256 * BK * 2;
+    constexpr int A0_OFF = 0, A1_OFF = 2 * ABUF, B_OFF = 4 * ABUF;
+    static_assert(B_OFF + 3 * BBUF == PP_LDS, "two A-half buffers per group and three B buffers");
+    constexpr int NQ = 4;   // loads per wave per K tile and operand stream
+    const bool g0 = wave < 4;
+    const int w4 = wave & 3;
+    const int ah = wm, bh = g0 ? 1 : 0;
+    // K-contiguous streams: wave w4 owns rows r0 + 32 w4 .. +31 of its
+    // operand (r0 = 128 x its half); load q fills rows 8 q .. 8 q + 7 of
+    // those, lane L taking row L/8 and LDS chunk L%8 = global chunk
+    // (L%8) ^ swz(row), swz(row) = L/8 ^ (q & 1).  One descriptor bounds the
+    // 32 rows; the K offset is the scalar offset.
+    const int lr = lane >> 3;
+    const int a_r0 = ah * 128 + 32 * w4, b_r0 = bh * 128 + 32 * w4;
+    auto a_rows_ptr = [&](int r0) -> const uint16_t* {
+      if (PARTS && t->a_rows) {
+        const int r = row0 + (r0 < rows ? r0 : 0);   // rows past the end: any part, size 0 below
+        const int ab = r / t->a_rows;
+        return t->a[ab] + (int64_t)(r - ab * t->a_rows) * p.lda;
+      }
+      return At + (int64_t)r0 * p.lda;
+    };
+    auto b_rows_ptr = [&](int r0, int kp) -> const uint16_t* {
+      if (PARTS && t->b_nrows) {
+        const int gb = grp * t->b_gstride;
+        if (cols - r0 <= 0) return t->b[gb + kp];
+        const int n = col0 + r0;
+        const int nb = n / t->b_nrows;
+        return t->b[gb + nb * t->b_nk + kp] + (int64_t)(n - nb * t->b_nrows) * p.ldb;
+      }
+      return Btile + (int64_t)r0 * p.ldb;
+    };
+    const uint32_t a_nrec = (uint32_t)(min(max(rows - a_r0, 0), 32) * p.lda * 2);
+    const uint32_t b_nrec = (uint32_t)(min(max(cols - b_r0, 0), 32) * p.ldb * 2);
+    const __amdgpu_buffer_rsrc_t rsa = make_rsrc(a_rows_ptr(a_r0), a_nrec);
+    __amdgpu_buffer_rsrc_t rsb = make_rsrc(b_rows_ptr(b_r0, 0), b_nrec);
+    uint32_t a_lo[2], b_lo[2];
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+      a_lo[e] = (uint32_t)(lr * p.lda * 2 + (((lane & 7) ^ lr ^ e) << 4));
+      b_lo[e] = (uint32_t)(lr * p.ldb * 2 + (((lane & 7) ^ lr ^ e) << 4));
+    }
+    // MN-major B: wave w4 owns k rows 32 bh + 8 w4 .. +7; load q fills k rows
+    // 2 q and 2 q + 1 of those, lane L taking row L/32 and LDS chunk L%32 =
+    // global chunk (L%32) ^ 4 (row & 3).  A descriptor per K tile bounds the
+    // rows at the end of K and the last row at the operand's last column.
+    uint32_t b_mv[NQ];
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      const int kr = 32 * bh + 8 * w4 + 2 * q + (lane >> 5);
+      b_mv[q] = BMN ? (uint32_t)(kr * p.ldb * 2 + (((lane & 31) ^ (4 * (kr & 3))) << 4)) : 0u;
+    }
+    int b_kpart = 0;
+    int b_kend = (PARTS && t->b_nrows) ? t->b_kcols : 0;
+    struct LoadSet {
+      __amdgpu_buffer_rsrc_t r;
+      uint32_t so;
+      uint32_t v[NQ];
+      char* lds;
+    };
+    // K-contiguous chunk e-parity mask: chunks past the end of K read zero
+    auto kmask = [&](int kb, int e) -> uint32_t {
+      return (kb + (((lane & 7) ^ lr ^ e) << 3) < k_end) ? 0u : OOB;
+    };
+    auto prep_a = [&](int kt, int buf) -> LoadSet {
+      LoadSet L;
+      const int kb = k_begin + kt * BK;
+      L.r = rsa;
+      L.so = (uint32_t)kb * 2;
+      const uint32_t m0 = kmask(kb, 0), m1 = kmask(kb, 1);
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) L.v[q] = (a_lo[q & 1] + (uint32_t)(q * 16 * p.lda)) | ((q & 1) ? m1 : m0);
+      L.lds = smem + (ah ? A1_OFF : A0_OFF) + buf * ABUF + w4 * 4096;
+      return L;
+    };
+    auto prep_b = [&](int kt, int buf) -> LoadSet {
+      LoadSet L;
+      const int kb = k_begin + kt * BK;
+      L.lds = smem + B_OFF + buf * BBUF + bh * (BBUF / 2) + w4 * 4096;
+      if constexpr (BMN) {
+        const uint32_t kvalid = (uint32_t)min(max(k_end - kb, 0), BK);
+        const uint32_t bytes = kvalid ? (uint32_t)(((int64_t)(kvalid - 1) * p.ldb + (p.N - col0)) * 2) : 0u;
+        L.r = make_rsrc(Bg + (int64_t)kb * p.ldb + col0, bytes);
+        L.so = 0;
+#pragma unroll
+        for (int q = 0; q < NQ; ++q) L.v[q] = b_mv[q];
+        return L;
+      }
+      uint32_t so = (uint32_t)kb * 2;
+      if (PARTS && t->b_nrows) {
+        // the all_gather of B along K: K tiles never straddle a part (a tail
+        // part may start several parts in); this wave's tiles come in order
+        if (kb >= b_kend && b_kpart + 1 < t->b_nk) {
+          while (kb >= b_kend && b_kpart + 1 < t->b_nk) {
+            ++b_kpart;
+            b_kend += t->b_kcols;
+          }
+          rsb = make_rsrc(b_rows_ptr(b_r0, b_kpart), b_nrec);
+        }
+        so = (uint32_t)(kb - (b_kend - t->b_kcols)) * 2;
+      }
+      L.r = rsb;
+      L.so = so;
+      const uint32_t m0 = kmask(kb, 0), m1 = kmask(kb, 1);
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) L.v[q] = (b_lo[q & 1] + (uint32_t)(q * 16 * p.ldb)) | ((q & 1) ? m1 : m0);
+      return L;
+    };
+    auto issue = [&](const LoadSet& L, int q) {
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(L.r, (lds_void*)(L.lds + q * 1024), 16, L.v[q], L.so, 0, 0);
+    };
+    auto issue_all = [&](const LoadSet& L) {
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) issue(L, q);
+    };
+    // fragments of k step kk of the tile in A buffer ai and B buffer bi
+    auto ldfrag2 = [&](int ai, int bi, int kk, bf16x8* a, bf16x8* b) {
+      const char* abuf = smem + (ah ? A1_OFF : A0_OFF) + ai * ABUF;
+      const char* bbuf = smem + B_OFF + bi * BBUF;
+      const int ko = ((2 * kk + h) ^ fsw) << 4;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) a[i] = *(const bf16x8*)(abuf + (i * 32 + (lane & 31)) * BK * 2 + ko);
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+        b[j] = BMN ? mn_frag(bbuf, kk, wn * 64 + j * 32)
+                   : *(const bf16x8*)(bbuf + (wn * 64 + j * 32 + (lane & 31)) * BK * 2 + ko);
+    };
+    auto barrier = [] {
+      __builtin_amdgcn_sched_barrier(0);
+      asm volatile("s_barrier" ::: "memory");
+      __builtin_amdgcn_sched_barrier(0);
+    };
+    bf16x8 fa[KK][4], fb[KK][2];
+    // prologue: this wave's A half of tile 0 and B half of tiles 0 and 1
+    issue_all(prep_a(0, 0));
+    issue_all(prep_b(0, 0));
+    issue_all(prep_b(1, 1));
+    WAIT_VMCNT(NQ);
+    barrier();
+    if (!g0) barrier();
+    int ai = 0, bi = 0;   // buffers of tile kt: kt % 2, kt % 3
+    for (int kt = 0; kt < nk; ++kt) {
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk) ldfrag2(ai, bi, kk, fa[kk], fb[kk]);
+      // the group's A half of tile kt+1 (into the A buffer read two phases
+      // ago) and its B half of tile kt+2 (into the B buffer of tile kt-1)
+      const LoadSet LA = prep_a(kt + 1, ai ^ 1);
+      const LoadSet LB = prep_b(kt + 2, bi == 0 ? 2 : bi - 1);
+      issue_all(LA);
+      issue_all(LB);
+      WAIT_LGKMCNT(0);
+      WAIT_VMCNT(2 * NQ);   // only the prologue's tile-1 loads can still be older
+      barrier();
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk) mma(fa[kk], fb[kk]);
+      __builtin_amdgcn_sched_barrier(0);
+      WAIT_VMCNT(0);   // this wave's loads of the read phase before
+      barrier();
+      ai ^= 1;
+      bi = (bi == 2) ? 0 : bi + 1;
+    }
+    if (g0) barrier();
+    WAIT_VMCNT(0);
+    __syncthreads();   // every wave's loads landed and reads done: the buffers are free
+    if (PHI_TAB) build_phi();
+  }
 
   // ---- tail parts ----------------------------------------------------------------
   // Accumulator register r (= 16 (2 i + j) + 4 g + e) of thread tid is float
@@ -418,7 +620,7 @@ __device__ __forceinline__ void gemm_body(const GemmParams& p, const GemmParts* 
               if (nl < cols) v += *(const f32x4*)(bias + col0 + nl);
             }
             if (ACT && apply_act) {
-              const float2* tab = (const float2*)(smem + MAIN);
+              const float2* tab = (const float2*)(smem + PHI_OFF);
 #pragma unroll
               for (int e = 0; e < 4; ++e) {
                 const float u = __builtin_amdgcn_fmed3f(__builtin_fmaf(v[e], PHI_SCALE, -PHI_LO * PHI_SCALE), 0.0f,
