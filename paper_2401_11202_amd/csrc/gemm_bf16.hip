@@ -25,6 +25,9 @@
 #include "device_math.h"
 #include "lds_dma.h"
 
+// s_waitcnt with only the LDS / scalar-memory counter constrained (gfx9 encoding)
+#define WAIT_LGKMCNT(n) __builtin_amdgcn_s_waitcnt((((n) & 15) << 8) | 0xF | (0x3 << 14) | (0x7 << 4))
+
 namespace partir {
 namespace {
 

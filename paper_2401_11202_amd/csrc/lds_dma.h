@@ -33,5 +33,3 @@ __device__ __forceinline__ lds_i16x4_t lds_read_tr16(const char* __restrict__ p)
 
 // s_waitcnt with only the vector-memory counter constrained (gfx9 encoding)
 #define WAIT_VMCNT(n) __builtin_amdgcn_s_waitcnt((((n) & 15) | (((n) >> 4) << 14)) | (0x7 << 4) | (0xF << 8))
-// s_waitcnt with only the LDS / scalar-memory counter constrained
-#define WAIT_LGKMCNT(n) __builtin_amdgcn_s_waitcnt((((n) & 15) << 8) | 0xF | (0x3 << 14) | (0x7 << 4))
