@@ -59,19 +59,23 @@ constexpr int PHI_N = 3072;
 constexpr float PHI_LO = -6.0f, PHI_SCALE = 256.0f;
 constexpr int PHI_BYTES = PHI_N * 8;
 
-// LDS reads to place after MFMA i of a k step that has nrd of them.
-template <int nrd>
-constexpr int lds_reads_after(int i) {
-  return nrd <= 8 ? (i < nrd ? 1 : 0) : (i < nrd - 8 ? 2 : 1);
-}
-
 template <typename T>
 __device__ __forceinline__ T pick3(int g, T a, T b, T c) { return g == 0 ? a : (g == 1 ? b : c); }
 
 // LDS tile layout: [row][64 k] = 128-byte rows of eight 16-byte chunks; chunk
-// c of row r sits at position c ^ swz(r), swz(r) = (r & 7) ^ ((r >> 3) & 1),
-// which spreads the 32 rows one MFMA operand read touches over all banks.
-__device__ __forceinline__ int swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
+// c of row r sits at position c ^ swz(r), swz(r) = bit1(r) | bit3(r) << 1 |
+// bit2(r) << 2.  A fragment read takes 16 rows (lane % 16) at 4 chunks
+// (lane / 16); the LDS serves it 8 lanes of each half-wave at a time, i.e.
+// 8 rows at two chunks 2 apart, and swz gives the 4 rows of each parity
+// distinct bits 0 and 2, so the 16 reads hit 16 different bank groups (as do
+// any 16 consecutive lanes: the 8 rows of each parity get all 8 values).
+__device__ __forceinline__ int swz(int r) { return ((r >> 1) & 1) | (((r >> 3) & 1) << 1) | (((r >> 2) & 1) << 2); }
+// MN-major tile layout: [k][256 columns] = 512-byte rows of 32 chunks; chunk
+// c of k row r sits at position c ^ mn_swz(r).  A transposed fragment read
+// covers 4 k rows x 16 columns per 16-lane group, groups 0 and 1 (one pass)
+// on rows 8 apart: the 4 (r & 3) term spreads the 4 rows over the banks, the
+// 2 bit3(r) term keeps the two groups apart.
+__device__ __forceinline__ int mn_swz(int r) { return (4 * (r & 3)) ^ (2 * ((r >> 3) & 1)); }
 
 // PARTS: operands in device-local arrays (`t`, a kernel argument); else the
 // plain pointers of `p` and t is unused.
@@ -81,7 +85,7 @@ __device__ __forceinline__ int swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
 template <int EPI, int ACT, int PARTS, int FIX, int AMN = 0, int BMN = 0>
 __device__ __forceinline__ void gemm_body(const GemmParams& p, const GemmParts* tb) {
   static_assert(!(PARTS && (AMN || BMN)), "device-local arrays are K-contiguous");
-  constexpr int OPB = BM * BK * 2, STAGE = 2 * OPB, KK = BK / 16, RB = 1024 / (BK * 2) /* rows per 1 KiB */;
+  constexpr int OPB = BM * BK * 2, STAGE = 2 * OPB, KK = BK / 32, RB = 1024 / (BK * 2) /* rows per 1 KiB */;
   constexpr int CPR = BK / 8;   // 16-byte chunks per row
   constexpr int MAIN = (NS * STAGE > C_LDS) ? NS * STAGE : C_LDS;
   constexpr bool PHI_TAB = ACT && (EPI == EPI_BF16 || EPI == EPI_BF16_SAVE);
@@ -215,7 +219,7 @@ __device__ __forceinline__ void gemm_body(const GemmParams& p, const GemmParts* 
   // transposed fragment reads below conflict-free.  A descriptor per k tile
   // bounds the rows at the end of K (rows past it read as zero).
   const int mn_r = 2 * wave + (lane >> 5);
-  const int mn_chunk = (lane & 31) ^ (4 * (mn_r & 3));
+  const int mn_chunk = (lane & 31) ^ mn_swz(mn_r);
   const uint32_t a_mvoff = AMN ? (uint32_t)(mn_r * p.lda * 2 + mn_chunk * 16) : 0u;
   const uint32_t b_mvoff = BMN ? (uint32_t)(mn_r * p.ldb * 2 + mn_chunk * 16) : 0u;
   auto gload = [&](int kt, int stage) {
@@ -272,70 +276,73 @@ __device__ __forceinline__ void gemm_body(const GemmParams& p, const GemmParts* 
   };
 
   // ---- MFMA operand reads -----------------------------------------------------
-  const int h = lane >> 5;
-  const int fsw = swz(lane & 31);
-  const int a_rd = (wm * 128 + (lane & 31)) * BK * 2;
-  const int b_rd = OPB + (wn * 64 + (lane & 31)) * BK * 2;
+  // v_mfma_f32_16x16x32_bf16 with the B fragment as the first operand: a
+  // fragment is 16 rows (of A or B^T) x 32 k, lane l holding row l % 16 at
+  // k = 8 (l / 16) .. +7, and the 16 x 16 result leaves lane l with output row
+  // l % 16 at the 4 consecutive output columns 4 (l / 16) .. +3.
+  const int fsw = swz(lane & 15);
+  const int g16 = lane >> 4;
+  const int a_rd = (wm * 128 + (lane & 15)) * BK * 2;
+  const int b_rd = OPB + (wn * 64 + (lane & 15)) * BK * 2;
 
-  f32x16 acc[4][2];
+  f32x4 acc[8][4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < 8; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < 4; ++j)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
+      for (int v = 0; v < 4; ++v) acc[i][j][v] = 0.0f;
 
-  // MN-major fragment of 32 columns from bc, k step kk: rows (k) 16 kk + 8 h
-  // + (j16 >> 2), and +4 for the high half, columns bc + 16 (G & 1) + 4 (j16
-  // & 3) .. +3; ds_read_b64_tr_b16 hands lane j16 of each 16-lane group one
-  // column over the group's 4 rows, i.e. lane l holds column bc + l % 32 at
-  // k = 16 kk + 8 h + 0..7, the layout of a K-contiguous fragment.
+  // MN-major fragment of 16 columns from bc, k step ks (32 k rows): group G
+  // = l / 16 reads k rows 32 ks + 8 G + (j16 >> 2) (and +4 for the high
+  // half), columns bc + 4 (j16 & 3) .. +3; ds_read_b64_tr_b16 hands lane j16
+  // of the group one column over the group's 4 rows, i.e. lane l holds
+  // column bc + l % 16 at k = 32 ks + 8 (l / 16) + 0..7, the layout of a
+  // K-contiguous fragment.
   const int j16 = lane & 15;
-  const int mn_row = 8 * h + (j16 >> 2);
-  const int mn_sw = 4 * ((j16 >> 2) & 3);
-  const int mn_col = 16 * ((lane >> 4) & 1) + 4 * (j16 & 3);
-  auto mn_frag = [&](const char* op, int kk, int bc) -> bf16x8 {
+  const int mn_row = 8 * g16 + (j16 >> 2);
+  const int mn_sw = mn_swz(mn_row);
+  const int mn_col = 4 * (j16 & 3);
+  auto mn_frag = [&](const char* op, int ks, int bc) -> bf16x8 {
     const int col = bc + mn_col;
-    const char* pl = op + (16 * kk + mn_row) * 512 + (((col >> 3) ^ mn_sw) << 4) + ((col & 4) << 1);
+    const char* pl = op + (32 * ks + mn_row) * 512 + (((col >> 3) ^ mn_sw) << 4) + ((col & 4) << 1);
     const i16x4 lo = lds_read_tr16(pl);
     const i16x4 hi = lds_read_tr16(pl + 4 * 512);
     return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
   };
-  // fragments of one 16-wide k step: 4 A row blocks and 2 B row blocks
-  bf16x8 fa0[4], fb0[2], fa1[4], fb1[2];
-  auto ldfrag = [&](int stage, int kk, bf16x8* a, bf16x8* b) {
+  // fragments of one 32-wide k step: 8 A row blocks and 4 B row blocks
+  bf16x8 fa0[8], fb0[4], fa1[8], fb1[4];
+  auto ldfrag = [&](int stage, int ks, bf16x8* a, bf16x8* b) {
     const char* st = smem + stage * STAGE;
-    const int ko = ((2 * kk + h) ^ fsw) << 4;
+    const int ko = ((4 * ks + g16) ^ fsw) << 4;
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      a[i] = AMN ? mn_frag(st, kk, wm * 128 + i * 32) : *(const bf16x8*)(st + a_rd + i * 32 * BK * 2 + ko);
+    for (int i = 0; i < 8; ++i)
+      a[i] = AMN ? mn_frag(st, ks, wm * 128 + i * 16) : *(const bf16x8*)(st + a_rd + i * 16 * BK * 2 + ko);
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
-      b[j] = BMN ? mn_frag(st + OPB, kk, wn * 64 + j * 32) : *(const bf16x8*)(st + b_rd + j * 32 * BK * 2 + ko);
+    for (int j = 0; j < 4; ++j)
+      b[j] = BMN ? mn_frag(st + OPB, ks, wn * 64 + j * 16) : *(const bf16x8*)(st + b_rd + j * 16 * BK * 2 + ko);
   };
-  // LDS reads per k step (a transposed fragment takes two) and how many go
-  // after each of the step's 8 MFMAs
-  constexpr int NRD = (AMN ? 8 : 4) + (BMN ? 4 : 2);
+  // LDS reads per k step (a transposed fragment takes two)
+  constexpr int NRD = (AMN ? 16 : 8) + (BMN ? 8 : 4);
   // B as the first operand: each lane ends up holding 4 consecutive output
   // columns of one output row.
   auto mma = [&](const bf16x8* a, const bf16x8* b) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < 8; ++i)
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b[j], a[i], acc[i][j], 0, 0, 0);
+      for (int j = 0; j < 4; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(b[j], a[i], acc[i][j], 0, 0, 0);
   };
   // instruction interleaving hints: mask bits MFMA 0x8, VMEM read 0x20, DS read 0x100
 #define SGB(mask, n) __builtin_amdgcn_sched_group_barrier(mask, n, 0)
-  // one k step: each of the 8 MFMAs followed by its share of the LDS reads
-  // and, when refilling, one of the first 6 global loads
-#define SLOT(i, rf)                                                 \
-  SGB(0x8, 1);                                                      \
-  if constexpr (lds_reads_after<NRD>(i) == 2) SGB(0x100, 2);        \
-  else if constexpr (lds_reads_after<NRD>(i) == 1) SGB(0x100, 1);   \
-  if ((rf) && (i) < 6) SGB(0x20, 1);
-#define SLOTS(rf) \
-  SLOT(0, rf) SLOT(1, rf) SLOT(2, rf) SLOT(3, rf) SLOT(4, rf) SLOT(5, rf) SLOT(6, rf) SLOT(7, rf)
+  // one k step: each of the 32 MFMAs followed by one of the next step's LDS
+  // reads and, when refilling, one of the global loads
+#define SLOTS(rf)                                              \
+  _Pragma("unroll") for (int sl = 0; sl < 32; ++sl) {          \
+    SGB(0x8, 1);                                               \
+    if (sl < NRD) SGB(0x100, 1);                               \
+    if ((rf) && sl < LPS) SGB(0x20, 1);                        \
+  }
 
   constexpr int LPS = 2 * NJ;   // wave loads per k tile
   // prologue: both stages in flight, then wait for tile 0.  In the loop, the
@@ -372,7 +379,6 @@ __device__ __forceinline__ void gemm_body(const GemmParams& p, const GemmParts* 
   for (; kt < nk; ++kt) stage = tile(kt, stage, false);
   }
 #undef SLOTS
-#undef SLOT
 #undef SGB
 
   // ---- main loop, A K-contiguous: two wave groups in ping-pong -------------
@@ -407,8 +413,8 @@ __device__ __forceinline__ void gemm_body(const GemmParams& p, const GemmParts* 
     // K-contiguous streams: wave w4 owns rows r0 + 32 w4 .. +31 of its
     // operand (r0 = 128 x its half); load q fills rows 8 q .. 8 q + 7 of
     // those, lane L taking row L/8 and LDS chunk L%8 = global chunk
-    // (L%8) ^ swz(row), swz(row) = L/8 ^ (q & 1).  One descriptor bounds the
-    // 32 rows; the K offset is the scalar offset.
+    // (L%8) ^ swz(row), swz(row) = swz(8 (q & 1) + L/8).  One descriptor
+    // bounds the 32 rows; the K offset is the scalar offset.
     const int lr = lane >> 3;
     const int a_r0 = ah * 128 + 32 * w4, b_r0 = bh * 128 + 32 * w4;
     auto a_rows_ptr = [&](int r0) -> const uint16_t* {
@@ -436,8 +442,8 @@ __device__ __forceinline__ void gemm_body(const GemmParams& p, const GemmParts* 
     uint32_t a_lo[2], b_lo[2];
 #pragma unroll
     for (int e = 0; e < 2; ++e) {
-      a_lo[e] = (uint32_t)(lr * p.lda * 2 + (((lane & 7) ^ lr ^ e) << 4));
-      b_lo[e] = (uint32_t)(lr * p.ldb * 2 + (((lane & 7) ^ lr ^ e) << 4));
+      a_lo[e] = (uint32_t)(lr * p.lda * 2 + (((lane & 7) ^ swz(8 * e + lr)) << 4));
+      b_lo[e] = (uint32_t)(lr * p.ldb * 2 + (((lane & 7) ^ swz(8 * e + lr)) << 4));
     }
     // MN-major B: wave w4 owns k rows 32 bh + 8 w4 .. +7; load q fills k rows
     // 2 q and 2 q + 1 of those, lane L taking row L/32 and LDS chunk L%32 =
@@ -447,7 +453,7 @@ __device__ __forceinline__ void gemm_body(const GemmParams& p, const GemmParts* 
 #pragma unroll
     for (int q = 0; q < NQ; ++q) {
       const int kr = 32 * bh + 8 * w4 + 2 * q + (lane >> 5);
-      b_mv[q] = BMN ? (uint32_t)(kr * p.ldb * 2 + (((lane & 31) ^ (4 * (kr & 3))) << 4)) : 0u;
+      b_mv[q] = BMN ? (uint32_t)(kr * p.ldb * 2 + (((lane & 31) ^ mn_swz(kr)) << 4)) : 0u;
     }
     int b_kpart = 0;
     int b_kend = (PARTS && t->b_nrows) ? t->b_kcols : 0;
@@ -459,7 +465,7 @@ __device__ __forceinline__ void gemm_body(const GemmParams& p, const GemmParts* 
     };
     // K-contiguous chunk e-parity mask: chunks past the end of K read zero
     auto kmask = [&](int kb, int e) -> uint32_t {
-      return (kb + (((lane & 7) ^ lr ^ e) << 3) < k_end) ? 0u : OOB;
+      return (kb + (((lane & 7) ^ swz(8 * e + lr)) << 3) < k_end) ? 0u : OOB;
     };
     auto prep_a = [&](int kt, int buf) -> LoadSet {
       LoadSet L;
@@ -512,24 +518,24 @@ __device__ __forceinline__ void gemm_body(const GemmParams& p, const GemmParts* 
 #pragma unroll
       for (int q = 0; q < NQ; ++q) issue(L, q);
     };
-    // fragments of k step kk of the tile in A buffer ai and B buffer bi
-    auto ldfrag2 = [&](int ai, int bi, int kk, bf16x8* a, bf16x8* b) {
+    // fragments of k step ks of the tile in A buffer ai and B buffer bi
+    auto ldfrag2 = [&](int ai, int bi, int ks, bf16x8* a, bf16x8* b) {
       const char* abuf = smem + (ah ? A1_OFF : A0_OFF) + ai * ABUF;
       const char* bbuf = smem + B_OFF + bi * BBUF;
-      const int ko = ((2 * kk + h) ^ fsw) << 4;
+      const int ko = ((4 * ks + g16) ^ fsw) << 4;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) a[i] = *(const bf16x8*)(abuf + (i * 32 + (lane & 31)) * BK * 2 + ko);
+      for (int i = 0; i < 8; ++i) a[i] = *(const bf16x8*)(abuf + (i * 16 + (lane & 15)) * BK * 2 + ko);
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
-        b[j] = BMN ? mn_frag(bbuf, kk, wn * 64 + j * 32)
-                   : *(const bf16x8*)(bbuf + (wn * 64 + j * 32 + (lane & 31)) * BK * 2 + ko);
+      for (int j = 0; j < 4; ++j)
+        b[j] = BMN ? mn_frag(bbuf, ks, wn * 64 + j * 16)
+                   : *(const bf16x8*)(bbuf + (wn * 64 + j * 16 + (lane & 15)) * BK * 2 + ko);
     };
     auto barrier = [] {
       __builtin_amdgcn_sched_barrier(0);
       asm volatile("s_barrier" ::: "memory");
       __builtin_amdgcn_sched_barrier(0);
     };
-    bf16x8 fa[KK][4], fb[KK][2];
+    bf16x8 fa[KK][8], fb[KK][4];
     // prologue: this wave's A half of tile 0 and B half of tiles 0 and 1
     issue_all(prep_a(0, 0));
     issue_all(prep_b(0, 0));
@@ -565,33 +571,25 @@ __device__ __forceinline__ void gemm_body(const GemmParams& p, const GemmParts* 
   }
 
   // ---- tail parts ----------------------------------------------------------------
-  // Accumulator register r (= 16 (2 i + j) + 4 g + e) of thread tid is float
-  // 4 (r/4 * NT + tid) + e of a part: float4 stores of consecutive threads.
+  // Accumulator block acc[i][j] (4 floats) of thread tid is floats
+  // 4 ((4 i + j) NT + tid) .. +3 of a part: float4 stores of consecutive threads.
   if constexpr (FIX) {
     const float* src = p.tail_ws + (size_t)blockIdx.x * p.tail_parts * (NT * 128);
     for (int q = 0; q < p.tail_parts; ++q) {   // ascending K
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < 8; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
-#pragma unroll
-          for (int g = 0; g < 4; ++g) {
-            const f32x4 v = *(const f32x4*)(src + (size_t)q * (NT * 128) + (((i * 2 + j) * 4 + g) * NT + tid) * 4);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) acc[i][j][4 * g + e] = q ? acc[i][j][4 * g + e] + v[e] : v[e];
-          }
+        for (int j = 0; j < 4; ++j) {
+          const f32x4 v = *(const f32x4*)(src + (size_t)q * (NT * 128) + ((i * 4 + j) * NT + tid) * 4);
+          acc[i][j] = q ? acc[i][j] + v : v;
+        }
     }
   } else if (tail_unit >= 0) {
     float* dst = p.tail_ws + (size_t)tail_unit * (NT * 128);
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < 8; ++i)
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const f32x4 v = {acc[i][j][4 * g + 0], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]};
-          *(f32x4*)(dst + (((i * 2 + j) * 4 + g) * NT + tid) * 4) = v;
-        }
+      for (int j = 0; j < 4; ++j) *(f32x4*)(dst + ((i * 4 + j) * NT + tid) * 4) = acc[i][j];
     return;
   }
 
@@ -611,14 +609,12 @@ __device__ __forceinline__ void gemm_body(const GemmParams& p, const GemmParts* 
     uint16_t* cs = (uint16_t*)smem;
     auto stage = [&](bool apply_act) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int ml = wm * 128 + i * 32 + (lane & 31);
+      for (int i = 0; i < 8; ++i) {
+        const int ml = wm * 128 + i * 16 + (lane & 15);
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
-#pragma unroll
-          for (int g = 0; g < 4; ++g) {
-            const int nl = wn * 64 + j * 32 + 8 * g + 4 * h;
-            f32x4 v = {acc[i][j][4 * g + 0], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]};
+        for (int j = 0; j < 4; ++j) {
+            const int nl = wn * 64 + j * 16 + 4 * g16;
+            f32x4 v = acc[i][j];
             if (bias) {
               if (nl < cols) v += *(const f32x4*)(bias + col0 + nl);
             }
@@ -635,7 +631,7 @@ __device__ __forceinline__ void gemm_body(const GemmParams& p, const GemmParts* 
             }
             const bf16x4 o = {(__bf16)v[0], (__bf16)v[1], (__bf16)v[2], (__bf16)v[3]};
             *(bf16x4*)(cs + ml * CPB + nl) = o;
-          }
+        }
       }
     };
     // 16 rows per pass: thread t writes 8 columns (16 B) of row t / 32
@@ -674,14 +670,12 @@ __device__ __forceinline__ void gemm_body(const GemmParams& p, const GemmParts* 
     for (int q = 0; q < 2; ++q) {
       if (wm == q) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int ml = i * 32 + (lane & 31);
+        for (int i = 0; i < 8; ++i) {
+          const int ml = i * 16 + (lane & 15);
 #pragma unroll
-          for (int j = 0; j < 2; ++j)
-#pragma unroll
-            for (int g = 0; g < 4; ++g) {
-              const int nl = wn * 64 + j * 32 + 8 * g + 4 * h;
-              f32x4 v = {acc[i][j][4 * g + 0], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]};
+          for (int j = 0; j < 4; ++j) {
+              const int nl = wn * 64 + j * 16 + 4 * g16;
+              f32x4 v = acc[i][j];
               if (EPI != EPI_PARTIAL) {
                 if (bias) {
                   if (nl < cols) v += *(const f32x4*)(bias + col0 + nl);
@@ -692,7 +686,7 @@ __device__ __forceinline__ void gemm_body(const GemmParams& p, const GemmParts* 
                 }
               }
               *(f32x4*)(cs + ml * CPF + nl) = v;
-            }
+          }
         }
       }
       __syncthreads();
