@@ -151,10 +151,8 @@ void attention_kernel(AttnParams p) {
           sacc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ds], sacc[t], 0, 0, 0);
         }
       }
-      // causal mask and block max on the raw scores; the scale (> 0, so it
-      // keeps the order) is folded into the exponent: p = 2^(s c - m), with m
-      // the running max of s c.
-      float mloc = -__builtin_inff();
+      // causal mask on the raw scores; the scale (> 0) is folded into the
+      // exponent: p = 2^(s c - m) with m the subtracted maximum in log2 units
       if (p.causal && k0 + BKV - 1 > q0 + 32 * w) {   // wave-uniform: only blocks on the diagonal
 #pragma unroll
         for (int t = 0; t < 2; ++t)
@@ -164,39 +162,53 @@ void attention_kernel(AttnParams p) {
             if (key > qi) sacc[t][v] = -__builtin_inff();
           }
       }
-#pragma unroll
-      for (int t = 0; t < 2; ++t)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) mloc = fmaxf(mloc, sacc[t][v]);
-      // the partner lane (lane ^ 32) holds the other keys of this query
-      mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
       const float sl2 = p.scale_log2;
-      // Lazy rescaling: the subtracted maximum m_run moves only when this
-      // block's maximum exceeds it by more than 8 (log2 units), so every p
-      // stays <= 2^8 (exact range in fp32 and bf16; the softmax does not
-      // depend on the constant subtracted) and O and l are rescaled in few
-      // blocks instead of almost every one.  The first block always sets
-      // m_run (alpha = 0 on the empty accumulators).
-      const float m_blk = mloc * sl2;
-      const bool move = m_blk > m_run + 8.0f;
-      if (__builtin_amdgcn_ballot_w64(move) != 0) {
-        const float m_new = move ? m_blk : m_run;
-        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);   // exactly 1 where m_run stays
-        l_run *= alpha;
-#pragma unroll
-        for (int d = 0; d < 4; ++d) oacc[d] *= alpha;
-        m_run = m_new;
-      }
       float lsum = 0.0f;
       bf16x8 pf[4];
+      auto weights = [&]() {
+        lsum = 0.0f;
 #pragma unroll
-      for (int t = 0; t < 2; ++t)
+        for (int t = 0; t < 2; ++t)
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const float e = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[t][v], sl2, -m_run));
-          lsum += e;
-          pf[2 * t + (v >> 3)][v & 7] = (__bf16)e;
+          for (int v = 0; v < 16; ++v) {
+            const float e = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[t][v], sl2, -m_run));
+            lsum += e;
+            pf[2 * t + (v >> 3)][v & 7] = (__bf16)e;
+          }
+      };
+      // Lazy rescaling: m moves only when the block's maximum exceeds it by
+      // more than 8 (log2 units), so every p stays <= 2^8 (exact range in
+      // fp32 and bf16; the softmax does not depend on the constant
+      // subtracted) and O and l are rescaled in few blocks.  The block
+      // maximum itself is needed only then: the weights are formed with the
+      // current m first, and a lane whose 32 weights sum to at most 2^8 has
+      // none above 2^8, i.e. no score that would move m.  Only when some
+      // lane's sum exceeds 2^8 (or is inf / NaN, as on the first block,
+      // where m starts at -1e30) does the wave take the maximum over both
+      // halves of each query's keys, move m where the rule says so, and
+      // form the weights again; m, the weights and the sums are those of
+      // taking the maximum on every block.
+      weights();
+      if (__builtin_amdgcn_ballot_w64(!(lsum <= 256.0f)) != 0) {
+        float mloc = -__builtin_inff();
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) mloc = fmaxf(mloc, sacc[t][v]);
+        // the partner lane (lane ^ 32) holds the other keys of this query
+        mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
+        const float m_blk = mloc * sl2;
+        const bool move = m_blk > m_run + 8.0f;
+        if (__builtin_amdgcn_ballot_w64(move) != 0) {
+          const float m_new = move ? m_blk : m_run;
+          const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);   // exactly 1 where m_run stays
+          l_run *= alpha;
+#pragma unroll
+          for (int d = 0; d < 4; ++d) oacc[d] *= alpha;
+          m_run = m_new;
+          weights();
         }
+      }
       l_run += lsum;
       // O^T += V^T P^T, 4 steps of 16 keys
 #pragma unroll
