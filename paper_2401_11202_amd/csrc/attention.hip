@@ -2,8 +2,8 @@
 //
 // One workgroup = one (sequence, head, 128-query block); four waves own 32
 // queries each.  Keys and values stream through a double-buffered LDS stage
-// 64 keys at a time.  Per key block each wave computes
-//     S^T[64 keys x 32 queries] = K_blk . Q^T       (v_mfma_f32_32x32x16_bf16)
+// BKV = 32 (or 64) keys at a time.  Per key block each wave computes
+//     S^T[BKV keys x 32 queries] = K_blk . Q^T      (v_mfma_f32_32x32x16_bf16)
 // so that every lane owns one query column: the running max and sum of the
 // online softmax are per-lane registers, and exp(S^T - max) converted to bf16
 // is directly the B operand of
@@ -26,23 +26,31 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int DH = 128, BQ = 128, BKV = 64, NT = 256;
-// K and V tiles: 64 rows of 256 B, written by direct-to-LDS buffer loads
+constexpr int DH = 128, BQ = 128, NT = 256;
+// K and V tiles: BKV rows of 256 B, written by direct-to-LDS buffer loads
 // (each wave load fills 1 KiB = 4 whole rows).  K: 16-byte chunk c of row r
 // at position c ^ (r & 15), so the 32 rows one S^T fragment read touches hit
 // all 64 banks.  V: 64-byte group g of row r at position g ^ (r & 3), so the
 // 4 rows x 64 B one half of a ds_read_b64_tr_b16 touches hit all 64 banks.
 constexpr int RP = 256;
-constexpr int T_BYTES = BKV * RP;
-constexpr int STAGE = 2 * T_BYTES;      // K tile, then V tile
 
 // LDS reads of K fragments through a restrict pointer, for the same reason
 // as lds_read_tr16: the alias scope keeps the wait insertion from making them
 // wait on the next tiles' DMA (which writes the other stage).
 __device__ __forceinline__ bf16x8 lds_read_b128(const char* __restrict__ p) { return *(const bf16x8*)p; }
 
-__global__ __launch_bounds__(NT, 2)
+// BKV = 32: three workgroups per CU (32 KiB of LDS each, at most 168
+// VGPRs); the third wave per SIMD hides more of the load, LDS and barrier
+// waits than the halved work between barriers costs.  BKV = 64: two per CU
+// (64 KiB), fewer barriers; the host takes it for grids smaller than the
+// CU count, where occupancy cannot help.
+template <int BKV>
+__global__ __launch_bounds__(NT, BKV == 32 ? 3 : 2)
 void attention_kernel(AttnParams p) {
+  static_assert(BKV == 32 || BKV == 64, "key blocks of 32 or 64");
+  constexpr int NSUB = BKV / 32;            // 32-key sub-tiles of S^T
+  constexpr int T_BYTES = BKV * RP;
+  constexpr int STAGE = 2 * T_BYTES;      // K tile, then V tile
   __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -69,7 +77,7 @@ void attention_kernel(AttnParams p) {
   // causal: a key shard that starts past this query block's last query holds
   // nothing for it; the combine does not read such a shard, so it is skipped
   // (workgroup-uniform, before any barrier)
-  if (p.nsplit > 1 && p.causal && split * p.kb_per * BKV > q0 + BQ - 1) return;
+  if (p.nsplit > 1 && p.causal && split * p.kb_per * 64 > q0 + BQ - 1) return;
 
   // ---- this lane's query fragments (B operand of S^T = K Q^T), kept in VGPRs
   const int qi = q0 + 32 * w + col;      // query position of this lane's column
@@ -95,7 +103,7 @@ void attention_kernel(AttnParams p) {
     char* ks = smem + buf * STAGE + w * 1024;
     char* vs = ks + T_BYTES;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < BKV / 16; ++i) {
       __builtin_amdgcn_raw_ptr_buffer_load_lds(krs, (lds_void*)(ks + i * 4096), 16, kvo,
                                                (uint32_t)kb * kstep + i * krow16, 0, 0);
       __builtin_amdgcn_raw_ptr_buffer_load_lds(vrs, (lds_void*)(vs + i * 4096), 16, vvo,
@@ -119,8 +127,9 @@ void attention_kernel(AttnParams p) {
   const int v_sw = v_row & 3;
 
   const int nkb_all = p.causal ? (q0 + BQ + BKV - 1) / BKV : p.S / BKV;
-  const int kb_begin = p.nsplit > 1 ? split * p.kb_per : 0;
-  const int nkb = p.nsplit > 1 ? min(nkb_all, kb_begin + p.kb_per) : nkb_all;   // one past the last block
+  // a shard's key range is kb_per blocks of 64 keys
+  const int kb_begin = p.nsplit > 1 ? split * p.kb_per * (64 / BKV) : 0;
+  const int nkb = p.nsplit > 1 ? min(nkb_all, kb_begin + p.kb_per * (64 / BKV)) : nkb_all;   // one past the last block
   const int wave_last_q = q0 + 32 * w + 31;
 
   if (kb_begin < nkb) gload(kb_begin, 0);
@@ -138,10 +147,12 @@ void attention_kernel(AttnParams p) {
     if (!p.causal || k0 <= wave_last_q) {
       const char* ks = smem + cur * STAGE;
       const char* vs = ks + T_BYTES;
-      // S^T = K Q^T for two 32-key sub-tiles
-      f32x16 sacc[2];
+      // S^T = K Q^T for NSUB 32-key sub-tiles: this lane's column holds
+      // query qi, keys k0 + 32 t + 8 (v / 4) + 4 h + v % 4 in element v of
+      // sub-tile t
+      f32x16 sacc[NSUB];
 #pragma unroll
-      for (int t = 0; t < 2; ++t) {
+      for (int t = 0; t < NSUB; ++t) {
 #pragma unroll
         for (int v = 0; v < 16; ++v) sacc[t][v] = 0.0f;
         const int r = 32 * t + col;
@@ -155,7 +166,7 @@ void attention_kernel(AttnParams p) {
       // exponent: p = 2^(s c - m) with m the subtracted maximum in log2 units
       if (p.causal && k0 + BKV - 1 > q0 + 32 * w) {   // wave-uniform: only blocks on the diagonal
 #pragma unroll
-        for (int t = 0; t < 2; ++t)
+        for (int t = 0; t < NSUB; ++t)
 #pragma unroll
           for (int v = 0; v < 16; ++v) {
             const int key = k0 + 32 * t + 8 * (v >> 2) + 4 * h + (v & 3);
@@ -164,11 +175,11 @@ void attention_kernel(AttnParams p) {
       }
       const float sl2 = p.scale_log2;
       float lsum = 0.0f;
-      bf16x8 pf[4];
+      bf16x8 pf[2 * NSUB];
       auto weights = [&]() {
         lsum = 0.0f;
 #pragma unroll
-        for (int t = 0; t < 2; ++t)
+        for (int t = 0; t < NSUB; ++t)
 #pragma unroll
           for (int v = 0; v < 16; ++v) {
             const float e = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[t][v], sl2, -m_run));
@@ -181,7 +192,7 @@ void attention_kernel(AttnParams p) {
       // fp32 and bf16; the softmax does not depend on the constant
       // subtracted) and O and l are rescaled in few blocks.  The block
       // maximum itself is needed only then: the weights are formed with the
-      // current m first, and a lane whose 32 weights sum to at most 2^8 has
+      // current m first, and a lane whose 16 * NSUB weights sum to at most 2^8 has
       // none above 2^8, i.e. no score that would move m.  Only when some
       // lane's sum exceeds 2^8 (or is inf / NaN, as on the first block,
       // where m starts at -1e30) does the wave take the maximum over both
@@ -192,7 +203,7 @@ void attention_kernel(AttnParams p) {
       if (__builtin_amdgcn_ballot_w64(!(lsum <= 256.0f)) != 0) {
         float mloc = -__builtin_inff();
 #pragma unroll
-        for (int t = 0; t < 2; ++t)
+        for (int t = 0; t < NSUB; ++t)
 #pragma unroll
           for (int v = 0; v < 16; ++v) mloc = fmaxf(mloc, sacc[t][v]);
         // the partner lane (lane ^ 32) holds the other keys of this query
@@ -210,9 +221,9 @@ void attention_kernel(AttnParams p) {
         }
       }
       l_run += lsum;
-      // O^T += V^T P^T, 4 steps of 16 keys
+      // O^T += V^T P^T, BKV / 16 steps of 16 keys
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
+      for (int u = 0; u < BKV / 16; ++u) {
 #pragma unroll
         for (int d = 0; d < 4; ++d) {
           const char* base = vs + (16 * u + v_row) * RP + 64 * (d ^ v_sw) + v_colb;
@@ -303,7 +314,20 @@ hipError_t launch_attention_combine(const AttnParams& p, hipStream_t s) {
 
 hipError_t launch_attention(const AttnParams& p, hipStream_t s) {
   const unsigned nwg = (unsigned)(p.S / BQ) * p.B * p.H * p.nsplit;
-  hipLaunchKernelGGL(attention_kernel, dim3(nwg), dim3(NT), 0, s, p);
+  // CU count per device, looked up once (racing first calls store the same value)
+  static int cus[64] = {};
+  int dev = 0, ncu = 256;
+  if (hipGetDevice(&dev) == hipSuccess && dev >= 0 && dev < 64) {
+    if (cus[dev] == 0) {
+      int n = 0;
+      if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && n > 0) cus[dev] = n;
+    }
+    if (cus[dev] > 0) ncu = cus[dev];
+  }
+  if (nwg < (unsigned)ncu)
+    hipLaunchKernelGGL(attention_kernel<64>, dim3(nwg), dim3(NT), 0, s, p);
+  else
+    hipLaunchKernelGGL(attention_kernel<32>, dim3(nwg), dim3(NT), 0, s, p);
   return hipGetLastError();
 }
 

@@ -2,8 +2,8 @@
 // B K-contiguous or stored [K, N].
 //
 // One workgroup computes a 256x256 output tile of one virtual shard with eight
-// waves (2 x 4, two per SIMD), each owning a 128x64 sub-tile as 4 x 2
-// accumulators of v_mfma_f32_32x32x16_bf16.  K advances in 64-wide tiles
+// waves (2 x 4, two per SIMD), each owning a 128x64 sub-tile as 8 x 4
+// accumulators of v_mfma_f32_16x16x32_bf16.  K advances in 64-wide tiles
 // through LDS buffers filled by buffer loads that write LDS directly (no
 // register staging).  With A K-contiguous (every forward product) the two
 // waves of a SIMD take turns: one runs a K tile's MFMAs on fragments already
@@ -388,7 +388,7 @@ __device__ __forceinline__ void gemm_body(const GemmParams& p, const GemmParts* 
   // buffers for each A half (16 KiB) and three for B (32 KiB): 160 KiB.
   // Workgroup barriers cut time into phases of one K tile's MFMAs; in each
   // phase one group multiplies a K tile whose fragments it already holds
-  // (32 MFMAs and nothing else, so nothing can hold them up) while the other
+  // (64 MFMAs and nothing else, so nothing can hold them up) while the other
   // group reads the fragments of its next K tile out of LDS and issues the
   // loads.  Group 1 runs one phase behind:
   //   phase 2t:   group 0 reads tile t, loads;  group 1 multiplies tile t-1
@@ -664,10 +664,34 @@ __device__ __forceinline__ void gemm_body(const GemmParams& p, const GemmParts* 
     __syncthreads();
     write((uint16_t*)Cg, PARTS && t->c_rows);
   } else {
-    // fp32 results (plain, residual or split partial): two halves of 128 rows
+    // fp32 results (plain, residual or split partial): two halves of 128 rows.
+    // Thread t writes 4 columns (16 B) of row t / 64 of each 8-row pass.  A
+    // residual is read for all 16 passes of a half before the half is
+    // staged, so the reads overlap the staging and are one round trip per
+    // half rather than one per few passes (it may alias C: each element is
+    // read and then written by the same thread).
     float* cs = (float*)smem;
+    constexpr int NPASS = (BM / 2) / (NT / 64);
+    const int cr = tid >> 6, cc = (tid & 63) * 4;
 #pragma unroll
     for (int q = 0; q < 2; ++q) {
+      f32x4 rv[NPASS];
+      if (EPI == EPI_RESID_F32) {
+#pragma unroll
+        for (int k = 0; k < NPASS; ++k) {
+          const int r0 = k * (NT / 64), r = q * (BM / 2) + r0 + cr;
+          rv[k] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+          if (r < rows && cc < cols) {
+            const int64_t m = row0 + r, n = col0 + cc;
+            if (PARTS && t->c_rows) {   // into a part: the residual is the part itself
+              const int cb = (row0 + q * (BM / 2) + r0) / t->c_rows;
+              rv[k] = *(const f32x4*)((const float*)t->c[cb] + (m - (int64_t)cb * t->c_rows) * p.ldc + n);
+            } else {
+              rv[k] = *(const f32x4*)(p.resid + m * p.ldr + n);
+            }
+          }
+        }
+      }
       if (wm == q) {
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
@@ -690,11 +714,9 @@ __device__ __forceinline__ void gemm_body(const GemmParams& p, const GemmParts* 
         }
       }
       __syncthreads();
-      // 8 rows per pass: thread t writes 4 columns (16 B) of row t / 64
-      const int cr = tid >> 6, cc = (tid & 63) * 4;
-#pragma unroll 4
-      for (int r0 = 0; r0 < BM / 2; r0 += NT / 64) {
-        const int rl = r0 + cr, r = q * (BM / 2) + rl;
+#pragma unroll
+      for (int k = 0; k < NPASS; ++k) {
+        const int r0 = k * (NT / 64), rl = r0 + cr, r = q * (BM / 2) + rl;
         if (r >= rows || cc >= cols) continue;
         const f32x4 v = *(const f32x4*)(cs + rl * CPF + cc);
         const int64_t m = row0 + r, n = col0 + cc;
@@ -707,13 +729,11 @@ __device__ __forceinline__ void gemm_body(const GemmParams& p, const GemmParts* 
           } else {
             __builtin_nontemporal_store(v, (f32x4*)((float*)Cg + m * p.ldc + n));
           }
-        } else if (PARTS && t->c_rows) {   // EPI_RESID_F32 into a part: the residual is the part itself
+        } else if (PARTS && t->c_rows) {   // EPI_RESID_F32 into a part
           const int cb = (row0 + q * (BM / 2) + r0) / t->c_rows;
-          float* dst = (float*)t->c[cb] + (m - (int64_t)cb * t->c_rows) * p.ldc + n;
-          __builtin_nontemporal_store(*(const f32x4*)dst + v, (f32x4*)dst);
+          __builtin_nontemporal_store(rv[k] + v, (f32x4*)((float*)t->c[cb] + (m - (int64_t)cb * t->c_rows) * p.ldc + n));
         } else {  // EPI_RESID_F32
-          const f32x4 rv = *(const f32x4*)(p.resid + m * p.ldr + n);
-          __builtin_nontemporal_store(rv + v, (f32x4*)((float*)Cg + m * p.ldc + n));
+          __builtin_nontemporal_store(rv[k] + v, (f32x4*)((float*)Cg + m * p.ldc + n));
         }
       }
       if (q == 0) __syncthreads();   // the second half reuses the buffer
