@@ -12,6 +12,8 @@
 // the key order inside each 16-key MFMA step is permuted identically on the P
 // and V sides (any order is exact for the contraction).
 // With causal masking a query sees keys at positions <= its own.
+#include <type_traits>
+
 #include "kernels.h"
 #include "lds_dma.h"
 
@@ -139,8 +141,10 @@ void attention_kernel(AttnParams p) {
   // before each S^T step.
   __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
   __syncthreads();
-  for (int kb = kb_begin; kb < nkb; ++kb) {
-    const int cur = (kb - kb_begin) & 1;
+  // Two blocks per loop trip, so that each block's stage is a constant and
+  // its LDS offset folds into the read instructions.
+  auto block = [&](auto stage_c, int kb) {
+    constexpr int cur = decltype(stage_c)::value;
     // the other stage was finished with before the last barrier
     if (kb + 1 < nkb) gload(kb + 1, cur ^ 1);
     const int k0 = kb * BKV;
@@ -238,6 +242,10 @@ void attention_kernel(AttnParams p) {
     }
     __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0): this wave's loads of the next tiles landed
     __syncthreads();
+  };
+  for (int kb = kb_begin; kb < nkb; kb += 2) {
+    block(std::integral_constant<int, 0>{}, kb);
+    if (kb + 1 < nkb) block(std::integral_constant<int, 1>{}, kb + 1);
   }
 
   const float l_tot = l_run + __shfl_xor(l_run, 32);
