@@ -90,6 +90,28 @@ def test_split_kv_long_sequence_sampled_rows():
     assert err <= TOL_BF16
 
 
+@pytest.mark.parametrize("causal", [True, False])
+@pytest.mark.parametrize("H", [15, 16])
+def test_key_block_size_choice_sampled_rows(H, causal):
+    """The kernel streams keys in blocks of 64 when the grid has fewer
+    workgroups than the GPU has CUs, else in blocks of 32 (three workgroups
+    per CU).  One sequence of 2048 keys gives 16 query blocks per head: 240
+    workgroups at 15 heads and 256 at 16 heads, the two sides of that choice
+    on a 256-CU GPU.  Rows from every 128-query block, the last position and
+    rows on both sides of 32- and 64-key block edges match the oracle."""
+    B, S = 1, 2048
+    Q, K, V = make_qkv(130 + H, B, S, H)
+    rng = np.random.default_rng(130 + H)
+    rows = np.unique(np.concatenate([[0, 31, 32, 63, 64, 95, 96, S - 1],
+                                     [128 * j + int(rng.integers(0, 128)) for j in range(S // 128)]]))
+    say(f"attention B={B} S={S} H={H} causal={causal} ({(S // 128) * H} workgroups): {len(rows)} sampled rows")
+    o = host(run(Q, K, V, B, S, H, causal, 1))[rows]
+    ref, nrm = reference(Q, K, V, B, S, H, causal, rows)
+    err = O.normalised_error(o, ref, nrm)
+    say(f"    max normalised error {err:.3e}")
+    assert err <= TOL_BF16
+
+
 @pytest.mark.parametrize("B,S,H,R", [(1, 8192, 2, 4), (1, 4096, 1, 2), (2, 4096, 1, 2)])
 def test_split_kv_causal_parts_sampled_rows(B, S, H, R):
     """Shards of >= 2048 keys on a small causal grid run as ordered parts
