@@ -64,15 +64,30 @@ void attention_kernel(AttnParams p) {
   const int nqb = p.S / BQ;
   const int nbh = p.B * p.H;
   const int per_qb = nbh * p.nsplit;
-  const int qs = blockIdx.x / per_qb;
+  // Workgroup i runs on XCD i mod 8.
+  int qs, split, bh;
+  if (p.nsplit == 1 && (nbh & 7) == 0) {
+    // Unsplit: XCD x takes (sequence, head)s x, x + 8, ... in groups of up
+    // to 8, each group's query blocks heaviest first, so the workgroups an
+    // XCD holds at once stream the same few heads' K / V through its L2.
+    const int x = blockIdx.x & 7, j = blockIdx.x >> 3;
+    int G = 8;
+    while ((nbh / 8) % G) G >>= 1;
+    const int gen = j / (G * nqb), r = j - gen * (G * nqb);
+    qs = r / G;
+    bh = (gen * G + (r - qs * G)) * 8 + x;
+    split = 0;
+  } else {
+    // Under a causal mask the shards of early keys carry most of the work,
+    // so (shard, head) must not stay tied to one XCD: rotating it by the
+    // query block spreads every shard over all XCDs.
+    qs = blockIdx.x / per_qb;
+    int inner = blockIdx.x - qs * per_qb;
+    if (p.nsplit > 1) inner = (inner + qs) % per_qb;
+    split = inner / nbh;
+    bh = inner - split * nbh;
+  }
   const int qb = nqb - 1 - qs;
-  // Workgroup i runs on XCD i mod 8.  Under a causal mask the shards of early
-  // keys carry most of the work, so (shard, head) must not stay tied to one
-  // XCD: rotating it by the query block spreads every shard over all XCDs.
-  int inner = blockIdx.x - qs * per_qb;
-  if (p.nsplit > 1) inner = (inner + qs) % per_qb;
-  const int split = inner / nbh;
-  const int bh = inner - split * nbh;
   const int b = bh / p.H, head = bh - b * p.H;
   const int q0 = qb * BQ;
   const int64_t tok0 = (int64_t)b * p.S;
