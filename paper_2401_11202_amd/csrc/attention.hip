@@ -169,6 +169,10 @@ void attention_kernel(AttnParams p) {
       // S^T = K Q^T for NSUB 32-key sub-tiles: this lane's column holds
       // query qi, keys k0 + 32 t + 8 (v / 4) + 4 h + v % 4 in element v of
       // sub-tile t
+      // While it issues the S^T products a wave takes issue priority over the
+      // other waves of its SIMD (in their softmax or P V steps), which keeps
+      // the matrix pipe fed between their shorter MFMA runs.
+      __builtin_amdgcn_s_setprio(1);
       f32x16 sacc[NSUB];
 #pragma unroll
       for (int t = 0; t < NSUB; ++t) {
@@ -181,6 +185,7 @@ void attention_kernel(AttnParams p) {
           sacc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ds], sacc[t], 0, 0, 0);
         }
       }
+      __builtin_amdgcn_s_setprio(0);
       // causal mask on the raw scores; the scale (> 0) is folded into the
       // exponent: p = 2^(s c - m) with m the subtracted maximum in log2 units
       if (p.causal && k0 + BKV - 1 > q0 + 32 * w) {   // wave-uniform: only blocks on the diagonal
